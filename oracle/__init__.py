@@ -1,0 +1,220 @@
+"""CPU oracle for the fused block-scaled FP8 MoE layer (paper Section 3.1.1).
+
+TEST INFRASTRUCTURE ONLY: tests/, ``__graft_entry__.smoke()`` and the
+``cpu_baseline`` leg of ``bench.py`` are the only users.  The product path
+(``paper_2608_14560_amd``) never imports this package, and this package never
+imports the product path: the two share no code.
+
+The arithmetic lives in ``moe_oracle.c`` (plain C, double accumulation);
+this module only builds it with gcc and marshals numpy arrays through ctypes.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+from dataclasses import dataclass
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "moe_oracle.c")
+_LIB = os.path.join(_HERE, "liboracle.so")
+
+CFLAGS = ["-O2", "-fopenmp", "-ffp-contract=off", "-fno-fast-math", "-std=c11",
+          "-Wall", "-shared", "-fPIC"]
+
+
+def build(force: bool = True) -> str:
+    """Compile ``moe_oracle.c`` into ``liboracle.so`` next to it."""
+    if force or not os.path.exists(_LIB):
+        tmp = _LIB + ".tmp"
+        subprocess.run(["gcc", *CFLAGS, _SRC, "-o", tmp, "-lm"], check=True)
+        os.replace(tmp, _LIB)
+    return _LIB
+
+
+class OracleShape(ctypes.Structure):
+    _fields_ = [("T", ctypes.c_int32), ("H", ctypes.c_int32), ("I", ctypes.c_int32),
+                ("num_experts", ctypes.c_int32), ("num_local_experts", ctypes.c_int32),
+                ("local_expert_offset", ctypes.c_int32), ("n_group", ctypes.c_int32),
+                ("topk_group", ctypes.c_int32), ("top_k", ctypes.c_int32),
+                ("routed_scaling_factor", ctypes.c_float)]
+
+
+_lib = None
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB):
+            build(force=False)
+        L = ctypes.CDLL(_LIB)
+        P = ctypes.c_void_p
+        L.oracle_e4m3_decode.argtypes = [ctypes.c_uint8]
+        L.oracle_e4m3_decode.restype = ctypes.c_double
+        L.oracle_e4m3_encode.argtypes = [ctypes.c_float]
+        L.oracle_e4m3_encode.restype = ctypes.c_uint8
+        L.oracle_bf16_from_double.argtypes = [ctypes.c_double]
+        L.oracle_bf16_from_double.restype = ctypes.c_uint16
+        L.oracle_sigmoid.argtypes = [ctypes.c_float]
+        L.oracle_sigmoid.restype = ctypes.c_float
+        L.oracle_sigmoid_array.argtypes = [P, P, ctypes.c_int64]
+        L.oracle_sigmoid_array.restype = None
+        L.oracle_route.argtypes = [ctypes.POINTER(OracleShape), P, P, P, P]
+        L.oracle_route.restype = ctypes.c_int
+        L.oracle_permute.argtypes = [ctypes.POINTER(OracleShape), P, P, P, P]
+        L.oracle_permute.restype = ctypes.c_int
+        L.oracle_expert_ffn.argtypes = [ctypes.c_int32, ctypes.c_int32] + [P] * 10
+        L.oracle_expert_ffn.restype = None
+        L.oracle_forward.argtypes = ([ctypes.POINTER(OracleShape)] + [P] * 8
+                                     + [P, ctypes.c_int32, P, P, P])
+        L.oracle_forward.restype = ctypes.c_int
+        L.oracle_num_threads.argtypes = []
+        L.oracle_num_threads.restype = ctypes.c_int
+        _lib = L
+    return _lib
+
+
+def _ptr(a: np.ndarray | None):
+    if a is None:
+        return None
+    assert a.flags.c_contiguous
+    return a.ctypes.data_as(ctypes.c_void_p)
+
+
+@dataclass(frozen=True)
+class Shape:
+    T: int
+    H: int
+    I: int
+    num_experts: int
+    num_local_experts: int
+    local_expert_offset: int
+    n_group: int
+    topk_group: int
+    top_k: int
+    routed_scaling_factor: float
+
+    def c(self) -> OracleShape:
+        return OracleShape(self.T, self.H, self.I, self.num_experts, self.num_local_experts,
+                           self.local_expert_offset, self.n_group, self.topk_group,
+                           self.top_k, self.routed_scaling_factor)
+
+
+def shape_of(cfg) -> Shape:
+    """Shape from any object carrying the same field names (a workload config)."""
+    return Shape(*(getattr(cfg, f) for f in Shape.__dataclass_fields__))
+
+
+def e4m3_decode(q: int) -> float:
+    return lib().oracle_e4m3_decode(q)
+
+
+def e4m3_encode(v: float) -> int:
+    return lib().oracle_e4m3_encode(v)
+
+
+def bf16_from_double(v: float) -> int:
+    return lib().oracle_bf16_from_double(v)
+
+
+def sigmoid(x: np.ndarray) -> np.ndarray:
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    y = np.empty_like(x)
+    lib().oracle_sigmoid_array(_ptr(x), _ptr(y), x.size)
+    return y
+
+
+def route(shape: Shape, logits: np.ndarray, bias: np.ndarray):
+    """Stage (1): returns (topk_ids int32 [T,k], topk_weights float32 [T,k])."""
+    logits = np.ascontiguousarray(logits, dtype=np.float32)
+    bias = np.ascontiguousarray(bias, dtype=np.float32)
+    ids = np.empty((shape.T, shape.top_k), np.int32)
+    w = np.empty((shape.T, shape.top_k), np.float32)
+    rc = lib().oracle_route(ctypes.byref(shape.c()), _ptr(logits), _ptr(bias), _ptr(ids), _ptr(w))
+    if rc:
+        raise ValueError(f"oracle_route: bad argument ({rc})")
+    return ids, w
+
+
+def permute(shape: Shape, topk_ids: np.ndarray):
+    """Stage (2) bookkeeping: (expert_offsets [E_l+1], perm_token [P], pair_row [T,k])."""
+    ids = np.ascontiguousarray(topk_ids, dtype=np.int32)
+    offs = np.empty(shape.num_local_experts + 1, np.int32)
+    perm = np.empty(max(1, shape.T * shape.top_k), np.int32)
+    pr = np.empty((shape.T, shape.top_k), np.int32)
+    rc = lib().oracle_permute(ctypes.byref(shape.c()), _ptr(ids), _ptr(offs), _ptr(perm), _ptr(pr))
+    if rc:
+        raise ValueError(f"oracle_permute: bad argument ({rc})")
+    return offs, perm[: offs[-1]].copy(), pr
+
+
+def expert_ffn(hidden_row, hidden_scale_row, w13, w13_scale, w2, w2_scale):
+    """Stage (3) for one token row and one expert.
+
+    Returns (y float64 [H], g float32 [2I], q uint8 [I], qscale float32 [I/128])."""
+    H = hidden_row.shape[0]
+    I = w2.shape[1]
+    args = [np.ascontiguousarray(a) for a in (hidden_row, hidden_scale_row, w13, w13_scale, w2, w2_scale)]
+    y = np.empty(H, np.float64)
+    g = np.empty(2 * I, np.float32)
+    q = np.empty(I, np.uint8)
+    qs = np.empty(I // 128, np.float32)
+    lib().oracle_expert_ffn(H, I, *[_ptr(a) for a in args], _ptr(y), _ptr(g), _ptr(q), _ptr(qs))
+    return y, g, q, qs
+
+
+def forward(shape: Shape, hidden, hidden_scale, logits, bias, w13, w13_scale, w2, w2_scale,
+            tokens=None):
+    """Stages (1)-(4) for the listed tokens (all tokens by default).
+
+    ``w13`` ... ``w2_scale`` are either arrays with a leading local-expert axis or
+    sequences with one entry (or None) per local expert.
+    Returns (out bf16 bits uint16 [n,H], topk_ids [n,k], topk_weights [n,k])."""
+    if tokens is None:
+        tokens = np.arange(shape.T, dtype=np.int32)
+    tokens = np.ascontiguousarray(tokens, dtype=np.int32)
+    n = tokens.shape[0]
+    El = shape.num_local_experts
+    keep = []
+
+    def table(ws, dtype):
+        arr = (ctypes.c_void_p * El)()
+        for e in range(El):
+            we = ws[e]
+            if we is None:
+                arr[e] = None
+                continue
+            we = np.ascontiguousarray(we, dtype=dtype)
+            keep.append(we)
+            arr[e] = we.ctypes.data
+        return arr
+
+    t13, t13s = table(w13, np.uint8), table(w13_scale, np.float32)
+    t2, t2s = table(w2, np.uint8), table(w2_scale, np.float32)
+    hidden = np.ascontiguousarray(hidden, dtype=np.uint8)
+    hidden_scale = np.ascontiguousarray(hidden_scale, dtype=np.float32)
+    logits = np.ascontiguousarray(logits, dtype=np.float32)
+    bias = np.ascontiguousarray(bias, dtype=np.float32)
+    out = np.empty((max(n, 1), shape.H), np.uint16)
+    ids = np.empty((max(n, 1), shape.top_k), np.int32)
+    w = np.empty((max(n, 1), shape.top_k), np.float32)
+    rc = lib().oracle_forward(ctypes.byref(shape.c()), _ptr(hidden), _ptr(hidden_scale),
+                              _ptr(logits), _ptr(bias),
+                              ctypes.cast(t13, ctypes.c_void_p), ctypes.cast(t13s, ctypes.c_void_p),
+                              ctypes.cast(t2, ctypes.c_void_p), ctypes.cast(t2s, ctypes.c_void_p),
+                              _ptr(tokens), n, _ptr(out), _ptr(ids), _ptr(w))
+    if rc:
+        raise ValueError(f"oracle_forward failed ({rc})")
+    return out[:n], ids[:n], w[:n]
+
+
+def num_threads() -> int:
+    return lib().oracle_num_threads()
+
+
+def bf16_bits_to_float(bits: np.ndarray) -> np.ndarray:
+    """Reads bf16 bit patterns as fp32 values (a reinterpretation, no arithmetic)."""
+    return (np.asarray(bits, dtype=np.uint16).astype(np.uint32) << 16).view(np.float32)

@@ -1,0 +1,456 @@
+/*
+ * moe_oracle.c -- plain, slow CPU oracle for the fused block-scaled FP8
+ * mixture-of-experts layer (the "Fused MoE" operator of the paper,
+ * Section 3.1.1, stages (1)-(4)).
+ *
+ * TEST INFRASTRUCTURE ONLY.  Nothing in the product path may call, link or
+ * load this file: only tests/, __graft_entry__.smoke() and the cpu_baseline
+ * leg of bench.py use it.  It shares no code, header, table or constant with
+ * the HIP implementation.
+ *
+ * Every step follows the paper's order: (1) routing scores from a sigmoid,
+ * group-limited top-k selection; (2) gathering the rows of each expert into a
+ * contiguous FP8 layout with 128-element fp32 block scales; (3) the gated MLP:
+ * FP8 block GEMM1 [rows,H]->[rows,2I], SwiGLU, re-quantisation, FP8 block
+ * GEMM2 [rows,I]->[rows,H]; (4) scattering the expert outputs back to the
+ * tokens, weighted by the routing scores.  Where the paper is silent the
+ * reading used here is stated next to the code; all readings are collected in
+ * the design notes of the repository.
+ *
+ * Precision: routing is fp32 (its integer decisions must be reproducible),
+ * the GEMMs accumulate in double, the SwiGLU is evaluated in double and
+ * rounded to fp32, the re-quantisation is fp32, the combine sums in double and
+ * rounds once to bf16 (round to nearest even).
+ *
+ * Build: gcc -O2 -fopenmp -ffp-contract=off -fno-fast-math -shared -fPIC
+ * (contraction must stay off: the fp32 routing sequence is a specification).
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+#ifdef _OPENMP
+#include <omp.h>
+#endif
+
+#define ORACLE_OK 0
+#define ORACLE_BAD_ARG 1
+#define ORACLE_NO_MEM 2
+
+typedef struct {
+  int32_t T, H, I;
+  int32_t num_experts;       /* E_g, width of the router            */
+  int32_t num_local_experts; /* E_l, experts whose weights are here */
+  int32_t local_expert_offset;
+  int32_t n_group, topk_group, top_k;
+  float routed_scaling_factor;
+} oracle_shape;
+
+/* ------------------------------------------------------------------------ */
+/* FP8 E4M3FN (OCP 8-bit floating point, E4M3 "FN": no infinities, a single  */
+/* NaN mantissa pattern, max finite 448).  Stage (2) of Section 3.1.1 stores */
+/* activations in FP8 with 128-element fp32 block scales.                     */
+/* ------------------------------------------------------------------------ */
+
+/* Decode one code from its bit fields: sign, 4-bit exponent (bias 7),
+ * 3-bit mantissa; exponent field 0 is subnormal (m * 2^-9); S.1111.111 is NaN. */
+double oracle_e4m3_decode(uint8_t q) {
+  int sign = (q >> 7) & 1;
+  int ef = (q >> 3) & 0xF;
+  int mf = q & 0x7;
+  double v;
+  if (ef == 0xF && mf == 0x7) return NAN;
+  if (ef == 0)
+    v = ldexp((double)mf, -9);
+  else
+    v = ldexp(1.0 + mf / 8.0, ef - 7);
+  return sign ? -v : v;
+}
+
+/* Encode an fp32 value: round to nearest, ties to even mantissa, saturating
+ * to +-448 (the re-quantised values never exceed 448 by more than a rounding
+ * error; saturation is the reading taken for that case).  NaN -> 0x7F. */
+uint8_t oracle_e4m3_encode(float v) {
+  uint8_t s;
+  double a, quantum, m, r;
+  int e, E;
+  if (isnan(v)) return 0x7F;
+  s = signbit(v) ? 0x80 : 0x00;
+  a = fabs((double)v);
+  if (a >= 448.0) return (uint8_t)(s | 0x7E);
+  if (a == 0.0) return s;
+  frexp(a, &e);           /* a in [2^(e-1), 2^e) */
+  E = e - 1;
+  if (E < -6) E = -6;     /* subnormal binade shares the quantum 2^-9 */
+  quantum = ldexp(1.0, E - 3);
+  m = nearbyint(a / quantum); /* exact division by a power of two; RNE */
+  r = m * quantum;
+  if (r == 0.0) return s;
+  frexp(r, &e);           /* re-derive the binade: rounding may carry up */
+  E = e - 1;
+  if (E < -6) {
+    return (uint8_t)(s | (int)(r / ldexp(1.0, -9)));
+  }
+  {
+    int mant = (int)(r / ldexp(1.0, E - 3)) - 8;
+    return (uint8_t)(s | ((E + 7) << 3) | mant);
+  }
+}
+
+/* bf16 (8 significant bits, fp32 exponent range) from a double, rounded once
+ * to nearest even; the combine of stage (4) writes bf16. */
+uint16_t oracle_bf16_from_double(double v) {
+  uint16_t sign;
+  double a, m, r;
+  int e, qexp;
+  float f;
+  uint32_t bits;
+  if (isnan(v)) return 0x7FC0;
+  sign = signbit(v) ? 0x8000 : 0;
+  a = fabs(v);
+  if (a == 0.0) return sign;
+  frexp(a, &e);           /* a in [2^(e-1), 2^e): quantum 2^(e-8) */
+  qexp = e - 8;
+  if (qexp < -133) qexp = -133; /* bf16 subnormal quantum */
+  m = nearbyint(ldexp(a, -qexp));
+  r = ldexp(m, qexp);
+  f = (float)r;           /* exact (or +inf past the bf16 range) */
+  memcpy(&bits, &f, 4);
+  return (uint16_t)(sign | (bits >> 16));
+}
+
+/* ------------------------------------------------------------------------ */
+/* Routing sigmoid.  Stage (1) applies a sigmoid to the router logits.  Two  */
+/* faithful fp32 sigmoids that differ in the last bit can pick different     */
+/* experts when two keys are within an ulp, so the layer fixes one fp32      */
+/* operation sequence (Cody-Waite reduction of exp, degree-7 Taylor          */
+/* polynomial in Horner form with fused multiply-adds, IEEE division).  The  */
+/* constants come from ln 2, log2 e and 1/k!, rounded to fp32.               */
+/* ------------------------------------------------------------------------ */
+float oracle_sigmoid(float x) {
+  const float log2e = 1.44269502f;          /* log2(e) rounded to fp32      */
+  const float ln2_hi = 0.693145751953125f;  /* ln 2 with 12 low bits clear  */
+  const float ln2_lo = 1.42860677e-6f;      /* fp32(ln 2 - ln2_hi)          */
+  float z, n, r, p, e;
+  if (x < -80.0f) x = -80.0f;
+  if (x > 80.0f) x = 80.0f;
+  z = -x;                                   /* sigma(x) = 1 / (1 + e^z) */
+  n = rintf(z * log2e);                     /* nearest, ties to even     */
+  r = fmaf(-n, ln2_hi, z);
+  r = fmaf(-n, ln2_lo, r);
+  p = 1.0f / 5040.0f;                       /* 1/7! */
+  p = fmaf(p, r, 1.0f / 720.0f);            /* 1/6! */
+  p = fmaf(p, r, 1.0f / 120.0f);            /* 1/5! */
+  p = fmaf(p, r, 1.0f / 24.0f);             /* 1/4! */
+  p = fmaf(p, r, 1.0f / 6.0f);              /* 1/3! */
+  p = fmaf(p, r, 0.5f);                     /* 1/2! */
+  p = fmaf(p, r, 1.0f);
+  p = fmaf(p, r, 1.0f);
+  e = ldexpf(p, (int)n);
+  return 1.0f / (1.0f + e);
+}
+
+void oracle_sigmoid_array(const float *x, float *y, int64_t n) {
+  int64_t i;
+#pragma omp parallel for schedule(static)
+  for (i = 0; i < n; ++i) y[i] = oracle_sigmoid(x[i]);
+}
+
+/* ------------------------------------------------------------------------ */
+/* Stage (1): DeepSeek-V3 group-limited routing for one token.               */
+/*   s_e   = sigmoid(logit_e)                       (fp32)                   */
+/*   key_e = s_e + bias_e                           (fp32; selection only)  */
+/*   gs_g  = sum of the two largest keys of group g (fp32)                   */
+/*   keep the topk_group groups of largest gs, then the top_k experts of     */
+/*   largest key inside them; order: larger value first, ties -> lower index */
+/*   w_j   = s_{id_j} / (sum over the k selected s) * routed_scaling_factor  */
+/*           (sum in selection order, over all k, local or not)              */
+/* ------------------------------------------------------------------------ */
+static int beats(float va, int ia, float vb, int ib) {
+  return va > vb || (va == vb && ia < ib);
+}
+
+static void route_token(const oracle_shape *s, const float *logit,
+                        const float *bias, int32_t *ids, float *w) {
+  int E = s->num_experts, G = s->n_group, gsz = E / G;
+  float *sc = (float *)malloc(sizeof(float) * E);
+  float *key = (float *)malloc(sizeof(float) * E);
+  float *gs = (float *)malloc(sizeof(float) * G);
+  char *gkeep = (char *)calloc(G, 1);
+  char *taken = (char *)calloc(E, 1);
+  int e, g, j, r;
+  float sum;
+
+  for (e = 0; e < E; ++e) {
+    sc[e] = oracle_sigmoid(logit[e]);
+    key[e] = sc[e] + bias[e];
+  }
+  for (g = 0; g < G; ++g) {
+    int b1 = -1, b2 = -1;
+    for (e = g * gsz; e < (g + 1) * gsz; ++e) {
+      if (b1 < 0 || beats(key[e], e, key[b1], b1)) {
+        b2 = b1;
+        b1 = e;
+      } else if (b2 < 0 || beats(key[e], e, key[b2], b2)) {
+        b2 = e;
+      }
+    }
+    gs[g] = key[b1] + key[b2];
+  }
+  for (r = 0; r < s->topk_group; ++r) {
+    int best = -1;
+    for (g = 0; g < G; ++g)
+      if (!gkeep[g] && (best < 0 || beats(gs[g], g, gs[best], best))) best = g;
+    gkeep[best] = 1;
+  }
+  for (j = 0; j < s->top_k; ++j) {
+    int best = -1;
+    for (e = 0; e < E; ++e) {
+      if (!gkeep[e / gsz] || taken[e]) continue;
+      if (best < 0 || beats(key[e], e, key[best], best)) best = e;
+    }
+    taken[best] = 1;
+    ids[j] = best;
+  }
+  sum = 0.0f;
+  for (j = 0; j < s->top_k; ++j) sum += sc[ids[j]];
+  for (j = 0; j < s->top_k; ++j)
+    w[j] = (sc[ids[j]] / sum) * s->routed_scaling_factor;
+
+  free(sc);
+  free(key);
+  free(gs);
+  free(gkeep);
+  free(taken);
+}
+
+int oracle_check_shape(const oracle_shape *s) {
+  if (!s) return ORACLE_BAD_ARG;
+  if (s->T < 0 || s->H <= 0 || s->I <= 0) return ORACLE_BAD_ARG;
+  if (s->H % 128 || s->I % 128) return ORACLE_BAD_ARG;
+  if (s->num_experts <= 0 || s->n_group <= 0) return ORACLE_BAD_ARG;
+  if (s->num_experts % s->n_group) return ORACLE_BAD_ARG;
+  if (s->num_experts / s->n_group < 2) return ORACLE_BAD_ARG;
+  if (s->topk_group <= 0 || s->topk_group > s->n_group) return ORACLE_BAD_ARG;
+  if (s->top_k <= 0 ||
+      s->top_k > s->topk_group * (s->num_experts / s->n_group))
+    return ORACLE_BAD_ARG;
+  if (s->num_local_experts <= 0 || s->local_expert_offset < 0 ||
+      s->local_expert_offset + s->num_local_experts > s->num_experts)
+    return ORACLE_BAD_ARG;
+  return ORACLE_OK;
+}
+
+int oracle_route(const oracle_shape *s, const float *logits, const float *bias,
+                 int32_t *topk_ids, float *topk_w) {
+  int t;
+  if (oracle_check_shape(s)) return ORACLE_BAD_ARG;
+#pragma omp parallel for schedule(dynamic, 16)
+  for (t = 0; t < s->T; ++t)
+    route_token(s, logits + (int64_t)t * s->num_experts, bias,
+                topk_ids + (int64_t)t * s->top_k, topk_w + (int64_t)t * s->top_k);
+  return ORACLE_OK;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Stage (2) bookkeeping: the (token, slot) pairs whose expert is resident   */
+/* are grouped by local expert into one contiguous layout.  Order inside an  */
+/* expert: ascending token (a token holds an expert at most once).           */
+/*   expert_offsets[e] = first row of local expert e, [E_l] = P              */
+/*   perm_token[row]   = token of that row                                   */
+/*   pair_row[t*k+j]   = row of pair (t, j), -1 when its expert is remote    */
+/* ------------------------------------------------------------------------ */
+int oracle_permute(const oracle_shape *s, const int32_t *topk_ids,
+                   int32_t *expert_offsets, int32_t *perm_token,
+                   int32_t *pair_row) {
+  int64_t pos = 0, p, npairs;
+  int e, t, j, k;
+  if (oracle_check_shape(s)) return ORACLE_BAD_ARG;
+  k = s->top_k;
+  npairs = (int64_t)s->T * k;
+  for (p = 0; p < npairs; ++p) pair_row[p] = -1;
+  for (e = 0; e < s->num_local_experts; ++e) {
+    int gid = s->local_expert_offset + e;
+    expert_offsets[e] = (int32_t)pos;
+    for (t = 0; t < s->T; ++t)
+      for (j = 0; j < k; ++j)
+        if (topk_ids[(int64_t)t * k + j] == gid) {
+          perm_token[pos] = t;
+          pair_row[(int64_t)t * k + j] = (int32_t)pos;
+          ++pos;
+        }
+  }
+  expert_offsets[s->num_local_experts] = (int32_t)pos;
+  return ORACLE_OK;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Stage (3): the gated MLP of one expert applied to one token row.          */
+/*   x[h]   = dec(hidden[h]) * hidden_scale[h/128]                (1x128)    */
+/*   W13[n,h] = dec(w13[n,h]) * w13_scale[n/128, h/128]           (128x128)  */
+/*   g[n]   = fp32( sum_h x[h] W13[n,h] )   rows [0,I) gate, [I,2I) up       */
+/*   a[i]   = fp32( silu(g[i]) * g[I+i] ),  silu(z) = z / (1 + e^-z)         */
+/*   per 128-block b of a: amax_b = max|a|, scale_b = amax_b / 448 (fp32),   */
+/*     q[i] = e4m3(a[i] / scale_b) (fp32 division, RNE, saturating);         */
+/*     amax_b = 0 gives scale_b = 1 and q = 0                                */
+/*   y[n]   = sum_i dec(q[i]) scale[i/128] dec(w2[n,i]) w2_scale[n/128,i/128] */
+/* Optional outputs: g (fp32, 2I), q (I codes), qscale (I/128).              */
+/* ------------------------------------------------------------------------ */
+void oracle_expert_ffn(int32_t H, int32_t I, const uint8_t *hidden_row,
+                       const float *hidden_scale_row, const uint8_t *w13,
+                       const float *w13_scale, const uint8_t *w2,
+                       const float *w2_scale, double *y, float *g_out,
+                       uint8_t *q_out, float *qscale_out) {
+  int HB = H / 128, IB = I / 128;
+  double *x = (double *)malloc(sizeof(double) * H);
+  float *g = (float *)malloc(sizeof(float) * 2 * I);
+  float *a = (float *)malloc(sizeof(float) * I);
+  uint8_t *q = (uint8_t *)malloc(I);
+  float *qs = (float *)malloc(sizeof(float) * IB);
+  double *aq = (double *)malloc(sizeof(double) * I);
+  int h, n, i, b;
+
+  for (h = 0; h < H; ++h)
+    x[h] = oracle_e4m3_decode(hidden_row[h]) * (double)hidden_scale_row[h / 128];
+  for (n = 0; n < 2 * I; ++n) {
+    const uint8_t *wr = w13 + (int64_t)n * H;
+    const float *sr = w13_scale + (int64_t)(n / 128) * HB;
+    double acc = 0.0;
+    for (h = 0; h < H; ++h)
+      acc += x[h] * (oracle_e4m3_decode(wr[h]) * (double)sr[h / 128]);
+    g[n] = (float)acc;
+  }
+  for (i = 0; i < I; ++i) {
+    double z = (double)g[i];
+    double silu = z / (1.0 + exp(-z));
+    a[i] = (float)(silu * (double)g[I + i]);
+  }
+  for (b = 0; b < IB; ++b) {
+    float amax = 0.0f, scale;
+    for (i = b * 128; i < (b + 1) * 128; ++i) {
+      float m = fabsf(a[i]);
+      if (m > amax) amax = m;
+    }
+    scale = (amax == 0.0f) ? 1.0f : amax / 448.0f;
+    qs[b] = scale;
+    for (i = b * 128; i < (b + 1) * 128; ++i) {
+      q[i] = (amax == 0.0f) ? 0 : oracle_e4m3_encode(a[i] / scale);
+      aq[i] = oracle_e4m3_decode(q[i]) * (double)scale;
+    }
+  }
+  for (n = 0; n < H; ++n) {
+    const uint8_t *wr = w2 + (int64_t)n * I;
+    const float *sr = w2_scale + (int64_t)(n / 128) * IB;
+    double acc = 0.0;
+    for (i = 0; i < I; ++i)
+      acc += aq[i] * (oracle_e4m3_decode(wr[i]) * (double)sr[i / 128]);
+    y[n] = acc;
+  }
+  if (g_out) memcpy(g_out, g, sizeof(float) * 2 * I);
+  if (q_out) memcpy(q_out, q, I);
+  if (qscale_out) memcpy(qscale_out, qs, sizeof(float) * IB);
+  free(x);
+  free(g);
+  free(a);
+  free(q);
+  free(qs);
+  free(aq);
+}
+
+/* ------------------------------------------------------------------------ */
+/* The whole layer for a list of tokens (stages 1-4).  Tokens are            */
+/* independent, so any subset of rows can be computed exactly.               */
+/*   out[r, n] = bf16( sum over local slots j of token_list[r], in slot      */
+/*               order, of w_j * y_j[n] )   (double sum, one rounding)       */
+/* A token with no resident expert gets +0.  Weight pointers are per local   */
+/* expert; an expert no listed token uses may be NULL.                       */
+/* ------------------------------------------------------------------------ */
+int oracle_forward(const oracle_shape *s, const uint8_t *hidden,
+                   const float *hidden_scale, const float *logits,
+                   const float *bias, const uint8_t *const *w13,
+                   const float *const *w13_scale, const uint8_t *const *w2,
+                   const float *const *w2_scale, const int32_t *token_list,
+                   int32_t n_tokens, uint16_t *out, int32_t *ids_out,
+                   float *w_out) {
+  int H = s->H, I = s->I, k = s->top_k, HB;
+  int32_t *ids, *pr_t, *pr_e, np = 0;
+  float *w;
+  double *acc, *ys;
+  int r, j, p, n, bad = 0;
+  if (oracle_check_shape(s)) return ORACLE_BAD_ARG;
+  if (n_tokens < 0 || (n_tokens > 0 && !token_list)) return ORACLE_BAD_ARG;
+  HB = H / 128;
+  ids = (int32_t *)malloc(sizeof(int32_t) * ((size_t)n_tokens * k + 1));
+  w = (float *)malloc(sizeof(float) * ((size_t)n_tokens * k + 1));
+  pr_t = (int32_t *)malloc(sizeof(int32_t) * ((size_t)n_tokens * k + 1));
+  pr_e = (int32_t *)malloc(sizeof(int32_t) * ((size_t)n_tokens * k + 1));
+  if (!ids || !w || !pr_t || !pr_e) return ORACLE_NO_MEM;
+
+  /* (1) routing */
+  for (r = 0; r < n_tokens; ++r) {
+    int t = token_list[r];
+    if (t < 0 || t >= s->T) return ORACLE_BAD_ARG;
+    route_token(s, logits + (int64_t)t * s->num_experts, bias,
+                ids + (int64_t)r * k, w + (int64_t)r * k);
+  }
+  /* (2) the resident (token, slot) pairs */
+  for (r = 0; r < n_tokens; ++r)
+    for (j = 0; j < k; ++j) {
+      int le = ids[r * k + j] - s->local_expert_offset;
+      if (le >= 0 && le < s->num_local_experts) {
+        pr_t[np] = r * k + j;
+        pr_e[np] = le;
+        ++np;
+      }
+    }
+  for (p = 0; p < np; ++p) {
+    int le = pr_e[p];
+    if (!w13[le] || !w13_scale[le] || !w2[le] || !w2_scale[le]) bad = 1;
+  }
+  if (bad) return ORACLE_BAD_ARG;
+
+  /* (3) the gated MLP of every resident pair */
+  ys = (double *)malloc(sizeof(double) * ((size_t)np * H + 1));
+  if (!ys) return ORACLE_NO_MEM;
+#pragma omp parallel for schedule(dynamic, 1)
+  for (p = 0; p < np; ++p) {
+    int le = pr_e[p];
+    int t = token_list[pr_t[p] / k];
+    oracle_expert_ffn(H, I, hidden + (int64_t)t * H,
+                      hidden_scale + (int64_t)t * HB, w13[le], w13_scale[le],
+                      w2[le], w2_scale[le], ys + (int64_t)p * H, NULL, NULL,
+                      NULL);
+  }
+
+  /* (4) weighted scatter back to the tokens (pairs are in slot order) */
+  acc = (double *)malloc(sizeof(double) * H);
+  p = 0;
+  for (r = 0; r < n_tokens; ++r) {
+    for (n = 0; n < H; ++n) acc[n] = 0.0;
+    while (p < np && pr_t[p] / k == r) {
+      double wj = (double)w[pr_t[p]];
+      for (n = 0; n < H; ++n) acc[n] += wj * ys[(int64_t)p * H + n];
+      ++p;
+    }
+    for (n = 0; n < H; ++n)
+      out[(int64_t)r * H + n] = oracle_bf16_from_double(acc[n]);
+  }
+  if (ids_out) memcpy(ids_out, ids, sizeof(int32_t) * (size_t)n_tokens * k);
+  if (w_out) memcpy(w_out, w, sizeof(float) * (size_t)n_tokens * k);
+  free(acc);
+  free(ys);
+  free(ids);
+  free(w);
+  free(pr_t);
+  free(pr_e);
+  return ORACLE_OK;
+}
+
+int oracle_num_threads(void) {
+#ifdef _OPENMP
+  return omp_get_max_threads();
+#else
+  return 1;
+#endif
+}

@@ -1,0 +1,484 @@
+"""Pins of the CPU oracle against facts that do not come from the oracle itself:
+format specifications, closed forms, library routines, brute force and
+invariants of the method (paper Section 3.1.1).  CPU only."""
+import itertools
+import math
+import os
+from fractions import Fraction
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import workloads as W
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+# ---------------------------------------------------------------- e4m3 decode
+def _read_anchors():
+    rows = []
+    with open(os.path.join(GOLDEN, "e4m3fn_anchors.txt")) as f:
+        for line in f:
+            line = line.split("#")[0].strip()
+            if line:
+                c, v = line.split()
+                rows.append((int(c, 16), float(v)))
+    return rows
+
+
+def test_e4m3_decode_matches_spec_anchors(oracle_lib):
+    for code, val in _read_anchors():
+        got = oracle_lib.e4m3_decode(code)
+        if math.isnan(val):
+            assert math.isnan(got), hex(code)
+        else:
+            assert got == val and math.copysign(1, got) == math.copysign(1, val), hex(code)
+
+
+def test_e4m3_decode_exhaustive_against_torch(oracle_lib):
+    codes = torch.arange(256, dtype=torch.int32).to(torch.uint8)
+    ref = codes.view(torch.float8_e4m3fn).to(torch.float64).numpy()
+    got = np.array([oracle_lib.e4m3_decode(c) for c in range(256)])
+    nan = np.isnan(ref)
+    assert (np.isnan(got) == nan).all()
+    assert (got[~nan] == ref[~nan]).all()
+    assert (np.signbit(got[~nan]) == np.signbit(ref[~nan])).all()
+
+
+def test_e4m3_decode_format_structure(oracle_lib):
+    """Positive finite codes 0x00..0x7E increase strictly; the gap is 2^-9 over the
+    subnormals and the first normal binade and doubles every 8 codes after."""
+    v = np.array([oracle_lib.e4m3_decode(c) for c in range(0x7F)])
+    d = np.diff(v)
+    assert (d > 0).all()
+    for c in range(0x7E):
+        binade = max(c // 8, 1)
+        assert d[c] == 2.0 ** (-9 + binade - 1), hex(c)
+    assert v[-1] == 448.0
+    neg = np.array([oracle_lib.e4m3_decode(0x80 | c) for c in range(0x7F)])
+    assert (neg == -v).all()
+
+
+# ---------------------------------------------------------------- e4m3 encode
+def _positive_codes(oracle_lib):
+    return np.array([oracle_lib.e4m3_decode(c) for c in range(0x7F)])
+
+
+def _brute_encode(x, vals):
+    """Nearest finite code by exhaustive search; ties to the even code; >= 448 saturates."""
+    s = 0x80 if math.copysign(1, x) < 0 else 0
+    a = abs(x)
+    if a >= 448.0:
+        return s | 0x7E
+    d = np.abs(vals - a)
+    best = np.flatnonzero(d == d.min())
+    c = int(best[0]) if len(best) == 1 else int([b for b in best if b % 2 == 0][0])
+    return s | c if c else s
+
+
+def test_e4m3_encode_at_every_midpoint(oracle_lib):
+    vals = _positive_codes(oracle_lib)
+    for c in range(0x7E):
+        lo, hi = vals[c], vals[c + 1]
+        mid = np.float32((lo + hi) / 2)
+        assert float(mid) == (lo + hi) / 2  # exactly representable
+        even = c if c % 2 == 0 else c + 1
+        for sgn in (1, -1):
+            sb = 0x80 if sgn < 0 else 0
+            assert oracle_lib.e4m3_encode(float(sgn * mid)) == sb | even or (even == 0 and oracle_lib.e4m3_encode(float(sgn * mid)) == sb)
+            up = np.nextafter(mid, np.float32(np.inf))
+            dn = np.nextafter(mid, np.float32(0))
+            assert oracle_lib.e4m3_encode(float(sgn * up)) == sb | (c + 1)
+            assert oracle_lib.e4m3_encode(float(sgn * dn)) == (sb | c if c else sb)
+
+
+def test_e4m3_encode_brute_force_random(oracle_lib):
+    vals = _positive_codes(oracle_lib)
+    rng = np.random.default_rng(1)
+    xs = (rng.choice([-1, 1], 20000) * np.exp2(rng.uniform(-12, 9.5, 20000))).astype(np.float32)
+    for x in xs:
+        assert oracle_lib.e4m3_encode(float(x)) == _brute_encode(float(x), vals), x
+
+
+def test_e4m3_encode_agrees_with_torch_below_448(oracle_lib):
+    rng = np.random.default_rng(2)
+    xs = (rng.standard_normal(50000) * np.exp2(rng.uniform(-10, 8, 50000))).astype(np.float32)
+    xs = xs[np.abs(xs) < 448]
+    ref = torch.from_numpy(xs).to(torch.float8_e4m3fn).view(torch.uint8).numpy()
+    got = np.array([oracle_lib.e4m3_encode(float(x)) for x in xs], np.uint8)
+    # torch keeps the sign of an underflow to zero; so does the oracle
+    assert (got == ref).all()
+
+
+def test_e4m3_encode_saturates(oracle_lib):
+    for x, c in [(448.0, 0x7E), (460.0, 0x7E), (1e30, 0x7E), (-500.0, 0xFE)]:
+        assert oracle_lib.e4m3_encode(x) == c
+
+
+# ---------------------------------------------------------------- bf16
+def _bf16_exact(x: float) -> int:
+    """Round a double to bf16 with exact rational arithmetic (ties to even)."""
+    if x == 0:
+        return 0x8000 if math.copysign(1, x) < 0 else 0
+    s = 0x8000 if x < 0 else 0
+    a = Fraction(abs(x))
+    e = math.frexp(abs(x))[1]
+    q = max(e - 8, -133)
+    m = a / Fraction(2) ** q
+    fl = m.numerator // m.denominator
+    rem = m - fl
+    if rem > Fraction(1, 2) or (rem == Fraction(1, 2) and fl % 2 == 1):
+        fl += 1
+    f = np.float32(fl * 2.0 ** q)
+    return s | int(f.view(np.uint32) >> 16)
+
+
+def test_bf16_rounding_exact_rational(oracle_lib):
+    rng = np.random.default_rng(3)
+    xs = list(rng.standard_normal(3000) * np.exp2(rng.uniform(-20, 20, 3000)))
+    # exact ties and near-ties around bf16 midpoints
+    for m in range(128, 256, 7):
+        for e in (-3, 0, 5):
+            mid = (m + 0.5) * 2.0 ** (e - 7)
+            xs += [mid, -mid, math.nextafter(mid, math.inf), math.nextafter(mid, 0.0)]
+    for x in xs:
+        assert oracle_lib.bf16_from_double(float(x)) == _bf16_exact(float(x)), x
+
+
+def test_bf16_agrees_with_torch_on_fp32_inputs(oracle_lib):
+    rng = np.random.default_rng(4)
+    xs = (rng.standard_normal(20000) * np.exp2(rng.uniform(-30, 30, 20000))).astype(np.float32)
+    ref = torch.from_numpy(xs).to(torch.bfloat16).view(torch.int16).numpy().astype(np.uint16)
+    got = np.array([oracle_lib.bf16_from_double(float(x)) for x in xs], np.uint16)
+    assert (got == ref).all()
+
+
+# ---------------------------------------------------------------- sigmoid
+def _ulp32(x):
+    x = np.abs(np.asarray(x, np.float32))
+    return np.spacing(x).astype(np.float64)
+
+
+def test_sigmoid_accuracy_dense_sample(oracle_lib):
+    # every 61st fp32 bit pattern over [-80, 80] (about 35 million inputs)
+    bits_hi = np.float32(80.0).view(np.uint32)
+    pos = np.arange(0, int(bits_hi) + 1, 61, dtype=np.uint32).view(np.float32)
+    xs = np.concatenate([-pos[::-1], pos]).astype(np.float32)
+    got = oracle_lib.sigmoid(xs).astype(np.float64)
+    ref = 1.0 / (1.0 + np.exp(-xs.astype(np.float64)))
+    err_ulp = np.abs(got - ref) / _ulp32(ref)
+    assert err_ulp.max() <= 3.0, err_ulp.max()
+    # monotone non-decreasing along the sorted sample (top-k by score equals
+    # top-k by logit when the bias is zero)
+    assert (np.diff(got) >= 0).all()
+
+
+def test_sigmoid_special_values(oracle_lib):
+    assert oracle_lib.sigmoid(np.array([0.0], np.float32))[0] == 0.5
+    big = oracle_lib.sigmoid(np.array([80.0, 100.0, -80.0, -100.0], np.float32))
+    assert big[0] == 1.0 and big[1] == 1.0
+    assert big[2] == big[3] > 0  # clamped at -80
+    xs = np.linspace(-20, 20, 4001).astype(np.float32)
+    s = oracle_lib.sigmoid(xs).astype(np.float64)
+    sm = oracle_lib.sigmoid(-xs).astype(np.float64)
+    assert np.abs(s + sm - 1.0).max() < 3e-7
+
+
+# ---------------------------------------------------------------- routing
+def _dominates(va, ia, vb, ib):
+    return va > vb or (va == vb and ia < ib)
+
+
+def _brute_route(shape, logits_row, bias):
+    """Exhaustive search: the kept groups and the chosen experts are the unique
+    subsets whose every member dominates every non-member."""
+    E, G = shape.num_experts, shape.n_group
+    gsz = E // G
+    s = oracle.sigmoid(logits_row)
+    key = (s + bias.astype(np.float32)).astype(np.float32)
+    gs = []
+    for g in range(G):
+        ks = sorted([(key[e], -e) for e in range(g * gsz, (g + 1) * gsz)], reverse=True)
+        gs.append(np.float32(ks[0][0] + ks[1][0]))
+    valid_groups = [c for c in itertools.combinations(range(G), shape.topk_group)
+                    if all(_dominates(gs[a], a, gs[b], b) for a in c for b in range(G) if b not in c)]
+    assert len(valid_groups) == 1
+    cand = [e for e in range(E) if e // gsz in valid_groups[0]]
+    valid = [c for c in itertools.combinations(cand, shape.top_k)
+             if all(_dominates(key[a], a, key[b], b) for a in c for b in cand if b not in c)]
+    assert len(valid) == 1
+    chosen = sorted(valid[0], key=lambda e: (-key[e], e))
+    ssum = np.float32(0)
+    for e in chosen:
+        ssum = np.float32(ssum + s[e])
+    w = [np.float32(np.float32(s[e] / ssum) * np.float32(shape.routed_scaling_factor)) for e in chosen]
+    return chosen, w
+
+
+@pytest.mark.parametrize("G,TG,E,K", [(4, 2, 16, 4), (4, 4, 12, 5), (3, 1, 9, 2), (2, 1, 8, 3)])
+def test_route_brute_force(oracle_lib, G, TG, E, K):
+    rng = np.random.default_rng(G * 100 + E)
+    shape = oracle.Shape(T=40, H=128, I=128, num_experts=E, num_local_experts=E,
+                         local_expert_offset=0, n_group=G, topk_group=TG, top_k=K,
+                         routed_scaling_factor=2.5)
+    logits = rng.standard_normal((40, E)).astype(np.float32)
+    logits[:20] = np.round(logits[:20] * 2) / 2  # coarse grid: many exact ties
+    bias = (rng.standard_normal(E) * 0.1).astype(np.float32)
+    bias[: E // 2] = 0.0
+    ids, w = oracle_lib.route(shape, logits, bias)
+    for t in range(40):
+        chosen, wref = _brute_route(shape, logits[t], bias)
+        assert list(ids[t]) == chosen, t
+        assert list(w[t]) == wref, t
+
+
+def test_route_all_groups_is_plain_topk(oracle_lib):
+    rng = np.random.default_rng(7)
+    E, K = 64, 8
+    shape = oracle.Shape(T=64, H=128, I=128, num_experts=E, num_local_experts=E,
+                         local_expert_offset=0, n_group=8, topk_group=8, top_k=K,
+                         routed_scaling_factor=1.0)
+    logits = rng.standard_normal((64, E)).astype(np.float32)
+    bias = (rng.standard_normal(E) * 0.1).astype(np.float32)
+    ids, _ = oracle_lib.route(shape, logits, bias)
+    key = (oracle_lib.sigmoid(logits) + bias).astype(np.float32)
+    for t in range(64):
+        order = np.lexsort((np.arange(E), -key[t].astype(np.float64)))
+        assert list(ids[t]) == list(order[:K])
+
+
+def test_route_zero_bias_follows_logits(oracle_lib):
+    """sigma is monotone: with zero bias and no group limit the experts are the
+    top-k logits (logits spaced far apart so no two scores tie)."""
+    rng = np.random.default_rng(8)
+    E, K = 32, 6
+    shape = oracle.Shape(T=16, H=128, I=128, num_experts=E, num_local_experts=E,
+                         local_expert_offset=0, n_group=4, topk_group=4, top_k=K,
+                         routed_scaling_factor=1.0)
+    logits = np.stack([rng.permutation(E) * 0.125 - 2.0 for _ in range(16)]).astype(np.float32)
+    ids, _ = oracle_lib.route(shape, logits, np.zeros(E, np.float32))
+    for t in range(16):
+        assert list(ids[t]) == list(np.argsort(-logits[t], kind="stable")[:K])
+
+
+def test_route_weights_sum_to_scaling_factor(oracle_lib):
+    cfg = W.CONFIGS["prefill"]
+    logits, bias, _ = W.gen_router(cfg, 0)
+    shape = oracle.shape_of(cfg)
+    ids, w = oracle_lib.route(shape, logits.numpy(), bias.numpy())
+    rsf = np.float32(cfg.routed_scaling_factor)
+    ulp = np.spacing(rsf)
+    assert np.abs(w.astype(np.float64).sum(1) - rsf).max() <= 4 * ulp
+    s = oracle_lib.sigmoid(logits.numpy())
+    ratio = w / np.take_along_axis(s, ids, 1)
+    assert np.allclose(ratio, ratio[:, :1], rtol=1e-6)
+    # distinct experts, at most topk_group groups
+    for t in range(cfg.T):
+        assert len(set(ids[t])) == cfg.top_k
+        assert len(set(ids[t] // (cfg.num_experts // cfg.n_group))) <= cfg.topk_group
+
+
+def test_route_skewed_hot_experts_dominate(oracle_lib):
+    cfg = W.CONFIGS["skewed"].with_(T=512)
+    logits, bias, hot = W.gen_router(cfg, 0)
+    ids, _ = oracle_lib.route(oracle.shape_of(cfg), logits.numpy(), bias.numpy())
+    counts = np.bincount(ids.ravel(), minlength=cfg.num_experts)
+    assert counts[hot.numpy()].sum() > 0.5 * ids.size
+
+
+# ---------------------------------------------------------------- permutation
+@pytest.mark.parametrize("name", ["tiny", "small_ragged", "small_many"])
+def test_permute_invariants(oracle_lib, name):
+    cfg = W.all_configs()[name]
+    logits, bias, _ = W.gen_router(cfg, 1)
+    shape = oracle.shape_of(cfg)
+    ids, _ = oracle_lib.route(shape, logits.numpy(), bias.numpy())
+    offs, perm, pr = oracle_lib.permute(shape, ids)
+    le = ids - cfg.local_expert_offset
+    local = (le >= 0) & (le < cfg.num_local_experts)
+    counts = np.bincount(le[local], minlength=cfg.num_local_experts)
+    assert (offs == np.concatenate([[0], np.cumsum(counts)])).all()
+    assert offs[-1] == local.sum() == len(perm)
+    # stable order: a sort of the local pairs by (expert, token)
+    tt, jj = np.nonzero(local)
+    order = np.lexsort((tt, le[tt, jj]))
+    assert (perm == tt[order]).all()
+    # pair_row is the inverse map
+    assert (pr[~local] == -1).all()
+    rows = pr[local]
+    assert sorted(rows) == list(range(offs[-1]))
+    assert (perm[pr[tt, jj]] == tt).all()
+    for e in range(cfg.num_local_experts):
+        seg = perm[offs[e]:offs[e + 1]]
+        assert (np.diff(seg) > 0).all()
+
+
+# ---------------------------------------------------------------- expert FFN
+def _dequant(q, s, br, bc):
+    v = torch.from_numpy(q).view(torch.float8_e4m3fn).to(torch.float64).numpy()
+    return v * np.repeat(np.repeat(s.astype(np.float64), br, 0), bc, 1)
+
+
+def _ffn_numpy(x_q, x_s, w13, s13, w2, s2):
+    """The same stage-(3) steps written with numpy float64 matmuls and torch's
+    FP8 encoder (an independent implementation of every step)."""
+    I = w2.shape[1]
+    x = _dequant(x_q[None, :], x_s[None, :], 1, 128)[0]
+    g = (_dequant(w13, s13, 128, 128) @ x).astype(np.float32)
+    gd = g[:I].astype(np.float64)
+    a = (gd / (1.0 + np.exp(-gd)) * g[I:].astype(np.float64)).astype(np.float32)
+    ab = a.reshape(-1, 128)
+    amax = np.abs(ab).max(1)
+    scale = np.where(amax > 0, (amax / np.float32(448.0)).astype(np.float32), np.float32(1.0)).astype(np.float32)
+    qa = torch.from_numpy((ab / scale[:, None]).astype(np.float32)).clamp(-448, 448).to(torch.float8_e4m3fn)
+    aq = qa.to(torch.float64).numpy() * scale[:, None].astype(np.float64)
+    y = _dequant(w2, s2, 128, 128) @ aq.reshape(-1)
+    return y, g, qa.view(torch.uint8).numpy().reshape(-1), scale
+
+
+def test_expert_ffn_against_independent_numpy(oracle_lib):
+    cfg = W.MoEConfig("t", T=6, H=512, I=384, num_experts=4, num_local_experts=4,
+                      local_expert_offset=0, n_group=2, topk_group=2, top_k=2)
+    hq, hs = W.gen_hidden(cfg, 5)
+    w13, s13, w2, s2 = [t.numpy() for t in W.gen_expert(cfg, 5, 1)]
+    flips = 0
+    for t in range(cfg.T):
+        y, g, q, qs = oracle_lib.expert_ffn(hq[t].numpy(), hs[t].numpy(), w13, s13, w2, s2)
+        yr, gr, qr, qsr = _ffn_numpy(hq[t].numpy(), hs[t].numpy(), w13, s13, w2, s2)
+        assert np.abs(g.view(np.int32) - gr.view(np.int32)).max() <= 1  # <= 1 fp32 ulp
+        flips += int((q != qr).sum())
+        assert np.abs(qs.view(np.int32) - qsr.view(np.int32)).max() <= 1
+        assert np.allclose(y, yr, rtol=1e-5, atol=1e-6)
+    assert flips <= 2
+
+
+def test_expert_ffn_exact_integer_gemm(oracle_lib):
+    """Codes with integer values and power-of-two scales make GEMM1 exact: g must
+    equal an int64 matrix product bit for bit."""
+    rng = np.random.default_rng(11)
+    H, I = 512, 256
+    int_codes = {v: torch.tensor([float(v)]).to(torch.float8_e4m3fn).view(torch.uint8).item()
+                 for v in range(-16, 17)}
+    xv = rng.integers(-16, 17, H)
+    wv = rng.integers(-16, 17, (2 * I, H))
+    xq = np.array([int_codes[v] for v in xv], np.uint8)
+    wq = np.vectorize(int_codes.get)(wv).astype(np.uint8)
+    xs = np.exp2(rng.integers(-3, 4, H // 128)).astype(np.float32)
+    ws = np.exp2(rng.integers(-3, 4, (2 * I // 128, H // 128))).astype(np.float32)
+    w2 = np.zeros((H, I), np.uint8)
+    s2 = np.ones((H // 128, I // 128), np.float32)
+    _, g, _, _ = oracle_lib.expert_ffn(xq, xs, wq, ws, w2, s2)
+    xs_full = np.repeat(xs, 128).astype(np.float64)
+    ws_full = np.repeat(np.repeat(ws, 128, 0), 128, 1).astype(np.float64)
+    ref = ((wv * ws_full) @ (xv * xs_full))  # exact: all terms are dyadic and small
+    assert (g.astype(np.float64) == ref).all()
+
+
+def test_expert_ffn_zero_and_power_of_two(oracle_lib):
+    H, I = 256, 256
+    hq, hs = W.gen_hidden(W.CONFIGS["tiny"].with_(H=H), 2)
+    w13 = np.zeros((2 * I, H), np.uint8)
+    s13 = np.ones((2 * I // 128, H // 128), np.float32)
+    w2 = np.full((H, I), 0x38, np.uint8)  # 1.0
+    s2 = np.ones((H // 128, I // 128), np.float32)
+    y, g, q, qs = oracle_lib.expert_ffn(hq[0].numpy(), hs[0].numpy(), w13, s13, w2, s2)
+    assert (g == 0).all() and (q == 0).all() and (qs == 1).all() and (y == 0).all()
+
+
+def test_expert_ffn_textbook_swiglu(oracle_lib):
+    """Without the re-quantisation the expert is the textbook SwiGLU FFN
+    W2 (silu(Wg x) * (Wu x)); the re-quantised result stays within FP8 error of it
+    (this catches swapped gate/up halves and transposed operands)."""
+    cfg = W.MoEConfig("t", T=4, H=512, I=256, num_experts=4, num_local_experts=4,
+                      local_expert_offset=0, n_group=2, topk_group=2, top_k=2)
+    hq, hs = W.gen_hidden(cfg, 9)
+    w13, s13, w2, s2 = [t.numpy() for t in W.gen_expert(cfg, 9, 0)]
+    Wd = _dequant(w13, s13, 128, 128)
+    W2d = _dequant(w2, s2, 128, 128)
+    for t in range(cfg.T):
+        x = _dequant(hq[t].numpy()[None], hs[t].numpy()[None], 1, 128)[0]
+        gate, up = Wd[: cfg.I] @ x, Wd[cfg.I:] @ x
+        ref = W2d @ (gate / (1 + np.exp(-gate)) * up)
+        y, _, _, _ = oracle_lib.expert_ffn(hq[t].numpy(), hs[t].numpy(), w13, s13, w2, s2)
+        rel = np.linalg.norm(y - ref) / np.linalg.norm(ref)
+        assert rel < 0.06, rel
+
+
+# ---------------------------------------------------------------- whole layer
+def _tiny_inputs(cfg, seed):
+    inp = W.generate(cfg, seed)
+    return inp, W.host_arrays(inp)
+
+
+def test_forward_token_permutation_invariance(oracle_lib):
+    cfg = W.all_configs()["small_ragged"]
+    inp, h = _tiny_inputs(cfg, 3)
+    shape = oracle.shape_of(cfg)
+    out, ids, w = oracle_lib.forward(shape, **h)
+    perm = np.random.default_rng(0).permutation(cfg.T)
+    h2 = dict(h)
+    for k in ("hidden", "hidden_scale", "logits"):
+        h2[k] = h[k][perm]
+    out2, ids2, w2 = oracle_lib.forward(shape, **h2)
+    assert (out2 == out[perm]).all()
+    assert (ids2 == ids[perm]).all() and (w2 == w[perm]).all()
+
+
+def test_forward_token_subset_is_exact(oracle_lib):
+    cfg = W.all_configs()["small_ragged"]
+    inp, h = _tiny_inputs(cfg, 4)
+    shape = oracle.shape_of(cfg)
+    out, _, _ = oracle_lib.forward(shape, **h)
+    sub = np.array([5, 0, 76, 33], np.int32)
+    out_s, _, _ = oracle_lib.forward(shape, **h, tokens=sub)
+    assert (out_s == out[sub]).all()
+
+
+def test_forward_dense_all_experts(oracle_lib):
+    """top_k = E with every group kept: the layer is sum_e w_e FFN_e(x), computed
+    here by a loop over all experts with no routing or permutation code."""
+    cfg = W.all_configs()["small_dense"]
+    inp, h = _tiny_inputs(cfg, 6)
+    shape = oracle.shape_of(cfg)
+    out, ids, w = oracle_lib.forward(shape, **h)
+    s = oracle_lib.sigmoid(h["logits"])
+    wt = (s / s.sum(1, keepdims=True)) * cfg.routed_scaling_factor
+    for t in range(cfg.T):
+        acc = np.zeros(cfg.H)
+        ys = [oracle_lib.expert_ffn(h["hidden"][t], h["hidden_scale"][t], h["w13"][e],
+                                    h["w13_scale"][e], h["w2"][e], h["w2_scale"][e])[0]
+              for e in range(cfg.num_experts)]
+        for e in range(cfg.num_experts):
+            acc += float(w[t][list(ids[t]).index(e)]) * ys[e]
+        ref = np.array([oracle_lib.bf16_from_double(v) for v in acc], np.uint16)
+        assert (out[t] == ref).all()
+        assert np.allclose(np.sort(w[t]), np.sort(wt[t]), rtol=1e-6)
+
+
+def test_forward_top1_is_scaled_ffn(oracle_lib):
+    cfg = W.MoEConfig("k1", T=12, H=256, I=256, num_experts=8, num_local_experts=8,
+                      local_expert_offset=0, n_group=2, topk_group=1, top_k=1,
+                      routed_scaling_factor=2.5)
+    inp, h = _tiny_inputs(cfg, 7)
+    out, ids, w = oracle_lib.forward(oracle.shape_of(cfg), **h)
+    assert (w == np.float32(2.5)).all()
+    for t in range(cfg.T):
+        e = ids[t, 0]
+        y = oracle_lib.expert_ffn(h["hidden"][t], h["hidden_scale"][t], h["w13"][e],
+                                  h["w13_scale"][e], h["w2"][e], h["w2_scale"][e])[0]
+        ref = np.array([oracle_lib.bf16_from_double(2.5 * v) for v in y], np.uint16)
+        assert (out[t] == ref).all()
+
+
+def test_forward_offslice_tokens_are_zero(oracle_lib):
+    cfg = W.all_configs()["small_ragged"]
+    inp, h = _tiny_inputs(cfg, 8)
+    shape = oracle.shape_of(cfg)
+    out, ids, _ = oracle_lib.forward(shape, **h)
+    le = ids - cfg.local_expert_offset
+    none_local = ~((le >= 0) & (le < cfg.num_local_experts)).any(1)
+    assert none_local.any()
+    assert (out[none_local] == 0).all()
+    assert (out[~none_local] != 0).any(1).all()

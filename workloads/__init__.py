@@ -1,0 +1,206 @@
+"""Seeded synthetic workloads for the fused FP8 MoE layer.
+
+This module is shared by the tests, the benchmark and the smoke check.  It
+holds the configuration registry and the input generators only: none of the
+layer's arithmetic lives here.  The paper evaluates on the FlashInfer-Bench
+Fused MoE workloads (DeepSeek-V3 shapes, Section 3.1.1 and the workload-regime
+table of Section 3.2.1); those are not available, so these seeded inputs of the
+same shapes stand in for them.
+
+Recipe (all draws from ``torch.Generator`` objects on the target device, one
+per (seed, tensor id, expert) sub-stream, so a single expert can be
+regenerated alone):
+  * router logits  fp32 N(0, 1)                       [T, E_g]        id 1
+  * routing bias   fp32 N(0, 0.1); in the skewed case  [E_g]           id 2
+    +2.0 on ``hot_experts`` experts drawn by randperm                 id 6
+  * hidden         N(0, 1) quantised to e4m3fn per 1x128 block          id 3
+                   with fp32 scale = amax / 448                       [T, H]
+  * w13 (gate rows [0,I), up rows [I,2I)), w2: N(0, 0.02) quantised   id 4, 5
+    per 128x128 block, fp32 scale = amax / 448
+Input quantisation uses torch's own float8_e4m3fn conversion (round to nearest
+even) after clamping to +-448; an all-zero block gets scale 1.
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass, replace
+
+import numpy as np
+import torch
+
+
+@dataclass(frozen=True)
+class MoEConfig:
+    name: str
+    T: int
+    H: int
+    I: int
+    num_experts: int
+    num_local_experts: int
+    local_expert_offset: int
+    n_group: int
+    topk_group: int
+    top_k: int
+    routed_scaling_factor: float = 2.5
+    hot_experts: int = 0
+    hot_bias: float = 2.0
+
+    def with_(self, **kw) -> "MoEConfig":
+        return replace(self, **kw)
+
+
+def _ds_v3(name: str, T: int, **kw) -> MoEConfig:
+    base = dict(H=7168, I=2048, num_experts=256, num_local_experts=32,
+                local_expert_offset=0, n_group=8, topk_group=4, top_k=8)
+    base.update(kw)
+    return MoEConfig(name=name, T=T, **base)
+
+
+CONFIGS: dict[str, MoEConfig] = {
+    # tiny case the oracle finishes in well under a second
+    "tiny": MoEConfig("tiny", T=8, H=512, I=256, num_experts=16, num_local_experts=16,
+                      local_expert_offset=0, n_group=4, topk_group=2, top_k=4),
+    # DeepSeek-V3 shapes, 32 resident experts of a 256-expert router
+    "decode": _ds_v3("decode", 16),
+    "mid": _ds_v3("mid", 256),
+    "prefill": _ds_v3("prefill", 4096),
+    # all 256 experts resident, 16 hot experts
+    "skewed": _ds_v3("skewed", 8192, num_local_experts=256, hot_experts=16),
+}
+
+# Extra parity shapes: several tiles plus ragged tails, still fast on the CPU.
+PARITY_CONFIGS: dict[str, MoEConfig] = {
+    "small_ragged": MoEConfig("small_ragged", T=77, H=640, I=384, num_experts=32,
+                              num_local_experts=12, local_expert_offset=8, n_group=4,
+                              topk_group=2, top_k=6),
+    "small_dense": MoEConfig("small_dense", T=40, H=256, I=256, num_experts=8,
+                             num_local_experts=8, local_expert_offset=0, n_group=2,
+                             topk_group=2, top_k=8),
+    "small_many": MoEConfig("small_many", T=300, H=384, I=256, num_experts=64,
+                            num_local_experts=64, local_expert_offset=0, n_group=8,
+                            topk_group=4, top_k=8, hot_experts=4),
+}
+
+
+def all_configs() -> dict[str, MoEConfig]:
+    d = dict(CONFIGS)
+    d.update(PARITY_CONFIGS)
+    return d
+
+
+# ---------------------------------------------------------------------------
+# seeded sub-streams
+# ---------------------------------------------------------------------------
+TID_LOGITS, TID_BIAS, TID_HIDDEN, TID_W13, TID_W2, TID_HOT = 1, 2, 3, 4, 5, 6
+
+
+def substream_seed(seed: int, tid: int, expert: int = 0) -> int:
+    st = np.random.SeedSequence([int(seed), int(tid), int(expert)]).generate_state(2, np.uint32)
+    return int((int(st[0]) << 31) ^ int(st[1])) & ((1 << 63) - 1)
+
+
+def _gen(device, seed: int, tid: int, expert: int = 0) -> torch.Generator:
+    g = torch.Generator(device=device)
+    g.manual_seed(substream_seed(seed, tid, expert))
+    return g
+
+
+def quantize_blocks(x: torch.Tensor, br: int, bc: int):
+    """Block quantisation used to synthesise inputs: (e4m3fn codes as uint8, fp32 scales)."""
+    R, C = x.shape
+    xb = x.reshape(R // br, br, C // bc, bc)
+    amax = xb.abs().amax(dim=(1, 3))
+    scale = torch.where(amax > 0, amax / 448.0, torch.ones_like(amax))
+    q = (xb / scale[:, None, :, None]).clamp(-448.0, 448.0).to(torch.float8_e4m3fn)
+    return q.reshape(R, C).view(torch.uint8), scale.to(torch.float32).contiguous()
+
+
+def gen_router(cfg: MoEConfig, seed: int, device="cpu"):
+    """(logits fp32 [T,E_g], bias fp32 [E_g], hot expert ids int64)."""
+    logits = torch.randn(cfg.T, cfg.num_experts, generator=_gen(device, seed, TID_LOGITS),
+                         device=device, dtype=torch.float32)
+    bias = torch.randn(cfg.num_experts, generator=_gen(device, seed, TID_BIAS),
+                       device=device, dtype=torch.float32) * 0.1
+    hot = torch.empty(0, dtype=torch.int64)
+    if cfg.hot_experts:
+        g = torch.Generator(device="cpu")
+        g.manual_seed(substream_seed(seed, TID_HOT))
+        hot = torch.randperm(cfg.num_experts, generator=g)[: cfg.hot_experts]
+        bias[hot.to(device)] += cfg.hot_bias
+    return logits, bias, hot
+
+
+def gen_hidden(cfg: MoEConfig, seed: int, device="cpu"):
+    """(hidden e4m3fn codes uint8 [T,H], hidden_scale fp32 [T,H/128])."""
+    x = torch.randn(max(cfg.T, 1), cfg.H, generator=_gen(device, seed, TID_HIDDEN),
+                    device=device, dtype=torch.float32)[: cfg.T]
+    if cfg.T == 0:
+        return (torch.empty(0, cfg.H, dtype=torch.uint8, device=device),
+                torch.empty(0, cfg.H // 128, dtype=torch.float32, device=device))
+    return quantize_blocks(x, 1, 128)
+
+
+def gen_expert(cfg: MoEConfig, seed: int, e: int, device="cpu"):
+    """Weights of local expert ``e``: (w13 [2I,H] u8, w13_scale [2I/128,H/128],
+    w2 [H,I] u8, w2_scale [H/128,I/128]).  The sub-stream is keyed by the
+    global expert id, so a slice regenerates the same bytes."""
+    gid = cfg.local_expert_offset + e
+    w13 = torch.randn(2 * cfg.I, cfg.H, generator=_gen(device, seed, TID_W13, gid),
+                      device=device, dtype=torch.float32) * 0.02
+    q13, s13 = quantize_blocks(w13, 128, 128)
+    del w13
+    w2 = torch.randn(cfg.H, cfg.I, generator=_gen(device, seed, TID_W2, gid),
+                     device=device, dtype=torch.float32) * 0.02
+    q2, s2 = quantize_blocks(w2, 128, 128)
+    return q13, s13, q2, s2
+
+
+def gen_weights(cfg: MoEConfig, seed: int, device="cpu"):
+    """All resident experts stacked: (w13 [E_l,2I,H], w13_scale, w2 [E_l,H,I], w2_scale)."""
+    El, H, I = cfg.num_local_experts, cfg.H, cfg.I
+    w13 = torch.empty(El, 2 * I, H, dtype=torch.uint8, device=device)
+    s13 = torch.empty(El, 2 * I // 128, H // 128, dtype=torch.float32, device=device)
+    w2 = torch.empty(El, H, I, dtype=torch.uint8, device=device)
+    s2 = torch.empty(El, H // 128, I // 128, dtype=torch.float32, device=device)
+    for e in range(El):
+        a, b, c, d = gen_expert(cfg, seed, e, device)
+        w13[e].copy_(a)
+        s13[e].copy_(b)
+        w2[e].copy_(c)
+        s2[e].copy_(d)
+    return w13, s13, w2, s2
+
+
+@dataclass
+class MoEInputs:
+    cfg: MoEConfig
+    seed: int
+    hidden: torch.Tensor
+    hidden_scale: torch.Tensor
+    logits: torch.Tensor
+    bias: torch.Tensor
+    w13: torch.Tensor
+    w13_scale: torch.Tensor
+    w2: torch.Tensor
+    w2_scale: torch.Tensor
+    hot: torch.Tensor
+
+
+def generate(cfg: MoEConfig, seed: int = 0, device="cpu") -> MoEInputs:
+    logits, bias, hot = gen_router(cfg, seed, device)
+    hidden, hscale = gen_hidden(cfg, seed, device)
+    w13, s13, w2, s2 = gen_weights(cfg, seed, device)
+    return MoEInputs(cfg, seed, hidden, hscale, logits, bias, w13, s13, w2, s2, hot)
+
+
+def host_arrays(inp: MoEInputs, experts=None) -> dict:
+    """numpy host copies for the oracle; weights only for ``experts`` (all by default)."""
+    El = inp.cfg.num_local_experts
+    want = set(range(El)) if experts is None else set(int(e) for e in experts)
+
+    def per_expert(t):
+        return [t[e].cpu().numpy() if e in want else None for e in range(El)]
+
+    return dict(hidden=inp.hidden.cpu().numpy(), hidden_scale=inp.hidden_scale.cpu().numpy(),
+                logits=inp.logits.cpu().numpy(), bias=inp.bias.cpu().numpy(),
+                w13=per_expert(inp.w13), w13_scale=per_expert(inp.w13_scale),
+                w2=per_expert(inp.w2), w2_scale=per_expert(inp.w2_scale))
