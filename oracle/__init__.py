@@ -56,6 +56,14 @@ def lib():
         L.oracle_e4m3_decode.restype = ctypes.c_double
         L.oracle_e4m3_encode.argtypes = [ctypes.c_float]
         L.oracle_e4m3_encode.restype = ctypes.c_uint8
+        L.oracle_e4m3_encode_array.argtypes = [P, P, ctypes.c_int64]
+        L.oracle_e4m3_encode_array.restype = None
+        L.oracle_fp8_block_dot.argtypes = [P, P]
+        L.oracle_fp8_block_dot.restype = ctypes.c_float
+        L.oracle_fp8_block_dot_array.argtypes = [P, P, P, ctypes.c_int64]
+        L.oracle_fp8_block_dot_array.restype = None
+        L.oracle_swiglu.argtypes = [ctypes.c_float, ctypes.c_float]
+        L.oracle_swiglu.restype = ctypes.c_float
         L.oracle_bf16_from_double.argtypes = [ctypes.c_double]
         L.oracle_bf16_from_double.restype = ctypes.c_uint16
         L.oracle_sigmoid.argtypes = [ctypes.c_float]
@@ -114,6 +122,27 @@ def e4m3_decode(q: int) -> float:
 
 def e4m3_encode(v: float) -> int:
     return lib().oracle_e4m3_encode(v)
+
+
+def e4m3_encode_array(x: np.ndarray) -> np.ndarray:
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    q = np.empty(x.shape, np.uint8)
+    lib().oracle_e4m3_encode_array(_ptr(x), _ptr(q), x.size)
+    return q
+
+
+def fp8_block_dot(a: np.ndarray, w: np.ndarray) -> np.ndarray:
+    """FP8 block dot products (the GEMM1 block rule) of [..., 128] code arrays."""
+    a = np.ascontiguousarray(a, dtype=np.uint8)
+    w = np.ascontiguousarray(w, dtype=np.uint8)
+    assert a.shape == w.shape and a.shape[-1] == 128
+    d = np.empty(a.shape[:-1], np.float32)
+    lib().oracle_fp8_block_dot_array(_ptr(a), _ptr(w), _ptr(d), d.size)
+    return d
+
+
+def swiglu(g: float, u: float) -> float:
+    return lib().oracle_swiglu(g, u)
 
 
 def bf16_from_double(v: float) -> int:
