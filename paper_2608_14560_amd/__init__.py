@@ -1,0 +1,271 @@
+"""MI355X (gfx950) fused block-scaled FP8 mixture-of-experts layer.
+
+Python binding of ``libmoe.so`` (the hand-written HIP kernels behind the C-ABI
+declared in ``include/moe.h``).  This module only marshals arguments: torch
+tensors provide device memory and the current stream; every step of the layer
+runs in the library's kernels.  There is no fallback: if the library is not
+built, or a tensor is not on the GPU, the call raises.
+
+Entry points (same names as the C-ABI):
+  workspace_size(shape)               bytes of scratch the calls need
+  route(shape, logits, bias, ...)     stage (1) + stage (2) bookkeeping
+  fused_fp8(shape, ...)               the whole layer, bf16 output
+  fused_fp8_staged(..., events)       same, recording an event before each kernel
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libmoe.so")
+
+MOE_OK, MOE_ERR_INVALID_ARG, MOE_ERR_UNSUPPORTED, MOE_ERR_WORKSPACE_TOO_SMALL, MOE_ERR_HIP = range(5)
+
+EXPORTED = ("moe_workspace_size", "moe_route", "moe_fused_fp8", "moe_fused_fp8_staged",
+            "moe_num_stages", "moe_stage_name", "moe_status_string", "moe_debug_sigmoid",
+            "moe_debug_e4m3_encode", "moe_debug_act_views", "moe_debug_mfma_block")
+
+
+class MoEError(RuntimeError):
+    def __init__(self, fn: str, code: int):
+        super().__init__(f"{fn}: {status_string(code)} ({code})")
+        self.code = code
+
+
+class CShape(ctypes.Structure):
+    _fields_ = [("T", ctypes.c_int32), ("H", ctypes.c_int32), ("I", ctypes.c_int32),
+                ("num_experts", ctypes.c_int32), ("num_local_experts", ctypes.c_int32),
+                ("local_expert_offset", ctypes.c_int32), ("n_group", ctypes.c_int32),
+                ("topk_group", ctypes.c_int32), ("top_k", ctypes.c_int32),
+                ("routed_scaling_factor", ctypes.c_float)]
+
+
+class CRouteOut(ctypes.Structure):
+    _fields_ = [("topk_ids", ctypes.c_void_p), ("topk_weights", ctypes.c_void_p),
+                ("expert_offsets", ctypes.c_void_p), ("perm_token", ctypes.c_void_p),
+                ("pair_row", ctypes.c_void_p)]
+
+
+@dataclass(frozen=True)
+class Shape:
+    T: int
+    H: int
+    I: int
+    num_experts: int
+    num_local_experts: int
+    local_expert_offset: int
+    n_group: int
+    topk_group: int
+    top_k: int
+    routed_scaling_factor: float = 2.5
+
+    @staticmethod
+    def of(cfg) -> "Shape":
+        return Shape(*(getattr(cfg, f) for f in Shape.__dataclass_fields__))
+
+    def c(self) -> CShape:
+        return CShape(self.T, self.H, self.I, self.num_experts, self.num_local_experts,
+                      self.local_expert_offset, self.n_group, self.topk_group, self.top_k,
+                      self.routed_scaling_factor)
+
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    """The loaded C-ABI library; raises if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with "
+                               "`python -m paper_2608_14560_amd.build`")
+        L = ctypes.CDLL(LIB_PATH)
+        P, S, Z = ctypes.c_void_p, ctypes.POINTER(CShape), ctypes.c_size_t
+        R = ctypes.POINTER(CRouteOut)
+        L.moe_workspace_size.argtypes = [S]
+        L.moe_workspace_size.restype = Z
+        L.moe_route.argtypes = [S, P, P, R, P, Z, P]
+        L.moe_route.restype = ctypes.c_int
+        L.moe_fused_fp8.argtypes = [S, P, P, P, P, P, P, P, P, P, R, P, Z, P]
+        L.moe_fused_fp8.restype = ctypes.c_int
+        L.moe_fused_fp8_staged.argtypes = [S, P, P, P, P, P, P, P, P, P, R, P, Z, P,
+                                           ctypes.POINTER(P), ctypes.c_int]
+        L.moe_fused_fp8_staged.restype = ctypes.c_int
+        L.moe_num_stages.argtypes = []
+        L.moe_num_stages.restype = ctypes.c_int
+        L.moe_stage_name.argtypes = [ctypes.c_int]
+        L.moe_stage_name.restype = ctypes.c_char_p
+        L.moe_status_string.argtypes = [ctypes.c_int]
+        L.moe_status_string.restype = ctypes.c_char_p
+        L.moe_debug_sigmoid.argtypes = [P, P, ctypes.c_int64, P]
+        L.moe_debug_sigmoid.restype = ctypes.c_int
+        L.moe_debug_e4m3_encode.argtypes = [P, P, ctypes.c_int64, P]
+        L.moe_debug_e4m3_encode.restype = ctypes.c_int
+        L.moe_debug_mfma_block.argtypes = [P, P, P, ctypes.c_int64, P]
+        L.moe_debug_mfma_block.restype = ctypes.c_int
+        L.moe_debug_act_views.argtypes = [S, P, ctypes.POINTER(P), ctypes.POINTER(P)]
+        L.moe_debug_act_views.restype = ctypes.c_int
+        _lib = L
+    return _lib
+
+
+def status_string(code: int) -> str:
+    return lib().moe_status_string(code).decode()
+
+
+def _check(fn: str, code: int):
+    if code != MOE_OK:
+        raise MoEError(fn, code)
+
+
+def _dev(t: torch.Tensor | None, dtype, name: str):
+    if t is None:
+        raise ValueError(f"{name} is required")
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a GPU tensor (the layer has no CPU path)")
+    if t.dtype != dtype:
+        raise ValueError(f"{name} must be {dtype}, got {t.dtype}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream) -> ctypes.c_void_p:
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+def workspace_size(shape: Shape) -> int:
+    return int(lib().moe_workspace_size(ctypes.byref(shape.c())))
+
+
+def alloc_workspace(shape: Shape, device="cuda") -> torch.Tensor:
+    return torch.empty(max(workspace_size(shape), 256), dtype=torch.uint8, device=device)
+
+
+def alloc_route_out(shape: Shape, device="cuda") -> dict:
+    # at least one row each, so an empty batch still gets non-null buffers
+    T, K, El = shape.T, shape.top_k, shape.num_local_experts
+    R = max(T, 1)
+    return dict(topk_ids=torch.empty(R, K, dtype=torch.int32, device=device)[:T],
+                topk_weights=torch.empty(R, K, dtype=torch.float32, device=device)[:T],
+                expert_offsets=torch.empty(El + 1, dtype=torch.int32, device=device),
+                perm_token=torch.empty(R * K, dtype=torch.int32, device=device),
+                pair_row=torch.empty(R, K, dtype=torch.int32, device=device)[:T])
+
+
+def _route_struct(ro: dict) -> CRouteOut:
+    return CRouteOut(_dev(ro["topk_ids"], torch.int32, "topk_ids"),
+                     _dev(ro["topk_weights"], torch.float32, "topk_weights"),
+                     _dev(ro["expert_offsets"], torch.int32, "expert_offsets"),
+                     _dev(ro["perm_token"], torch.int32, "perm_token"),
+                     _dev(ro["pair_row"], torch.int32, "pair_row"))
+
+
+def route(shape: Shape, logits: torch.Tensor, bias: torch.Tensor, route_out: dict | None = None,
+          workspace: torch.Tensor | None = None, stream=None) -> dict:
+    """Stage (1) and the permutation of stage (2); returns the route-out tensors."""
+    ro = route_out if route_out is not None else alloc_route_out(shape, logits.device)
+    ws = workspace if workspace is not None else alloc_workspace(shape, logits.device)
+    cro = _route_struct(ro)
+    rc = lib().moe_route(ctypes.byref(shape.c()), _dev(logits, torch.float32, "logits"),
+                         _dev(bias, torch.float32, "bias"), ctypes.byref(cro),
+                         _dev(ws, torch.uint8, "workspace"), ws.numel(), _stream(stream))
+    _check("moe_route", rc)
+    return ro
+
+
+def _fused_args(shape, hidden, hidden_scale, logits, bias, w13, w13_scale, w2, w2_scale, out,
+                route_out, workspace):
+    return [ctypes.byref(shape.c()),
+            _dev(hidden, torch.uint8, "hidden"), _dev(hidden_scale, torch.float32, "hidden_scale"),
+            _dev(logits, torch.float32, "logits"), _dev(bias, torch.float32, "bias"),
+            _dev(w13, torch.uint8, "w13"), _dev(w13_scale, torch.float32, "w13_scale"),
+            _dev(w2, torch.uint8, "w2"), _dev(w2_scale, torch.float32, "w2_scale"),
+            _dev(out, torch.bfloat16, "out"),
+            ctypes.byref(_route_struct(route_out)) if route_out is not None else None,
+            _dev(workspace, torch.uint8, "workspace"), ctypes.c_size_t(workspace.numel())]
+
+
+def fused_fp8(shape: Shape, hidden, hidden_scale, logits, bias, w13, w13_scale, w2, w2_scale,
+              out: torch.Tensor | None = None, route_out: dict | None = None,
+              workspace: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+    """The whole layer (stages (1)-(4)); returns out [T, H] bf16."""
+    if out is None:
+        out = torch.empty(shape.T, shape.H, dtype=torch.bfloat16, device=hidden.device)
+    if workspace is None:
+        workspace = alloc_workspace(shape, hidden.device)
+    args = _fused_args(shape, hidden, hidden_scale, logits, bias, w13, w13_scale, w2, w2_scale,
+                       out, route_out, workspace)
+    _check("moe_fused_fp8", lib().moe_fused_fp8(*args, _stream(stream)))
+    return out
+
+
+def num_stages() -> int:
+    return lib().moe_num_stages()
+
+
+def stage_names() -> list[str]:
+    return [lib().moe_stage_name(i).decode() for i in range(num_stages())]
+
+
+def fused_fp8_staged(shape: Shape, hidden, hidden_scale, logits, bias, w13, w13_scale, w2,
+                     w2_scale, out, workspace, events: list, route_out: dict | None = None,
+                     stream=None) -> torch.Tensor:
+    """fused_fp8 recording ``events[i]`` (torch.cuda.Event, timing enabled) on the
+    stream before kernel i and ``events[-1]`` after the last kernel."""
+    n = num_stages() + 1
+    if len(events) != n:
+        raise ValueError(f"need {n} events")
+    for ev in events:  # torch creates the HIP event lazily, on its first record
+        if ev.cuda_event == 0:
+            ev.record()
+    arr = (ctypes.c_void_p * n)(*[ev.cuda_event for ev in events])
+    args = _fused_args(shape, hidden, hidden_scale, logits, bias, w13, w13_scale, w2, w2_scale,
+                       out, route_out, workspace)
+    _check("moe_fused_fp8_staged",
+           lib().moe_fused_fp8_staged(*args, _stream(stream), arr, n))
+    return out
+
+
+# ----------------------------------------------------------------- test hooks
+def debug_sigmoid(x: torch.Tensor, stream=None) -> torch.Tensor:
+    y = torch.empty_like(x)
+    _check("moe_debug_sigmoid", lib().moe_debug_sigmoid(
+        _dev(x, torch.float32, "x"), _dev(y, torch.float32, "y"), x.numel(), _stream(stream)))
+    return y
+
+
+def debug_e4m3_encode(x: torch.Tensor, stream=None) -> torch.Tensor:
+    q = torch.empty(x.shape, dtype=torch.uint8, device=x.device)
+    _check("moe_debug_e4m3_encode", lib().moe_debug_e4m3_encode(
+        _dev(x, torch.float32, "x"), _dev(q, torch.uint8, "q"), x.numel(), _stream(stream)))
+    return q
+
+
+def debug_mfma_block(a: torch.Tensor, b: torch.Tensor, stream=None) -> torch.Tensor:
+    """a, b: [n, 16, 128] uint8 e4m3 codes -> d [n, 16, 16] with d = a @ b^T per case."""
+    n = a.shape[0]
+    d = torch.empty(n, 16, 16, dtype=torch.float32, device=a.device)
+    _check("moe_debug_mfma_block", lib().moe_debug_mfma_block(
+        _dev(a, torch.uint8, "a"), _dev(b, torch.uint8, "b"), _dev(d, torch.float32, "d"), n,
+        _stream(stream)))
+    return d
+
+
+def debug_act_views(shape: Shape, workspace: torch.Tensor):
+    """(act [P_max, I] uint8, act_scale [P_max, I/128] f32) views into the workspace."""
+    a, s = ctypes.c_void_p(), ctypes.c_void_p()
+    _check("moe_debug_act_views", lib().moe_debug_act_views(
+        ctypes.byref(shape.c()), _dev(workspace, torch.uint8, "workspace"),
+        ctypes.byref(a), ctypes.byref(s)))
+    base = workspace.data_ptr()
+    P = max(shape.T * shape.top_k, 1)
+    act = workspace[a.value - base: a.value - base + P * shape.I].view(P, shape.I)
+    sc = workspace[s.value - base: s.value - base + P * (shape.I // 128) * 4]
+    return act, sc.view(torch.float32).view(P, shape.I // 128)

@@ -1,0 +1,364 @@
+// api.cpp -- the C-ABI of the fused FP8 MoE layer: argument validation,
+// workspace carving and the launch sequence.  No allocation and no host
+// synchronisation happen here: every size that depends on the routing stays
+// on the device and the grids are sized from host-known upper bounds.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdint>
+
+#include "../../include/moe.h"
+#include "../../include/moe_debug.h"
+#include "moe_device.h"
+
+namespace moe {
+hipError_t launch_permute_count(const PermuteParams &p, hipStream_t st);
+hipError_t launch_permute_scatter(const PermuteParams &p, hipStream_t st);
+hipError_t launch_debug_sigmoid(const float *x, float *y, int64_t n, hipStream_t st);
+hipError_t launch_debug_e4m3_encode(const float *x, uint8_t *q, int64_t n, hipStream_t st);
+hipError_t launch_debug_mfma_block(const uint8_t *a, const uint8_t *b, float *d, int64_t n,
+                                   hipStream_t st);
+}  // namespace moe
+
+namespace {
+
+using namespace moe;
+
+constexpr int kStages = 6;
+const char *const kStageNames[kStages] = {"route", "permute_count", "permute_scatter",
+                                          "gemm1_swiglu_quant", "gemm2", "combine_finalize"};
+
+constexpr size_t kAlign = 256;
+size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+bool aligned(const void *p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+moe_status_t check_shape(const moe_shape_t *s) {
+  if (!s) return MOE_ERR_INVALID_ARG;
+  if (s->T < 0 || s->H <= 0 || s->I <= 0 || s->H % 128 || s->I % 128) return MOE_ERR_INVALID_ARG;
+  if (s->num_experts < 2 || s->n_group < 1 || s->num_experts % s->n_group) return MOE_ERR_INVALID_ARG;
+  const int gsz = s->num_experts / s->n_group;
+  if (gsz < 2) return MOE_ERR_INVALID_ARG;
+  if (s->topk_group < 1 || s->topk_group > s->n_group) return MOE_ERR_INVALID_ARG;
+  if (s->top_k < 1 || s->top_k > s->topk_group * gsz) return MOE_ERR_INVALID_ARG;
+  if (s->num_local_experts < 1 || s->local_expert_offset < 0 ||
+      (int64_t)s->local_expert_offset + s->num_local_experts > s->num_experts)
+    return MOE_ERR_INVALID_ARG;
+  if (!std::isfinite(s->routed_scaling_factor)) return MOE_ERR_INVALID_ARG;
+  // limits of this build
+  if (s->num_experts > 1024 || s->num_local_experts > 1024 || s->n_group > 64 || s->top_k > 16)
+    return MOE_ERR_UNSUPPORTED;
+  if ((int64_t)s->T * s->top_k >= (int64_t)1 << 31) return MOE_ERR_UNSUPPORTED;
+  return MOE_OK;
+}
+
+// Host-side plan: tile shape, split factors, grid bounds and the workspace map.
+struct Plan {
+  int BM, S1, S2, NB1, NB2, nchunks, max_tiles, n_counters;
+  int64_t P_max;
+  size_t off_ids, off_w, off_offsets, off_perm_token, off_perm_pair, off_pair_row, off_chunk_counts,
+      off_tile_base, off_n_items, off_counters, off_act, off_act_scale, off_partial, off_Y, total;
+};
+
+Plan make_plan(const moe_shape_t *s) {
+  Plan p{};
+  const int64_t TK = (int64_t)s->T * s->top_k;
+  p.P_max = TK > 0 ? TK : 1;
+  // expected rows per resident expert under uniform routing picks the M tile
+  const double avg = (double)TK / s->num_experts;
+  p.BM = avg <= 16 ? 16 : (avg <= 48 ? 32 : (avg <= 160 ? 64 : 128));
+  // GEMM1 promotes its K blocks in order (its output decides the re-quantised
+  // codes), so it never splits K.  GEMM2 splits K in halves for small batches,
+  // which stream the weights with too few tiles to fill 256 CUs.
+  p.S1 = 1;
+  p.S2 = TK <= 512 ? 2 : 1;
+  p.NB1 = s->I / 128;
+  p.NB2 = (s->H + 255) / 256;
+  p.nchunks = (int)((s->T + kChunkTokens - 1) / kChunkTokens);
+  if (p.nchunks < 1) p.nchunks = 1;
+  const int64_t touched = TK < s->num_local_experts ? TK : s->num_local_experts;
+  p.max_tiles = (int)((p.P_max + p.BM - 1) / p.BM + touched);
+  p.n_counters = p.S1 > 1 ? p.max_tiles * p.NB1 : 1;
+
+  size_t o = 0;
+  auto take = [&](size_t bytes) {
+    const size_t at = o;
+    o = align_up(o + bytes);
+    return at;
+  };
+  p.off_ids = take(sizeof(int32_t) * p.P_max);
+  p.off_w = take(sizeof(float) * p.P_max);
+  p.off_offsets = take(sizeof(int32_t) * (s->num_local_experts + 1));
+  p.off_perm_token = take(sizeof(int32_t) * p.P_max);
+  p.off_perm_pair = take(sizeof(int32_t) * p.P_max);
+  p.off_pair_row = take(sizeof(int32_t) * p.P_max);
+  p.off_chunk_counts = take(sizeof(int32_t) * (size_t)p.nchunks * s->num_local_experts);
+  p.off_tile_base = take(sizeof(int32_t) * (s->num_local_experts + 1));
+  p.off_n_items = take(sizeof(int32_t) * 2);
+  p.off_counters = take(sizeof(int32_t) * (size_t)p.n_counters);
+  p.off_act = take((size_t)p.P_max * s->I);
+  p.off_act_scale = take(sizeof(float) * (size_t)p.P_max * (s->I / 128));
+  p.off_partial = take(p.S1 > 1 ? sizeof(float) * (size_t)p.S1 * p.P_max * 2 * s->I : 0);
+  p.off_Y = take(sizeof(float) * (size_t)p.S2 * p.P_max * s->H);
+  p.total = o;
+  return p;
+}
+
+template <class T>
+T *at(void *ws, size_t off) {
+  return reinterpret_cast<T *>(static_cast<uint8_t *>(ws) + off);
+}
+
+int round8(int64_t x) { return (int)((x + 7) / 8 * 8); }
+
+struct Ptrs {
+  int32_t *ids;
+  float *w;
+  int32_t *offsets, *perm_token, *pair_row;
+};
+
+Ptrs route_ptrs(const Plan &pl, void *ws, const moe_route_out_t *ro) {
+  Ptrs r;
+  r.ids = (ro && ro->topk_ids) ? ro->topk_ids : at<int32_t>(ws, pl.off_ids);
+  r.w = (ro && ro->topk_weights) ? ro->topk_weights : at<float>(ws, pl.off_w);
+  r.offsets = (ro && ro->expert_offsets) ? ro->expert_offsets : at<int32_t>(ws, pl.off_offsets);
+  r.perm_token = (ro && ro->perm_token) ? ro->perm_token : at<int32_t>(ws, pl.off_perm_token);
+  r.pair_row = (ro && ro->pair_row) ? ro->pair_row : at<int32_t>(ws, pl.off_pair_row);
+  return r;
+}
+
+moe_status_t check_route_out(const moe_route_out_t *ro) {
+  if (!ro) return MOE_OK;
+  const void *ps[] = {ro->topk_ids, ro->topk_weights, ro->expert_offsets, ro->perm_token, ro->pair_row};
+  for (const void *q : ps)
+    if (!q || !aligned(q, 16)) return MOE_ERR_INVALID_ARG;
+  return MOE_OK;
+}
+
+#define MOE_TRY_HIP(expr)                    \
+  do {                                       \
+    if ((expr) != hipSuccess) return MOE_ERR_HIP; \
+  } while (0)
+
+moe_status_t enqueue_route(const moe_shape_t *s, const Plan &pl, const float *logits,
+                           const float *bias, const Ptrs &r, void *ws, hipStream_t st,
+                           void *const *ev, int &stage) {
+  auto mark = [&]() {
+    if (ev) (void)hipEventRecord(static_cast<hipEvent_t>(ev[stage]), st);
+    ++stage;
+  };
+  RouteParams rp{logits, bias, r.ids, r.w, s->T, s->num_experts, s->n_group, s->topk_group,
+                 s->top_k, s->routed_scaling_factor};
+  mark();
+  MOE_TRY_HIP(launch_route(rp, st));
+
+  PermuteParams pp{};
+  pp.topk_ids = r.ids;
+  pp.chunk_counts = at<int32_t>(ws, pl.off_chunk_counts);
+  pp.expert_offsets = r.offsets;
+  pp.perm_token = r.perm_token;
+  pp.perm_pair = at<int32_t>(ws, pl.off_perm_pair);
+  pp.pair_row = r.pair_row;
+  pp.tile_base = at<int32_t>(ws, pl.off_tile_base);
+  pp.n_items = at<int32_t>(ws, pl.off_n_items);
+  pp.counters = at<int32_t>(ws, pl.off_counters);
+  pp.T = s->T;
+  pp.K = s->top_k;
+  pp.El = s->num_local_experts;
+  pp.offset = s->local_expert_offset;
+  pp.nchunks = pl.nchunks;
+  pp.BM = pl.BM;
+  pp.items_per_tile1 = pl.NB1 * pl.S1;
+  pp.items_per_tile2 = pl.NB2 * pl.S2;
+  pp.n_counters = pl.n_counters;
+  mark();
+  MOE_TRY_HIP(launch_permute_count(pp, st));
+  mark();
+  MOE_TRY_HIP(launch_permute_scatter(pp, st));
+  return MOE_OK;
+}
+
+moe_status_t fused_impl(const moe_shape_t *s, const uint8_t *hidden, const float *hidden_scale,
+                        const float *logits, const float *bias, const uint8_t *w13,
+                        const float *w13_scale, const uint8_t *w2, const float *w2_scale,
+                        uint16_t *out, const moe_route_out_t *ro, void *ws, size_t ws_bytes,
+                        void *stream, void *const *ev, int n_ev) {
+  moe_status_t rc = check_shape(s);
+  if (rc != MOE_OK) return rc;
+  if (ev && n_ev != kStages + 1) return MOE_ERR_INVALID_ARG;
+  if (s->T == 0) return MOE_OK;
+  const void *ptrs[] = {hidden, hidden_scale, logits, bias, w13, w13_scale, w2, w2_scale, out};
+  for (const void *q : ptrs)
+    if (!q || !aligned(q, 16)) return MOE_ERR_INVALID_ARG;
+  if ((rc = check_route_out(ro)) != MOE_OK) return rc;
+  const Plan pl = make_plan(s);
+  if (!ws || !aligned(ws, kAlign)) return MOE_ERR_INVALID_ARG;
+  if (ws_bytes < pl.total) return MOE_ERR_WORKSPACE_TOO_SMALL;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+
+  const Ptrs r = route_ptrs(pl, ws, ro);
+  int stage = 0;
+  if ((rc = enqueue_route(s, pl, logits, bias, r, ws, st, ev, stage)) != MOE_OK) return rc;
+  auto mark = [&]() {
+    if (ev) (void)hipEventRecord(static_cast<hipEvent_t>(ev[stage]), st);
+    ++stage;
+  };
+
+  GemmParams g{};
+  g.expert_offsets = r.offsets;
+  g.tile_base = at<int32_t>(ws, pl.off_tile_base);
+  g.perm_token = r.perm_token;
+  g.counters = at<int32_t>(ws, pl.off_counters);
+  g.partial = at<float>(ws, pl.off_partial);
+  g.act = at<uint8_t>(ws, pl.off_act);
+  g.act_scale = at<float>(ws, pl.off_act_scale);
+  g.Y = at<float>(ws, pl.off_Y);
+  g.I = s->I;
+  g.H = s->H;
+  g.P_max = (int)pl.P_max;
+  g.El = s->num_local_experts;
+
+  // GEMM1: hidden rows (gathered) x W13, SwiGLU + FP8 re-quantisation
+  GemmParams g1 = g;
+  g1.A = hidden;
+  g1.A_scale = hidden_scale;
+  g1.B = w13;
+  g1.B_scale = w13_scale;
+  g1.n_items = at<int32_t>(ws, pl.off_n_items);
+  g1.K = s->H;
+  g1.KB = s->H / 128;
+  g1.N_total = 2 * s->I;
+  g1.NB = pl.NB1;
+  g1.S = pl.S1;
+  mark();
+  MOE_TRY_HIP(launch_gemm1(g1, pl.BM, round8((int64_t)pl.max_tiles * pl.NB1 * pl.S1), st));
+
+  // GEMM2: permuted activation rows x W2 -> Y
+  GemmParams g2 = g;
+  g2.A = g.act;
+  g2.A_scale = g.act_scale;
+  g2.B = w2;
+  g2.B_scale = w2_scale;
+  g2.n_items = at<int32_t>(ws, pl.off_n_items) + 1;
+  g2.K = s->I;
+  g2.KB = s->I / 128;
+  g2.N_total = s->H;
+  g2.NB = pl.NB2;
+  g2.S = pl.S2;
+  mark();
+  MOE_TRY_HIP(launch_gemm2(g2, pl.BM, round8((int64_t)pl.max_tiles * pl.NB2 * pl.S2), st));
+
+  // weighted combine in slot order, one bf16 rounding per element
+  FinalizeParams f{g.Y, r.pair_row, r.w, out, s->T, s->H, s->top_k, pl.S2, (int)pl.P_max};
+  mark();
+  MOE_TRY_HIP(launch_finalize(f, st));
+  if (ev) (void)hipEventRecord(static_cast<hipEvent_t>(ev[stage]), st);
+  return MOE_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t moe_workspace_size(const moe_shape_t *s) {
+  if (check_shape(s) != MOE_OK) return 0;
+  return make_plan(s).total;
+}
+
+moe_status_t moe_route(const moe_shape_t *s, const float *router_logits,
+                       const float *routing_bias, const moe_route_out_t *out, void *workspace,
+                       size_t ws_bytes, void *stream) {
+  moe_status_t rc = check_shape(s);
+  if (rc != MOE_OK) return rc;
+  if (!out) return MOE_ERR_INVALID_ARG;
+  if (s->T == 0) {
+    // empty batch: only expert_offsets (all zero) is written; the other
+    // arrays have zero size and may be null
+    if (!out->expert_offsets || !aligned(out->expert_offsets, 16) || !out->perm_token)
+      return MOE_ERR_INVALID_ARG;
+  } else {
+    if (!router_logits || !routing_bias || !aligned(router_logits, 16) ||
+        !aligned(routing_bias, 16))
+      return MOE_ERR_INVALID_ARG;
+    if ((rc = check_route_out(out)) != MOE_OK) return rc;
+  }
+  const Plan pl = make_plan(s);
+  if (!workspace || !aligned(workspace, kAlign)) return MOE_ERR_INVALID_ARG;
+  if (ws_bytes < pl.total) return MOE_ERR_WORKSPACE_TOO_SMALL;
+  const Ptrs r = route_ptrs(pl, workspace, out);
+  int stage = 0;
+  return enqueue_route(s, pl, router_logits, routing_bias, r, workspace,
+                       static_cast<hipStream_t>(stream), nullptr, stage);
+}
+
+moe_status_t moe_fused_fp8(const moe_shape_t *s, const uint8_t *hidden, const float *hidden_scale,
+                           const float *router_logits, const float *routing_bias,
+                           const uint8_t *w13, const float *w13_scale, const uint8_t *w2,
+                           const float *w2_scale, uint16_t *out, const moe_route_out_t *route_out,
+                           void *workspace, size_t ws_bytes, void *stream) {
+  return fused_impl(s, hidden, hidden_scale, router_logits, routing_bias, w13, w13_scale, w2,
+                    w2_scale, out, route_out, workspace, ws_bytes, stream, nullptr, 0);
+}
+
+moe_status_t moe_fused_fp8_staged(const moe_shape_t *s, const uint8_t *hidden,
+                                  const float *hidden_scale, const float *router_logits,
+                                  const float *routing_bias, const uint8_t *w13,
+                                  const float *w13_scale, const uint8_t *w2, const float *w2_scale,
+                                  uint16_t *out, const moe_route_out_t *route_out, void *workspace,
+                                  size_t ws_bytes, void *stream, void *const *stage_events,
+                                  int n_events) {
+  if (!stage_events) return MOE_ERR_INVALID_ARG;
+  for (int i = 0; i < n_events; ++i)
+    if (!stage_events[i]) return MOE_ERR_INVALID_ARG;
+  return fused_impl(s, hidden, hidden_scale, router_logits, routing_bias, w13, w13_scale, w2,
+                    w2_scale, out, route_out, workspace, ws_bytes, stream, stage_events, n_events);
+}
+
+int moe_num_stages(void) { return kStages; }
+
+const char *moe_stage_name(int i) { return (i >= 0 && i < kStages) ? kStageNames[i] : nullptr; }
+
+const char *moe_status_string(moe_status_t st) {
+  switch (st) {
+    case MOE_OK: return "ok";
+    case MOE_ERR_INVALID_ARG: return "invalid argument";
+    case MOE_ERR_UNSUPPORTED: return "unsupported shape";
+    case MOE_ERR_WORKSPACE_TOO_SMALL: return "workspace too small";
+    case MOE_ERR_HIP: return "HIP runtime error";
+  }
+  return "unknown status";
+}
+
+moe_status_t moe_debug_sigmoid(const float *x, float *y, int64_t n, void *stream) {
+  if (n < 0 || (n > 0 && (!x || !y))) return MOE_ERR_INVALID_ARG;
+  return launch_debug_sigmoid(x, y, n, static_cast<hipStream_t>(stream)) == hipSuccess
+             ? MOE_OK
+             : MOE_ERR_HIP;
+}
+
+moe_status_t moe_debug_e4m3_encode(const float *x, uint8_t *q, int64_t n, void *stream) {
+  if (n < 0 || (n > 0 && (!x || !q))) return MOE_ERR_INVALID_ARG;
+  return launch_debug_e4m3_encode(x, q, n, static_cast<hipStream_t>(stream)) == hipSuccess
+             ? MOE_OK
+             : MOE_ERR_HIP;
+}
+
+moe_status_t moe_debug_mfma_block(const uint8_t *a, const uint8_t *b, float *d, int64_t n,
+                                  void *stream) {
+  if (n < 0 || (n > 0 && (!a || !b || !d))) return MOE_ERR_INVALID_ARG;
+  if (!aligned(a, 32) || !aligned(b, 32) || !aligned(d, 16)) return MOE_ERR_INVALID_ARG;
+  return launch_debug_mfma_block(a, b, d, n, static_cast<hipStream_t>(stream)) == hipSuccess
+             ? MOE_OK
+             : MOE_ERR_HIP;
+}
+
+moe_status_t moe_debug_act_views(const moe_shape_t *s, void *workspace, uint8_t **act,
+                                 float **act_scale) {
+  if (check_shape(s) != MOE_OK || !workspace || !act || !act_scale) return MOE_ERR_INVALID_ARG;
+  const Plan pl = make_plan(s);
+  *act = at<uint8_t>(workspace, pl.off_act);
+  *act_scale = at<float>(workspace, pl.off_act_scale);
+  return MOE_OK;
+}
+
+}  // extern "C"

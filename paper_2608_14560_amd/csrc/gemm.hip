@@ -1,0 +1,400 @@
+// gemm.hip -- stage (3) and (4) of the Fused MoE block (paper Section 3.1.1)
+// on CDNA4 FP8 matrix cores.
+//
+//  GEMM1: per resident expert e, rows = the tokens routed to e (gathered
+//         through perm_token while the A tile is loaded: the paper's separate
+//         gather kernel is folded into the GEMM's loads),
+//         G = sum_kb (A_kb W13_kb^T) * sa[row,kb] * sw[n/128,kb]   (fp32)
+//         epilogue: a = silu(gate) * up, per-row 1x128 amax, scale =
+//         amax/448, FP8 re-quantisation -> act [P, I] e4m3 + act_scale.
+//  GEMM2: Y = sum_kb (act_kb W2_kb^T) * sa2 * sw2 -> Y [S, P, H] fp32
+//  finalize: out[t] = bf16( sum over resident slots j (slot order) of
+//            w_j * sum_s Y[s, pair_row[t,j]] ).
+//
+// Work item = (M-tile of one expert, column block, K split).  Items of one
+// expert are contiguous with the M-tile index fastest, so the M-tiles that
+// share a weight panel are adjacent; workgroup b is mapped to item
+// (b % 8) * ceil(n/8) + b / 8 so those neighbours land on the same XCD
+// (workgroups are dispatched round-robin over the 8 XCDs) and reuse the panel
+// from that XCD's L2.
+//
+// Tiles: BM rows x 256 columns x 128 K per step, 4 waves.  In GEMM1 wave w
+// owns gate columns [32w, 32w+32) and the matching up columns of the
+// 128-wide intermediate block, so SwiGLU pairs live in the same lane.  Each
+// 128-K step is one v_mfma_f32_16x16x128_f8f6f4 per 16x16 sub-tile, started
+// from zero and promoted into the fp32 accumulator with one FMA by the
+// product of the row's activation scale and the block's weight scale.
+// A and B tiles are staged through LDS (double buffered, rows padded to
+// 144 bytes so the MFMA operand reads are bank-conflict free).
+#include "moe_device.h"
+
+namespace moe {
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kRowBytes = 144;  // 128 data bytes + 16 pad
+constexpr int kBN = 256;
+
+template <int BM>
+struct Layout {
+  static constexpr int A = BM * kRowBytes;
+  static constexpr int B = kBN * kRowBytes;
+  static constexpr int SA = BM * 4;
+  static constexpr int STAGE = A + B + SA + 16;
+  static constexpr int AMAX = 4 * BM * 4;
+  static constexpr int TB = 4 * 1028;  // tile_base copy (El <= 1024)
+  static constexpr int TOTAL = 2 * STAGE + AMAX + TB;
+};
+
+__device__ __forceinline__ v8i lds_frag(const uint8_t *p) {
+  const v4i lo = *reinterpret_cast<const v4i *>(p);
+  const v4i hi = *reinterpret_cast<const v4i *>(p + 16);
+  return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+}
+
+template <int BM, bool G1>
+__global__ __launch_bounds__(kThreads) void gemm_kernel(GemmParams p) {
+  using L = Layout<BM>;
+  constexpr int MT = BM / 16;
+  constexpr int A_CHUNKS = BM * 8;
+  constexpr int A_PER = (A_CHUNKS + kThreads - 1) / kThreads;
+  constexpr int B_PER = kBN * 8 / kThreads;
+
+  extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
+  float *amax_lds = reinterpret_cast<float *>(smem + 2 * L::STAGE);
+  int *tb = reinterpret_cast<int *>(smem + 2 * L::STAGE + L::AMAX);
+
+  const int tid = threadIdx.x;
+  const int lane = tid & (kWave - 1);
+  const int wave = tid / kWave;
+
+  const int n_items = *p.n_items;
+  const int per_xcd = (n_items + 7) / 8;
+  const int item = (blockIdx.x & 7) * per_xcd + (blockIdx.x >> 3);
+  if ((int)(blockIdx.x >> 3) >= per_xcd || item >= n_items) return;
+
+  for (int i = tid; i <= p.El; i += kThreads) tb[i] = p.tile_base[i];
+  __syncthreads();
+
+  // ---- decode the work item
+  const int X = p.NB * p.S;
+  const int qt = item / X;
+  int lo = 0, hi = p.El;
+  while (hi - lo > 1) {
+    const int mid = (lo + hi) >> 1;
+    if (tb[mid] <= qt) lo = mid; else hi = mid;
+  }
+  const int e = lo;
+  const int nt_e = tb[e + 1] - tb[e];
+  const int local = item - tb[e] * X;
+  const int mt_idx = local % nt_e;
+  const int rest = local / nt_e;
+  const int s = rest % p.S;
+  const int nb = rest / p.S;
+  const int seg0 = p.expert_offsets[e];
+  const int seg1 = p.expert_offsets[e + 1];
+  const int row0 = seg0 + mt_idx * BM;
+  const int nrows = min(BM, seg1 - row0);
+  const int kb0 = (s * p.KB) / p.S;
+  const int kb1 = ((s + 1) * p.KB) / p.S;
+  const size_t K = (size_t)p.K;
+
+  // ---- per-thread load assignments (fixed over the K loop)
+  const uint8_t *a_src[A_PER];
+  int a_dst[A_PER];
+#pragma unroll
+  for (int i = 0; i < A_PER; ++i) {
+    const int idx = tid + i * kThreads;
+    const int r = idx >> 3, c = idx & 7;
+    const int rr = min(r, nrows - 1);
+    const int src = G1 ? p.perm_token[row0 + rr] : row0 + rr;
+    a_src[i] = p.A + (size_t)src * K + c * 16;
+    a_dst[i] = (idx < A_CHUNKS) ? r * kRowBytes + c * 16 : -1;
+  }
+  const float *sa_src = nullptr;
+  if (tid < BM) {
+    const int rr = min(tid, nrows - 1);
+    const int src = G1 ? p.perm_token[row0 + rr] : row0 + rr;
+    sa_src = p.A_scale + (size_t)src * p.KB;
+  }
+  const uint8_t *Bexp = p.B + (size_t)e * p.N_total * K;
+  const uint8_t *b_src[B_PER];
+#pragma unroll
+  for (int i = 0; i < B_PER; ++i) {
+    const int r = (tid >> 3) + 32 * i, c = tid & 7;
+    int brow;
+    if (G1)
+      brow = (r < 128) ? nb * 128 + r : p.I + nb * 128 + (r - 128);
+    else
+      brow = min(nb * kBN + r, p.N_total - 1);  // ragged last block (H % 256 == 128)
+    b_src[i] = Bexp + (size_t)brow * K + c * 16;
+  }
+  const float *sb_src = nullptr;
+  if (tid < 2) {
+    const int nblk = G1 ? (tid == 0 ? nb : p.I / 128 + nb) : min(2 * nb + tid, p.N_total / 128 - 1);
+    sb_src = p.B_scale + ((size_t)e * (p.N_total / 128) + nblk) * p.KB;
+  }
+
+  u32x4 ra[A_PER], rb[B_PER];
+  float rsa = 0.0f, rsb = 0.0f;
+#define MOE_GLOAD(kb)                                                                   \
+  do {                                                                                  \
+    _Pragma("unroll") for (int i = 0; i < A_PER; ++i) if (a_dst[i] >= 0) ra[i] =        \
+        *reinterpret_cast<const u32x4 *>(a_src[i] + (size_t)(kb) * 128);                \
+    _Pragma("unroll") for (int i = 0; i < B_PER; ++i) rb[i] =                           \
+        *reinterpret_cast<const u32x4 *>(b_src[i] + (size_t)(kb) * 128);                \
+    if (tid < BM) rsa = sa_src[kb];                                                     \
+    if (tid < 2) rsb = sb_src[kb];                                                      \
+  } while (0)
+#define MOE_LSTORE(buf)                                                                 \
+  do {                                                                                  \
+    uint8_t *st_ = smem + (buf) * L::STAGE;                                             \
+    _Pragma("unroll") for (int i = 0; i < A_PER; ++i) if (a_dst[i] >= 0)                \
+        *reinterpret_cast<u32x4 *>(st_ + a_dst[i]) = ra[i];                              \
+    _Pragma("unroll") for (int i = 0; i < B_PER; ++i)                                   \
+        *reinterpret_cast<u32x4 *>(st_ + L::A + ((tid >> 3) + 32 * i) * kRowBytes +     \
+                                   (tid & 7) * 16) = rb[i];                              \
+    float *sa_ = reinterpret_cast<float *>(st_ + L::A + L::B);                          \
+    if (tid < BM) sa_[tid] = rsa;                                                       \
+    if (tid < 2) sa_[BM + tid] = rsb;                                                   \
+  } while (0)
+
+  // LDS rows of this wave's four 16-column B sub-tiles
+  int brow_lds[4];
+#pragma unroll
+  for (int nt = 0; nt < 4; ++nt)
+    brow_lds[nt] = G1 ? ((nt < 2 ? 0 : 128) + 32 * wave + 16 * (nt & 1)) : (64 * wave + 16 * nt);
+
+  v4f acc[MT][4];
+#pragma unroll
+  for (int m = 0; m < MT; ++m)
+#pragma unroll
+    for (int nt = 0; nt < 4; ++nt) acc[m][nt] = v4f{0.f, 0.f, 0.f, 0.f};
+
+  const int frag_off = (lane >> 4) * 32;
+  const int r16 = lane & 15;
+
+  MOE_GLOAD(kb0);
+  MOE_LSTORE(0);
+  __syncthreads();
+  for (int kb = kb0; kb < kb1; ++kb) {
+    const int cur = (kb - kb0) & 1;
+    const bool more = kb + 1 < kb1;
+    if (more) MOE_GLOAD(kb + 1);
+
+    const uint8_t *st = smem + cur * L::STAGE;
+    const uint8_t *As = st;
+    const uint8_t *Bs = st + L::A;
+    const float *sa = reinterpret_cast<const float *>(st + L::A + L::B);
+    const float sb0 = sa[BM], sb1 = sa[BM + 1];
+    v8i bf[4];
+#pragma unroll
+    for (int nt = 0; nt < 4; ++nt) bf[nt] = lds_frag(Bs + (brow_lds[nt] + r16) * kRowBytes + frag_off);
+    float sbn[4];
+#pragma unroll
+    for (int nt = 0; nt < 4; ++nt)
+      sbn[nt] = G1 ? (nt < 2 ? sb0 : sb1) : (wave < 2 ? sb0 : sb1);
+#pragma unroll
+    for (int m = 0; m < MT; ++m) {
+      const v8i af = lds_frag(As + (m * 16 + r16) * kRowBytes + frag_off);
+      const float4 sav = *reinterpret_cast<const float4 *>(sa + m * 16 + 4 * (lane >> 4));
+#pragma unroll
+      for (int nt = 0; nt < 4; ++nt) {
+        const v4f z = {0.f, 0.f, 0.f, 0.f};
+        const v4f t = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(af, bf[nt], z, 0, 0, 0, 0, 0, 0);
+        acc[m][nt][0] = __builtin_fmaf(t[0], sav.x * sbn[nt], acc[m][nt][0]);
+        acc[m][nt][1] = __builtin_fmaf(t[1], sav.y * sbn[nt], acc[m][nt][1]);
+        acc[m][nt][2] = __builtin_fmaf(t[2], sav.z * sbn[nt], acc[m][nt][2]);
+        acc[m][nt][3] = __builtin_fmaf(t[3], sav.w * sbn[nt], acc[m][nt][3]);
+      }
+    }
+    if (more) MOE_LSTORE(cur ^ 1);
+    __syncthreads();
+  }
+
+#undef MOE_GLOAD
+#undef MOE_LSTORE
+
+  // accumulator element (m, nt, i) of this lane is row m*16 + 4*(lane/16) + i,
+  // column r16 of sub-tile nt
+  if (!G1) {
+    if (nb * kBN + 64 * wave >= p.H) return;  // this wave's columns are past H
+    float *Ys = p.Y + (size_t)s * p.P_max * p.H;
+#pragma unroll
+    for (int m = 0; m < MT; ++m)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int r = m * 16 + 4 * (lane >> 4) + i;
+        if (r < nrows) {
+          float *yrow = Ys + (size_t)(row0 + r) * p.H + nb * kBN + 64 * wave + r16;
+#pragma unroll
+          for (int nt = 0; nt < 4; ++nt) yrow[16 * nt] = acc[m][nt][i];
+        }
+      }
+    return;
+  }
+
+  // SwiGLU in registers: sub-tiles 0/1 are gate, 2/3 the matching up columns
+  float av[MT][4][2];
+#pragma unroll
+  for (int m = 0; m < MT; ++m)
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        av[m][i][h] = swiglu_spec(acc[m][h][i], acc[m][2 + h][i]);
+      }
+  // per-row amax over the 128-column block: 16 lanes x 2 columns x 4 waves
+#pragma unroll
+  for (int m = 0; m < MT; ++m)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      float mx = fmaxf(fabsf(av[m][i][0]), fabsf(av[m][i][1]));
+#pragma unroll
+      for (int off = 1; off < 16; off <<= 1) mx = fmaxf(mx, __shfl_xor(mx, off));
+      if (r16 == 0) amax_lds[wave * BM + m * 16 + 4 * (lane >> 4) + i] = mx;
+    }
+  __syncthreads();
+  const int IB = p.I / 128;
+#pragma unroll
+  for (int m = 0; m < MT; ++m)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int r = m * 16 + 4 * (lane >> 4) + i;
+      const float amax = fmaxf(fmaxf(amax_lds[r], amax_lds[BM + r]),
+                               fmaxf(amax_lds[2 * BM + r], amax_lds[3 * BM + r]));
+      const float scale = (amax > 0.0f) ? amax / 448.0f : 1.0f;
+      if (r < nrows) {
+        const uint32_t q2 = (amax > 0.0f)
+                                ? e4m3x2_rne_sat(av[m][i][0] / scale, av[m][i][1] / scale)
+                                : 0u;
+        uint8_t *arow = p.act + (size_t)(row0 + r) * p.I + nb * 128 + 32 * wave + r16;
+        arow[0] = (uint8_t)(q2 & 0xff);
+        arow[16] = (uint8_t)(q2 >> 8);
+        if (wave == 0 && r16 == 0) p.act_scale[(size_t)(row0 + r) * IB + nb] = scale;
+      }
+    }
+}
+
+__global__ __launch_bounds__(256) void finalize_kernel(FinalizeParams p) {
+  const int t = blockIdx.x;
+  const int n0 = (blockIdx.y * 256 + threadIdx.x) * 8;
+  if (n0 >= p.H) return;
+  float acc[8];
+#pragma unroll
+  for (int c = 0; c < 8; ++c) acc[c] = 0.0f;
+  for (int j = 0; j < p.K; ++j) {
+    const int pr = p.pair_row[(size_t)t * p.K + j];
+    if (pr < 0) continue;
+    const float w = p.topk_w[(size_t)t * p.K + j];
+    float y[8];
+#pragma unroll
+    for (int c = 0; c < 8; ++c) y[c] = 0.0f;
+    for (int q = 0; q < p.S; ++q) {
+      const float *src = p.Y + ((size_t)q * p.P_max + pr) * p.H + n0;
+      const float4 v0 = *reinterpret_cast<const float4 *>(src);
+      const float4 v1 = *reinterpret_cast<const float4 *>(src + 4);
+      y[0] += v0.x; y[1] += v0.y; y[2] += v0.z; y[3] += v0.w;
+      y[4] += v1.x; y[5] += v1.y; y[6] += v1.z; y[7] += v1.w;
+    }
+#pragma unroll
+    for (int c = 0; c < 8; ++c) acc[c] = __builtin_fmaf(w, y[c], acc[c]);
+  }
+  uint4 o;
+  o.x = (uint32_t)f32_to_bf16_rne(acc[0]) | ((uint32_t)f32_to_bf16_rne(acc[1]) << 16);
+  o.y = (uint32_t)f32_to_bf16_rne(acc[2]) | ((uint32_t)f32_to_bf16_rne(acc[3]) << 16);
+  o.z = (uint32_t)f32_to_bf16_rne(acc[4]) | ((uint32_t)f32_to_bf16_rne(acc[5]) << 16);
+  o.w = (uint32_t)f32_to_bf16_rne(acc[6]) | ((uint32_t)f32_to_bf16_rne(acc[7]) << 16);
+  *reinterpret_cast<uint4 *>(p.out + (size_t)t * p.H + n0) = o;
+}
+
+template <int BM, bool G1>
+hipError_t launch_gemm_bm(const GemmParams &p, int grid, hipStream_t st) {
+  auto k = gemm_kernel<BM, G1>;
+  const int lds = Layout<BM>::TOTAL;
+  hipError_t err = hipFuncSetAttribute(reinterpret_cast<const void *>(k),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, lds);
+  if (err != hipSuccess) return err;
+  hipLaunchKernelGGL(k, dim3(grid), dim3(kThreads), lds, st, p);
+  return hipGetLastError();
+}
+
+template <bool G1>
+hipError_t launch_gemm(const GemmParams &p, int BM, int grid, hipStream_t st) {
+  if (grid <= 0) return hipSuccess;
+  switch (BM) {
+    case 16: return launch_gemm_bm<16, G1>(p, grid, st);
+    case 32: return launch_gemm_bm<32, G1>(p, grid, st);
+    case 64: return launch_gemm_bm<64, G1>(p, grid, st);
+    case 128: return launch_gemm_bm<128, G1>(p, grid, st);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+// Test hook: the FP8 encoder of the re-quantisation epilogue, elementwise.
+__global__ void e4m3_encode_kernel(const float *x, uint8_t *q, int64_t n) {
+  const int64_t i = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) * 2;
+  if (i >= n) return;
+  const float b = (i + 1 < n) ? x[i + 1] : 0.0f;
+  const uint32_t c = e4m3x2_rne_sat(x[i], b);
+  q[i] = (uint8_t)(c & 0xff);
+  if (i + 1 < n) q[i + 1] = (uint8_t)(c >> 8);
+}
+
+// Test hook: one v_mfma_f32_16x16x128_f8f6f4 per case with the operand and
+// result lane layouts the GEMM kernels use.  a, b: [n, 16, 128] e4m3 (rows of
+// A and of W); d: [n, 16, 16] fp32 with d[i][j] = sum_k a[i][k] * b[j][k].
+__global__ __launch_bounds__(64) void mfma_block_kernel(const uint8_t *a, const uint8_t *b,
+                                                        float *d) {
+  const int lane = threadIdx.x;
+  const size_t c = blockIdx.x;
+  const int r16 = lane & 15, off = (lane >> 4) * 32;
+  const v8i af = *reinterpret_cast<const v8i *>(a + c * 2048 + r16 * 128 + off);
+  const v8i bf = *reinterpret_cast<const v8i *>(b + c * 2048 + r16 * 128 + off);
+  const v4f z = {0.f, 0.f, 0.f, 0.f};
+  const v4f t = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(af, bf, z, 0, 0, 0, 0, 0, 0);
+#pragma unroll
+  for (int i = 0; i < 4; ++i) d[c * 256 + (4 * (lane >> 4) + i) * 16 + r16] = t[i];
+}
+
+}  // namespace
+
+hipError_t launch_debug_mfma_block(const uint8_t *a, const uint8_t *b, float *d, int64_t n,
+                                   hipStream_t st) {
+  if (n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(mfma_block_kernel, dim3((unsigned)n), dim3(64), 0, st, a, b, d);
+  return hipGetLastError();
+}
+
+hipError_t launch_gemm1(const GemmParams &p, int BM, int grid, hipStream_t st) {
+  return launch_gemm<true>(p, BM, grid, st);
+}
+hipError_t launch_gemm2(const GemmParams &p, int BM, int grid, hipStream_t st) {
+  return launch_gemm<false>(p, BM, grid, st);
+}
+size_t gemm_lds_bytes(int BM) {
+  switch (BM) {
+    case 16: return Layout<16>::TOTAL;
+    case 32: return Layout<32>::TOTAL;
+    case 64: return Layout<64>::TOTAL;
+    case 128: return Layout<128>::TOTAL;
+    default: return 0;
+  }
+}
+
+hipError_t launch_finalize(const FinalizeParams &p, hipStream_t st) {
+  if (p.T == 0) return hipSuccess;
+  dim3 grid(p.T, (p.H + 2047) / 2048);
+  hipLaunchKernelGGL(finalize_kernel, grid, dim3(256), 0, st, p);
+  return hipGetLastError();
+}
+
+hipError_t launch_debug_e4m3_encode(const float *x, uint8_t *q, int64_t n, hipStream_t st) {
+  if (n <= 0) return hipSuccess;
+  const int64_t threads = (n + 1) / 2;
+  hipLaunchKernelGGL(e4m3_encode_kernel, dim3((unsigned)((threads + 255) / 256)), dim3(256), 0, st,
+                     x, q, n);
+  return hipGetLastError();
+}
+
+}  // namespace moe

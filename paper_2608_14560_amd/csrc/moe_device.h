@@ -1,0 +1,150 @@
+// moe_device.h -- device helpers and launch-parameter blocks shared by the
+// gfx950 kernels of the fused FP8 MoE layer.  Internal to the library.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace moe {
+
+constexpr int kWave = 64;
+
+typedef int v8i __attribute__((ext_vector_type(8)));
+typedef int v4i __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+typedef float v4f __attribute__((ext_vector_type(4)));
+
+// ---------------------------------------------------------------- numerics
+
+// Round an fp32 value to bf16 (nearest, ties to even); NaN stays a quiet NaN.
+__device__ __forceinline__ uint16_t f32_to_bf16_rne(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return 0x7fc0;
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
+}
+
+// Two fp32 values -> two OCP e4m3fn codes (round to nearest even).  The inputs
+// are clamped to +-448 first, so the conversion saturates instead of
+// overflowing to NaN.  Result: code(a) in bits [7:0], code(b) in [15:8].
+__device__ __forceinline__ uint32_t e4m3x2_rne_sat(float a, float b) {
+  a = fminf(fmaxf(a, -448.0f), 448.0f);
+  b = fminf(fmaxf(b, -448.0f), 448.0f);
+  return (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32(a, b, 0, false) & 0xffffu;
+}
+
+// fp32 sigmoid with a fixed operation sequence: clamp to [-80, 80],
+// e^z for z = -x by Cody-Waite reduction n = rint(z log2 e),
+// r = z - n ln2 (two-part ln2), degree-7 Taylor polynomial of e^r in Horner
+// form with fused multiply-adds, e^z = p * 2^n, and sigma = 1 / (1 + e^z)
+// with a correctly rounded division.  Constants: log2 e, ln 2 split into a
+// 12-trailing-zero head and its fp32 remainder, 1/k! rounded to fp32.
+__device__ __forceinline__ float sigmoid_spec(float x) {
+#pragma clang fp contract(off)
+  const float kLog2e = 0x1.715476p+0f;
+  const float kLn2Hi = 0x1.62e400p-1f;
+  const float kLn2Lo = 0x1.7f7d1cp-20f;
+  x = fminf(fmaxf(x, -80.0f), 80.0f);
+  const float z = -x;
+  const float n = __builtin_rintf(z * kLog2e);
+  float r = __builtin_fmaf(-n, kLn2Hi, z);
+  r = __builtin_fmaf(-n, kLn2Lo, r);
+  float p = 1.0f / 5040.0f;
+  p = __builtin_fmaf(p, r, 1.0f / 720.0f);
+  p = __builtin_fmaf(p, r, 1.0f / 120.0f);
+  p = __builtin_fmaf(p, r, 1.0f / 24.0f);
+  p = __builtin_fmaf(p, r, 1.0f / 6.0f);
+  p = __builtin_fmaf(p, r, 0.5f);
+  p = __builtin_fmaf(p, r, 1.0f);
+  p = __builtin_fmaf(p, r, 1.0f);
+  const float e = __builtin_ldexpf(p, (int)n);
+  return 1.0f / (1.0f + e);
+}
+
+// SwiGLU of the expert MLP: silu(g) * u with silu(g) = g * sigmoid(g), in
+// fp32 with the sigmoid above (a fixed sequence, so the re-quantised codes it
+// feeds are reproducible).
+__device__ __forceinline__ float swiglu_spec(float g, float u) {
+#pragma clang fp contract(off)
+  const float silu = g * sigmoid_spec(g);
+  return silu * u;
+}
+
+// Total order used by every selection of the routing stage: the larger value
+// wins, equal values go to the lower index.
+__device__ __forceinline__ bool beats(float va, int ia, float vb, int ib) {
+  return va > vb || (va == vb && ia < ib);
+}
+
+// ---------------------------------------------------------------- launch blocks
+
+struct RouteParams {
+  const float *logits;   // [T, E]
+  const float *bias;     // [E]
+  int32_t *topk_ids;     // [T, K]
+  float *topk_w;         // [T, K]
+  int T, E, G, TG, K;
+  float rsf;
+};
+
+struct PermuteParams {
+  const int32_t *topk_ids;   // [T, K]
+  int32_t *chunk_counts;     // [nchunks, El]
+  int32_t *expert_offsets;   // [El + 1]
+  int32_t *perm_token;       // [T*K]
+  int32_t *perm_pair;        // [T*K]  t*K + j of each permuted row
+  int32_t *pair_row;         // [T, K]
+  int32_t *tile_base;        // [El + 1] first M-tile of each expert
+  int32_t *n_items;          // [2] work items of GEMM1 and GEMM2
+  int32_t *counters;         // [n_counters] split-K arrival counters
+  int T, K, El, offset, nchunks;
+  int BM, items_per_tile1, items_per_tile2, n_counters;
+};
+
+constexpr int kChunkTokens = 256;   // tokens per permute workgroup
+
+struct GemmParams {
+  // A operand: GEMM1 gathers hidden rows through perm_token; GEMM2 reads the
+  // permuted activation rows directly.
+  const uint8_t *A;          // [rows, K]
+  const float *A_scale;      // [rows, K/128]
+  // B operand: the expert weights, [El, N_total, K] with [El, N_total/128, K/128] scales
+  const uint8_t *B;
+  const float *B_scale;
+  const int32_t *expert_offsets;
+  const int32_t *tile_base;
+  const int32_t *perm_token;
+  const int32_t *n_items;    // device count of work items
+  int32_t *counters;         // GEMM1 split-K arrival counters
+  float *partial;            // GEMM1 split-K partial sums [S, P_max, 2I]
+  uint8_t *act;              // GEMM1 out: [P_max, I] e4m3
+  float *act_scale;          // GEMM1 out: [P_max, I/128]
+  float *Y;                  // GEMM2 out: [S, P_max, H] fp32
+  int K, KB;                 // reduction length and its 128-blocks
+  int N_total;               // rows of one expert's weight matrix (2I or H)
+  int I;                     // intermediate size (GEMM1 gate/up split)
+  int NB;                    // column blocks per M-tile
+  int S;                     // split-K factor
+  int P_max;                 // row capacity of act / partial / Y
+  int H;                     // GEMM2 output width (row stride of Y)
+  int El;
+};
+
+struct FinalizeParams {
+  const float *Y;            // [S, P_max, H]
+  const int32_t *pair_row;   // [T, K]
+  const float *topk_w;       // [T, K]
+  uint16_t *out;             // [T, H] bf16
+  int T, H, K, S, P_max;
+};
+
+// ---------------------------------------------------------------- launchers
+// (defined in the .hip files, called by the C-ABI layer)
+hipError_t launch_route(const RouteParams &p, hipStream_t st);
+hipError_t launch_permute(const PermuteParams &p, hipStream_t st);
+hipError_t launch_gemm1(const GemmParams &p, int BM, int grid, hipStream_t st);
+hipError_t launch_gemm2(const GemmParams &p, int BM, int grid, hipStream_t st);
+hipError_t launch_finalize(const FinalizeParams &p, hipStream_t st);
+size_t gemm_lds_bytes(int BM);
+
+}  // namespace moe
