@@ -1,0 +1,305 @@
+"""Benchmark of the fused block-scaled FP8 MoE layer on one MI355X.
+
+    python bench.py [--steps K] [--warmup W] [--config decode|mid|prefill|skewed]
+
+A step is one call of the whole layer (routing, permutation, GEMM1 + SwiGLU +
+re-quantisation, GEMM2, combine) on one batch of seeded synthetic inputs
+already resident in HBM.  Activation batches rotate over --rotate seeds (the
+resident expert weights are the model's and stay fixed), so consecutive calls
+route to different experts.  K calls run back to back between two stream
+synchronisations; each kernel is bracketed by HIP events recorded on the
+library's stream (moe_fused_fp8_staged), which gives the per-kernel durations
+behind the roofline figure.  Prints one JSON line.
+
+--cold additionally times calls after a 512 MiB write that evicts L2 and the
+256 MB Infinity Cache (reported separately, never as `value`).
+--copy-calibration runs only a plain 1 GiB device copy, the reference
+kernel for scaling the HBM byte counters of rocprofv3.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+import torch
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+import paper_2608_14560_amd as M  # noqa: E402
+import workloads as W  # noqa: E402
+
+METRIC = "fused FP8 MoE µs/call + effective TFLOP/s (% FP8 MFMA peak), T=16..8192"
+HBM_PEAK_GBS = 8000.0
+FP8_PEAK_TFLOPS = 5000.0
+PROFILE_TRAFFIC = os.path.join(ROOT, "profiles", "gemm1_traffic_{cfg}.txt")
+
+
+def flops_per_pair(cfg) -> int:
+    return 2 * cfg.H * 2 * cfg.I + 2 * cfg.I * cfg.H
+
+
+def gemm1_bytes(cfg, P: int, touched: int) -> int:
+    """Algorithmic HBM bytes of one GEMM1 launch: each touched expert's W13 and
+    its scales once, each routed row of hidden (and scales) once, the FP8
+    intermediate (and scales) written once."""
+    H, I = cfg.H, cfg.I
+    w = touched * (2 * I * H + 4 * (2 * I // 128) * (H // 128))
+    a = P * (H + 4 * (H // 128))
+    o = P * (I + 4 * (I // 128))
+    return w + a + o
+
+
+def layer_bytes(cfg, P: int, touched: int) -> int:
+    """Algorithmic HBM bytes of the layer: weights of touched experts once, and
+    per token its hidden row, scales, router logits and bf16 output."""
+    H, I = cfg.H, cfg.I
+    w = touched * (3 * I * H + 4 * ((2 * I // 128) * (H // 128) + (H // 128) * (I // 128)))
+    per_tok = H + 4 * (H // 128) + 4 * cfg.num_experts + 2 * H
+    return w + cfg.T * per_tok + 4 * cfg.num_experts
+
+
+def source_digest() -> str:
+    h = hashlib.sha256()
+    for f in ("gemm.hip", "moe_device.h"):
+        with open(os.path.join(ROOT, "paper_2608_14560_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def read_traffic(cfg_name: str):
+    """Per-launch HBM bytes of GEMM1 measured with rocprofv3 counters (scaled by a
+    plain copy), if taken on the current kernel source; else None."""
+    path = PROFILE_TRAFFIC.format(cfg=cfg_name)
+    if not os.path.exists(path):
+        return None
+    kv = {}
+    with open(path) as f:
+        for line in f:
+            if "=" in line and not line.startswith("#"):
+                k, v = line.split("=", 1)
+                kv[k.strip()] = v.strip()
+    if kv.get("source_digest") != source_digest():
+        return None
+    try:
+        return int(float(kv["fetch_bytes_per_launch"]) + float(kv["write_bytes_per_launch"]))
+    except (KeyError, ValueError):
+        return None
+
+
+def copy_calibration():
+    n = 1 << 30
+    src = torch.empty(n, dtype=torch.uint8, device="cuda").fill_(1)
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_bytes_read": n, "copy_bytes_written": n, "launches": 3}))
+
+
+def cpu_baseline(cfg, batches, weights_dev, max_tokens: int):
+    """The CPU oracle on this host, on the bench's own batches (all tokens, or a
+    seeded sample of max_tokens per batch), scaled to microseconds per call."""
+    import oracle
+    oracle.build(force=False)
+    shape = oracle.shape_of(cfg)
+    total_s, pairs_done, pairs_all = 0.0, 0, 0
+    for b in batches:
+        logits = b["logits"].cpu().numpy()
+        bias = b["bias"].cpu().numpy()
+        ids, _ = oracle.route(shape, logits, bias)
+        le = ids - cfg.local_expert_offset
+        local = (le >= 0) & (le < cfg.num_local_experts)
+        pairs_all += int(local.sum())
+        if cfg.T <= max_tokens:
+            toks = np.arange(cfg.T, dtype=np.int32)
+        else:
+            toks = np.sort(np.random.default_rng(0).choice(cfg.T, max_tokens, replace=False)).astype(np.int32)
+        need = sorted(set(int(e) for e in le[toks][local[toks]]))
+        w13, s13, w2, s2 = weights_dev
+        host = lambda t: [t[e].cpu().numpy() if e in need else None for e in range(cfg.num_local_experts)]
+        hw = dict(w13=host(w13), w13_scale=host(s13), w2=host(w2), w2_scale=host(s2))
+        t0 = time.perf_counter()
+        oracle.forward(shape, b["hidden"].cpu().numpy(), b["hidden_scale"].cpu().numpy(), logits, bias,
+                       **hw, tokens=toks)
+        total_s += time.perf_counter() - t0
+        pairs_done += int(local[toks].sum())
+    # scale the sample to whole calls by the resident-pair count (the oracle's
+    # time is proportional to it)
+    per_call_s = total_s / len(batches) * (pairs_all / max(pairs_done, 1))
+    sample = (f"{len(batches)} batches x {'all' if cfg.T <= max_tokens else max_tokens} of {cfg.T} "
+              f"tokens ({pairs_done} resident pairs), scaled by resident pairs")
+    return {"value": per_call_s * 1e6, "unit": "us/call", "cores": oracle.num_threads(),
+            "kind": "oracle", "sample": sample, "wall_s": round(total_s, 2)}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--config", default="decode", choices=sorted(W.CONFIGS))
+    ap.add_argument("--rotate", type=int, default=4, help="distinct activation batches")
+    ap.add_argument("--cold", action="store_true")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-max-tokens", type=int, default=16)
+    ap.add_argument("--copy-calibration", action="store_true")
+    args = ap.parse_args()
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py: this build runs on one GPU only (no multi-GPU path); use --gpus 1",
+              file=sys.stderr)
+        sys.exit(2)
+    if not torch.cuda.is_available():
+        print("bench.py: no GPU visible", file=sys.stderr)
+        sys.exit(2)
+    if args.copy_calibration:
+        copy_calibration()
+        return
+
+    cfg = W.CONFIGS[args.config]
+    shape = M.Shape.of(cfg)
+    dev = "cuda"
+    weights = W.gen_weights(cfg, 0, device=dev)
+    _, bias, _ = W.gen_router(cfg, 0, device=dev)
+    batches = []
+    for seed in range(args.rotate):
+        logits, _, _ = W.gen_router(cfg, seed, device=dev)
+        hidden, hscale = W.gen_hidden(cfg, seed, device=dev)
+        batches.append(dict(logits=logits, bias=bias, hidden=hidden, hidden_scale=hscale))
+    ws = M.alloc_workspace(shape, dev)
+    out = torch.empty(cfg.T, cfg.H, dtype=torch.bfloat16, device=dev)
+
+    # work per batch (from the layer's own routing)
+    Ps, touched = [], []
+    for b in batches:
+        ro = M.route(shape, b["logits"], b["bias"], workspace=ws)
+        offs = ro["expert_offsets"].cpu().numpy()
+        Ps.append(int(offs[-1]))
+        touched.append(int((np.diff(offs) > 0).sum()))
+
+    stream = torch.cuda.current_stream()
+    nst = M.num_stages()
+
+    def call(i, events=None):
+        b = batches[i % len(batches)]
+        if events is None:
+            M.fused_fp8(shape, b["hidden"], b["hidden_scale"], b["logits"], b["bias"], *weights,
+                        out=out, workspace=ws, stream=stream)
+        else:
+            M.fused_fp8_staged(shape, b["hidden"], b["hidden_scale"], b["logits"], b["bias"],
+                               *weights, out, ws, events, stream=stream)
+
+    for i in range(args.warmup):
+        call(i)
+    torch.cuda.synchronize()
+
+    K = args.steps
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(nst + 1)] for _ in range(K)]
+    for row in evs:  # create the HIP events before the timed region
+        for e in row:
+            e.record(stream)
+    torch.cuda.synchronize()
+    t_start = torch.cuda.Event(enable_timing=True)
+    t_end = torch.cuda.Event(enable_timing=True)
+    wall0 = time.perf_counter()
+    t_start.record(stream)
+    for i in range(K):
+        call(i, evs[i])
+    t_end.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    ms_total = t_start.elapsed_time(t_end)
+    ms_per_step = ms_total / K
+
+    stage_ms = np.array([[evs[i][s].elapsed_time(evs[i][s + 1]) for s in range(nst)] for i in range(K)])
+    stage_avg = stage_ms.mean(0)
+    names = M.stage_names()
+
+    P_avg = float(np.mean([Ps[i % len(Ps)] for i in range(K)]))
+    T_avg = float(np.mean([touched[i % len(touched)] for i in range(K)]))
+    flop = flops_per_pair(cfg) * P_avg
+    lbytes = float(np.mean([layer_bytes(cfg, Ps[i % len(Ps)], touched[i % len(touched)]) for i in range(K)]))
+    g1bytes = float(np.mean([gemm1_bytes(cfg, Ps[i % len(Ps)], touched[i % len(touched)]) for i in range(K)]))
+    us = ms_per_step * 1e3
+    tflops = flop / (ms_per_step * 1e-3) / 1e12
+    gbs = lbytes / (ms_per_step * 1e-3) / 1e9
+
+    g1 = names.index("gemm1_swiglu_quant")
+    g1_ms = float(stage_avg[g1])
+    g1_flop = flop * (2 * cfg.H * 2 * cfg.I) / flops_per_pair(cfg)
+    t_hbm = g1bytes / (HBM_PEAK_GBS * 1e9)
+    t_mfma = g1_flop / (FP8_PEAK_TFLOPS * 1e12)
+    if t_hbm >= t_mfma:
+        ach = g1bytes / (g1_ms * 1e-3) / 1e9
+        roof = {"bound": "hbm", "achieved": round(ach, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": round(ach / HBM_PEAK_GBS, 4)}
+    else:
+        ach = g1_flop / (g1_ms * 1e-3) / 1e12
+        roof = {"bound": "mfma", "achieved": round(ach, 2), "peak": FP8_PEAK_TFLOPS, "unit": "TFLOP/s",
+                "frac": round(ach / FP8_PEAK_TFLOPS, 4)}
+    roof["kernel"] = "gemm1_swiglu_quant"
+    roof["avg_launch_us"] = round(g1_ms * 1e3, 2)
+    roof["algorithmic_bytes_per_launch"] = int(g1bytes)
+    traffic = read_traffic(cfg.name)
+    roof["traffic"] = traffic
+
+    cold = None
+    if args.cold:
+        flush = torch.empty(512 << 20, dtype=torch.uint8, device=dev)
+        times = []
+        for i in range(min(K, 10)):
+            flush.fill_(i & 0xFF)
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            call(i)
+            e1.record(stream)
+            torch.cuda.synchronize()
+            times.append(e0.elapsed_time(e1))
+        cold = round(float(np.median(times)) * 1e3, 2)
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(cfg, batches, weights, args.cpu_max_tokens)
+
+    rec = {
+        "metric": METRIC,
+        "value": round(us, 2),
+        "unit": "us/call",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 5),
+        "higher_is_better": False,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "fp8e4m3 (fp32 accumulate)",
+        "data": "synthetic (seeded; DeepSeek-V3 shapes)",
+        "config": {"workload": f"{cfg.name}: T={cfg.T}, H={cfg.H}, I={cfg.I}, {cfg.num_local_experts} of "
+                               f"{cfg.num_experts} experts resident, top-{cfg.top_k} of {cfg.topk_group}/"
+                               f"{cfg.n_group} groups",
+                   "T": cfg.T, "H": cfg.H, "I": cfg.I, "num_experts": cfg.num_experts,
+                   "num_local_experts": cfg.num_local_experts, "top_k": cfg.top_k,
+                   "batches": args.rotate, "resident_pairs_avg": P_avg, "touched_experts_avg": T_avg},
+        "tflops": round(tflops, 4),
+        "pct_fp8_mfma_peak": round(100 * tflops / FP8_PEAK_TFLOPS, 4),
+        "gbps": round(gbs, 1),
+        "pct_hbm_peak": round(100 * gbs / HBM_PEAK_GBS, 2),
+        "stage_us": {n: round(float(v) * 1e3, 2) for n, v in zip(names, stage_avg)},
+        "roofline": roof,
+        "cpu_baseline": cpu,
+        "us_per_call_cold": cold,
+        "host_wall_s": round(wall, 3),
+    }
+    print(json.dumps(rec))
+
+
+if __name__ == "__main__":
+    main()
