@@ -206,6 +206,47 @@ def fused_fp8(shape: Shape, hidden, hidden_scale, logits, bias, w13, w13_scale, 
     return out
 
 
+class FusedCall:
+    """A prepared moe_fused_fp8 call: the arguments are validated and marshalled
+    once, each call() only enqueues the layer on the stream.  The tensors must
+    stay alive (and keep their addresses) while the object is used; their
+    contents may change between calls."""
+
+    def __init__(self, shape: Shape, hidden, hidden_scale, logits, bias, w13, w13_scale, w2,
+                 w2_scale, out, workspace, route_out: dict | None = None, stream=None):
+        self._keep = (shape.c(), route_out and _route_struct(route_out))
+        args = _fused_args(shape, hidden, hidden_scale, logits, bias, w13, w13_scale, w2,
+                           w2_scale, out, route_out, workspace)
+        args[0] = ctypes.byref(self._keep[0])
+        if route_out is not None:
+            args[10] = ctypes.byref(self._keep[1])
+        self._args = (*args, _stream(stream))
+        self._fn = lib().moe_fused_fp8
+        self._staged = lib().moe_fused_fp8_staged
+        self.out = out
+
+    def __call__(self):
+        rc = self._fn(*self._args)
+        if rc:
+            raise MoEError("moe_fused_fp8", rc)
+        return self.out
+
+    def staged(self, events_array, n: int):
+        """events_array: a ctypes array of n raw hipEvent_t handles."""
+        rc = self._staged(*self._args, events_array, n)
+        if rc:
+            raise MoEError("moe_fused_fp8_staged", rc)
+        return self.out
+
+
+def event_array(events: list):
+    """ctypes array of the raw HIP handles of torch.cuda.Events (created here)."""
+    for ev in events:
+        if ev.cuda_event == 0:
+            ev.record()
+    return (ctypes.c_void_p * len(events))(*[ev.cuda_event for ev in events])
+
+
 def num_stages() -> int:
     return lib().moe_num_stages()
 

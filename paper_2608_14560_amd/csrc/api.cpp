@@ -24,9 +24,10 @@ namespace {
 
 using namespace moe;
 
-constexpr int kStages = 6;
-const char *const kStageNames[kStages] = {"route", "permute_count", "permute_scatter",
-                                          "gemm1_swiglu_quant", "gemm2", "combine_finalize"};
+constexpr int kStages = 7;
+const char *const kStageNames[kStages] = {"route",        "permute_count", "permute_scatter",
+                                          "gemm1_swiglu", "requant",       "gemm2",
+                                          "combine_finalize"};
 
 constexpr size_t kAlign = 256;
 size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
@@ -49,15 +50,17 @@ moe_status_t check_shape(const moe_shape_t *s) {
   if (s->num_experts > 1024 || s->num_local_experts > 1024 || s->n_group > 64 || s->top_k > 16)
     return MOE_ERR_UNSUPPORTED;
   if ((int64_t)s->T * s->top_k >= (int64_t)1 << 31) return MOE_ERR_UNSUPPORTED;
+  if (s->H > 65536 || s->I > 65536) return MOE_ERR_UNSUPPORTED;  // staged scales fit LDS
   return MOE_OK;
 }
 
 // Host-side plan: tile shape, split factors, grid bounds and the workspace map.
 struct Plan {
-  int BM, S1, S2, NB1, NB2, nchunks, max_tiles, n_counters;
+  int BM, S1, S2, NB1, NB2, nchunks, max_tiles;
+  bool narrow1;  // GEMM1 split over 32-column groups (small batches)
   int64_t P_max;
   size_t off_ids, off_w, off_offsets, off_perm_token, off_perm_pair, off_pair_row, off_chunk_counts,
-      off_tile_base, off_n_items, off_counters, off_act, off_act_scale, off_partial, off_Y, total;
+      off_tile_base, off_n_items, off_act, off_act_scale, off_abuf, off_Y, total;
 };
 
 Plan make_plan(const moe_shape_t *s) {
@@ -68,17 +71,19 @@ Plan make_plan(const moe_shape_t *s) {
   const double avg = (double)TK / s->num_experts;
   p.BM = avg <= 16 ? 16 : (avg <= 48 ? 32 : (avg <= 160 ? 64 : 128));
   // GEMM1 promotes its K blocks in order (its output decides the re-quantised
-  // codes), so it never splits K.  GEMM2 splits K in halves for small batches,
-  // which stream the weights with too few tiles to fill 256 CUs.
+  // codes), so it never splits K; GEMM2 could (S2 > 1 sums the halves in the
+  // combine) but the small-tile kernel already has enough work items.
   p.S1 = 1;
-  p.S2 = TK <= 512 ? 2 : 1;
-  p.NB1 = s->I / 128;
-  p.NB2 = (s->H + 255) / 256;
+  // small-tile batches: GEMM1 split over 32-column groups, GEMM2 over K halves
+  p.narrow1 = p.BM == 16;
+  p.S2 = p.BM == 16 ? 2 : 1;
+  p.NB1 = p.narrow1 ? s->I / gemm1_narrow_cols() : s->I / 128;
+  // GEMM2 column blocks: 128 wide for the small-tile kernel, 256 otherwise
+  p.NB2 = p.BM == 16 ? s->H / 128 : (s->H + 255) / 256;
   p.nchunks = (int)((s->T + kChunkTokens - 1) / kChunkTokens);
   if (p.nchunks < 1) p.nchunks = 1;
   const int64_t touched = TK < s->num_local_experts ? TK : s->num_local_experts;
   p.max_tiles = (int)((p.P_max + p.BM - 1) / p.BM + touched);
-  p.n_counters = p.S1 > 1 ? p.max_tiles * p.NB1 : 1;
 
   size_t o = 0;
   auto take = [&](size_t bytes) {
@@ -95,10 +100,9 @@ Plan make_plan(const moe_shape_t *s) {
   p.off_chunk_counts = take(sizeof(int32_t) * (size_t)p.nchunks * s->num_local_experts);
   p.off_tile_base = take(sizeof(int32_t) * (s->num_local_experts + 1));
   p.off_n_items = take(sizeof(int32_t) * 2);
-  p.off_counters = take(sizeof(int32_t) * (size_t)p.n_counters);
   p.off_act = take((size_t)p.P_max * s->I);
   p.off_act_scale = take(sizeof(float) * (size_t)p.P_max * (s->I / 128));
-  p.off_partial = take(p.S1 > 1 ? sizeof(float) * (size_t)p.S1 * p.P_max * 2 * s->I : 0);
+  p.off_abuf = take(p.narrow1 ? sizeof(float) * (size_t)p.P_max * s->I : 0);
   p.off_Y = take(sizeof(float) * (size_t)p.S2 * p.P_max * s->H);
   p.total = o;
   return p;
@@ -161,7 +165,6 @@ moe_status_t enqueue_route(const moe_shape_t *s, const Plan &pl, const float *lo
   pp.pair_row = r.pair_row;
   pp.tile_base = at<int32_t>(ws, pl.off_tile_base);
   pp.n_items = at<int32_t>(ws, pl.off_n_items);
-  pp.counters = at<int32_t>(ws, pl.off_counters);
   pp.T = s->T;
   pp.K = s->top_k;
   pp.El = s->num_local_experts;
@@ -170,7 +173,6 @@ moe_status_t enqueue_route(const moe_shape_t *s, const Plan &pl, const float *lo
   pp.BM = pl.BM;
   pp.items_per_tile1 = pl.NB1 * pl.S1;
   pp.items_per_tile2 = pl.NB2 * pl.S2;
-  pp.n_counters = pl.n_counters;
   mark();
   MOE_TRY_HIP(launch_permute_count(pp, st));
   mark();
@@ -208,8 +210,7 @@ moe_status_t fused_impl(const moe_shape_t *s, const uint8_t *hidden, const float
   g.expert_offsets = r.offsets;
   g.tile_base = at<int32_t>(ws, pl.off_tile_base);
   g.perm_token = r.perm_token;
-  g.counters = at<int32_t>(ws, pl.off_counters);
-  g.partial = at<float>(ws, pl.off_partial);
+  g.abuf = at<float>(ws, pl.off_abuf);
   g.act = at<uint8_t>(ws, pl.off_act);
   g.act_scale = at<float>(ws, pl.off_act_scale);
   g.Y = at<float>(ws, pl.off_Y);
@@ -231,7 +232,11 @@ moe_status_t fused_impl(const moe_shape_t *s, const uint8_t *hidden, const float
   g1.NB = pl.NB1;
   g1.S = pl.S1;
   mark();
-  MOE_TRY_HIP(launch_gemm1(g1, pl.BM, round8((int64_t)pl.max_tiles * pl.NB1 * pl.S1), st));
+  const int grid1 = round8((int64_t)pl.max_tiles * pl.NB1 * pl.S1);
+  MOE_TRY_HIP(pl.narrow1 ? launch_gemm1_narrow(g1, grid1, st) : launch_gemm1(g1, pl.BM, grid1, st));
+  // the column-split GEMM1 leaves its re-quantisation to a launch of its own
+  mark();
+  if (pl.narrow1) MOE_TRY_HIP(launch_requant(g1, (int)pl.P_max, st));
 
   // GEMM2: permuted activation rows x W2 -> Y
   GemmParams g2 = g;

@@ -276,6 +276,340 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(GemmParams p) {
     }
 }
 
+// Small-tile variant (BM = 16): the weight fragments are streamed from HBM
+// straight into registers through a D-stage prefetch ring, with no LDS round
+// trip and no barrier in the K loop.  Prefetches are issued unconditionally
+// (past the end they re-read the last K block) so the compiler can keep D
+// loads in flight instead of draining the queue at every branch.
+//   GEMM1: 8 waves; wave w owns the gate and up columns [16w, 16w+16) of the
+//          128-wide intermediate block (SwiGLU pairs in one lane).
+//   GEMM2: 4 waves; wave w owns output columns [32w, 32w+32) of a 128-wide block.
+// Every wave loads the tile's A fragment itself (16 rows x 128 bytes per K
+// step; the waves of a workgroup hit it in L1).  Activation and weight block
+// scales of the whole K range are staged in LDS once.  The per-element
+// arithmetic (MFMA block products, promotion order, epilogue) is the same as
+// the LDS-staged kernel's.
+template <bool G1>
+struct Stream {
+  static constexpr int kWaves = G1 ? 8 : 4;
+  static constexpr int kCols = 128;  // columns of the block per work item
+};
+
+template <bool G1, int D>
+__global__ __launch_bounds__(Stream<G1>::kWaves * kWave) void gemm_stream_kernel(GemmParams p) {
+  constexpr int NW = Stream<G1>::kWaves;
+  __shared__ int tb[1028];
+  __shared__ float amax_lds[NW][16];
+  extern __shared__ __attribute__((aligned(16))) float scales[];  // sa[16][KB], sb[2][KB]
+
+  const int tid = threadIdx.x;
+  const int lane = tid & (kWave - 1);
+  const int wave = tid / kWave;
+  const int r16 = lane & 15;
+  const int frag_off = (lane >> 4) * 32;
+
+  const int n_items = *p.n_items;
+  const int per_xcd = (n_items + 7) / 8;
+  const int item = (blockIdx.x & 7) * per_xcd + (blockIdx.x >> 3);
+  if ((int)(blockIdx.x >> 3) >= per_xcd || item >= n_items) return;
+
+  for (int i = tid; i <= p.El; i += NW * kWave) tb[i] = p.tile_base[i];
+  __syncthreads();
+
+  const int X = p.NB * p.S;
+  const int qt = item / X;
+  int lo = 0, hi = p.El;
+  while (hi - lo > 1) {
+    const int mid = (lo + hi) >> 1;
+    if (tb[mid] <= qt) lo = mid; else hi = mid;
+  }
+  const int e = lo;
+  const int nt_e = tb[e + 1] - tb[e];
+  const int local = item - tb[e] * X;
+  const int mt_idx = local % nt_e;
+  const int rest = local / nt_e;
+  const int s = rest % p.S;
+  const int nb = rest / p.S;
+  const int seg0 = p.expert_offsets[e];
+  const int seg1 = p.expert_offsets[e + 1];
+  const int row0 = seg0 + mt_idx * 16;
+  const int nrows = min(16, seg1 - row0);
+  const int kb0 = (s * p.KB) / p.S;
+  const int kb1 = ((s + 1) * p.KB) / p.S;
+  const int n = kb1 - kb0;
+  const size_t K = (size_t)p.K;
+  const int KB = p.KB;
+
+  // B rows of the wave's two sub-tiles and their 128-row scale blocks
+  int brow0, brow1, bblk0, bblk1;
+  if (G1) {
+    brow0 = nb * 128 + 16 * wave + r16;
+    brow1 = p.I + nb * 128 + 16 * wave + r16;
+    bblk0 = nb;
+    bblk1 = p.I / 128 + nb;
+  } else {
+    brow0 = nb * 128 + 32 * wave + r16;
+    brow1 = brow0 + 16;
+    bblk0 = bblk1 = nb;
+  }
+
+  // stage the scales: sa[r][kb] of the tile's rows, sb[0/1][kb] of the blocks
+  float *sa_l = scales;
+  float *sb_l = scales + 16 * KB;
+  for (int i = tid; i < 16 * KB; i += NW * kWave) {
+    const int r = i / KB, kb = i % KB;
+    const int rr = min(r, nrows - 1);
+    const int src = G1 ? p.perm_token[row0 + rr] : row0 + rr;
+    sa_l[i] = p.A_scale[(size_t)src * KB + kb];
+  }
+  {
+    const int blk0 = G1 ? bblk0 : nb, blk1 = G1 ? p.I / 128 + nb : nb;
+    const float *sb0 = p.B_scale + ((size_t)e * (p.N_total / 128) + blk0) * KB;
+    const float *sb1 = p.B_scale + ((size_t)e * (p.N_total / 128) + blk1) * KB;
+    for (int i = tid; i < KB; i += NW * kWave) {
+      sb_l[i] = sb0[i];
+      sb_l[KB + i] = sb1[i];
+    }
+  }
+
+  // A fragment source: the lane's row (ragged tails repeat the last row)
+  const int arow = min(r16, nrows - 1);
+  const int asrc = G1 ? p.perm_token[row0 + arow] : row0 + arow;
+  const uint8_t *a_ptr = p.A + (size_t)asrc * K + frag_off;
+  const uint8_t *Bexp = p.B + (size_t)e * p.N_total * K;
+  const uint8_t *b_ptr0 = Bexp + (size_t)brow0 * K + frag_off;
+  const uint8_t *b_ptr1 = Bexp + (size_t)brow1 * K + frag_off;
+
+  v8i ra[D], rb0[D], rb1[D];
+#define MOE_SLOAD(d, kb)                                                  \
+  do {                                                                    \
+    ra[d] = *reinterpret_cast<const v8i *>(a_ptr + (size_t)(kb) * 128);   \
+    rb0[d] = *reinterpret_cast<const v8i *>(b_ptr0 + (size_t)(kb) * 128); \
+    rb1[d] = *reinterpret_cast<const v8i *>(b_ptr1 + (size_t)(kb) * 128); \
+  } while (0)
+
+#pragma unroll
+  for (int d = 0; d < D; ++d) MOE_SLOAD(d, kb0 + min(d, n - 1));
+  __syncthreads();  // scales staged
+
+  v4f acc0 = {0.f, 0.f, 0.f, 0.f}, acc1 = {0.f, 0.f, 0.f, 0.f};
+  const int srow = 4 * (lane >> 4);
+  const int sb1_off = G1 ? KB : 0;
+  for (int base = 0; base < n; base += D) {
+#pragma unroll
+    for (int d = 0; d < D; ++d) {
+      const int it = base + d;
+      if (it < n) {
+        const int kb = kb0 + it;
+        const v4f z = {0.f, 0.f, 0.f, 0.f};
+        const v4f t0 = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(ra[d], rb0[d], z, 0, 0, 0, 0, 0, 0);
+        const v4f t1 = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(ra[d], rb1[d], z, 0, 0, 0, 0, 0, 0);
+        const float s0 = sb_l[kb], s1 = sb_l[sb1_off + kb];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const float sa = sa_l[(srow + i) * KB + kb];
+          acc0[i] = __builtin_fmaf(t0[i], sa * s0, acc0[i]);
+          acc1[i] = __builtin_fmaf(t1[i], sa * s1, acc1[i]);
+        }
+      }
+      MOE_SLOAD(d, kb0 + min(it + D, n - 1));
+    }
+  }
+#undef MOE_SLOAD
+
+  if (!G1) {
+    float *Ys = p.Y + (size_t)s * p.P_max * p.H;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int r = srow + i;
+      if (r < nrows) {
+        float *yrow = Ys + (size_t)(row0 + r) * p.H + nb * 128 + 32 * wave + r16;
+        yrow[0] = acc0[i];
+        yrow[16] = acc1[i];
+      }
+    }
+    return;
+  }
+
+  // SwiGLU, then the per-row amax over the 128 columns (16 lanes x 8 waves)
+  float av[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    av[i] = swiglu_spec(acc0[i], acc1[i]);
+    float mx = fabsf(av[i]);
+#pragma unroll
+    for (int off = 1; off < 16; off <<= 1) mx = fmaxf(mx, __shfl_xor(mx, off));
+    if (r16 == 0) amax_lds[wave][srow + i] = mx;
+  }
+  __syncthreads();
+  const int IB = p.I / 128;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int r = srow + i;
+    float amax = amax_lds[0][r];
+#pragma unroll
+    for (int w = 1; w < NW; ++w) amax = fmaxf(amax, amax_lds[w][r]);
+    const float scale = (amax > 0.0f) ? amax / 448.0f : 1.0f;
+    if (r < nrows) {
+      const uint32_t q = (amax > 0.0f) ? e4m3x2_rne_sat(av[i] / scale, 0.0f) : 0u;
+      p.act[(size_t)(row0 + r) * p.I + nb * 128 + 16 * wave + r16] = (uint8_t)(q & 0xff);
+      if (wave == 0 && r16 == 0) p.act_scale[(size_t)(row0 + r) * IB + nb] = scale;
+    }
+  }
+}
+
+// GEMM1 for small batches, split over columns: a work item is one 16-row
+// M-tile and 32 intermediate columns (gate and up), so a handful of resident
+// experts still yields several work items per CU (HBM streaming needs all
+// 256 CUs busy; splitting K instead would change the promotion order that
+// decides the FP8 codes).  4 waves: waves 0/1 stream the gate rows
+// [32j + 16w, +16), waves 2/3 the matching up rows; each wave runs one MFMA
+// per 128-K step with a D-stage register prefetch ring (unconditional, so
+// loads stay in flight).  The SwiGLU output goes to a_buf [P, I] fp32 and
+// requant_kernel (the next launch) re-quantises it: no cross-workgroup
+// synchronisation.  Values and codes are bit-identical to the single-item
+// epilogue.
+constexpr int kNarrowCols = 32;
+
+template <int D>
+__global__ __launch_bounds__(256) void gemm1_narrow_kernel(GemmParams p) {
+  __shared__ int tb[1028];
+  __shared__ float up_lds[16][kNarrowCols + 1];
+  extern __shared__ __attribute__((aligned(16))) float scales[];  // sa[16][KB], sb[2][KB]
+
+  const int tid = threadIdx.x;
+  const int lane = tid & (kWave - 1);
+  const int wave = tid / kWave;
+  const int r16 = lane & 15;
+  const int frag_off = (lane >> 4) * 32;
+
+  const int n_items = *p.n_items;
+  const int per_xcd = (n_items + 7) / 8;
+  const int item = (blockIdx.x & 7) * per_xcd + (blockIdx.x >> 3);
+  if ((int)(blockIdx.x >> 3) >= per_xcd || item >= n_items) return;
+
+  for (int i = tid; i <= p.El; i += 256) tb[i] = p.tile_base[i];
+  __syncthreads();
+
+  const int X = p.NB;  // column groups per M-tile (no K split)
+  const int qt = item / X;
+  int lo = 0, hi = p.El;
+  while (hi - lo > 1) {
+    const int mid = (lo + hi) >> 1;
+    if (tb[mid] <= qt) lo = mid; else hi = mid;
+  }
+  const int e = lo;
+  const int nt_e = tb[e + 1] - tb[e];
+  const int local = item - tb[e] * X;
+  const int mt_idx = local % nt_e;
+  const int j = local / nt_e;          // 32-column group
+  const int blk = j * kNarrowCols / 128;  // its 128-column block
+  const int seg0 = p.expert_offsets[e];
+  const int seg1 = p.expert_offsets[e + 1];
+  const int row0 = seg0 + mt_idx * 16;
+  const int nrows = min(16, seg1 - row0);
+  const int KB = p.KB;
+  const size_t K = (size_t)p.K;
+
+  float *sa_l = scales;
+  float *sb_l = scales + 16 * KB;
+  for (int i = tid; i < 16 * KB; i += 256) {
+    const int r = i / KB, kb = i % KB;
+    const int src = p.perm_token[row0 + min(r, nrows - 1)];
+    sa_l[i] = p.A_scale[(size_t)src * KB + kb];
+  }
+  {
+    const float *sg = p.B_scale + ((size_t)e * (p.N_total / 128) + blk) * KB;
+    const float *su = p.B_scale + ((size_t)e * (p.N_total / 128) + p.I / 128 + blk) * KB;
+    for (int i = tid; i < KB; i += 256) {
+      sb_l[i] = sg[i];
+      sb_l[KB + i] = su[i];
+    }
+  }
+
+  const bool up = wave >= 2;
+  const int brow = (up ? p.I : 0) + j * kNarrowCols + 16 * (wave & 1) + r16;
+  const int asrc = p.perm_token[row0 + min(r16, nrows - 1)];
+  const uint8_t *a_ptr = p.A + (size_t)asrc * K + frag_off;
+  const uint8_t *b_ptr = p.B + (size_t)e * p.N_total * K + (size_t)brow * K + frag_off;
+
+  v8i ra[D], rb[D];
+#pragma unroll
+  for (int d = 0; d < D; ++d) {
+    const int kb = min(d, KB - 1);
+    ra[d] = *reinterpret_cast<const v8i *>(a_ptr + (size_t)kb * 128);
+    rb[d] = *reinterpret_cast<const v8i *>(b_ptr + (size_t)kb * 128);
+  }
+  __syncthreads();  // scales staged
+
+  v4f acc = {0.f, 0.f, 0.f, 0.f};
+  const int srow = 4 * (lane >> 4);
+  const float *sb_w = sb_l + (up ? KB : 0);
+  for (int base = 0; base < KB; base += D) {
+#pragma unroll
+    for (int d = 0; d < D; ++d) {
+      const int kb = base + d;
+      if (kb < KB) {
+        const v4f z = {0.f, 0.f, 0.f, 0.f};
+        const v4f t = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(ra[d], rb[d], z, 0, 0, 0, 0, 0, 0);
+        const float sbv = sb_w[kb];
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          acc[i] = __builtin_fmaf(t[i], sa_l[(srow + i) * KB + kb] * sbv, acc[i]);
+      }
+      const int nk = min(kb + D, KB - 1);
+      ra[d] = *reinterpret_cast<const v8i *>(a_ptr + (size_t)nk * 128);
+      rb[d] = *reinterpret_cast<const v8i *>(b_ptr + (size_t)nk * 128);
+    }
+  }
+
+  // SwiGLU: the up waves hand their columns to the gate waves through LDS
+  if (up) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) up_lds[srow + i][16 * (wave & 1) + r16] = acc[i];
+  }
+  __syncthreads();
+  if (!up) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int r = srow + i;
+      if (r < nrows)
+        p.abuf[(size_t)(row0 + r) * p.I + j * kNarrowCols + 16 * wave + r16] =
+            swiglu_spec(acc[i], up_lds[r][16 * wave + r16]);
+    }
+  }
+}
+
+// Re-quantisation of the column-split GEMM1 output: rows [0, P) of a_buf
+// (P = expert_offsets[El], on the device), one 128-column block per 16
+// threads: amax, scale = amax / 448, e4m3 codes -- the same operations on the
+// same fp32 values as the single-item GEMM1 epilogue.
+__global__ __launch_bounds__(256) void requant_kernel(GemmParams p) {
+  const int P = p.expert_offsets[p.El];
+  const int IB = p.I / 128;
+  const int g = blockIdx.x * 16 + (threadIdx.x >> 4);  // (row, block) pair
+  if (g >= P * IB) return;
+  const int row = g / IB, blk = g % IB;
+  const int c0 = (threadIdx.x & 15) * 8;
+  const float *src = p.abuf + (size_t)row * p.I + blk * 128 + c0;
+  const float4 x0 = *reinterpret_cast<const float4 *>(src);
+  const float4 x1 = *reinterpret_cast<const float4 *>(src + 4);
+  const float v[8] = {x0.x, x0.y, x0.z, x0.w, x1.x, x1.y, x1.z, x1.w};
+  float mx = 0.0f;
+#pragma unroll
+  for (int c = 0; c < 8; ++c) mx = fmaxf(mx, fabsf(v[c]));
+#pragma unroll
+  for (int off = 1; off < 16; off <<= 1) mx = fmaxf(mx, __shfl_xor(mx, off));
+  const float scale = (mx > 0.0f) ? mx / 448.0f : 1.0f;
+  uint2 w2 = {0u, 0u};
+  if (mx > 0.0f) {
+    w2.x = e4m3x2_rne_sat(v[0] / scale, v[1] / scale) | (e4m3x2_rne_sat(v[2] / scale, v[3] / scale) << 16);
+    w2.y = e4m3x2_rne_sat(v[4] / scale, v[5] / scale) | (e4m3x2_rne_sat(v[6] / scale, v[7] / scale) << 16);
+  }
+  *reinterpret_cast<uint2 *>(p.act + (size_t)row * p.I + blk * 128 + c0) = w2;
+  if (c0 == 0) p.act_scale[(size_t)row * IB + blk] = scale;
+}
+
 __global__ __launch_bounds__(256) void finalize_kernel(FinalizeParams p) {
   const int t = blockIdx.x;
   const int n0 = (blockIdx.y * 256 + threadIdx.x) * 8;
@@ -312,18 +646,27 @@ template <int BM, bool G1>
 hipError_t launch_gemm_bm(const GemmParams &p, int grid, hipStream_t st) {
   auto k = gemm_kernel<BM, G1>;
   const int lds = Layout<BM>::TOTAL;
-  hipError_t err = hipFuncSetAttribute(reinterpret_cast<const void *>(k),
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, lds);
-  if (err != hipSuccess) return err;
+  // raise the dynamic LDS limit once per kernel instantiation (per process;
+  // the attribute is a property of the code object, not of the device)
+  static hipError_t attr = hipFuncSetAttribute(reinterpret_cast<const void *>(k),
+                                               hipFuncAttributeMaxDynamicSharedMemorySize, lds);
+  if (attr != hipSuccess) return attr;
   hipLaunchKernelGGL(k, dim3(grid), dim3(kThreads), lds, st, p);
   return hipGetLastError();
 }
+
+constexpr int kStreamDepth = 4;
 
 template <bool G1>
 hipError_t launch_gemm(const GemmParams &p, int BM, int grid, hipStream_t st) {
   if (grid <= 0) return hipSuccess;
   switch (BM) {
-    case 16: return launch_gemm_bm<16, G1>(p, grid, st);
+    case 16: {
+      const size_t lds = sizeof(float) * 18 * (size_t)p.KB;
+      hipLaunchKernelGGL((gemm_stream_kernel<G1, kStreamDepth>), dim3(grid),
+                         dim3(Stream<G1>::kWaves * kWave), lds, st, p);
+      return hipGetLastError();
+    }
     case 32: return launch_gemm_bm<32, G1>(p, grid, st);
     case 64: return launch_gemm_bm<64, G1>(p, grid, st);
     case 128: return launch_gemm_bm<128, G1>(p, grid, st);
@@ -368,6 +711,19 @@ hipError_t launch_debug_mfma_block(const uint8_t *a, const uint8_t *b, float *d,
 
 hipError_t launch_gemm1(const GemmParams &p, int BM, int grid, hipStream_t st) {
   return launch_gemm<true>(p, BM, grid, st);
+}
+hipError_t launch_gemm1_narrow(const GemmParams &p, int grid, hipStream_t st) {
+  if (grid <= 0) return hipSuccess;
+  const size_t lds = sizeof(float) * 18 * (size_t)p.KB;
+  hipLaunchKernelGGL(gemm1_narrow_kernel<kStreamDepth>, dim3(grid), dim3(256), lds, st, p);
+  return hipGetLastError();
+}
+int gemm1_narrow_cols() { return kNarrowCols; }
+hipError_t launch_requant(const GemmParams &p, int P_max, hipStream_t st) {
+  const int pairs = P_max * (p.I / 128);
+  if (pairs <= 0) return hipSuccess;
+  hipLaunchKernelGGL(requant_kernel, dim3((pairs + 15) / 16), dim3(256), 0, st, p);
+  return hipGetLastError();
 }
 hipError_t launch_gemm2(const GemmParams &p, int BM, int grid, hipStream_t st) {
   return launch_gemm<false>(p, BM, grid, st);

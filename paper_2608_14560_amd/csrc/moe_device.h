@@ -96,9 +96,8 @@ struct PermuteParams {
   int32_t *pair_row;         // [T, K]
   int32_t *tile_base;        // [El + 1] first M-tile of each expert
   int32_t *n_items;          // [2] work items of GEMM1 and GEMM2
-  int32_t *counters;         // [n_counters] split-K arrival counters
   int T, K, El, offset, nchunks;
-  int BM, items_per_tile1, items_per_tile2, n_counters;
+  int BM, items_per_tile1, items_per_tile2;
 };
 
 constexpr int kChunkTokens = 256;   // tokens per permute workgroup
@@ -115,8 +114,7 @@ struct GemmParams {
   const int32_t *tile_base;
   const int32_t *perm_token;
   const int32_t *n_items;    // device count of work items
-  int32_t *counters;         // GEMM1 split-K arrival counters
-  float *partial;            // GEMM1 split-K partial sums [S, P_max, 2I]
+  float *abuf;               // GEMM1 column-split SwiGLU output [P_max, I] fp32
   uint8_t *act;              // GEMM1 out: [P_max, I] e4m3
   float *act_scale;          // GEMM1 out: [P_max, I/128]
   float *Y;                  // GEMM2 out: [S, P_max, H] fp32
@@ -125,7 +123,7 @@ struct GemmParams {
   int I;                     // intermediate size (GEMM1 gate/up split)
   int NB;                    // column blocks per M-tile
   int S;                     // split-K factor
-  int P_max;                 // row capacity of act / partial / Y
+  int P_max;                 // row capacity of act / abuf / Y
   int H;                     // GEMM2 output width (row stride of Y)
   int El;
 };
@@ -143,6 +141,9 @@ struct FinalizeParams {
 hipError_t launch_route(const RouteParams &p, hipStream_t st);
 hipError_t launch_permute(const PermuteParams &p, hipStream_t st);
 hipError_t launch_gemm1(const GemmParams &p, int BM, int grid, hipStream_t st);
+hipError_t launch_gemm1_narrow(const GemmParams &p, int grid, hipStream_t st);
+int gemm1_narrow_cols();
+hipError_t launch_requant(const GemmParams &p, int P_max, hipStream_t st);
 hipError_t launch_gemm2(const GemmParams &p, int BM, int grid, hipStream_t st);
 hipError_t launch_finalize(const FinalizeParams &p, hipStream_t st);
 size_t gemm_lds_bytes(int BM);

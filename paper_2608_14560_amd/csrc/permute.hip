@@ -12,8 +12,7 @@
 //            bitmaps (deterministic: a pair's position depends only on the
 //            routing, never on timing), and writes perm_token / perm_pair /
 //            pair_row.  Workgroup 0 also writes expert_offsets, the M-tile
-//            prefix of every expert, the GEMM work-item counts, and clears
-//            the split-K arrival counters.
+//            prefix of every expert and the GEMM work-item counts.
 #include "moe_device.h"
 
 namespace moe {
@@ -62,9 +61,13 @@ __device__ int block_exclusive_scan(int v, int *wsum, int *total) {
   return before + x - v;
 }
 
+// SINGLE: the batch is one chunk; the workgroup counts its own pairs (an LDS
+// histogram) instead of reading the count kernel's output.
+template <bool SINGLE>
 __global__ __launch_bounds__(kThreads) void scatter_kernel(PermuteParams p) {
   // per expert: start of this chunk's rows, then per-wave occupancy bitmaps
   __shared__ int base[kMaxEl];
+  __shared__ int hist[SINGLE ? kMaxEl : 1];
   __shared__ unsigned long long bits[kWaves][kMaxEl];
   __shared__ int wsum[kWaves];
 
@@ -72,8 +75,24 @@ __global__ __launch_bounds__(kThreads) void scatter_kernel(PermuteParams p) {
   const int lane = threadIdx.x & (kWave - 1);
   const int w = threadIdx.x / kWave;
 
-  for (int e = threadIdx.x; e < p.El; e += kThreads)
+  for (int e = threadIdx.x; e < p.El; e += kThreads) {
     for (int i = 0; i < kWaves; ++i) bits[i][e] = 0ull;
+    if (SINGLE) hist[e] = 0;
+  }
+  if (SINGLE) {
+    __syncthreads();
+    const int t = threadIdx.x;
+    if (t < p.T)
+      for (int j = 0; j < p.K; ++j) {
+        const int le = p.topk_ids[(size_t)t * p.K + j] - p.offset;
+        if (le >= 0 && le < p.El) atomicAdd(&hist[le], 1);
+      }
+    __syncthreads();
+  }
+  // count of local expert e in chunk c
+  auto cnt = [&](int c, int e) {
+    return SINGLE ? hist[e] : p.chunk_counts[(size_t)c * p.El + e];
+  };
 
   // expert offsets: exclusive scan of the per-expert totals over all chunks.
   // Each thread owns a contiguous run of experts.
@@ -83,7 +102,7 @@ __global__ __launch_bounds__(kThreads) void scatter_kernel(PermuteParams p) {
   for (int e = e0; e < e0 + per && e < p.El; ++e) {
     int tot = 0, before = 0;
     for (int c = 0; c < p.nchunks; ++c) {
-      const int n = p.chunk_counts[(size_t)c * p.El + e];
+      const int n = cnt(c, e);
       tot += n;
       if (c < chunk) before += n;
     }
@@ -96,7 +115,7 @@ __global__ __launch_bounds__(kThreads) void scatter_kernel(PermuteParams p) {
   int acc = run_start;
   for (int e = e0; e < e0 + per && e < p.El; ++e) {
     int tot = 0;
-    for (int c = 0; c < p.nchunks; ++c) tot += p.chunk_counts[(size_t)c * p.El + e];
+    for (int c = 0; c < p.nchunks; ++c) tot += cnt(c, e);
     if (chunk == 0) p.expert_offsets[e] = acc;
     base[e] += acc;
     acc += tot;
@@ -138,14 +157,14 @@ __global__ __launch_bounds__(kThreads) void scatter_kernel(PermuteParams p) {
   int tiles_run = 0;
   for (int e = e0; e < e0 + per && e < p.El; ++e) {
     int tot = 0;
-    for (int c = 0; c < p.nchunks; ++c) tot += p.chunk_counts[(size_t)c * p.El + e];
+    for (int c = 0; c < p.nchunks; ++c) tot += cnt(c, e);
     tiles_run += (tot + p.BM - 1) / p.BM;
   }
   int n_tiles = 0;
   int tacc = block_exclusive_scan(tiles_run, wsum, &n_tiles);
   for (int e = e0; e < e0 + per && e < p.El; ++e) {
     int tot = 0;
-    for (int c = 0; c < p.nchunks; ++c) tot += p.chunk_counts[(size_t)c * p.El + e];
+    for (int c = 0; c < p.nchunks; ++c) tot += cnt(c, e);
     p.tile_base[e] = tacc;
     tacc += (tot + p.BM - 1) / p.BM;
   }
@@ -154,18 +173,22 @@ __global__ __launch_bounds__(kThreads) void scatter_kernel(PermuteParams p) {
     p.n_items[0] = n_tiles * p.items_per_tile1;
     p.n_items[1] = n_tiles * p.items_per_tile2;
   }
-  for (int i = threadIdx.x; i < p.n_counters; i += kThreads) p.counters[i] = 0;
 }
 
 }  // namespace
 
+// A batch of one chunk needs no count launch: the scatter counts for itself.
 hipError_t launch_permute_count(const PermuteParams &p, hipStream_t st) {
+  if (p.nchunks == 1) return hipSuccess;
   hipLaunchKernelGGL(count_kernel, dim3(p.nchunks), dim3(kThreads), 0, st, p);
   return hipGetLastError();
 }
 
 hipError_t launch_permute_scatter(const PermuteParams &p, hipStream_t st) {
-  hipLaunchKernelGGL(scatter_kernel, dim3(p.nchunks), dim3(kThreads), 0, st, p);
+  if (p.nchunks == 1)
+    hipLaunchKernelGGL(scatter_kernel<true>, dim3(1), dim3(kThreads), 0, st, p);
+  else
+    hipLaunchKernelGGL(scatter_kernel<false>, dim3(p.nchunks), dim3(kThreads), 0, st, p);
   return hipGetLastError();
 }
 

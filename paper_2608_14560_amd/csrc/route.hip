@@ -11,22 +11,52 @@
 namespace moe {
 namespace {
 
-// Wave-wide argmax of (value, index) under `beats`, carrying a payload.
-__device__ __forceinline__ void wave_argmax(float &v, int &i, float &pay) {
-#pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) {
-    const float ov = __shfl_xor(v, off);
-    const int oi = __shfl_xor(i, off);
-    const float op = __shfl_xor(pay, off);
-    if (beats(ov, oi, v, i)) {
-      v = ov;
-      i = oi;
-      pay = op;
-    }
-  }
+// Wave-wide argmax under `beats` with DPP: (value, index) is packed into one
+// 64-bit key that orders like `beats` (value bits mapped to an unsigned order,
+// index complemented so that the lower index wins a tie), reduced with
+// row_shr 1/2/4/8 inside each 16-lane row and row_bcast 15/31 across rows,
+// and read back from lane 63.  Returns the winner's index; every lane gets it.
+__device__ __forceinline__ uint32_t ordered_bits(float v) {
+  const uint32_t u = __float_as_uint(v);
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
+template <int CTRL, int ROW_MASK>
+__device__ __forceinline__ void dpp_max_step(uint32_t &hi, uint32_t &lo) {
+  // lanes whose DPP source is outside the row (or not selected) see key 0,
+  // which no packed key of a real score undercuts
+  const uint32_t nh = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)hi, CTRL, ROW_MASK, 0xf, false);
+  const uint32_t nl = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)lo, CTRL, ROW_MASK, 0xf, false);
+  const bool take = nh > hi || (nh == hi && nl > lo);
+  hi = take ? nh : hi;
+  lo = take ? nl : lo;
+}
+
+__device__ __forceinline__ int wave_argmax(float v, int idx) {
+  uint32_t hi = ordered_bits(v);
+  uint32_t lo = ~(uint32_t)idx;
+  dpp_max_step<0x111, 0xf>(hi, lo);  // row_shr:1
+  dpp_max_step<0x112, 0xf>(hi, lo);  // row_shr:2
+  dpp_max_step<0x114, 0xf>(hi, lo);  // row_shr:4
+  dpp_max_step<0x118, 0xf>(hi, lo);  // row_shr:8
+  dpp_max_step<0x142, 0xa>(hi, lo);  // row_bcast:15 into rows 1 and 3
+  dpp_max_step<0x143, 0xc>(hi, lo);  // row_bcast:31 into rows 2 and 3
+  return (int)~(uint32_t)__builtin_amdgcn_readlane((int)lo, 63);
 }
 
 constexpr int kNoIdx = 0x7fffffff;
+
+// Value of expert `e` (wave-uniform) from the per-lane slots: lane e % 64,
+// slot e / 64.
+template <int EPL>
+__device__ __forceinline__ float key_of(const float (&v)[EPL], int e) {
+  const int slot = e / kWave, src = e % kWave;
+  float x = v[0];
+#pragma unroll
+  for (int q = 1; q < EPL; ++q)
+    if (q == slot) x = v[q];
+  return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, x), src));
+}
 
 // EPL = experts held per lane (expert e lives in lane e % 64, slot e / 64).
 template <int EPL>
@@ -54,7 +84,7 @@ __global__ __launch_bounds__(256) void route_kernel(RouteParams p) {
   // group score = sum of the two largest keys of the group
   float my_gs = -INFINITY;  // lane g keeps the score of group g
   for (int g = 0; g < p.G; ++g) {
-    float v1 = -INFINITY, v2 = -INFINITY, dummy = 0.0f;
+    float v1 = -INFINITY, v2 = -INFINITY;
     int i1 = kNoIdx, i2 = kNoIdx;
 #pragma unroll
     for (int q = 0; q < EPL; ++q) {
@@ -68,14 +98,14 @@ __global__ __launch_bounds__(256) void route_kernel(RouteParams p) {
         }
       }
     }
-    // best of the group
-    float bv = v1, bp = 0.0f;
-    int bi = i1;
-    wave_argmax(bv, bi, bp);
-    // second best: the lane that held the best offers its runner-up instead
-    float sv = (i1 == bi) ? v2 : v1;
-    int si = (i1 == bi) ? i2 : i1;
-    wave_argmax(sv, si, dummy);
+    // best of the group, then the second best: the lane that held the best
+    // offers its runner-up instead
+    const int bi = wave_argmax(v1, i1);
+    const bool had = (i1 == bi);
+    const int si = wave_argmax(had ? v2 : v1, had ? i2 : i1);
+    // both values live in known lanes/slots: fetch them by index
+    const float bv = key_of(key, bi);
+    const float sv = key_of(key, si);
     const float gs = bv + sv;
     if (lane == g) my_gs = gs;
   }
@@ -84,23 +114,23 @@ __global__ __launch_bounds__(256) void route_kernel(RouteParams p) {
   // topk_group groups beat it
   int rank = 0;
   for (int g = 0; g < p.G; ++g) {
-    const float og = __shfl(my_gs, g);
+    const float og = __builtin_bit_cast(
+        float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, my_gs), g));
     if (lane < p.G && g != lane && beats(og, g, my_gs, lane)) ++rank;
   }
-  const int kept_lane = (lane < p.G && rank < p.TG) ? 1 : 0;
+  const uint64_t kept = __ballot(lane < p.G && rank < p.TG);
   bool cand[EPL];
 #pragma unroll
   for (int q = 0; q < EPL; ++q) {
     const int e = q * kWave + lane;
-    const int g = (e < p.E) ? e / gsz : 0;
-    cand[q] = (e < p.E) && (__shfl(kept_lane, g) != 0);
+    cand[q] = (e < p.E) && ((kept >> (e / gsz)) & 1ull);
   }
 
   // top-k experts among the kept groups, in selection order
   int my_id = 0;
   float my_s = 0.0f;
   for (int j = 0; j < p.K; ++j) {
-    float bv = -INFINITY, bs = 0.0f;
+    float bv = -INFINITY;
     int bi = kNoIdx;
 #pragma unroll
     for (int q = 0; q < EPL; ++q) {
@@ -108,23 +138,24 @@ __global__ __launch_bounds__(256) void route_kernel(RouteParams p) {
       if (cand[q] && beats(key[q], e, bv, bi)) {
         bv = key[q];
         bi = e;
-        bs = sc[q];
       }
     }
-    wave_argmax(bv, bi, bs);
+    const int win = wave_argmax(bv, bi);
 #pragma unroll
     for (int q = 0; q < EPL; ++q)
-      if (q * kWave + lane == bi) cand[q] = false;
+      if (q * kWave + lane == win) cand[q] = false;
+    const float ws = key_of(sc, win);
     if (lane == j) {
-      my_id = bi;
-      my_s = bs;
+      my_id = win;
+      my_s = ws;
     }
   }
 
   // weights: unbiased scores normalised over the k selections (summed in
   // selection order), times the routed scaling factor
   float sum = 0.0f;
-  for (int j = 0; j < p.K; ++j) sum += __shfl(my_s, j);
+  for (int j = 0; j < p.K; ++j)
+    sum += __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, my_s), j));
   if (lane < p.K) {
     p.topk_ids[(size_t)t * p.K + lane] = my_id;
     p.topk_w[(size_t)t * p.K + lane] = (my_s / sum) * p.rsf;

@@ -40,7 +40,7 @@ def test_every_declared_symbol_is_exported(M):
 
 
 def test_stage_names(M):
-    assert M.num_stages() == 6
+    assert M.num_stages() == 7
     assert M.stage_names()[3].startswith("gemm1")
 
 
