@@ -74,8 +74,9 @@ Plan make_plan(const moe_shape_t *s) {
   // codes), so it never splits K; GEMM2 could (S2 > 1 sums the halves in the
   // combine) but the small-tile kernel already has enough work items.
   p.S1 = 1;
-  // small-tile batches: GEMM1 split over 32-column groups, GEMM2 over K halves
-  p.narrow1 = p.BM == 16;
+  // small-tile batches: GEMM1 split over 32-column groups when the batch is
+  // too small to give every CU a 128-column item, GEMM2 over K halves
+  p.narrow1 = p.BM == 16 && TK <= 1024;
   p.S2 = p.BM == 16 ? 2 : 1;
   p.NB1 = p.narrow1 ? s->I / gemm1_narrow_cols() : s->I / 128;
   // GEMM2 column blocks: 128 wide for the small-tile kernel, 256 otherwise

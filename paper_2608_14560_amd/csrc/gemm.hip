@@ -295,12 +295,15 @@ struct Stream {
   static constexpr int kCols = 128;  // columns of the block per work item
 };
 
-template <bool G1, int D>
+// ALDS: the item's whole A tile (16 rows x its K range) is staged in LDS once
+// (rows padded by 16 bytes) instead of every wave loading it from L2 at each
+// K step; used when the tile fits (GEMM2 at small batches).
+template <bool G1, int D, bool ALDS>
 __global__ __launch_bounds__(Stream<G1>::kWaves * kWave) void gemm_stream_kernel(GemmParams p) {
   constexpr int NW = Stream<G1>::kWaves;
   __shared__ int tb[1028];
   __shared__ float amax_lds[NW][16];
-  extern __shared__ __attribute__((aligned(16))) float scales[];  // sa[16][KB], sb[2][KB]
+  extern __shared__ __attribute__((aligned(16))) float scales[];  // sa[16][KB], sb[2][KB], A tile
 
   const int tid = threadIdx.x;
   const int lane = tid & (kWave - 1);
@@ -380,10 +383,25 @@ __global__ __launch_bounds__(Stream<G1>::kWaves * kWave) void gemm_stream_kernel
   const uint8_t *b_ptr0 = Bexp + (size_t)brow0 * K + frag_off;
   const uint8_t *b_ptr1 = Bexp + (size_t)brow1 * K + frag_off;
 
+  // A tile in LDS: row r, K step kb -> a_l + r * astride + (kb - kb0) * 128
+  uint8_t *a_l = reinterpret_cast<uint8_t *>(scales) + ((18 * KB * 4 + 15) & ~15);
+  const int astride = n * 128 + 16;
+  if (ALDS) {
+    const int chunks = 16 * n * 8;  // 16-byte chunks
+    for (int c = tid; c < chunks; c += NW * kWave) {
+      const int r = c / (n * 8), off = (c % (n * 8)) * 16;
+      const int rr = min(r, nrows - 1);
+      const int src = G1 ? p.perm_token[row0 + rr] : row0 + rr;
+      *reinterpret_cast<u32x4 *>(a_l + r * astride + off) =
+          *reinterpret_cast<const u32x4 *>(p.A + (size_t)src * K + (size_t)kb0 * 128 + off);
+    }
+  }
+  const uint8_t *a_lds = a_l + r16 * astride + frag_off;
+
   v8i ra[D], rb0[D], rb1[D];
 #define MOE_SLOAD(d, kb)                                                  \
   do {                                                                    \
-    ra[d] = *reinterpret_cast<const v8i *>(a_ptr + (size_t)(kb) * 128);   \
+    if (!ALDS) ra[d] = *reinterpret_cast<const v8i *>(a_ptr + (size_t)(kb) * 128); \
     rb0[d] = *reinterpret_cast<const v8i *>(b_ptr0 + (size_t)(kb) * 128); \
     rb1[d] = *reinterpret_cast<const v8i *>(b_ptr1 + (size_t)(kb) * 128); \
   } while (0)
@@ -402,8 +420,9 @@ __global__ __launch_bounds__(Stream<G1>::kWaves * kWave) void gemm_stream_kernel
       if (it < n) {
         const int kb = kb0 + it;
         const v4f z = {0.f, 0.f, 0.f, 0.f};
-        const v4f t0 = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(ra[d], rb0[d], z, 0, 0, 0, 0, 0, 0);
-        const v4f t1 = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(ra[d], rb1[d], z, 0, 0, 0, 0, 0, 0);
+        const v8i af = ALDS ? lds_frag(a_lds + it * 128) : ra[d];
+        const v4f t0 = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(af, rb0[d], z, 0, 0, 0, 0, 0, 0);
+        const v4f t1 = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(af, rb1[d], z, 0, 0, 0, 0, 0, 0);
         const float s0 = sb_l[kb], s1 = sb_l[sb1_off + kb];
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
@@ -662,9 +681,18 @@ hipError_t launch_gemm(const GemmParams &p, int BM, int grid, hipStream_t st) {
   if (grid <= 0) return hipSuccess;
   switch (BM) {
     case 16: {
-      const size_t lds = sizeof(float) * 18 * (size_t)p.KB;
-      hipLaunchKernelGGL((gemm_stream_kernel<G1, kStreamDepth>), dim3(grid),
-                         dim3(Stream<G1>::kWaves * kWave), lds, st, p);
+      // the A tile of one item (16 rows x its K range) goes to LDS when it is
+      // at most 32 KB (GEMM2 at small batches)
+      const int n_max = (p.KB + p.S - 1) / p.S;
+      const size_t a_bytes = 16 * ((size_t)n_max * 128 + 16);
+      const bool alds = !G1 && a_bytes <= 32768 + 256;
+      const size_t lds = ((sizeof(float) * 18 * (size_t)p.KB + 15) & ~(size_t)15) + (alds ? a_bytes : 0);
+      if (alds)
+        hipLaunchKernelGGL((gemm_stream_kernel<G1, kStreamDepth, true>), dim3(grid),
+                           dim3(Stream<G1>::kWaves * kWave), lds, st, p);
+      else
+        hipLaunchKernelGGL((gemm_stream_kernel<G1, kStreamDepth, false>), dim3(grid),
+                           dim3(Stream<G1>::kWaves * kWave), lds, st, p);
       return hipGetLastError();
     }
     case 32: return launch_gemm_bm<32, G1>(p, grid, st);

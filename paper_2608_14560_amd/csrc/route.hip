@@ -59,13 +59,17 @@ __device__ __forceinline__ float key_of(const float (&v)[EPL], int e) {
 }
 
 // EPL = experts held per lane (expert e lives in lane e % 64, slot e / 64).
-template <int EPL>
+// GC = number of groups when known at compile time (its group reductions are
+// then independent chains the compiler interleaves), 0 for a runtime count.
+template <int EPL, int GC>
 __global__ __launch_bounds__(256) void route_kernel(RouteParams p) {
+  constexpr int GMAX = GC > 0 ? GC : 64;
+  const int G = GC > 0 ? GC : p.G;
   const int lane = threadIdx.x & (kWave - 1);
   const int t = blockIdx.x * (blockDim.x / kWave) + (threadIdx.x / kWave);
   if (t >= p.T) return;  // whole wave leaves; the kernel has no block barrier
 
-  const int gsz = p.E / p.G;
+  const int gsz = p.E / G;
   const float *lrow = p.logits + (size_t)t * p.E;
 
   float sc[EPL], key[EPL];
@@ -83,42 +87,74 @@ __global__ __launch_bounds__(256) void route_kernel(RouteParams p) {
 
   // group score = sum of the two largest keys of the group
   float my_gs = -INFINITY;  // lane g keeps the score of group g
-  for (int g = 0; g < p.G; ++g) {
-    float v1 = -INFINITY, v2 = -INFINITY;
-    int i1 = kNoIdx, i2 = kNoIdx;
+  if (GC > 0) {
+    float v1[GMAX], v2[GMAX];
+    int i1[GMAX], i2[GMAX];
 #pragma unroll
-    for (int q = 0; q < EPL; ++q) {
-      const int e = q * kWave + lane;
-      if (e < p.E && e / gsz == g) {
-        if (beats(key[q], e, v1, i1)) {
-          v2 = v1; i2 = i1;
-          v1 = key[q]; i1 = e;
-        } else if (beats(key[q], e, v2, i2)) {
-          v2 = key[q]; i2 = e;
+    for (int g = 0; g < GMAX; ++g) {
+      v1[g] = v2[g] = -INFINITY;
+      i1[g] = i2[g] = kNoIdx;
+#pragma unroll
+      for (int q = 0; q < EPL; ++q) {
+        const int e = q * kWave + lane;
+        if (e < p.E && e / gsz == g) {
+          if (beats(key[q], e, v1[g], i1[g])) {
+            v2[g] = v1[g]; i2[g] = i1[g];
+            v1[g] = key[q]; i1[g] = e;
+          } else if (beats(key[q], e, v2[g], i2[g])) {
+            v2[g] = key[q]; i2[g] = e;
+          }
         }
       }
     }
-    // best of the group, then the second best: the lane that held the best
-    // offers its runner-up instead
-    const int bi = wave_argmax(v1, i1);
-    const bool had = (i1 == bi);
-    const int si = wave_argmax(had ? v2 : v1, had ? i2 : i1);
-    // both values live in known lanes/slots: fetch them by index
-    const float bv = key_of(key, bi);
-    const float sv = key_of(key, si);
-    const float gs = bv + sv;
-    if (lane == g) my_gs = gs;
+    int b[GMAX];
+#pragma unroll
+    for (int g = 0; g < GMAX; ++g) b[g] = wave_argmax(v1[g], i1[g]);
+#pragma unroll
+    for (int g = 0; g < GMAX; ++g) {
+      const bool had = (i1[g] == b[g]);
+      const int si = wave_argmax(had ? v2[g] : v1[g], had ? i2[g] : i1[g]);
+      const float gs = key_of(key, b[g]) + key_of(key, si);
+      if (lane == g) my_gs = gs;
+    }
+  } else {
+    for (int g = 0; g < G; ++g) {
+      float v1 = -INFINITY, v2 = -INFINITY;
+      int i1 = kNoIdx, i2 = kNoIdx;
+#pragma unroll
+      for (int q = 0; q < EPL; ++q) {
+        const int e = q * kWave + lane;
+        if (e < p.E && e / gsz == g) {
+          if (beats(key[q], e, v1, i1)) {
+            v2 = v1; i2 = i1;
+            v1 = key[q]; i1 = e;
+          } else if (beats(key[q], e, v2, i2)) {
+            v2 = key[q]; i2 = e;
+          }
+        }
+      }
+      // best of the group, then the second best: the lane that held the best
+      // offers its runner-up instead
+      const int bi = wave_argmax(v1, i1);
+      const bool had = (i1 == bi);
+      const int si = wave_argmax(had ? v2 : v1, had ? i2 : i1);
+      const float gs = key_of(key, bi) + key_of(key, si);
+      if (lane == g) my_gs = gs;
+    }
   }
 
   // keep the topk_group best groups: a group is kept when fewer than
   // topk_group groups beat it
   int rank = 0;
-  for (int g = 0; g < p.G; ++g) {
-    const float og = __builtin_bit_cast(
-        float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, my_gs), g));
-    if (lane < p.G && g != lane && beats(og, g, my_gs, lane)) ++rank;
+#pragma unroll
+  for (int g = 0; g < GMAX; ++g) {
+    if (g < G) {
+      const float og = __builtin_bit_cast(
+          float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, my_gs), g));
+      if (lane < G && g != lane && beats(og, g, my_gs, lane)) ++rank;
+    }
   }
-  const uint64_t kept = __ballot(lane < p.G && rank < p.TG);
+  const uint64_t kept = __ballot(lane < G && rank < p.TG);
   bool cand[EPL];
 #pragma unroll
   for (int q = 0; q < EPL; ++q) {
@@ -162,6 +198,173 @@ __global__ __launch_bounds__(256) void route_kernel(RouteParams p) {
   }
 }
 
+// ---------------------------------------------------------------------------
+// Fast path for groups of S = E/G experts, S a power of two dividing 64: the
+// experts of a group then sit in S consecutive lanes of one slot, and one
+// segmented DPP pass (row_shr 1/2/4/8 masked to the segment, row_bcast 15/31
+// for 32- and 64-lane segments) leaves every group's best and runner-up keys
+// in the last lane of its segment -- all groups and slots at once instead of
+// 2*G wave-wide reductions.  Keys travel as 64-bit ordered words (value bits,
+// complemented index) so that every comparison is the `beats` order.
+// ---------------------------------------------------------------------------
+struct Key2 {  // best (a) and runner-up (b)
+  uint32_t ah, al, bh, bl;
+};
+
+__device__ __forceinline__ bool key_gt(uint32_t h1, uint32_t l1, uint32_t h0, uint32_t l0) {
+  return h1 > h0 || (h1 == h0 && l1 > l0);
+}
+
+// merge a neighbour's top-2 (n) into k; `ok` false discards the neighbour
+__device__ __forceinline__ void key2_merge(Key2 &k, const Key2 &n, bool ok) {
+  const bool nw = ok && key_gt(n.ah, n.al, k.ah, k.al);
+  // runner-up candidates: the loser of the two bests, and the winner's own second
+  const uint32_t ch = nw ? k.ah : k.bh, cl = nw ? k.al : k.bl;
+  const uint32_t dh = nw ? n.bh : (ok ? n.ah : 0u), dl = nw ? n.bl : (ok ? n.al : 0u);
+  const bool dw = key_gt(dh, dl, ch, cl);
+  k.ah = nw ? n.ah : k.ah;
+  k.al = nw ? n.al : k.al;
+  k.bh = dw ? dh : ch;
+  k.bl = dw ? dl : cl;
+}
+
+template <int CTRL, int ROW_MASK>
+__device__ __forceinline__ Key2 key2_dpp(const Key2 &k) {
+  Key2 n;
+  n.ah = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)k.ah, CTRL, ROW_MASK, 0xf, false);
+  n.al = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)k.al, CTRL, ROW_MASK, 0xf, false);
+  n.bh = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)k.bh, CTRL, ROW_MASK, 0xf, false);
+  n.bl = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)k.bl, CTRL, ROW_MASK, 0xf, false);
+  return n;
+}
+
+__device__ __forceinline__ float key_value(uint32_t h) {
+  const uint32_t u = (h & 0x80000000u) ? (h & 0x7fffffffu) : ~h;
+  return __uint_as_float(u);
+}
+
+template <int EPL, int S>
+__global__ __launch_bounds__(256) void route_seg_kernel(RouteParams p) {
+  const int lane = threadIdx.x & (kWave - 1);
+  const int t = blockIdx.x * (blockDim.x / kWave) + (threadIdx.x / kWave);
+  if (t >= p.T) return;
+  const float *lrow = p.logits + (size_t)t * p.E;
+  const int seg_lane = lane & (S - 1);
+
+  float sc[EPL], key[EPL];
+  Key2 k2[EPL];
+#pragma unroll
+  for (int q = 0; q < EPL; ++q) {
+    const int e = q * kWave + lane;
+    const bool v = e < p.E;
+    sc[q] = v ? sigmoid_spec(lrow[e]) : 0.0f;
+    key[q] = v ? sc[q] + p.bias[e] : -INFINITY;
+    k2[q].ah = v ? ordered_bits(key[q]) : 0u;
+    k2[q].al = ~(uint32_t)e;
+    k2[q].bh = 0u;
+    k2[q].bl = 0u;
+  }
+  // segmented top-2: after the steps the last lane of each segment holds its
+  // group's best and runner-up
+#pragma unroll
+  for (int q = 0; q < EPL; ++q) {
+    if (S >= 2) key2_merge(k2[q], key2_dpp<0x111, 0xf>(k2[q]), seg_lane >= 1);
+    if (S >= 4) key2_merge(k2[q], key2_dpp<0x112, 0xf>(k2[q]), seg_lane >= 2);
+    if (S >= 8) key2_merge(k2[q], key2_dpp<0x114, 0xf>(k2[q]), seg_lane >= 4);
+    if (S >= 16) key2_merge(k2[q], key2_dpp<0x118, 0xf>(k2[q]), seg_lane >= 8);
+    if (S >= 32) key2_merge(k2[q], key2_dpp<0x142, 0xa>(k2[q]), seg_lane >= 16);
+    if (S >= 64) key2_merge(k2[q], key2_dpp<0x143, 0xc>(k2[q]), seg_lane >= 32);
+  }
+  // group score of the segment ending in this lane
+  float seg_gs[EPL];
+#pragma unroll
+  for (int q = 0; q < EPL; ++q) seg_gs[q] = key_value(k2[q].ah) + key_value(k2[q].bh);
+
+  // lane g collects the score of group g (group g = slot * 64/S + segment)
+  constexpr int SEGS = kWave / S;
+  const int G = p.G;
+  float my_gs = -INFINITY;
+#pragma unroll
+  for (int q = 0; q < EPL; ++q) {
+#pragma unroll
+    for (int sg = 0; sg < SEGS; ++sg) {
+      const int g = q * SEGS + sg;
+      if (g < G) {
+        const float v = __builtin_bit_cast(
+            float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, seg_gs[q]), sg * S + S - 1));
+        my_gs = (lane == g) ? v : my_gs;
+      }
+    }
+  }
+  int rank = 0;
+  for (int g = 0; g < G; ++g) {
+    const float og = __builtin_bit_cast(
+        float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, my_gs), g));
+    rank += (lane < G && g != lane && beats(og, g, my_gs, lane)) ? 1 : 0;
+  }
+  const uint64_t kept = __ballot(lane < G && rank < p.TG);
+  bool cand[EPL];
+#pragma unroll
+  for (int q = 0; q < EPL; ++q) {
+    const int e = q * kWave + lane;
+    cand[q] = (e < p.E) && ((kept >> (e / S)) & 1ull);
+  }
+
+  // top-k experts among the kept groups, in selection order
+  int my_id = 0;
+  float my_s = 0.0f;
+  for (int j = 0; j < p.K; ++j) {
+    float bv = -INFINITY;
+    int bi = kNoIdx;
+#pragma unroll
+    for (int q = 0; q < EPL; ++q) {
+      const int e = q * kWave + lane;
+      const bool take = cand[q] && beats(key[q], e, bv, bi);
+      bv = take ? key[q] : bv;
+      bi = take ? e : bi;
+    }
+    const int win = wave_argmax(bv, bi);
+#pragma unroll
+    for (int q = 0; q < EPL; ++q) cand[q] = cand[q] && (q * kWave + lane != win);
+    const float ws = key_of(sc, win);
+    my_id = (lane == j) ? win : my_id;
+    my_s = (lane == j) ? ws : my_s;
+  }
+
+  float sum = 0.0f;
+  for (int j = 0; j < p.K; ++j)
+    sum += __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, my_s), j));
+  if (lane < p.K) {
+    p.topk_ids[(size_t)t * p.K + lane] = my_id;
+    p.topk_w[(size_t)t * p.K + lane] = (my_s / sum) * p.rsf;
+  }
+}
+
+template <int EPL>
+bool launch_route_seg(const RouteParams &p, dim3 grid, dim3 block, hipStream_t st) {
+  const int S = p.E / p.G;
+  if (p.E > kWave && p.E % kWave) return false;
+  switch (S) {
+    case 4: hipLaunchKernelGGL((route_seg_kernel<EPL, 4>), grid, block, 0, st, p); return true;
+    case 8: hipLaunchKernelGGL((route_seg_kernel<EPL, 8>), grid, block, 0, st, p); return true;
+    case 16: hipLaunchKernelGGL((route_seg_kernel<EPL, 16>), grid, block, 0, st, p); return true;
+    case 32: hipLaunchKernelGGL((route_seg_kernel<EPL, 32>), grid, block, 0, st, p); return true;
+    case 64: hipLaunchKernelGGL((route_seg_kernel<EPL, 64>), grid, block, 0, st, p); return true;
+    default: return false;
+  }
+}
+
+template <int EPL>
+void launch_route_epl(const RouteParams &p, dim3 grid, dim3 block, hipStream_t st) {
+  if (launch_route_seg<EPL>(p, grid, block, st)) return;
+  switch (p.G) {
+    case 8: hipLaunchKernelGGL((route_kernel<EPL, 8>), grid, block, 0, st, p); break;
+    case 4: hipLaunchKernelGGL((route_kernel<EPL, 4>), grid, block, 0, st, p); break;
+    case 2: hipLaunchKernelGGL((route_kernel<EPL, 2>), grid, block, 0, st, p); break;
+    default: hipLaunchKernelGGL((route_kernel<EPL, 0>), grid, block, 0, st, p); break;
+  }
+}
+
 }  // namespace
 
 hipError_t launch_route(const RouteParams &p, hipStream_t st) {
@@ -169,15 +372,15 @@ hipError_t launch_route(const RouteParams &p, hipStream_t st) {
   const int waves_per_block = 4;
   dim3 grid((p.T + waves_per_block - 1) / waves_per_block), block(waves_per_block * kWave);
   if (p.E <= 64)
-    hipLaunchKernelGGL(route_kernel<1>, grid, block, 0, st, p);
+    launch_route_epl<1>(p, grid, block, st);
   else if (p.E <= 128)
-    hipLaunchKernelGGL(route_kernel<2>, grid, block, 0, st, p);
+    launch_route_epl<2>(p, grid, block, st);
   else if (p.E <= 256)
-    hipLaunchKernelGGL(route_kernel<4>, grid, block, 0, st, p);
+    launch_route_epl<4>(p, grid, block, st);
   else if (p.E <= 512)
-    hipLaunchKernelGGL(route_kernel<8>, grid, block, 0, st, p);
+    launch_route_epl<8>(p, grid, block, st);
   else
-    hipLaunchKernelGGL(route_kernel<16>, grid, block, 0, st, p);
+    launch_route_epl<16>(p, grid, block, st);
   return hipGetLastError();
 }
 

@@ -122,7 +122,7 @@ def test_mfma_block_rule(M, kind):
 
 
 # ------------------------------------------------------------ routing
-ROUTE_CASES = [("tiny", 0), ("tiny", 1), ("small_ragged", 0), ("small_dense", 0), ("small_many", 0),
+ROUTE_CASES = [("tiny", 0), ("tiny", 1), ("small_ragged", 0), ("small_dense", 0), ("small_g6", 0), ("small_many", 0),
                ("small_many", 3), ("decode", 0), ("decode", 1), ("decode", 2), ("mid", 0), ("mid", 1),
                ("prefill", 0), ("skewed", 0)]
 
@@ -158,7 +158,7 @@ def test_route_ties_bitexact(M):
 
 
 # ------------------------------------------------------------ whole layer
-FULL_CASES = [("tiny", 0), ("small_ragged", 0), ("small_ragged", 1), ("small_dense", 0),
+FULL_CASES = [("tiny", 0), ("small_ragged", 0), ("small_ragged", 1), ("small_dense", 0), ("small_g6", 0),
               ("small_many", 0), ("decode", 0), ("decode", 1), ("mid", 0)]
 
 

@@ -75,6 +75,10 @@ PARITY_CONFIGS: dict[str, MoEConfig] = {
     "small_dense": MoEConfig("small_dense", T=40, H=256, I=256, num_experts=8,
                              num_local_experts=8, local_expert_offset=0, n_group=2,
                              topk_group=2, top_k=8),
+    # a group count the routing kernel has no compile-time variant for
+    "small_g6": MoEConfig("small_g6", T=50, H=256, I=256, num_experts=96,
+                          num_local_experts=24, local_expert_offset=24, n_group=6,
+                          topk_group=3, top_k=6),
     "small_many": MoEConfig("small_many", T=300, H=384, I=256, num_experts=64,
                             num_local_experts=64, local_expert_offset=0, n_group=8,
                             topk_group=4, top_k=8, hot_experts=4),
