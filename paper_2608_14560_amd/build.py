@@ -28,6 +28,7 @@ SOURCES = {
     "route.hip": ["-ffp-contract=off"],
     "permute.hip": [],
     "gemm.hip": [],
+    "gemm_tile.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"],
     "api.cpp": ["-x", "hip"],
 }
 

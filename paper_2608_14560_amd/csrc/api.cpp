@@ -58,6 +58,7 @@ moe_status_t check_shape(const moe_shape_t *s) {
 struct Plan {
   int BM, S1, S2, NB1, NB2, nchunks, max_tiles;
   bool narrow1;  // GEMM1 split over 32-column groups (small batches)
+  bool tile;     // large-tile kernels (BM >= 64)
   int64_t P_max;
   size_t off_ids, off_w, off_offsets, off_perm_token, off_perm_pair, off_pair_row, off_chunk_counts,
       off_tile_base, off_n_items, off_act, off_act_scale, off_abuf, off_Y, total;
@@ -69,7 +70,8 @@ Plan make_plan(const moe_shape_t *s) {
   p.P_max = TK > 0 ? TK : 1;
   // expected rows per resident expert under uniform routing picks the M tile
   const double avg = (double)TK / s->num_experts;
-  p.BM = avg <= 16 ? 16 : (avg <= 48 ? 32 : (avg <= 160 ? 64 : 128));
+  p.BM = avg <= 16 ? 16 : (avg <= 48 ? 32 : (avg <= 96 ? 64 : 128));
+  p.tile = p.BM >= 64;
   // GEMM1 promotes its K blocks in order (its output decides the re-quantised
   // codes), so it never splits K; GEMM2 could (S2 > 1 sums the halves in the
   // combine) but the small-tile kernel already has enough work items.
@@ -234,7 +236,12 @@ moe_status_t fused_impl(const moe_shape_t *s, const uint8_t *hidden, const float
   g1.S = pl.S1;
   mark();
   const int grid1 = round8((int64_t)pl.max_tiles * pl.NB1 * pl.S1);
-  MOE_TRY_HIP(pl.narrow1 ? launch_gemm1_narrow(g1, grid1, st) : launch_gemm1(g1, pl.BM, grid1, st));
+  if (pl.narrow1)
+    MOE_TRY_HIP(launch_gemm1_narrow(g1, grid1, st));
+  else if (pl.tile)
+    MOE_TRY_HIP(launch_gemm_tile(g1, true, pl.BM, grid1, st));
+  else
+    MOE_TRY_HIP(launch_gemm1(g1, pl.BM, grid1, st));
   // the column-split GEMM1 leaves its re-quantisation to a launch of its own
   mark();
   if (pl.narrow1) MOE_TRY_HIP(launch_requant(g1, (int)pl.P_max, st));
@@ -252,7 +259,9 @@ moe_status_t fused_impl(const moe_shape_t *s, const uint8_t *hidden, const float
   g2.NB = pl.NB2;
   g2.S = pl.S2;
   mark();
-  MOE_TRY_HIP(launch_gemm2(g2, pl.BM, round8((int64_t)pl.max_tiles * pl.NB2 * pl.S2), st));
+  const int grid2 = round8((int64_t)pl.max_tiles * pl.NB2 * pl.S2);
+  MOE_TRY_HIP(pl.tile ? launch_gemm_tile(g2, false, pl.BM, grid2, st)
+                      : launch_gemm2(g2, pl.BM, grid2, st));
 
   // weighted combine in slot order, one bf16 rounding per element
   FinalizeParams f{g.Y, r.pair_row, r.w, out, s->T, s->H, s->top_k, pl.S2, (int)pl.P_max};

@@ -1,0 +1,407 @@
+// gemm_tile.hip -- the grouped FP8 GEMMs of stage (3) of the Fused MoE block
+// (paper Section 3.1.1) for batches with many rows per expert (prefill-sized
+// and skewed loads), on CDNA4 FP8 matrix cores.
+//
+// Work item = (M-tile of BM = 16*MT rows of one expert, 256-column block), the
+// whole K range.  Items of one expert are ordered in groups of four column
+// blocks: all M-tiles of a group, column block fastest, so the 32 items that
+// an XCD runs side by side share four weight panels and eight A tiles in that
+// XCD's L2 (workgroup b runs item (b % 8) * ceil(n/8) + b / 8, and workgroups
+// are dispatched round-robin over the 8 XCDs).
+//
+// One workgroup of 4 waves per item, each wave 64 columns x all BM rows:
+//   GEMM1: waves 0/1 own gate columns [0,64) / [64,128) of the 128-wide
+//          intermediate block, waves 2/3 the matching up columns, so a wave's
+//          columns share one 128x128 weight-scale block;
+//   GEMM2: wave w owns output columns [64w, 64w+64) of the 256-wide block.
+// The weight fragments stream from global memory straight into registers
+// through a D-deep ring (loads issued D K-steps ahead, unconditionally, with
+// the K index clamped at the end).  The A tile (rows gathered through
+// perm_token for GEMM1) is shared by the 4 waves: it goes straight from
+// global memory into an S-stage LDS ring (issued S-1 K-steps ahead, no
+// registers), with one barrier per K-step.
+//
+// The weight fragment is the MFMA's first operand and the activation fragment
+// its second, so lane l holds output columns 4*(l/16)+i (i = 0..3) of token
+// row l%16 of each 16x16 sub-tile: one activation scale per lane and sub-tile
+// row block.  Each 128-K step is one v_mfma_f32_16x16x128_f8f6f4 per
+// sub-tile, started from zero and promoted into the fp32 accumulator with
+// one FMA by (activation scale * weight-block scale), in K order -- the same
+// arithmetic as the small-tile kernels (the matrix cores' block sum does not
+// depend on which operand comes first).
+#include "moe_device.h"
+
+namespace moe {
+namespace {
+
+constexpr int kTileThreads = 256;
+constexpr int kTileCols = 256;
+constexpr int kGroupN = 4;     // column blocks per item group
+// LDS operand layout: row-major 128-byte rows with an XOR swizzle (each
+// direct load fetches whole cache lines) or fragment order (see the kernel)
+constexpr bool kRowMajor = true;
+
+template <int MT, int S>
+struct TileLayout {
+  static constexpr int BM = 16 * MT;
+  static constexpr int A_BYTES = BM * 128;              // A tile, fragment order
+  static constexpr int SCL = A_BYTES + 4 * 8192;        // + 4 waves' weight rows
+  static constexpr int STAGE = SCL + 1024;              // + 256 row-scale slots
+  static constexpr int RING = S * STAGE;
+  static constexpr int XCH = 2 * MT * 4 * 4 * kWave * 4;  // GEMM1 up -> gate hand-over
+  static constexpr int MAIN = RING > XCH ? RING : XCH;
+  static size_t bytes(bool g1, int KB) {
+    return (size_t)(g1 ? MAIN : RING) + sizeof(float) * 2 * (size_t)KB;
+  }
+};
+
+typedef __attribute__((address_space(3))) void lds_void;
+
+// Direct global -> LDS loads.  The builtin sits in plain device functions:
+// used inside the kernel template, it keeps the host compilation pass from
+// emitting the kernel's launch stub.
+__device__ __forceinline__ void lds_load16(const void *g, uint8_t *lds) {
+  __builtin_amdgcn_global_load_lds(g, (lds_void *)lds, 16, 0, 0);
+}
+__device__ __forceinline__ void lds_load4(const void *g, uint8_t *lds) {
+  __builtin_amdgcn_global_load_lds(g, (lds_void *)lds, 4, 0, 0);
+}
+
+// LDS reads of the K loop go through restrict-qualified pointers, so after
+// inlining they carry alias-scope metadata.  Without it the compiler cannot
+// tell them from the in-flight direct-to-LDS writes of later stages and waits
+// for every outstanding load (the weight prefetch included) before each read;
+// the K loop's explicit waits and barriers order the accesses instead.
+__device__ __forceinline__ v8i tile_frag(const uint8_t *__restrict__ st, int lo, int hi) {
+  const v4i a = *reinterpret_cast<const v4i *>(st + lo);
+  const v4i b = *reinterpret_cast<const v4i *>(st + hi);
+  return __builtin_shufflevector(a, b, 0, 1, 2, 3, 4, 5, 6, 7);
+}
+__device__ __forceinline__ float4 tile_f4(const float *__restrict__ q) {
+  return *reinterpret_cast<const float4 *>(q);
+}
+__device__ __forceinline__ float tile_f1(const float *__restrict__ q) { return *q; }
+
+template <bool G1, int MT, int S>
+__global__ __launch_bounds__(kTileThreads) void gemm_tile_kernel(GemmParams p) {
+  using L = TileLayout<MT, S>;
+  constexpr int BM = L::BM;
+  static_assert(MT % 4 == 0, "row scales are read four at a time");
+
+  __shared__ int tb[1028];
+  __shared__ float amax_l[2][BM];
+  extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & (kWave - 1);
+  const int wave = tid / kWave;
+  const int r16 = lane & 15;
+  const int g4 = lane >> 4;
+  const int frag_off = g4 * 32;
+
+  const int n_items = *p.n_items;
+  const int per_xcd = (n_items + 7) / 8;
+  const int item = (blockIdx.x & 7) * per_xcd + (blockIdx.x >> 3);
+  if ((int)(blockIdx.x >> 3) >= per_xcd || item >= n_items) return;
+
+  for (int i = tid; i <= p.El; i += kTileThreads) tb[i] = p.tile_base[i];
+  __syncthreads();
+
+  // ---- decode the work item
+  const int NB = p.NB;
+  const int qt = item / NB;
+  int lo = 0, hi = p.El;
+  while (hi - lo > 1) {
+    const int mid = (lo + hi) >> 1;
+    if (tb[mid] <= qt) lo = mid; else hi = mid;
+  }
+  const int e = lo;
+  const int nt_e = tb[e + 1] - tb[e];
+  const int local = item - tb[e] * NB;
+  const int G = (NB + kGroupN - 1) / kGroupN;
+  const int grp = min(local / (kGroupN * nt_e), G - 1);
+  const int wi = local - grp * kGroupN * nt_e;
+  const int gsz = min(kGroupN, NB - kGroupN * grp);
+  const int mt_idx = wi / gsz;
+  const int nb = kGroupN * grp + wi % gsz;
+  const int seg0 = p.expert_offsets[e];
+  const int seg1 = p.expert_offsets[e + 1];
+  const int row0 = seg0 + mt_idx * BM;
+  const int nrows = min(BM, seg1 - row0);
+  const int KB = p.KB;
+  const size_t K = (size_t)p.K;
+
+  // ---- this wave's weight rows and scale blocks
+  const int half = wave >> 1;  // GEMM1: 0 gate, 1 up.  GEMM2: 128-column half
+  int wrow0, nblk0, nblk1;
+  if (G1) {
+    wrow0 = half * p.I + nb * 128 + 64 * (wave & 1);
+    nblk0 = nb;
+    nblk1 = p.I / 128 + nb;
+  } else {
+    wrow0 = nb * kTileCols + 64 * wave;
+    nblk0 = min(2 * nb, p.N_total / 128 - 1);
+    nblk1 = min(2 * nb + 1, p.N_total / 128 - 1);
+  }
+
+  // weight-block scales of the whole K range: sb_l[0][kb] (waves 0/1), sb_l[1][kb]
+  float *sb_l = reinterpret_cast<float *>(smem + (G1 ? L::MAIN : L::RING));
+  {
+    const float *s0 = p.B_scale + ((size_t)e * (p.N_total / 128) + nblk0) * KB;
+    const float *s1 = p.B_scale + ((size_t)e * (p.N_total / 128) + nblk1) * KB;
+    for (int i = tid; i < KB; i += kTileThreads) {
+      sb_l[i] = s0[i];
+      sb_l[KB + i] = s1[i];
+    }
+  }
+  const float *sb_w = sb_l + half * KB;
+  __syncthreads();
+
+  // ---- operand staging: every K-step's A tile, row scales and weight rows
+  // go straight from global memory into an S-stage LDS ring (no registers),
+  // issued S-1 K-steps ahead.  Both operands are laid out in fragment order:
+  // a 16x128-byte fragment is two 1 KB halves, lane l's 16 bytes of half h at
+  // 16 l, holding row l % 16, bytes 32 (l / 16) + 16 h of the K block -- the
+  // bytes an MFMA operand register pair of lane l needs -- so a wave-wide
+  // 16-byte direct load fills one half and every fragment read is a
+  // contiguous 1 KB LDS read.
+  //   A: fragment m (rows 16m..16m+15) at m * 2 KB, shared by the 4 waves;
+  //      wave w loads halves q = 4w..4w+3 of BM/16 fragments (JW per wave).
+  //   B: wave-private, fragment n of wave w at A_BYTES + w * 8 KB + n * 2 KB.
+  //   row scales: slot s = (row % 16) * MT + row / 16 at SCL; lane L of wave w
+  //      loads slot 64 w + L (slots >= BM are loaded but never read).
+  constexpr int JW = BM / 32;  // A loads per wave and K-step
+  const uint8_t *a_src[JW];
+#pragma unroll
+  for (int j = 0; j < JW; ++j) {
+    const int q = wave * JW + j;
+    int r, off;
+    if (kRowMajor) {  // 8 rows of whole 128-byte lines per load, chunk c in slot c ^ f(r)
+      r = 8 * q + (lane >> 3);
+      off = 16 * ((lane & 7) ^ ((r >> 1) & 7));
+    } else {          // one half of fragment q / 2
+      r = 16 * (q >> 1) + r16;
+      off = frag_off + 16 * (q & 1);
+    }
+    const int rr = min(r, nrows - 1);  // ragged tail: repeat the last row
+    const int src = G1 ? p.perm_token[row0 + rr] : row0 + rr;
+    a_src[j] = p.A + (size_t)src * K + off;
+  }
+  const uint8_t *Bexp = p.B + (size_t)e * p.N_total * K;
+  const uint8_t *b_src[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    int r, off;
+    if (kRowMajor) {
+      r = 8 * i + (lane >> 3);
+      off = 16 * ((lane & 7) ^ ((r >> 1) & 7));
+    } else {
+      r = 16 * (i >> 1) + r16;
+      off = frag_off + 16 * (i & 1);
+    }
+    r = min(wrow0 + r, p.N_total - 1);  // ragged last GEMM2 block
+    b_src[i] = Bexp + (size_t)r * K + off;
+  }
+  const float *s_src;
+  {
+    const int sl = 64 * wave + lane;
+    const int r = sl < BM ? 16 * (sl % MT) + sl / MT : nrows - 1;
+    const int rr = min(r, nrows - 1);
+    s_src = p.A_scale + (size_t)(G1 ? p.perm_token[row0 + rr] : row0 + rr) * KB;
+  }
+
+  // this lane's two 16-byte pieces of a fragment (rows 16m + r16) in the stage
+  const int fr = (r16 >> 1) & 7;
+  const int rd_lo = kRowMajor ? r16 * 128 + 16 * ((2 * g4) ^ fr) : 16 * lane;
+  const int rd_hi = kRowMajor ? r16 * 128 + 16 * ((2 * g4 + 1) ^ fr) : 1024 + 16 * lane;
+
+  v4f acc[MT][4];
+#pragma unroll
+  for (int m = 0; m < MT; ++m)
+#pragma unroll
+    for (int n = 0; n < 4; ++n) acc[m][n] = v4f{0.f, 0.f, 0.f, 0.f};
+
+  // Each K-step every wave issues one group of kGroup direct loads.  At the
+  // end of step `it` stage it+1 must have landed: its group was issued S-2
+  // steps earlier, so at most (S-2) groups may still be outstanding.
+  constexpr int kGroup = JW + 8 + 1;
+  constexpr int kWait = (S - 2) * kGroup;
+  static_assert(kWait < 64, "vmcnt holds 6 bits");
+  static_assert(S >= 2, "A ring depth");
+
+#define TILE_STAGE(st) (smem + (st) * L::STAGE)
+#define TILE_DMA(st, kb)                                                                \
+  do {                                                                                  \
+    uint8_t *d_ = TILE_STAGE(st);                                                       \
+    const size_t ko_ = (size_t)(kb) * 128;                                              \
+    _Pragma("unroll") for (int j = 0; j < JW; ++j)                                      \
+        lds_load16(a_src[j] + ko_, d_ + (wave * JW + j) * 1024);                        \
+    _Pragma("unroll") for (int i = 0; i < 8; ++i)                                       \
+        lds_load16(b_src[i] + ko_, d_ + L::A_BYTES + wave * 8192 + i * 1024);          \
+    lds_load4(s_src + (kb), d_ + L::SCL + wave * 256);                                  \
+  } while (0)
+#define TILE_COMPUTE(st, kb)                                                            \
+  do {                                                                                  \
+    const uint8_t *as_ = TILE_STAGE(st);                                                \
+    const uint8_t *bs_ = as_ + L::A_BYTES + wave * 8192;                                \
+    const float *sa_ = reinterpret_cast<const float *>(as_ + L::SCL) + r16 * MT;        \
+    const float sbv_ = tile_f1(sb_w + (kb));                                            \
+    float sav_[MT];                                                                     \
+    _Pragma("unroll") for (int q_ = 0; q_ < MT / 4; ++q_) {                             \
+      const float4 v_ = tile_f4(sa_ + 4 * q_);                                          \
+      sav_[4 * q_ + 0] = v_.x;                                                          \
+      sav_[4 * q_ + 1] = v_.y;                                                          \
+      sav_[4 * q_ + 2] = v_.z;                                                          \
+      sav_[4 * q_ + 3] = v_.w;                                                          \
+    }                                                                                   \
+    v8i bf_[4];                                                                         \
+    _Pragma("unroll") for (int n = 0; n < 4; ++n) bf_[n] =                              \
+        tile_frag(bs_ + n * 2048, rd_lo, rd_hi);                                        \
+    v8i an_ = tile_frag(as_, rd_lo, rd_hi);                                             \
+    _Pragma("unroll") for (int m = 0; m < MT; ++m) {                                    \
+      const v8i af_ = an_;                                                              \
+      if (m + 1 < MT) an_ = tile_frag(as_ + (m + 1) * 2048, rd_lo, rd_hi);              \
+      const float c_ = sav_[m] * sbv_;                                                  \
+      const v4f z_ = {0.f, 0.f, 0.f, 0.f};                                              \
+      v4f t_[4];                                                                        \
+      _Pragma("unroll") for (int n = 0; n < 4; ++n) t_[n] =                             \
+          __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(bf_[n], af_, z_, 0, 0, 0,    \
+                                                           0, 0, 0);                    \
+      _Pragma("unroll") for (int n = 0; n < 4; ++n)                                     \
+          _Pragma("unroll") for (int i = 0; i < 4; ++i)                                 \
+              acc[m][n][i] = __builtin_fmaf(t_[n][i], c_, acc[m][n][i]);               \
+      __builtin_amdgcn_sched_barrier(0);                                                \
+    }                                                                                   \
+  } while (0)
+
+  // prologue: stages 0 .. S-2 in flight, wait for stage 0.  The barriers are
+  // plain s_barrier after an explicit vmcnt wait: the generic workgroup
+  // barrier would wait for every outstanding load.
+#pragma unroll
+  for (int st = 0; st < S - 1; ++st) {
+    TILE_DMA(st, min(st, KB - 1));
+    __builtin_amdgcn_sched_barrier(0);
+  }
+  asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(kWait) : "memory");
+
+  int st_rd = 0, st_ld = S - 1;
+  for (int it = 0; it < KB; ++it) {
+    TILE_DMA(st_ld, min(it + S - 1, KB - 1));
+    __builtin_amdgcn_sched_barrier(0);
+    TILE_COMPUTE(st_rd, it);
+    __builtin_amdgcn_sched_barrier(0);
+    asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(kWait) : "memory");
+    st_rd = st_rd + 1 == S ? 0 : st_rd + 1;
+    st_ld = st_ld + 1 == S ? 0 : st_ld + 1;
+  }
+  // the last steps' (clamped) loads may still be landing in the ring, which
+  // the GEMM1 epilogue reuses
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  __syncthreads();
+
+#undef TILE_COMPUTE
+#undef TILE_DMA
+#undef TILE_STAGE
+
+  // accumulator element (m, n, i) of this lane: row 16m + r16, column
+  // 16n + 4*g4 + i of the wave's 64 columns
+  if (!G1) {
+    if (wrow0 >= p.N_total) return;  // columns past H (ragged last block)
+    float *Ys = p.Y;
+#pragma unroll
+    for (int m = 0; m < MT; ++m) {
+      const int r = 16 * m + r16;
+      if (r < nrows) {
+        float *yrow = Ys + (size_t)(row0 + r) * p.H + wrow0 + 4 * g4;
+#pragma unroll
+        for (int n = 0; n < 4; ++n) *reinterpret_cast<v4f *>(yrow + 16 * n) = acc[m][n];
+      }
+    }
+    return;
+  }
+
+  // SwiGLU: the up waves hand their accumulators to the gate waves through
+  // LDS (lane-private slots), the gate waves apply silu(gate) * up.
+  float *xch = reinterpret_cast<float *>(smem);
+  if (wave >= 2) {
+#pragma unroll
+    for (int m = 0; m < MT; ++m)
+#pragma unroll
+      for (int n = 0; n < 4; ++n)
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          xch[((((wave - 2) * MT + m) * 4 + n) * 4 + i) * kWave + lane] = acc[m][n][i];
+  }
+  __syncthreads();
+  if (wave < 2) {
+#pragma unroll
+    for (int m = 0; m < MT; ++m) {
+      float mx = 0.0f;
+#pragma unroll
+      for (int n = 0; n < 4; ++n)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const float u = xch[(((wave * MT + m) * 4 + n) * 4 + i) * kWave + lane];
+          acc[m][n][i] = swiglu_spec(acc[m][n][i], u);
+          mx = fmaxf(mx, fabsf(acc[m][n][i]));
+        }
+      // the row's 64 columns of this wave sit in lanes r16, r16+16, r16+32, r16+48
+      mx = fmaxf(mx, __shfl_xor(mx, 16));
+      mx = fmaxf(mx, __shfl_xor(mx, 32));
+      if (g4 == 0) amax_l[wave][16 * m + r16] = mx;
+    }
+  }
+  __syncthreads();
+  if (wave >= 2) return;
+  const int IB = p.I / 128;
+#pragma unroll
+  for (int m = 0; m < MT; ++m) {
+    const int r = 16 * m + r16;
+    const float amax = fmaxf(amax_l[0][r], amax_l[1][r]);
+    const float scale = (amax > 0.0f) ? amax / 448.0f : 1.0f;
+    if (r < nrows) {
+      uint8_t *arow = p.act + (size_t)(row0 + r) * p.I + nb * 128 + 64 * wave + 4 * g4;
+#pragma unroll
+      for (int n = 0; n < 4; ++n) {
+        uint32_t q = 0u;
+        if (amax > 0.0f)
+          q = e4m3x2_rne_sat(acc[m][n][0] / scale, acc[m][n][1] / scale) |
+              (e4m3x2_rne_sat(acc[m][n][2] / scale, acc[m][n][3] / scale) << 16);
+        *reinterpret_cast<uint32_t *>(arow + 16 * n) = q;
+      }
+      if (wave == 0 && g4 == 0) p.act_scale[(size_t)(row0 + r) * IB + nb] = scale;
+    }
+  }
+}
+
+template <bool G1, int MT, int S>
+hipError_t launch_tile_mt(const GemmParams &p, int grid, hipStream_t st) {
+  auto k = gemm_tile_kernel<G1, MT, S>;
+  const size_t lds = TileLayout<MT, S>::bytes(G1, p.KB);
+  // the dynamic LDS limit is a property of the code object: raise it once
+  static hipError_t attr = hipFuncSetAttribute(reinterpret_cast<const void *>(k),
+                                               hipFuncAttributeMaxDynamicSharedMemorySize,
+                                               (int)TileLayout<MT, S>::bytes(G1, 512));
+  if (attr != hipSuccess) return attr;
+  hipLaunchKernelGGL(k, dim3(grid), dim3(kTileThreads), lds, st, p);
+  return hipGetLastError();
+}
+
+constexpr int kTileStages = 3;  // LDS ring: loads issued 2 K-steps ahead
+
+}  // namespace
+
+int gemm_tile_cols() { return kTileCols; }
+
+hipError_t launch_gemm_tile(const GemmParams &p, bool g1, int BM, int grid, hipStream_t st) {
+  if (grid <= 0) return hipSuccess;
+  switch (BM) {
+    case 64: return g1 ? launch_tile_mt<true, 4, kTileStages>(p, grid, st)
+                       : launch_tile_mt<false, 4, kTileStages>(p, grid, st);
+    case 128: return g1 ? launch_tile_mt<true, 8, kTileStages>(p, grid, st)
+                        : launch_tile_mt<false, 8, kTileStages>(p, grid, st);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+}  // namespace moe

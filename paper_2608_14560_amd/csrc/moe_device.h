@@ -145,6 +145,9 @@ hipError_t launch_gemm1_narrow(const GemmParams &p, int grid, hipStream_t st);
 int gemm1_narrow_cols();
 hipError_t launch_requant(const GemmParams &p, int P_max, hipStream_t st);
 hipError_t launch_gemm2(const GemmParams &p, int BM, int grid, hipStream_t st);
+// large-tile GEMM1 / GEMM2 (BM = 64 or 128 rows x 256 columns, full K per item)
+hipError_t launch_gemm_tile(const GemmParams &p, bool g1, int BM, int grid, hipStream_t st);
+int gemm_tile_cols();
 hipError_t launch_finalize(const FinalizeParams &p, hipStream_t st);
 size_t gemm_lds_bytes(int BM);
 

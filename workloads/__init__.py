@@ -82,6 +82,16 @@ PARITY_CONFIGS: dict[str, MoEConfig] = {
     "small_many": MoEConfig("small_many", T=300, H=384, I=256, num_experts=64,
                             num_local_experts=64, local_expert_offset=0, n_group=8,
                             topk_group=4, top_k=8, hot_experts=4),
+    # ~60 rows per expert: 64-row M-tiles; H = 384 leaves a 128-wide last
+    # 256-column GEMM2 block, I = 256 a group of two column blocks
+    "small_t64": MoEConfig("small_t64", T=160, H=384, I=256, num_experts=16,
+                           num_local_experts=16, local_expert_offset=0, n_group=4,
+                           topk_group=2, top_k=6),
+    # ~128 rows per expert: 128-row M-tiles, 6 of 8 experts resident, three
+    # intermediate blocks (I = 384), ragged GEMM2 columns (H = 640)
+    "small_t128": MoEConfig("small_t128", T=256, H=640, I=384, num_experts=8,
+                            num_local_experts=6, local_expert_offset=1, n_group=2,
+                            topk_group=2, top_k=4),
 }
 
 
