@@ -70,7 +70,7 @@ Plan make_plan(const moe_shape_t *s) {
   p.P_max = TK > 0 ? TK : 1;
   // expected rows per resident expert under uniform routing picks the M tile
   const double avg = (double)TK / s->num_experts;
-  p.BM = avg <= 16 ? 16 : (avg <= 48 ? 32 : (avg <= 96 ? 64 : 128));
+  p.BM = avg <= 16 ? 16 : (avg <= 48 ? 32 : (avg <= 96 ? 64 : (avg <= 192 ? 128 : 256)));
   p.tile = p.BM >= 64;
   // GEMM1 promotes its K blocks in order (its output decides the re-quantised
   // codes), so it never splits K; GEMM2 could (S2 > 1 sums the halves in the

@@ -2,24 +2,24 @@
 // (paper Section 3.1.1) for batches with many rows per expert (prefill-sized
 // and skewed loads), on CDNA4 FP8 matrix cores.
 //
-// Work item = (M-tile of BM = 16*MT rows of one expert, 256-column block), the
-// whole K range.  Items of one expert are ordered in groups of four column
-// blocks: all M-tiles of a group, column block fastest, so the 32 items that
-// an XCD runs side by side share four weight panels and eight A tiles in that
-// XCD's L2 (workgroup b runs item (b % 8) * ceil(n/8) + b / 8, and workgroups
-// are dispatched round-robin over the 8 XCDs).
+// Work item = (M-tile of BM rows of one expert, 256-column block), the whole
+// K range.  Items of one expert are ordered in groups of four column blocks:
+// all M-tiles of a group, column block fastest, so the items an XCD runs side
+// by side share four weight panels and a few A tiles in that XCD's L2
+// (workgroup b runs item (b % 8) * ceil(n/8) + b / 8, and workgroups are
+// dispatched round-robin over the 8 XCDs).
 //
-// One workgroup of 4 waves per item, each wave 64 columns x all BM rows:
-//   GEMM1: waves 0/1 own gate columns [0,64) / [64,128) of the 128-wide
-//          intermediate block, waves 2/3 the matching up columns, so a wave's
+// One workgroup of 4 x WM waves per item.  Wave (wm, wn) = (wave / 4,
+// wave % 4) owns rows [16 MT wm, 16 MT (wm+1)) of the tile (BM = 16 MT WM)
+// and 64 columns:
+//   GEMM1: wn = 0/1 own gate columns [0,64) / [64,128) of the 128-wide
+//          intermediate block, wn = 2/3 the matching up columns, so a wave's
 //          columns share one 128x128 weight-scale block;
-//   GEMM2: wave w owns output columns [64w, 64w+64) of the 256-wide block.
-// The weight fragments stream from global memory straight into registers
-// through a D-deep ring (loads issued D K-steps ahead, unconditionally, with
-// the K index clamped at the end).  The A tile (rows gathered through
-// perm_token for GEMM1) is shared by the 4 waves: it goes straight from
-// global memory into an S-stage LDS ring (issued S-1 K-steps ahead, no
-// registers), with one barrier per K-step.
+//   GEMM2: wn owns output columns [64 wn, 64 wn + 64) of the 256-wide block.
+// Every K-step's operands -- the A tile (rows gathered through perm_token
+// for GEMM1), its row scales and the 256 weight rows -- go straight from
+// global memory into an S-stage LDS ring (direct loads issued S-1 K-steps
+// ahead, no registers), with one barrier per K-step.
 //
 // The weight fragment is the MFMA's first operand and the activation fragment
 // its second, so lane l holds output columns 4*(l/16)+i (i = 0..3) of token
@@ -34,21 +34,25 @@
 namespace moe {
 namespace {
 
-constexpr int kTileThreads = 256;
 constexpr int kTileCols = 256;
-constexpr int kGroupN = 4;     // column blocks per item group
-// LDS operand layout: row-major 128-byte rows with an XOR swizzle (each
-// direct load fetches whole cache lines) or fragment order (see the kernel)
-constexpr bool kRowMajor = true;
+constexpr int kGroupN = 4;  // column blocks per item group
 
-template <int MT, int S>
+// LDS stage: A tile (BM rows x 128 bytes), the 256 weight rows (4 blocks of
+// 64, one per column wave), the row-scale slots (64 per wave).  Rows are
+// 128 bytes; 16-byte chunk c of row r sits in slot c ^ f(r), f(r) = (r/2) % 8,
+// so the 16 rows an MFMA fragment read touches spread over the LDS banks,
+// while each direct load fetches whole 128-byte lines (8 rows per wave-wide
+// load).
+template <int MT, int WM, int S>
 struct TileLayout {
-  static constexpr int BM = 16 * MT;
-  static constexpr int A_BYTES = BM * 128;              // A tile, fragment order
-  static constexpr int SCL = A_BYTES + 4 * 8192;        // + 4 waves' weight rows
-  static constexpr int STAGE = SCL + 1024;              // + 256 row-scale slots
+  static constexpr int THREADS = 256 * WM;
+  static constexpr int BM = 16 * MT * WM;
+  static constexpr int A_BYTES = BM * 128;
+  static constexpr int SCL = A_BYTES + 4 * 8192;
+  static constexpr int STAGE = SCL + 4 * WM * 256;
   static constexpr int RING = S * STAGE;
-  static constexpr int XCH = 2 * MT * 4 * 4 * kWave * 4;  // GEMM1 up -> gate hand-over
+  // GEMM1: the up waves hand their accumulators to the gate waves
+  static constexpr int XCH = 2 * WM * MT * 4 * 4 * kWave * 4;
   static constexpr int MAIN = RING > XCH ? RING : XCH;
   static size_t bytes(bool g1, int KB) {
     return (size_t)(g1 ? MAIN : RING) + sizeof(float) * 2 * (size_t)KB;
@@ -70,8 +74,8 @@ __device__ __forceinline__ void lds_load4(const void *g, uint8_t *lds) {
 // LDS reads of the K loop go through restrict-qualified pointers, so after
 // inlining they carry alias-scope metadata.  Without it the compiler cannot
 // tell them from the in-flight direct-to-LDS writes of later stages and waits
-// for every outstanding load (the weight prefetch included) before each read;
-// the K loop's explicit waits and barriers order the accesses instead.
+// for every outstanding load before each read; the K loop's explicit waits
+// and barriers order the accesses instead.
 __device__ __forceinline__ v8i tile_frag(const uint8_t *__restrict__ st, int lo, int hi) {
   const v4i a = *reinterpret_cast<const v4i *>(st + lo);
   const v4i b = *reinterpret_cast<const v4i *>(st + hi);
@@ -82,10 +86,13 @@ __device__ __forceinline__ float4 tile_f4(const float *__restrict__ q) {
 }
 __device__ __forceinline__ float tile_f1(const float *__restrict__ q) { return *q; }
 
-template <bool G1, int MT, int S>
-__global__ __launch_bounds__(kTileThreads) void gemm_tile_kernel(GemmParams p) {
-  using L = TileLayout<MT, S>;
+template <bool G1, int MT, int WM, int S>
+__global__ __launch_bounds__(256 * WM) void gemm_tile_kernel(GemmParams p) {
+  using L = TileLayout<MT, WM, S>;
+  constexpr int NT = L::THREADS;
+  static_assert(NT == 256 * WM, "launch bound");
   constexpr int BM = L::BM;
+  constexpr int MTW = MT * WM;  // 16-row blocks of the tile
   static_assert(MT % 4 == 0, "row scales are read four at a time");
 
   __shared__ int tb[1028];
@@ -95,16 +102,17 @@ __global__ __launch_bounds__(kTileThreads) void gemm_tile_kernel(GemmParams p) {
   const int tid = threadIdx.x;
   const int lane = tid & (kWave - 1);
   const int wave = tid / kWave;
+  const int wn = wave & 3;
+  const int wm = wave >> 2;
   const int r16 = lane & 15;
   const int g4 = lane >> 4;
-  const int frag_off = g4 * 32;
 
   const int n_items = *p.n_items;
   const int per_xcd = (n_items + 7) / 8;
   const int item = (blockIdx.x & 7) * per_xcd + (blockIdx.x >> 3);
   if ((int)(blockIdx.x >> 3) >= per_xcd || item >= n_items) return;
 
-  for (int i = tid; i <= p.El; i += kTileThreads) tb[i] = p.tile_base[i];
+  for (int i = tid; i <= p.El; i += NT) tb[i] = p.tile_base[i];
   __syncthreads();
 
   // ---- decode the work item
@@ -132,24 +140,24 @@ __global__ __launch_bounds__(kTileThreads) void gemm_tile_kernel(GemmParams p) {
   const size_t K = (size_t)p.K;
 
   // ---- this wave's weight rows and scale blocks
-  const int half = wave >> 1;  // GEMM1: 0 gate, 1 up.  GEMM2: 128-column half
+  const int half = wn >> 1;  // GEMM1: 0 gate, 1 up.  GEMM2: 128-column half
   int wrow0, nblk0, nblk1;
   if (G1) {
-    wrow0 = half * p.I + nb * 128 + 64 * (wave & 1);
+    wrow0 = half * p.I + nb * 128 + 64 * (wn & 1);
     nblk0 = nb;
     nblk1 = p.I / 128 + nb;
   } else {
-    wrow0 = nb * kTileCols + 64 * wave;
+    wrow0 = nb * kTileCols + 64 * wn;
     nblk0 = min(2 * nb, p.N_total / 128 - 1);
     nblk1 = min(2 * nb + 1, p.N_total / 128 - 1);
   }
 
-  // weight-block scales of the whole K range: sb_l[0][kb] (waves 0/1), sb_l[1][kb]
+  // weight-block scales of the whole K range: sb_l[0][kb] (wn 0/1), sb_l[1][kb]
   float *sb_l = reinterpret_cast<float *>(smem + (G1 ? L::MAIN : L::RING));
   {
     const float *s0 = p.B_scale + ((size_t)e * (p.N_total / 128) + nblk0) * KB;
     const float *s1 = p.B_scale + ((size_t)e * (p.N_total / 128) + nblk1) * KB;
-    for (int i = tid; i < KB; i += kTileThreads) {
+    for (int i = tid; i < KB; i += NT) {
       sb_l[i] = s0[i];
       sb_l[KB + i] = s1[i];
     }
@@ -157,63 +165,43 @@ __global__ __launch_bounds__(kTileThreads) void gemm_tile_kernel(GemmParams p) {
   const float *sb_w = sb_l + half * KB;
   __syncthreads();
 
-  // ---- operand staging: every K-step's A tile, row scales and weight rows
-  // go straight from global memory into an S-stage LDS ring (no registers),
-  // issued S-1 K-steps ahead.  Both operands are laid out in fragment order:
-  // a 16x128-byte fragment is two 1 KB halves, lane l's 16 bytes of half h at
-  // 16 l, holding row l % 16, bytes 32 (l / 16) + 16 h of the K block -- the
-  // bytes an MFMA operand register pair of lane l needs -- so a wave-wide
-  // 16-byte direct load fills one half and every fragment read is a
-  // contiguous 1 KB LDS read.
-  //   A: fragment m (rows 16m..16m+15) at m * 2 KB, shared by the 4 waves;
-  //      wave w loads halves q = 4w..4w+3 of BM/16 fragments (JW per wave).
-  //   B: wave-private, fragment n of wave w at A_BYTES + w * 8 KB + n * 2 KB.
-  //   row scales: slot s = (row % 16) * MT + row / 16 at SCL; lane L of wave w
-  //      loads slot 64 w + L (slots >= BM are loaded but never read).
-  constexpr int JW = BM / 32;  // A loads per wave and K-step
-  const uint8_t *a_src[JW];
+  // ---- direct-load assignments.  A wave-wide 16-byte load fills 1 KB of a
+  // stage: lane L writes slot L, i.e. row 8q + L/8, slot L % 8 of 8-row block
+  // q, and so fetches chunk (L % 8) ^ f(row) of that row.
+  constexpr int JA = BM / 8 / (4 * WM);  // A blocks per wave
+  constexpr int JB = 8 / WM;             // weight blocks per wave
+  const int sw_l = lane >> 3;
+  const uint8_t *a_src[JA];
 #pragma unroll
-  for (int j = 0; j < JW; ++j) {
-    const int q = wave * JW + j;
-    int r, off;
-    if (kRowMajor) {  // 8 rows of whole 128-byte lines per load, chunk c in slot c ^ f(r)
-      r = 8 * q + (lane >> 3);
-      off = 16 * ((lane & 7) ^ ((r >> 1) & 7));
-    } else {          // one half of fragment q / 2
-      r = 16 * (q >> 1) + r16;
-      off = frag_off + 16 * (q & 1);
-    }
+  for (int j = 0; j < JA; ++j) {
+    const int r = 8 * (wave * JA + j) + sw_l;
     const int rr = min(r, nrows - 1);  // ragged tail: repeat the last row
     const int src = G1 ? p.perm_token[row0 + rr] : row0 + rr;
-    a_src[j] = p.A + (size_t)src * K + off;
+    a_src[j] = p.A + (size_t)src * K + 16 * ((lane & 7) ^ ((r >> 1) & 7));
   }
+  // weight rows: the column wave wn's 64 rows are 8 blocks, loaded JB each by
+  // the WM waves of that column
   const uint8_t *Bexp = p.B + (size_t)e * p.N_total * K;
-  const uint8_t *b_src[8];
+  const uint8_t *b_src[JB];
 #pragma unroll
-  for (int i = 0; i < 8; ++i) {
-    int r, off;
-    if (kRowMajor) {
-      r = 8 * i + (lane >> 3);
-      off = 16 * ((lane & 7) ^ ((r >> 1) & 7));
-    } else {
-      r = 16 * (i >> 1) + r16;
-      off = frag_off + 16 * (i & 1);
-    }
-    r = min(wrow0 + r, p.N_total - 1);  // ragged last GEMM2 block
-    b_src[i] = Bexp + (size_t)r * K + off;
+  for (int j = 0; j < JB; ++j) {
+    const int r = 8 * (wm * JB + j) + sw_l;
+    const int rg = min(wrow0 + r, p.N_total - 1);  // ragged last GEMM2 block
+    b_src[j] = Bexp + (size_t)rg * K + 16 * ((lane & 7) ^ ((r >> 1) & 7));
   }
+  // row scales: slot s = (row % 16) * MTW + row / 16; lane L of wave w loads
+  // slot 64 w + L (slots >= BM are loaded but never read)
   const float *s_src;
   {
     const int sl = 64 * wave + lane;
-    const int r = sl < BM ? 16 * (sl % MT) + sl / MT : nrows - 1;
+    const int r = sl < BM ? 16 * (sl % MTW) + sl / MTW : nrows - 1;
     const int rr = min(r, nrows - 1);
     s_src = p.A_scale + (size_t)(G1 ? p.perm_token[row0 + rr] : row0 + rr) * KB;
   }
-
-  // this lane's two 16-byte pieces of a fragment (rows 16m + r16) in the stage
+  // this lane's two 16-byte pieces of a fragment (rows 16m + r16 of a block)
   const int fr = (r16 >> 1) & 7;
-  const int rd_lo = kRowMajor ? r16 * 128 + 16 * ((2 * g4) ^ fr) : 16 * lane;
-  const int rd_hi = kRowMajor ? r16 * 128 + 16 * ((2 * g4 + 1) ^ fr) : 1024 + 16 * lane;
+  const int rd_lo = r16 * 128 + 16 * ((2 * g4) ^ fr);
+  const int rd_hi = r16 * 128 + 16 * ((2 * g4 + 1) ^ fr);
 
   v4f acc[MT][4];
 #pragma unroll
@@ -224,27 +212,28 @@ __global__ __launch_bounds__(kTileThreads) void gemm_tile_kernel(GemmParams p) {
   // Each K-step every wave issues one group of kGroup direct loads.  At the
   // end of step `it` stage it+1 must have landed: its group was issued S-2
   // steps earlier, so at most (S-2) groups may still be outstanding.
-  constexpr int kGroup = JW + 8 + 1;
+  constexpr int kGroup = JA + JB + 1;
   constexpr int kWait = (S - 2) * kGroup;
   static_assert(kWait < 64, "vmcnt holds 6 bits");
-  static_assert(S >= 2, "A ring depth");
+  static_assert(S >= 2, "LDS ring depth");
 
 #define TILE_STAGE(st) (smem + (st) * L::STAGE)
 #define TILE_DMA(st, kb)                                                                \
   do {                                                                                  \
     uint8_t *d_ = TILE_STAGE(st);                                                       \
     const size_t ko_ = (size_t)(kb) * 128;                                              \
-    _Pragma("unroll") for (int j = 0; j < JW; ++j)                                      \
-        lds_load16(a_src[j] + ko_, d_ + (wave * JW + j) * 1024);                        \
-    _Pragma("unroll") for (int i = 0; i < 8; ++i)                                       \
-        lds_load16(b_src[i] + ko_, d_ + L::A_BYTES + wave * 8192 + i * 1024);          \
+    _Pragma("unroll") for (int j = 0; j < JA; ++j)                                      \
+        lds_load16(a_src[j] + ko_, d_ + (wave * JA + j) * 1024);                        \
+    _Pragma("unroll") for (int j = 0; j < JB; ++j)                                      \
+        lds_load16(b_src[j] + ko_, d_ + L::A_BYTES + wn * 8192 + (wm * JB + j) * 1024); \
     lds_load4(s_src + (kb), d_ + L::SCL + wave * 256);                                  \
   } while (0)
 #define TILE_COMPUTE(st, kb)                                                            \
   do {                                                                                  \
-    const uint8_t *as_ = TILE_STAGE(st);                                                \
-    const uint8_t *bs_ = as_ + L::A_BYTES + wave * 8192;                                \
-    const float *sa_ = reinterpret_cast<const float *>(as_ + L::SCL) + r16 * MT;        \
+    const uint8_t *as_ = TILE_STAGE(st) + wm * MT * 2048;                               \
+    const uint8_t *bs_ = TILE_STAGE(st) + L::A_BYTES + wn * 8192;                       \
+    const float *sa_ =                                                                  \
+        reinterpret_cast<const float *>(TILE_STAGE(st) + L::SCL) + r16 * MTW + wm * MT; \
     const float sbv_ = tile_f1(sb_w + (kb));                                            \
     float sav_[MT];                                                                     \
     _Pragma("unroll") for (int q_ = 0; q_ < MT / 4; ++q_) {                             \
@@ -303,16 +292,16 @@ __global__ __launch_bounds__(kTileThreads) void gemm_tile_kernel(GemmParams p) {
 #undef TILE_DMA
 #undef TILE_STAGE
 
-  // accumulator element (m, n, i) of this lane: row 16m + r16, column
-  // 16n + 4*g4 + i of the wave's 64 columns
+  // accumulator element (m, n, i) of this lane: tile row 16 MT wm + 16m + r16,
+  // column 16n + 4*g4 + i of the wave's 64 columns
+  const int wrow = 16 * MT * wm;
   if (!G1) {
     if (wrow0 >= p.N_total) return;  // columns past H (ragged last block)
-    float *Ys = p.Y;
 #pragma unroll
     for (int m = 0; m < MT; ++m) {
-      const int r = 16 * m + r16;
+      const int r = wrow + 16 * m + r16;
       if (r < nrows) {
-        float *yrow = Ys + (size_t)(row0 + r) * p.H + wrow0 + 4 * g4;
+        float *yrow = p.Y + (size_t)(row0 + r) * p.H + wrow0 + 4 * g4;
 #pragma unroll
         for (int n = 0; n < 4; ++n) *reinterpret_cast<v4f *>(yrow + 16 * n) = acc[m][n];
       }
@@ -320,20 +309,22 @@ __global__ __launch_bounds__(kTileThreads) void gemm_tile_kernel(GemmParams p) {
     return;
   }
 
-  // SwiGLU: the up waves hand their accumulators to the gate waves through
-  // LDS (lane-private slots), the gate waves apply silu(gate) * up.
+  // SwiGLU: the up waves hand their accumulators to the gate waves of the
+  // same rows through LDS (lane-private slots), the gate waves apply
+  // silu(gate) * up.
   float *xch = reinterpret_cast<float *>(smem);
-  if (wave >= 2) {
+  const int pair = 2 * wm + (wn & 1);  // gate wave <-> up wave pair
+  if (wn >= 2) {
 #pragma unroll
     for (int m = 0; m < MT; ++m)
 #pragma unroll
       for (int n = 0; n < 4; ++n)
 #pragma unroll
         for (int i = 0; i < 4; ++i)
-          xch[((((wave - 2) * MT + m) * 4 + n) * 4 + i) * kWave + lane] = acc[m][n][i];
+          xch[(((pair * MT + m) * 4 + n) * 4 + i) * kWave + lane] = acc[m][n][i];
   }
   __syncthreads();
-  if (wave < 2) {
+  if (wn < 2) {
 #pragma unroll
     for (int m = 0; m < MT; ++m) {
       float mx = 0.0f;
@@ -341,26 +332,26 @@ __global__ __launch_bounds__(kTileThreads) void gemm_tile_kernel(GemmParams p) {
       for (int n = 0; n < 4; ++n)
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          const float u = xch[(((wave * MT + m) * 4 + n) * 4 + i) * kWave + lane];
+          const float u = xch[(((pair * MT + m) * 4 + n) * 4 + i) * kWave + lane];
           acc[m][n][i] = swiglu_spec(acc[m][n][i], u);
           mx = fmaxf(mx, fabsf(acc[m][n][i]));
         }
       // the row's 64 columns of this wave sit in lanes r16, r16+16, r16+32, r16+48
       mx = fmaxf(mx, __shfl_xor(mx, 16));
       mx = fmaxf(mx, __shfl_xor(mx, 32));
-      if (g4 == 0) amax_l[wave][16 * m + r16] = mx;
+      if (g4 == 0) amax_l[wn][wrow + 16 * m + r16] = mx;
     }
   }
   __syncthreads();
-  if (wave >= 2) return;
+  if (wn >= 2) return;
   const int IB = p.I / 128;
 #pragma unroll
   for (int m = 0; m < MT; ++m) {
-    const int r = 16 * m + r16;
+    const int r = wrow + 16 * m + r16;
     const float amax = fmaxf(amax_l[0][r], amax_l[1][r]);
     const float scale = (amax > 0.0f) ? amax / 448.0f : 1.0f;
     if (r < nrows) {
-      uint8_t *arow = p.act + (size_t)(row0 + r) * p.I + nb * 128 + 64 * wave + 4 * g4;
+      uint8_t *arow = p.act + (size_t)(row0 + r) * p.I + nb * 128 + 64 * wn + 4 * g4;
 #pragma unroll
       for (int n = 0; n < 4; ++n) {
         uint32_t q = 0u;
@@ -369,25 +360,24 @@ __global__ __launch_bounds__(kTileThreads) void gemm_tile_kernel(GemmParams p) {
               (e4m3x2_rne_sat(acc[m][n][2] / scale, acc[m][n][3] / scale) << 16);
         *reinterpret_cast<uint32_t *>(arow + 16 * n) = q;
       }
-      if (wave == 0 && g4 == 0) p.act_scale[(size_t)(row0 + r) * IB + nb] = scale;
+      if (wn == 0 && g4 == 0) p.act_scale[(size_t)(row0 + r) * IB + nb] = scale;
     }
   }
 }
 
-template <bool G1, int MT, int S>
-hipError_t launch_tile_mt(const GemmParams &p, int grid, hipStream_t st) {
-  auto k = gemm_tile_kernel<G1, MT, S>;
-  const size_t lds = TileLayout<MT, S>::bytes(G1, p.KB);
+template <bool G1, int MT, int WM, int S>
+hipError_t launch_tile(const GemmParams &p, int grid, hipStream_t st) {
+  using L = TileLayout<MT, WM, S>;
+  auto k = gemm_tile_kernel<G1, MT, WM, S>;
   // the dynamic LDS limit is a property of the code object: raise it once
+  // (to the size at the largest supported K, 512 blocks)
   static hipError_t attr = hipFuncSetAttribute(reinterpret_cast<const void *>(k),
                                                hipFuncAttributeMaxDynamicSharedMemorySize,
-                                               (int)TileLayout<MT, S>::bytes(G1, 512));
+                                               (int)L::bytes(G1, 512));
   if (attr != hipSuccess) return attr;
-  hipLaunchKernelGGL(k, dim3(grid), dim3(kTileThreads), lds, st, p);
+  hipLaunchKernelGGL(k, dim3(grid), dim3(L::THREADS), L::bytes(G1, p.KB), st, p);
   return hipGetLastError();
 }
-
-constexpr int kTileStages = 3;  // LDS ring: loads issued 2 K-steps ahead
 
 }  // namespace
 
@@ -396,10 +386,11 @@ int gemm_tile_cols() { return kTileCols; }
 hipError_t launch_gemm_tile(const GemmParams &p, bool g1, int BM, int grid, hipStream_t st) {
   if (grid <= 0) return hipSuccess;
   switch (BM) {
-    case 64: return g1 ? launch_tile_mt<true, 4, kTileStages>(p, grid, st)
-                       : launch_tile_mt<false, 4, kTileStages>(p, grid, st);
-    case 128: return g1 ? launch_tile_mt<true, 8, kTileStages>(p, grid, st)
-                        : launch_tile_mt<false, 8, kTileStages>(p, grid, st);
+    // 64 / 128 rows: 4 waves, three-stage ring (loads two K-steps ahead)
+    case 64: return g1 ? launch_tile<true, 4, 1, 3>(p, grid, st) : launch_tile<false, 4, 1, 3>(p, grid, st);
+    case 128: return g1 ? launch_tile<true, 8, 1, 3>(p, grid, st) : launch_tile<false, 8, 1, 3>(p, grid, st);
+    // 256 rows: 8 waves (two per SIMD), two-stage ring
+    case 256: return g1 ? launch_tile<true, 8, 2, 2>(p, grid, st) : launch_tile<false, 8, 2, 2>(p, grid, st);
     default: return hipErrorInvalidValue;
   }
 }

@@ -92,6 +92,10 @@ PARITY_CONFIGS: dict[str, MoEConfig] = {
     "small_t128": MoEConfig("small_t128", T=256, H=640, I=384, num_experts=8,
                             num_local_experts=6, local_expert_offset=1, n_group=2,
                             topk_group=2, top_k=4),
+    # ~320 rows per expert: 256-row M-tiles with a ragged second tile
+    "small_t256": MoEConfig("small_t256", T=640, H=384, I=256, num_experts=8,
+                            num_local_experts=8, local_expert_offset=0, n_group=2,
+                            topk_group=2, top_k=4),
 }
 
 
