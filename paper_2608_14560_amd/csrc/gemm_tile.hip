@@ -39,10 +39,10 @@ constexpr int kGroupN = 4;  // column blocks per item group
 
 // LDS stage: A tile (BM rows x 128 bytes), the 256 weight rows (4 blocks of
 // 64, one per column wave), the row-scale slots (64 per wave).  Rows are
-// 128 bytes; 16-byte chunk c of row r sits in slot c ^ f(r), f(r) = (r/2) % 8,
-// so the 16 rows an MFMA fragment read touches spread over the LDS banks,
-// while each direct load fetches whole 128-byte lines (8 rows per wave-wide
-// load).
+// 128 bytes; 16-byte chunk c of row r sits in slot c ^ f(r), f(r) =
+// (r % 8) ^ ((r / 8) % 2): measured on gfx950, the fragment reads (16 rows,
+// two 16-byte pieces per lane) then run without bank conflicts, while each
+// direct load fetches whole 128-byte lines (8 rows per wave-wide load).
 template <int MT, int WM, int S>
 struct TileLayout {
   static constexpr int THREADS = 256 * WM;
@@ -50,7 +50,8 @@ struct TileLayout {
   static constexpr int A_BYTES = BM * 128;
   static constexpr int SCL = A_BYTES + 4 * 8192;
   static constexpr int STAGE = SCL + 4 * WM * 256;
-  static constexpr int RING = S * STAGE;
+  static constexpr int JUNK = 4 * WM * 256;  // landing area of the L2 prefetches
+  static constexpr int RING = S * STAGE + JUNK;
   // GEMM1: the up waves hand their accumulators to the gate waves
   static constexpr int XCH = 2 * WM * MT * 4 * 4 * kWave * 4;
   static constexpr int MAIN = RING > XCH ? RING : XCH;
@@ -60,6 +61,8 @@ struct TileLayout {
 };
 
 typedef __attribute__((address_space(3))) void lds_void;
+
+__device__ __forceinline__ int tile_swz(int r) { return (r & 7) ^ ((r >> 3) & 1); }
 
 // Direct global -> LDS loads.  The builtin sits in plain device functions:
 // used inside the kernel template, it keeps the host compilation pass from
@@ -167,7 +170,8 @@ __global__ __launch_bounds__(256 * WM) void gemm_tile_kernel(GemmParams p) {
 
   // ---- direct-load assignments.  A wave-wide 16-byte load fills 1 KB of a
   // stage: lane L writes slot L, i.e. row 8q + L/8, slot L % 8 of 8-row block
-  // q, and so fetches chunk (L % 8) ^ f(row) of that row.
+  // q, and so fetches chunk (L % 8) ^ f(row) of that row (f depends on the
+  // row's position in its 16-row fragment only).
   constexpr int JA = BM / 8 / (4 * WM);  // A blocks per wave
   constexpr int JB = 8 / WM;             // weight blocks per wave
   const int sw_l = lane >> 3;
@@ -177,7 +181,7 @@ __global__ __launch_bounds__(256 * WM) void gemm_tile_kernel(GemmParams p) {
     const int r = 8 * (wave * JA + j) + sw_l;
     const int rr = min(r, nrows - 1);  // ragged tail: repeat the last row
     const int src = G1 ? p.perm_token[row0 + rr] : row0 + rr;
-    a_src[j] = p.A + (size_t)src * K + 16 * ((lane & 7) ^ ((r >> 1) & 7));
+    a_src[j] = p.A + (size_t)src * K + 16 * ((lane & 7) ^ tile_swz(r));
   }
   // weight rows: the column wave wn's 64 rows are 8 blocks, loaded JB each by
   // the WM waves of that column
@@ -187,7 +191,26 @@ __global__ __launch_bounds__(256 * WM) void gemm_tile_kernel(GemmParams p) {
   for (int j = 0; j < JB; ++j) {
     const int r = 8 * (wm * JB + j) + sw_l;
     const int rg = min(wrow0 + r, p.N_total - 1);  // ragged last GEMM2 block
-    b_src[j] = Bexp + (size_t)rg * K + 16 * ((lane & 7) ^ ((r >> 1) & 7));
+    b_src[j] = Bexp + (size_t)rg * K + 16 * ((lane & 7) ^ tile_swz(r));
+  }
+  // L2 prefetch one K-step beyond the ring: one dword of each 128-byte line
+  // of the step's A rows and weight rows, 64 lines per load, spread over the
+  // waves; the dwords land in a junk LDS area and are never read.
+  constexpr int kPfLoads = (BM + 256 + 4 * WM * kWave - 1) / (4 * WM * kWave);
+  const uint8_t *pf_src[kPfLoads];
+#pragma unroll
+  for (int j = 0; j < kPfLoads; ++j) {
+    const int line = (wave * kPfLoads + j) * kWave + lane;  // 0 .. BM+256 (clamped)
+    const int r = min(line, BM + 255);
+    if (r < BM) {
+      const int rr = min(r, nrows - 1);
+      pf_src[j] = p.A + (size_t)(G1 ? p.perm_token[row0 + rr] : row0 + rr) * K;
+    } else {
+      const int c = r - BM;  // weight row c % 64 of column wave c / 64
+      const int w2 = c >> 6;
+      const int base = G1 ? (w2 >> 1) * p.I + nb * 128 + 64 * (w2 & 1) : nb * kTileCols + 64 * w2;
+      pf_src[j] = Bexp + (size_t)min(base + (c & 63), p.N_total - 1) * K;
+    }
   }
   // row scales: slot s = (row % 16) * MTW + row / 16; lane L of wave w loads
   // slot 64 w + L (slots >= BM are loaded but never read)
@@ -199,7 +222,7 @@ __global__ __launch_bounds__(256 * WM) void gemm_tile_kernel(GemmParams p) {
     s_src = p.A_scale + (size_t)(G1 ? p.perm_token[row0 + rr] : row0 + rr) * KB;
   }
   // this lane's two 16-byte pieces of a fragment (rows 16m + r16 of a block)
-  const int fr = (r16 >> 1) & 7;
+  const int fr = tile_swz(r16);
   const int rd_lo = r16 * 128 + 16 * ((2 * g4) ^ fr);
   const int rd_hi = r16 * 128 + 16 * ((2 * g4 + 1) ^ fr);
 
@@ -209,11 +232,12 @@ __global__ __launch_bounds__(256 * WM) void gemm_tile_kernel(GemmParams p) {
 #pragma unroll
     for (int n = 0; n < 4; ++n) acc[m][n] = v4f{0.f, 0.f, 0.f, 0.f};
 
-  // Each K-step every wave issues one group of kGroup direct loads.  At the
-  // end of step `it` stage it+1 must have landed: its group was issued S-2
-  // steps earlier, so at most (S-2) groups may still be outstanding.
+  // Each K-step every wave issues one group of kGroup direct loads (stage
+  // it+S-1), then kPfLoads prefetches (step it+S).  At the end of step `it`
+  // stage it+1 must have landed: its group was issued S-2 steps earlier, so
+  // the (S-2) later groups and this step's prefetches may be outstanding.
   constexpr int kGroup = JA + JB + 1;
-  constexpr int kWait = (S - 2) * kGroup;
+  constexpr int kWait = (S - 2) * (kGroup + kPfLoads) + kPfLoads;
   static_assert(kWait < 64, "vmcnt holds 6 bits");
   static_assert(S >= 2, "LDS ring depth");
 
@@ -228,6 +252,16 @@ __global__ __launch_bounds__(256 * WM) void gemm_tile_kernel(GemmParams p) {
         lds_load16(b_src[j] + ko_, d_ + L::A_BYTES + wn * 8192 + (wm * JB + j) * 1024); \
     lds_load4(s_src + (kb), d_ + L::SCL + wave * 256);                                  \
   } while (0)
+#define TILE_PREFETCH(kb)                                                               \
+  do {                                                                                  \
+    _Pragma("unroll") for (int j = 0; j < kPfLoads; ++j)                                \
+        lds_load4(pf_src[j] + (size_t)(kb) * 128, smem + S * L::STAGE + wave * 256);    \
+  } while (0)
+// One K-step of the wave's 16 MT x 64 block: per 16-row block m, four MFMAs
+// (one per 16-column sub-tile), each started from zero and promoted with one
+// FMA per accumulator; the next block's A fragment is read while this one
+// is multiplied.  Two waves per SIMD (8-wave tiles) fill each other's
+// MFMA-to-FMA latency.
 #define TILE_COMPUTE(st, kb)                                                            \
   do {                                                                                  \
     const uint8_t *as_ = TILE_STAGE(st) + wm * MT * 2048;                               \
@@ -266,9 +300,12 @@ __global__ __launch_bounds__(256 * WM) void gemm_tile_kernel(GemmParams p) {
   // prologue: stages 0 .. S-2 in flight, wait for stage 0.  The barriers are
   // plain s_barrier after an explicit vmcnt wait: the generic workgroup
   // barrier would wait for every outstanding load.
+  // (the prologue issues stages 0 .. S-2 each followed by its prefetch, so
+  // it has the same shape as S-1 loop steps)
 #pragma unroll
   for (int st = 0; st < S - 1; ++st) {
     TILE_DMA(st, min(st, KB - 1));
+    TILE_PREFETCH(min(st + 1, KB - 1));
     __builtin_amdgcn_sched_barrier(0);
   }
   asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(kWait) : "memory");
@@ -276,6 +313,7 @@ __global__ __launch_bounds__(256 * WM) void gemm_tile_kernel(GemmParams p) {
   int st_rd = 0, st_ld = S - 1;
   for (int it = 0; it < KB; ++it) {
     TILE_DMA(st_ld, min(it + S - 1, KB - 1));
+    TILE_PREFETCH(min(it + S, KB - 1));
     __builtin_amdgcn_sched_barrier(0);
     TILE_COMPUTE(st_rd, it);
     __builtin_amdgcn_sched_barrier(0);
@@ -289,6 +327,7 @@ __global__ __launch_bounds__(256 * WM) void gemm_tile_kernel(GemmParams p) {
   __syncthreads();
 
 #undef TILE_COMPUTE
+#undef TILE_PREFETCH
 #undef TILE_DMA
 #undef TILE_STAGE
 
