@@ -73,13 +73,14 @@ Plan make_plan(const moe_shape_t *s) {
   p.BM = avg <= 16 ? 16 : (avg <= 48 ? 32 : (avg <= 96 ? 64 : (avg <= 192 ? 128 : 256)));
   p.tile = p.BM >= 64;
   // GEMM1 promotes its K blocks in order (its output decides the re-quantised
-  // codes), so it never splits K; GEMM2 could (S2 > 1 sums the halves in the
-  // combine) but the small-tile kernel already has enough work items.
+  // codes), so it never splits K.  GEMM2 could (S2 > 1 planes of Y, summed by
+  // the combine), but measured at decode the full-K items are faster and the
+  // combine then reads one plane.
   p.S1 = 1;
+  p.S2 = 1;
   // small-tile batches: GEMM1 split over 32-column groups when the batch is
-  // too small to give every CU a 128-column item, GEMM2 over K halves
+  // too small to give every CU a 128-column item
   p.narrow1 = p.BM == 16 && TK <= 1024;
-  p.S2 = p.BM == 16 ? 2 : 1;
   p.NB1 = p.narrow1 ? s->I / gemm1_narrow_cols() : s->I / 128;
   // GEMM2 column blocks: 128 wide for the small-tile kernel, 256 otherwise
   p.NB2 = p.BM == 16 ? s->H / 128 : (s->H + 255) / 256;
@@ -156,9 +157,6 @@ moe_status_t enqueue_route(const moe_shape_t *s, const Plan &pl, const float *lo
   };
   RouteParams rp{logits, bias, r.ids, r.w, s->T, s->num_experts, s->n_group, s->topk_group,
                  s->top_k, s->routed_scaling_factor};
-  mark();
-  MOE_TRY_HIP(launch_route(rp, st));
-
   PermuteParams pp{};
   pp.topk_ids = r.ids;
   pp.chunk_counts = at<int32_t>(ws, pl.off_chunk_counts);
@@ -176,6 +174,8 @@ moe_status_t enqueue_route(const moe_shape_t *s, const Plan &pl, const float *lo
   pp.BM = pl.BM;
   pp.items_per_tile1 = pl.NB1 * pl.S1;
   pp.items_per_tile2 = pl.NB2 * pl.S2;
+  mark();
+  MOE_TRY_HIP(launch_route(rp, st));
   mark();
   MOE_TRY_HIP(launch_permute_count(pp, st));
   mark();

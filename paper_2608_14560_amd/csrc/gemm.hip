@@ -478,22 +478,23 @@ __global__ __launch_bounds__(Stream<G1>::kWaves * kWave) void gemm_stream_kernel
 }
 
 // GEMM1 for small batches, split over columns: a work item is one 16-row
-// M-tile and 32 intermediate columns (gate and up), so a handful of resident
-// experts still yields several work items per CU (HBM streaming needs all
-// 256 CUs busy; splitting K instead would change the promotion order that
-// decides the FP8 codes).  4 waves: waves 0/1 stream the gate rows
-// [32j + 16w, +16), waves 2/3 the matching up rows; each wave runs one MFMA
-// per 128-K step with a D-stage register prefetch ring (unconditional, so
-// loads stay in flight).  The SwiGLU output goes to a_buf [P, I] fp32 and
-// requant_kernel (the next launch) re-quantises it: no cross-workgroup
-// synchronisation.  Values and codes are bit-identical to the single-item
-// epilogue.
+// M-tile and 32 intermediate columns, so a handful of resident experts still
+// yields several work items per CU (HBM streaming needs all 256 CUs busy;
+// splitting K instead would change the promotion order that decides the FP8
+// codes).  2 waves: wave w streams the gate rows [32j + 16w, +16) and the
+// matching up rows against one A fragment (the tile's 16 gathered rows), two
+// MFMAs per 128-K step with a D-stage register prefetch ring (unconditional,
+// so loads stay in flight); SwiGLU pairs then sit in the same lane.  The
+// SwiGLU output goes to a_buf [P, I] fp32 and requant_kernel (the next launch)
+// re-quantises it: no cross-workgroup synchronisation.  Values and codes are
+// bit-identical to the single-item epilogue.
 constexpr int kNarrowCols = 32;
+constexpr int kNarrowWaves = kNarrowCols / 16;
 
 template <int D>
-__global__ __launch_bounds__(256) void gemm1_narrow_kernel(GemmParams p) {
+__global__ __launch_bounds__(kNarrowWaves * kWave) void gemm1_narrow_kernel(GemmParams p) {
+  constexpr int NT = kNarrowWaves * kWave;
   __shared__ int tb[1028];
-  __shared__ float up_lds[16][kNarrowCols + 1];
   extern __shared__ __attribute__((aligned(16))) float scales[];  // sa[16][KB], sb[2][KB]
 
   const int tid = threadIdx.x;
@@ -507,7 +508,7 @@ __global__ __launch_bounds__(256) void gemm1_narrow_kernel(GemmParams p) {
   const int item = (blockIdx.x & 7) * per_xcd + (blockIdx.x >> 3);
   if ((int)(blockIdx.x >> 3) >= per_xcd || item >= n_items) return;
 
-  for (int i = tid; i <= p.El; i += 256) tb[i] = p.tile_base[i];
+  for (int i = tid; i <= p.El; i += NT) tb[i] = p.tile_base[i];
   __syncthreads();
 
   const int X = p.NB;  // column groups per M-tile (no K split)
@@ -532,7 +533,7 @@ __global__ __launch_bounds__(256) void gemm1_narrow_kernel(GemmParams p) {
 
   float *sa_l = scales;
   float *sb_l = scales + 16 * KB;
-  for (int i = tid; i < 16 * KB; i += 256) {
+  for (int i = tid; i < 16 * KB; i += NT) {
     const int r = i / KB, kb = i % KB;
     const int src = p.perm_token[row0 + min(r, nrows - 1)];
     sa_l[i] = p.A_scale[(size_t)src * KB + kb];
@@ -540,62 +541,58 @@ __global__ __launch_bounds__(256) void gemm1_narrow_kernel(GemmParams p) {
   {
     const float *sg = p.B_scale + ((size_t)e * (p.N_total / 128) + blk) * KB;
     const float *su = p.B_scale + ((size_t)e * (p.N_total / 128) + p.I / 128 + blk) * KB;
-    for (int i = tid; i < KB; i += 256) {
+    for (int i = tid; i < KB; i += NT) {
       sb_l[i] = sg[i];
       sb_l[KB + i] = su[i];
     }
   }
 
-  const bool up = wave >= 2;
-  const int brow = (up ? p.I : 0) + j * kNarrowCols + 16 * (wave & 1) + r16;
+  const int col = j * kNarrowCols + 16 * wave + r16;  // this lane's weight row (gate)
   const int asrc = p.perm_token[row0 + min(r16, nrows - 1)];
   const uint8_t *a_ptr = p.A + (size_t)asrc * K + frag_off;
-  const uint8_t *b_ptr = p.B + (size_t)e * p.N_total * K + (size_t)brow * K + frag_off;
+  const uint8_t *bg_ptr = p.B + (size_t)e * p.N_total * K + (size_t)col * K + frag_off;
+  const uint8_t *bu_ptr = bg_ptr + (size_t)p.I * K;
 
-  v8i ra[D], rb[D];
+  v8i ra[D], rg[D], ru[D];
 #pragma unroll
   for (int d = 0; d < D; ++d) {
     const int kb = min(d, KB - 1);
     ra[d] = *reinterpret_cast<const v8i *>(a_ptr + (size_t)kb * 128);
-    rb[d] = *reinterpret_cast<const v8i *>(b_ptr + (size_t)kb * 128);
+    rg[d] = *reinterpret_cast<const v8i *>(bg_ptr + (size_t)kb * 128);
+    ru[d] = *reinterpret_cast<const v8i *>(bu_ptr + (size_t)kb * 128);
   }
   __syncthreads();  // scales staged
 
-  v4f acc = {0.f, 0.f, 0.f, 0.f};
+  v4f accg = {0.f, 0.f, 0.f, 0.f}, accu = {0.f, 0.f, 0.f, 0.f};
   const int srow = 4 * (lane >> 4);
-  const float *sb_w = sb_l + (up ? KB : 0);
   for (int base = 0; base < KB; base += D) {
 #pragma unroll
     for (int d = 0; d < D; ++d) {
       const int kb = base + d;
       if (kb < KB) {
         const v4f z = {0.f, 0.f, 0.f, 0.f};
-        const v4f t = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(ra[d], rb[d], z, 0, 0, 0, 0, 0, 0);
-        const float sbv = sb_w[kb];
+        const v4f tg = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(ra[d], rg[d], z, 0, 0, 0, 0, 0, 0);
+        const v4f tu = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(ra[d], ru[d], z, 0, 0, 0, 0, 0, 0);
+        const float sg = sb_l[kb], su = sb_l[KB + kb];
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
-          acc[i] = __builtin_fmaf(t[i], sa_l[(srow + i) * KB + kb] * sbv, acc[i]);
+        for (int i = 0; i < 4; ++i) {
+          const float sa = sa_l[(srow + i) * KB + kb];
+          accg[i] = __builtin_fmaf(tg[i], sa * sg, accg[i]);
+          accu[i] = __builtin_fmaf(tu[i], sa * su, accu[i]);
+        }
       }
       const int nk = min(kb + D, KB - 1);
       ra[d] = *reinterpret_cast<const v8i *>(a_ptr + (size_t)nk * 128);
-      rb[d] = *reinterpret_cast<const v8i *>(b_ptr + (size_t)nk * 128);
+      rg[d] = *reinterpret_cast<const v8i *>(bg_ptr + (size_t)nk * 128);
+      ru[d] = *reinterpret_cast<const v8i *>(bu_ptr + (size_t)nk * 128);
     }
   }
 
-  // SwiGLU: the up waves hand their columns to the gate waves through LDS
-  if (up) {
+  // accumulator element i of this lane: row srow + i, column `col`
 #pragma unroll
-    for (int i = 0; i < 4; ++i) up_lds[srow + i][16 * (wave & 1) + r16] = acc[i];
-  }
-  __syncthreads();
-  if (!up) {
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int r = srow + i;
-      if (r < nrows)
-        p.abuf[(size_t)(row0 + r) * p.I + j * kNarrowCols + 16 * wave + r16] =
-            swiglu_spec(acc[i], up_lds[r][16 * wave + r16]);
-    }
+  for (int i = 0; i < 4; ++i) {
+    const int r = srow + i;
+    if (r < nrows) p.abuf[(size_t)(row0 + r) * p.I + col] = swiglu_spec(accg[i], accu[i]);
   }
 }
 
@@ -743,7 +740,7 @@ hipError_t launch_gemm1(const GemmParams &p, int BM, int grid, hipStream_t st) {
 hipError_t launch_gemm1_narrow(const GemmParams &p, int grid, hipStream_t st) {
   if (grid <= 0) return hipSuccess;
   const size_t lds = sizeof(float) * 18 * (size_t)p.KB;
-  hipLaunchKernelGGL(gemm1_narrow_kernel<kStreamDepth>, dim3(grid), dim3(256), lds, st, p);
+  hipLaunchKernelGGL(gemm1_narrow_kernel<kStreamDepth>, dim3(grid), dim3(kNarrowWaves * kWave), lds, st, p);
   return hipGetLastError();
 }
 int gemm1_narrow_cols() { return kNarrowCols; }

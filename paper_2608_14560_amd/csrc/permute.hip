@@ -13,14 +13,13 @@
 //            routing, never on timing), and writes perm_token / perm_pair /
 //            pair_row.  Workgroup 0 also writes expert_offsets, the M-tile
 //            prefix of every expert and the GEMM work-item counts.
-#include "moe_device.h"
+#include "scatter_device.h"
 
 namespace moe {
 namespace {
 
 constexpr int kThreads = 256;
-constexpr int kWaves = kThreads / kWave;
-constexpr int kMaxEl = 1024;
+constexpr int kMaxEl = kPermMaxEl;
 
 __global__ __launch_bounds__(kThreads) void count_kernel(PermuteParams p) {
   __shared__ int hist[kMaxEl];
@@ -38,141 +37,10 @@ __global__ __launch_bounds__(kThreads) void count_kernel(PermuteParams p) {
     p.chunk_counts[(size_t)blockIdx.x * p.El + e] = hist[e];
 }
 
-// Exclusive scan of v over the block (one value per thread); returns the
-// exclusive prefix and writes the block total to *total.
-__device__ int block_exclusive_scan(int v, int *wsum, int *total) {
-  const int lane = threadIdx.x & (kWave - 1);
-  const int w = threadIdx.x / kWave;
-  int x = v;
-#pragma unroll
-  for (int off = 1; off < kWave; off <<= 1) {
-    const int y = __shfl_up(x, off);
-    if (lane >= off) x += y;
-  }
-  if (lane == kWave - 1) wsum[w] = x;
-  __syncthreads();
-  int before = 0, all = 0;
-  for (int i = 0; i < kWaves; ++i) {
-    if (i < w) before += wsum[i];
-    all += wsum[i];
-  }
-  __syncthreads();
-  *total = all;
-  return before + x - v;
-}
-
-// SINGLE: the batch is one chunk; the workgroup counts its own pairs (an LDS
-// histogram) instead of reading the count kernel's output.
 template <bool SINGLE>
 __global__ __launch_bounds__(kThreads) void scatter_kernel(PermuteParams p) {
-  // per expert: start of this chunk's rows, then per-wave occupancy bitmaps
-  __shared__ int base[kMaxEl];
-  __shared__ int hist[SINGLE ? kMaxEl : 1];
-  __shared__ unsigned long long bits[kWaves][kMaxEl];
-  __shared__ int wsum[kWaves];
-
-  const int chunk = blockIdx.x;
-  const int lane = threadIdx.x & (kWave - 1);
-  const int w = threadIdx.x / kWave;
-
-  for (int e = threadIdx.x; e < p.El; e += kThreads) {
-    for (int i = 0; i < kWaves; ++i) bits[i][e] = 0ull;
-    if (SINGLE) hist[e] = 0;
-  }
-  if (SINGLE) {
-    __syncthreads();
-    const int t = threadIdx.x;
-    if (t < p.T)
-      for (int j = 0; j < p.K; ++j) {
-        const int le = p.topk_ids[(size_t)t * p.K + j] - p.offset;
-        if (le >= 0 && le < p.El) atomicAdd(&hist[le], 1);
-      }
-    __syncthreads();
-  }
-  // count of local expert e in chunk c
-  auto cnt = [&](int c, int e) {
-    return SINGLE ? hist[e] : p.chunk_counts[(size_t)c * p.El + e];
-  };
-
-  // expert offsets: exclusive scan of the per-expert totals over all chunks.
-  // Each thread owns a contiguous run of experts.
-  const int per = (p.El + kThreads - 1) / kThreads;
-  const int e0 = threadIdx.x * per;
-  int tot_run = 0;
-  for (int e = e0; e < e0 + per && e < p.El; ++e) {
-    int tot = 0, before = 0;
-    for (int c = 0; c < p.nchunks; ++c) {
-      const int n = cnt(c, e);
-      tot += n;
-      if (c < chunk) before += n;
-    }
-    base[e] = before;   // chunk-local part; the expert offset is added below
-    tot_run += tot;
-  }
-  int P = 0;
-  const int run_start = block_exclusive_scan(tot_run, wsum, &P);
-  // walk the run again to turn totals into offsets
-  int acc = run_start;
-  for (int e = e0; e < e0 + per && e < p.El; ++e) {
-    int tot = 0;
-    for (int c = 0; c < p.nchunks; ++c) tot += cnt(c, e);
-    if (chunk == 0) p.expert_offsets[e] = acc;
-    base[e] += acc;
-    acc += tot;
-  }
-  if (chunk == 0 && threadIdx.x == 0) p.expert_offsets[p.El] = P;
-  __syncthreads();
-
-  // rank the chunk's pairs: bit `lane` of bits[w][e] marks that the lane's
-  // token holds local expert e
-  const int t = chunk * kChunkTokens + threadIdx.x;
-  const bool live = t < p.T;
-  if (live) {
-    for (int j = 0; j < p.K; ++j) {
-      const int le = p.topk_ids[(size_t)t * p.K + j] - p.offset;
-      if (le >= 0 && le < p.El) atomicOr(&bits[w][le], 1ull << lane);
-    }
-  }
-  __syncthreads();
-  if (live) {
-    const unsigned long long below = (lane == 0) ? 0ull : (~0ull >> (kWave - lane));
-    for (int j = 0; j < p.K; ++j) {
-      const int le = p.topk_ids[(size_t)t * p.K + j] - p.offset;
-      int row = -1;
-      if (le >= 0 && le < p.El) {
-        row = base[le];
-        for (int i = 0; i < w; ++i) row += __popcll(bits[i][le]);
-        row += __popcll(bits[w][le] & below);
-        p.perm_token[row] = t;
-        p.perm_pair[row] = t * p.K + j;
-      }
-      p.pair_row[(size_t)t * p.K + j] = row;
-    }
-  }
-
-  if (chunk != 0) return;
-
-  // M-tile prefix per expert and the GEMM work-item counts
-  __syncthreads();
-  int tiles_run = 0;
-  for (int e = e0; e < e0 + per && e < p.El; ++e) {
-    int tot = 0;
-    for (int c = 0; c < p.nchunks; ++c) tot += cnt(c, e);
-    tiles_run += (tot + p.BM - 1) / p.BM;
-  }
-  int n_tiles = 0;
-  int tacc = block_exclusive_scan(tiles_run, wsum, &n_tiles);
-  for (int e = e0; e < e0 + per && e < p.El; ++e) {
-    int tot = 0;
-    for (int c = 0; c < p.nchunks; ++c) tot += cnt(c, e);
-    p.tile_base[e] = tacc;
-    tacc += (tot + p.BM - 1) / p.BM;
-  }
-  if (threadIdx.x == 0) {
-    p.tile_base[p.El] = n_tiles;
-    p.n_items[0] = n_tiles * p.items_per_tile1;
-    p.n_items[1] = n_tiles * p.items_per_tile2;
-  }
+  __shared__ ScatterLds<kThreads, SINGLE> sh;
+  scatter_chunk<kThreads, SINGLE>(p, blockIdx.x, p.topk_ids, sh);
 }
 
 }  // namespace

@@ -243,11 +243,11 @@ __device__ __forceinline__ float key_value(uint32_t h) {
   return __uint_as_float(u);
 }
 
+// Routing of token t by one wave (power-of-two group size S): writes the
+// token's ids and weights.
 template <int EPL, int S>
-__global__ __launch_bounds__(256) void route_seg_kernel(RouteParams p) {
+__device__ __forceinline__ void route_token_seg(const RouteParams &p, int t) {
   const int lane = threadIdx.x & (kWave - 1);
-  const int t = blockIdx.x * (blockDim.x / kWave) + (threadIdx.x / kWave);
-  if (t >= p.T) return;
   const float *lrow = p.logits + (size_t)t * p.E;
   const int seg_lane = lane & (S - 1);
 
@@ -338,6 +338,13 @@ __global__ __launch_bounds__(256) void route_seg_kernel(RouteParams p) {
     p.topk_ids[(size_t)t * p.K + lane] = my_id;
     p.topk_w[(size_t)t * p.K + lane] = (my_s / sum) * p.rsf;
   }
+}
+
+template <int EPL, int S>
+__global__ __launch_bounds__(256) void route_seg_kernel(RouteParams p) {
+  const int t = blockIdx.x * (blockDim.x / kWave) + (threadIdx.x / kWave);
+  if (t >= p.T) return;
+  route_token_seg<EPL, S>(p, t);
 }
 
 template <int EPL>

@@ -141,6 +141,21 @@ def test_route_bitexact(M, name, seed):
                               perm_token=perm, pair_row=pr))
 
 
+@pytest.mark.parametrize("T", [1, 31, 32, 33, 255, 256, 257])
+def test_route_batch_sizes(M, T):
+    """Routing and permutation at batch sizes around a wave of tokens and the
+    256-token permutation chunk (one chunk, one chunk full, two chunks), bit
+    for bit."""
+    cfg = W.CONFIGS["decode"].with_(T=T)
+    logits, bias, _ = W.gen_router(cfg, 7, device="cuda")
+    ro = M.route(M.Shape.of(cfg), logits, bias)
+    torch.cuda.synchronize()
+    ref_ids, ref_w = oracle.route(oracle.shape_of(cfg), logits.cpu().numpy(), bias.cpu().numpy())
+    offs, perm, pr = oracle.permute(oracle.shape_of(cfg), ref_ids)
+    check_route(cfg, ro, dict(topk_ids=ref_ids, topk_weights=ref_w, expert_offsets=offs,
+                              perm_token=perm, pair_row=pr))
+
+
 def test_route_ties_bitexact(M):
     """Logits on a coarse grid and zero bias produce many exactly equal keys; the
     lower expert / group index must win every tie."""
