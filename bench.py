@@ -72,9 +72,13 @@ def layer_bytes(cfg, P: int, touched: int) -> int:
 
 
 def source_digest() -> str:
+    """Digest of the kernel sources (every file of the library's csrc): a
+    traffic measurement is reported only while it matches."""
     h = hashlib.sha256()
-    for f in ("gemm.hip", "moe_device.h"):
-        with open(os.path.join(ROOT, "paper_2608_14560_amd", "csrc", f), "rb") as fh:
+    d = os.path.join(ROOT, "paper_2608_14560_amd", "csrc")
+    for f in sorted(os.listdir(d)):
+        with open(os.path.join(d, f), "rb") as fh:
+            h.update(f.encode())
             h.update(fh.read())
     return h.hexdigest()[:16]
 
