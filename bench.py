@@ -46,8 +46,8 @@ def flops_per_pair(cfg) -> int:
 
 def small_tile_path(cfg) -> bool:
     """The library's choice of the column-split GEMM1 (plus a re-quantisation
-    launch): 16-row M-tiles and at most 1024 (token, slot) pairs."""
-    return cfg.T * cfg.top_k / cfg.num_experts <= 16 and cfg.T * cfg.top_k <= 1024
+    launch): batches with 16-row M-tiles (at most 16 expected rows per expert)."""
+    return cfg.T * cfg.top_k / cfg.num_experts <= 16
 
 
 def gemm1_bytes(cfg, P: int, touched: int) -> int:

@@ -78,9 +78,9 @@ Plan make_plan(const moe_shape_t *s) {
   // combine then reads one plane.
   p.S1 = 1;
   p.S2 = 1;
-  // small-tile batches: GEMM1 split over 32-column groups when the batch is
-  // too small to give every CU a 128-column item
-  p.narrow1 = p.BM == 16 && TK <= 1024;
+  // 16-row tiles: GEMM1 split over 32-column groups, so that a batch with few
+  // rows per expert still gives every CU work items (it streams weights)
+  p.narrow1 = p.BM == 16;
   p.NB1 = p.narrow1 ? s->I / gemm1_narrow_cols() : s->I / 128;
   // GEMM2 column blocks: 128 wide for the small-tile kernel, 256 otherwise
   p.NB2 = p.BM == 16 ? s->H / 128 : (s->H + 255) / 256;

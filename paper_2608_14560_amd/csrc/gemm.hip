@@ -1,31 +1,34 @@
-// gemm.hip -- stage (3) and (4) of the Fused MoE block (paper Section 3.1.1)
-// on CDNA4 FP8 matrix cores.
+// gemm.hip -- stages (3) and (4) of the Fused MoE block (paper Section
+// 3.1.1) for small and mid-sized batches, on CDNA4 FP8 matrix cores, and the
+// combine of every batch size.
 //
 //  GEMM1: per resident expert e, rows = the tokens routed to e (gathered
 //         through perm_token while the A tile is loaded: the paper's separate
 //         gather kernel is folded into the GEMM's loads),
 //         G = sum_kb (A_kb W13_kb^T) * sa[row,kb] * sw[n/128,kb]   (fp32)
-//         epilogue: a = silu(gate) * up, per-row 1x128 amax, scale =
-//         amax/448, FP8 re-quantisation -> act [P, I] e4m3 + act_scale.
-//  GEMM2: Y = sum_kb (act_kb W2_kb^T) * sa2 * sw2 -> Y [S, P, H] fp32
+//         then a = silu(gate) * up, per-row 1x128 amax, scale = amax/448,
+//         FP8 re-quantisation -> act [P, I] e4m3 + act_scale.
+//  GEMM2: Y = sum_kb (act_kb W2_kb^T) * sa2 * sw2 -> Y [P, H] fp32
 //  finalize: out[t] = bf16( sum over resident slots j (slot order) of
-//            w_j * sum_s Y[s, pair_row[t,j]] ).
+//            w_j * Y[pair_row[t,j]] ).
 //
-// Work item = (M-tile of one expert, column block, K split).  Items of one
-// expert are contiguous with the M-tile index fastest, so the M-tiles that
-// share a weight panel are adjacent; workgroup b is mapped to item
-// (b % 8) * ceil(n/8) + b / 8 so those neighbours land on the same XCD
-// (workgroups are dispatched round-robin over the 8 XCDs) and reuse the panel
-// from that XCD's L2.
+// Kernels here: the column-split GEMM1 and its re-quantisation launch plus
+// the streaming GEMM2 (16-row tiles), the LDS-staged GEMM1/GEMM2 for 32-row
+// tiles, the finalize, and test hooks.  Larger tiles are in gemm_tile.hip.
 //
-// Tiles: BM rows x 256 columns x 128 K per step, 4 waves.  In GEMM1 wave w
-// owns gate columns [32w, 32w+32) and the matching up columns of the
-// 128-wide intermediate block, so SwiGLU pairs live in the same lane.  Each
-// 128-K step is one v_mfma_f32_16x16x128_f8f6f4 per 16x16 sub-tile, started
-// from zero and promoted into the fp32 accumulator with one FMA by the
-// product of the row's activation scale and the block's weight scale.
-// A and B tiles are staged through LDS (double buffered, rows padded to
-// 144 bytes so the MFMA operand reads are bank-conflict free).
+// Work items of an expert are contiguous; workgroup b is mapped to item
+// (b % 8) * ceil(n/8) + b / 8 so neighbouring items land on the same XCD
+// (workgroups are dispatched round-robin over the 8 XCDs) and share weight
+// panels and A tiles in that XCD's L2.  Each 128-K step is one
+// v_mfma_f32_16x16x128_f8f6f4 per 16x16 sub-tile, started from zero and
+// promoted into the fp32 accumulator with one FMA by the product of the
+// row's activation scale and the block's weight scale.
+//
+// The LDS-staged kernel: BM rows x 256 columns x 128 K per step, 4 waves;
+// in GEMM1 wave w owns gate columns [32w, 32w+32) and the matching up
+// columns of the 128-wide intermediate block, so SwiGLU pairs live in the
+// same lane.  A and B tiles are staged through LDS (double buffered, rows
+// padded to 144 bytes).
 #include "moe_device.h"
 
 namespace moe {
@@ -276,34 +279,25 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(GemmParams p) {
     }
 }
 
-// Small-tile variant (BM = 16): the weight fragments are streamed from HBM
-// straight into registers through a D-stage prefetch ring, with no LDS round
-// trip and no barrier in the K loop.  Prefetches are issued unconditionally
-// (past the end they re-read the last K block) so the compiler can keep D
-// loads in flight instead of draining the queue at every branch.
-//   GEMM1: 8 waves; wave w owns the gate and up columns [16w, 16w+16) of the
-//          128-wide intermediate block (SwiGLU pairs in one lane).
-//   GEMM2: 4 waves; wave w owns output columns [32w, 32w+32) of a 128-wide block.
-// Every wave loads the tile's A fragment itself (16 rows x 128 bytes per K
-// step; the waves of a workgroup hit it in L1).  Activation and weight block
-// scales of the whole K range are staged in LDS once.  The per-element
-// arithmetic (MFMA block products, promotion order, epilogue) is the same as
-// the LDS-staged kernel's.
-template <bool G1>
-struct Stream {
-  static constexpr int kWaves = G1 ? 8 : 4;
-  static constexpr int kCols = 128;  // columns of the block per work item
-};
+// GEMM2 for small batches (BM = 16): the weight fragments are streamed from
+// HBM straight into registers through a D-stage prefetch ring, with no LDS
+// round trip and no barrier in the K loop.  Prefetches are issued
+// unconditionally (past the end they re-read the last K block) so the
+// compiler can keep D loads in flight instead of draining the queue at every
+// branch.  4 waves; wave w owns output columns [32w, 32w+32) of a 128-wide
+// block.  Activation and weight block scales of the whole K range are staged
+// in LDS once.  The per-element arithmetic (MFMA block products, promotion
+// order) is the same as the other GEMM kernels'.
+constexpr int kStreamWaves = 4;
 
 // ALDS: the item's whole A tile (16 rows x its K range) is staged in LDS once
 // (rows padded by 16 bytes) instead of every wave loading it from L2 at each
 // K step; used when the tile fits (GEMM2 at small batches).
-template <bool G1, int D, bool ALDS>
-__global__ __launch_bounds__(Stream<G1>::kWaves * kWave) void gemm_stream_kernel(GemmParams p) {
-  constexpr int NW = Stream<G1>::kWaves;
+template <int D, bool ALDS>
+__global__ __launch_bounds__(kStreamWaves * kWave) void gemm2_stream_kernel(GemmParams p) {
+  constexpr int NW = kStreamWaves;
   __shared__ int tb[1028];
-  __shared__ float amax_lds[NW][16];
-  extern __shared__ __attribute__((aligned(16))) float scales[];  // sa[16][KB], sb[2][KB], A tile
+  extern __shared__ __attribute__((aligned(16))) float scales[];  // sa[16][KB], sb[KB] (+1 row), A tile
 
   const int tid = threadIdx.x;
   const int lane = tid & (kWave - 1);
@@ -343,18 +337,9 @@ __global__ __launch_bounds__(Stream<G1>::kWaves * kWave) void gemm_stream_kernel
   const size_t K = (size_t)p.K;
   const int KB = p.KB;
 
-  // B rows of the wave's two sub-tiles and their 128-row scale blocks
-  int brow0, brow1, bblk0, bblk1;
-  if (G1) {
-    brow0 = nb * 128 + 16 * wave + r16;
-    brow1 = p.I + nb * 128 + 16 * wave + r16;
-    bblk0 = nb;
-    bblk1 = p.I / 128 + nb;
-  } else {
-    brow0 = nb * 128 + 32 * wave + r16;
-    brow1 = brow0 + 16;
-    bblk0 = bblk1 = nb;
-  }
+  // B rows of the wave's two sub-tiles (one 128-row scale block)
+  const int brow0 = nb * 128 + 32 * wave + r16;
+  const int brow1 = brow0 + 16;
 
   // stage the scales: sa[r][kb] of the tile's rows, sb[0/1][kb] of the blocks
   float *sa_l = scales;
@@ -362,22 +347,17 @@ __global__ __launch_bounds__(Stream<G1>::kWaves * kWave) void gemm_stream_kernel
   for (int i = tid; i < 16 * KB; i += NW * kWave) {
     const int r = i / KB, kb = i % KB;
     const int rr = min(r, nrows - 1);
-    const int src = G1 ? p.perm_token[row0 + rr] : row0 + rr;
+    const int src = row0 + rr;
     sa_l[i] = p.A_scale[(size_t)src * KB + kb];
   }
   {
-    const int blk0 = G1 ? bblk0 : nb, blk1 = G1 ? p.I / 128 + nb : nb;
-    const float *sb0 = p.B_scale + ((size_t)e * (p.N_total / 128) + blk0) * KB;
-    const float *sb1 = p.B_scale + ((size_t)e * (p.N_total / 128) + blk1) * KB;
-    for (int i = tid; i < KB; i += NW * kWave) {
-      sb_l[i] = sb0[i];
-      sb_l[KB + i] = sb1[i];
-    }
+    const float *sb0 = p.B_scale + ((size_t)e * (p.N_total / 128) + nb) * KB;
+    for (int i = tid; i < KB; i += NW * kWave) sb_l[i] = sb0[i];
   }
 
   // A fragment source: the lane's row (ragged tails repeat the last row)
   const int arow = min(r16, nrows - 1);
-  const int asrc = G1 ? p.perm_token[row0 + arow] : row0 + arow;
+  const int asrc = row0 + arow;
   const uint8_t *a_ptr = p.A + (size_t)asrc * K + frag_off;
   const uint8_t *Bexp = p.B + (size_t)e * p.N_total * K;
   const uint8_t *b_ptr0 = Bexp + (size_t)brow0 * K + frag_off;
@@ -391,7 +371,7 @@ __global__ __launch_bounds__(Stream<G1>::kWaves * kWave) void gemm_stream_kernel
     for (int c = tid; c < chunks; c += NW * kWave) {
       const int r = c / (n * 8), off = (c % (n * 8)) * 16;
       const int rr = min(r, nrows - 1);
-      const int src = G1 ? p.perm_token[row0 + rr] : row0 + rr;
+      const int src = row0 + rr;
       *reinterpret_cast<u32x4 *>(a_l + r * astride + off) =
           *reinterpret_cast<const u32x4 *>(p.A + (size_t)src * K + (size_t)kb0 * 128 + off);
     }
@@ -412,7 +392,6 @@ __global__ __launch_bounds__(Stream<G1>::kWaves * kWave) void gemm_stream_kernel
 
   v4f acc0 = {0.f, 0.f, 0.f, 0.f}, acc1 = {0.f, 0.f, 0.f, 0.f};
   const int srow = 4 * (lane >> 4);
-  const int sb1_off = G1 ? KB : 0;
   for (int base = 0; base < n; base += D) {
 #pragma unroll
     for (int d = 0; d < D; ++d) {
@@ -423,12 +402,12 @@ __global__ __launch_bounds__(Stream<G1>::kWaves * kWave) void gemm_stream_kernel
         const v8i af = ALDS ? lds_frag(a_lds + it * 128) : ra[d];
         const v4f t0 = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(af, rb0[d], z, 0, 0, 0, 0, 0, 0);
         const v4f t1 = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(af, rb1[d], z, 0, 0, 0, 0, 0, 0);
-        const float s0 = sb_l[kb], s1 = sb_l[sb1_off + kb];
+        const float s0 = sb_l[kb];
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
           const float sa = sa_l[(srow + i) * KB + kb];
           acc0[i] = __builtin_fmaf(t0[i], sa * s0, acc0[i]);
-          acc1[i] = __builtin_fmaf(t1[i], sa * s1, acc1[i]);
+          acc1[i] = __builtin_fmaf(t1[i], sa * s0, acc1[i]);
         }
       }
       MOE_SLOAD(d, kb0 + min(it + D, n - 1));
@@ -436,43 +415,14 @@ __global__ __launch_bounds__(Stream<G1>::kWaves * kWave) void gemm_stream_kernel
   }
 #undef MOE_SLOAD
 
-  if (!G1) {
-    float *Ys = p.Y + (size_t)s * p.P_max * p.H;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int r = srow + i;
-      if (r < nrows) {
-        float *yrow = Ys + (size_t)(row0 + r) * p.H + nb * 128 + 32 * wave + r16;
-        yrow[0] = acc0[i];
-        yrow[16] = acc1[i];
-      }
-    }
-    return;
-  }
-
-  // SwiGLU, then the per-row amax over the 128 columns (16 lanes x 8 waves)
-  float av[4];
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    av[i] = swiglu_spec(acc0[i], acc1[i]);
-    float mx = fabsf(av[i]);
-#pragma unroll
-    for (int off = 1; off < 16; off <<= 1) mx = fmaxf(mx, __shfl_xor(mx, off));
-    if (r16 == 0) amax_lds[wave][srow + i] = mx;
-  }
-  __syncthreads();
-  const int IB = p.I / 128;
+  float *Ys = p.Y + (size_t)s * p.P_max * p.H;
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     const int r = srow + i;
-    float amax = amax_lds[0][r];
-#pragma unroll
-    for (int w = 1; w < NW; ++w) amax = fmaxf(amax, amax_lds[w][r]);
-    const float scale = (amax > 0.0f) ? amax / 448.0f : 1.0f;
     if (r < nrows) {
-      const uint32_t q = (amax > 0.0f) ? e4m3x2_rne_sat(av[i] / scale, 0.0f) : 0u;
-      p.act[(size_t)(row0 + r) * p.I + nb * 128 + 16 * wave + r16] = (uint8_t)(q & 0xff);
-      if (wave == 0 && r16 == 0) p.act_scale[(size_t)(row0 + r) * IB + nb] = scale;
+      float *yrow = Ys + (size_t)(row0 + r) * p.H + nb * 128 + 32 * wave + r16;
+      yrow[0] = acc0[i];
+      yrow[16] = acc1[i];
     }
   }
 }
@@ -673,30 +623,20 @@ hipError_t launch_gemm_bm(const GemmParams &p, int grid, hipStream_t st) {
 
 constexpr int kStreamDepth = 4;
 
-template <bool G1>
-hipError_t launch_gemm(const GemmParams &p, int BM, int grid, hipStream_t st) {
-  if (grid <= 0) return hipSuccess;
-  switch (BM) {
-    case 16: {
-      // the A tile of one item (16 rows x its K range) goes to LDS when it is
-      // at most 32 KB (GEMM2 at small batches)
-      const int n_max = (p.KB + p.S - 1) / p.S;
-      const size_t a_bytes = 16 * ((size_t)n_max * 128 + 16);
-      const bool alds = !G1 && a_bytes <= 32768 + 256;
-      const size_t lds = ((sizeof(float) * 18 * (size_t)p.KB + 15) & ~(size_t)15) + (alds ? a_bytes : 0);
-      if (alds)
-        hipLaunchKernelGGL((gemm_stream_kernel<G1, kStreamDepth, true>), dim3(grid),
-                           dim3(Stream<G1>::kWaves * kWave), lds, st, p);
-      else
-        hipLaunchKernelGGL((gemm_stream_kernel<G1, kStreamDepth, false>), dim3(grid),
-                           dim3(Stream<G1>::kWaves * kWave), lds, st, p);
-      return hipGetLastError();
-    }
-    case 32: return launch_gemm_bm<32, G1>(p, grid, st);
-    case 64: return launch_gemm_bm<64, G1>(p, grid, st);
-    case 128: return launch_gemm_bm<128, G1>(p, grid, st);
-    default: return hipErrorInvalidValue;
-  }
+// GEMM2 for 16-row tiles: the streaming kernel (its item's A tile in LDS
+// when it is at most 32 KB)
+hipError_t launch_gemm2_stream(const GemmParams &p, int grid, hipStream_t st) {
+  const int n_max = (p.KB + p.S - 1) / p.S;
+  const size_t a_bytes = 16 * ((size_t)n_max * 128 + 16);
+  const bool alds = a_bytes <= 32768 + 256;
+  const size_t lds = ((sizeof(float) * 18 * (size_t)p.KB + 15) & ~(size_t)15) + (alds ? a_bytes : 0);
+  if (alds)
+    hipLaunchKernelGGL((gemm2_stream_kernel<kStreamDepth, true>), dim3(grid), dim3(kStreamWaves * kWave),
+                       lds, st, p);
+  else
+    hipLaunchKernelGGL((gemm2_stream_kernel<kStreamDepth, false>), dim3(grid), dim3(kStreamWaves * kWave),
+                       lds, st, p);
+  return hipGetLastError();
 }
 
 // Test hook: the FP8 encoder of the re-quantisation epilogue, elementwise.
@@ -734,8 +674,11 @@ hipError_t launch_debug_mfma_block(const uint8_t *a, const uint8_t *b, float *d,
   return hipGetLastError();
 }
 
+// GEMM1 with the LDS-staged kernel: 32-row tiles (16-row batches use the
+// column-split kernel, 64 rows and more the large-tile kernels)
 hipError_t launch_gemm1(const GemmParams &p, int BM, int grid, hipStream_t st) {
-  return launch_gemm<true>(p, BM, grid, st);
+  if (grid <= 0) return hipSuccess;
+  return BM == 32 ? launch_gemm_bm<32, true>(p, grid, st) : hipErrorInvalidValue;
 }
 hipError_t launch_gemm1_narrow(const GemmParams &p, int grid, hipStream_t st) {
   if (grid <= 0) return hipSuccess;
@@ -750,16 +693,13 @@ hipError_t launch_requant(const GemmParams &p, int P_max, hipStream_t st) {
   hipLaunchKernelGGL(requant_kernel, dim3((pairs + 15) / 16), dim3(256), 0, st, p);
   return hipGetLastError();
 }
+// GEMM2 for 16- and 32-row tiles (64 rows and more: the large-tile kernels)
 hipError_t launch_gemm2(const GemmParams &p, int BM, int grid, hipStream_t st) {
-  return launch_gemm<false>(p, BM, grid, st);
-}
-size_t gemm_lds_bytes(int BM) {
+  if (grid <= 0) return hipSuccess;
   switch (BM) {
-    case 16: return Layout<16>::TOTAL;
-    case 32: return Layout<32>::TOTAL;
-    case 64: return Layout<64>::TOTAL;
-    case 128: return Layout<128>::TOTAL;
-    default: return 0;
+    case 16: return launch_gemm2_stream(p, grid, st);
+    case 32: return launch_gemm_bm<32, false>(p, grid, st);
+    default: return hipErrorInvalidValue;
   }
 }
 

@@ -149,6 +149,5 @@ hipError_t launch_gemm2(const GemmParams &p, int BM, int grid, hipStream_t st);
 hipError_t launch_gemm_tile(const GemmParams &p, bool g1, int BM, int grid, hipStream_t st);
 int gemm_tile_cols();
 hipError_t launch_finalize(const FinalizeParams &p, hipStream_t st);
-size_t gemm_lds_bytes(int BM);
 
 }  // namespace moe
