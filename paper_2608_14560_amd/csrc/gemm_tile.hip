@@ -193,20 +193,29 @@ __global__ __launch_bounds__(256 * WM) void gemm_tile_kernel(GemmParams p) {
     const int rg = min(wrow0 + r, p.N_total - 1);  // ragged last GEMM2 block
     b_src[j] = Bexp + (size_t)rg * K + 16 * ((lane & 7) ^ tile_swz(r));
   }
-  // L2 prefetch one K-step beyond the ring: one dword of each 128-byte line
-  // of the step's A rows and weight rows, 64 lines per load, spread over the
-  // waves; the dwords land in a junk LDS area and are never read.
-  constexpr int kPfLoads = (BM + 256 + 4 * WM * kWave - 1) / (4 * WM * kWave);
+  // L2 prefetch one K-step beyond the ring: one dword per 128-byte line,
+  // landing in a junk LDS area that is never read.  Each line is prefetched
+  // by one of the items that share it and run side by side on the XCD (the
+  // others then hit in L2 instead of all waiting on the same miss): the A
+  // rows of an M-tile are split over the kGroupN column blocks of its group,
+  // the weight rows of a column block over MS consecutive M-tiles.  Lanes
+  // past the item's share repeat its first line (one request per load).
+  const int ms = nt_e >= 4 ? 4 : (nt_e >= 2 ? 2 : 1);
+  const int a_share = BM / kGroupN;
+  const int w_share = 256 / ms;
+  const int a_first = (nb % kGroupN) * a_share;
+  const int w_first = (mt_idx % ms) * w_share;
+  constexpr int kPfLoads = (BM / kGroupN + 256 + 4 * WM * kWave - 1) / (4 * WM * kWave);
   const uint8_t *pf_src[kPfLoads];
 #pragma unroll
   for (int j = 0; j < kPfLoads; ++j) {
-    const int line = (wave * kPfLoads + j) * kWave + lane;  // 0 .. BM+256 (clamped)
-    const int r = min(line, BM + 255);
-    if (r < BM) {
-      const int rr = min(r, nrows - 1);
+    int line = (wave * kPfLoads + j) * kWave + lane;
+    if (line >= a_share + w_share) line = 0;
+    if (line < a_share) {
+      const int rr = min(a_first + line, nrows - 1);
       pf_src[j] = p.A + (size_t)(G1 ? p.perm_token[row0 + rr] : row0 + rr) * K;
     } else {
-      const int c = r - BM;  // weight row c % 64 of column wave c / 64
+      const int c = w_first + line - a_share;  // weight row c % 64 of column wave c / 64
       const int w2 = c >> 6;
       const int base = G1 ? (w2 >> 1) * p.I + nb * 128 + 64 * (w2 & 1) : nb * kTileCols + 64 * w2;
       pf_src[j] = Bexp + (size_t)min(base + (c & 63), p.N_total - 1) * K;
@@ -260,8 +269,12 @@ __global__ __launch_bounds__(256 * WM) void gemm_tile_kernel(GemmParams p) {
 // One K-step of the wave's 16 MT x 64 block: per 16-row block m, four MFMAs
 // (one per 16-column sub-tile), each started from zero and promoted with one
 // FMA per accumulator; the next block's A fragment is read while this one
-// is multiplied.  Two waves per SIMD (8-wave tiles) fill each other's
-// MFMA-to-FMA latency.
+// is multiplied.  The compiler is left free to interleave the blocks: an
+// FMA that reads the result of the MFMA issued just before it stalls for
+// the whole matrix-core pass, so promotions are scheduled a few MFMAs late
+// (a register-only probe on gfx950: 42 cycles per MFMA with one wave per
+// SIMD, 62 when each block's promotions are pinned behind its MFMAs; 32 is
+// the issue rate).  Two waves per SIMD (8-wave tiles) fill the rest.
 #define TILE_COMPUTE(st, kb)                                                            \
   do {                                                                                  \
     const uint8_t *as_ = TILE_STAGE(st) + wm * MT * 2048;                               \
@@ -293,7 +306,6 @@ __global__ __launch_bounds__(256 * WM) void gemm_tile_kernel(GemmParams p) {
       _Pragma("unroll") for (int n = 0; n < 4; ++n)                                     \
           _Pragma("unroll") for (int i = 0; i < 4; ++i)                                 \
               acc[m][n][i] = __builtin_fmaf(t_[n][i], c_, acc[m][n][i]);               \
-      __builtin_amdgcn_sched_barrier(0);                                                \
     }                                                                                   \
   } while (0)
 
