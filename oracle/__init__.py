@@ -72,6 +72,8 @@ def lib():
         L.oracle_sigmoid_array.restype = None
         L.oracle_route.argtypes = [ctypes.POINTER(OracleShape), P, P, P, P]
         L.oracle_route.restype = ctypes.c_int
+        L.oracle_router_logits.argtypes = [ctypes.POINTER(OracleShape), P, P, P, P]
+        L.oracle_router_logits.restype = ctypes.c_int
         L.oracle_permute.argtypes = [ctypes.POINTER(OracleShape), P, P, P, P]
         L.oracle_permute.restype = ctypes.c_int
         L.oracle_expert_ffn.argtypes = [ctypes.c_int32, ctypes.c_int32] + [P] * 10
@@ -166,6 +168,24 @@ def route(shape: Shape, logits: np.ndarray, bias: np.ndarray):
     if rc:
         raise ValueError(f"oracle_route: bad argument ({rc})")
     return ids, w
+
+
+def router_logits(shape: Shape, hidden, hidden_scale, weight) -> np.ndarray:
+    """Stage (1)'s router projection: fp32 logits [T, E_g] of the FP8 hidden rows
+    (with their 1x128 scales) against the fp32 router weight [E_g, H], in the
+    layer's fixed blockwise fused-multiply-add sequence."""
+    hidden = np.ascontiguousarray(hidden, dtype=np.uint8)
+    hidden_scale = np.ascontiguousarray(hidden_scale, dtype=np.float32)
+    weight = np.ascontiguousarray(weight, dtype=np.float32)
+    assert hidden.shape == (shape.T, shape.H)
+    assert hidden_scale.shape == (shape.T, shape.H // 128)
+    assert weight.shape == (shape.num_experts, shape.H)
+    out = np.empty((shape.T, shape.num_experts), np.float32)
+    rc = lib().oracle_router_logits(ctypes.byref(shape.c()), _ptr(hidden), _ptr(hidden_scale),
+                                    _ptr(weight), _ptr(out))
+    if rc:
+        raise ValueError(f"oracle_router_logits: bad argument ({rc})")
+    return out
 
 
 def permute(shape: Shape, topk_ids: np.ndarray):

@@ -262,6 +262,50 @@ int oracle_route(const oracle_shape *s, const float *logits, const float *bias,
 }
 
 /* ------------------------------------------------------------------------ */
+/* Stage (1)'s router projection: the routing scores start from a linear     */
+/* projection of the token's hidden state onto one weight row per expert.   */
+/* Here the hidden state is the FP8 row with its 1x128 block scales (the     */
+/* input of stage (2)), the router weight is fp32 [E_g, H], and the logits   */
+/* are fp32.  The paper does not fix the projection's precision; since the   */
+/* logits decide the expert choice, the layer fixes one fp32 sequence:      */
+/*   p_kb    = fused multiply-add chain over the 128 elements of block kb,   */
+/*             ascending, from 0:  p = fmaf(dec(q[h]), W[e][h], p)           */
+/*             (dec(q) is exact in fp32; the block scale is not applied)    */
+/*   logit_e = fused multiply-add chain over the blocks, ascending, from 0:  */
+/*             acc = fmaf(scale[kb], p_kb, acc)                              */
+/* Reading: the logits are the dequantised hidden row times the weight row, */
+/* accumulated blockwise in fp32 (error bound: (128 + H/128) u sum |x w|).  */
+/* ------------------------------------------------------------------------ */
+int oracle_router_logits(const oracle_shape *s, const uint8_t *hidden,
+                         const float *hidden_scale, const float *weight,
+                         float *logits) {
+  int64_t t;
+  int HB;
+  if (oracle_check_shape(s)) return ORACLE_BAD_ARG;
+  HB = s->H / 128;
+#pragma omp parallel for schedule(dynamic, 1)
+  for (t = 0; t < s->T; ++t) {
+    const uint8_t *q = hidden + t * s->H;
+    const float *sc = hidden_scale + t * HB;
+    int e, kb, i;
+    for (e = 0; e < s->num_experts; ++e) {
+      const float *w = weight + (int64_t)e * s->H;
+      float acc = 0.0f;
+      for (kb = 0; kb < HB; ++kb) {
+        float p = 0.0f;
+        for (i = 0; i < 128; ++i) {
+          int h = kb * 128 + i;
+          p = fmaf((float)oracle_e4m3_decode(q[h]), w[h], p);
+        }
+        acc = fmaf(sc[kb], p, acc);
+      }
+      logits[t * s->num_experts + e] = acc;
+    }
+  }
+  return ORACLE_OK;
+}
+
+/* ------------------------------------------------------------------------ */
 /* Stage (2) bookkeeping: the (token, slot) pairs whose expert is resident   */
 /* are grouped by local expert into one contiguous layout.  Order inside an  */
 /* expert: ascending token (a token holds an expert at most once).           */

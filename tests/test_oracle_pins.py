@@ -561,3 +561,91 @@ def test_forward_offslice_tokens_are_zero(oracle_lib):
     assert none_local.any()
     assert (out[none_local] == 0).all()
     assert (out[~none_local] != 0).any(1).all()
+
+
+# ------------------------------------------------------ router projection
+def _proj_shape(T, H, E, G=4, K=4):
+    return oracle.Shape(T, H, 128, E, E, 0, G, min(2, G), K, 2.5)
+
+
+def test_router_logits_error_bound(oracle_lib):
+    """On the workload distributions (N(0,1) hidden rows block-quantised, N(0,1/H)
+    weights) the fp32 logits differ from the exact dot product of the dequantised
+    row and the weight row by at most the blockwise recursive-summation bound
+    (128 + H/128 + 1) u sum |x w|.  A dropped or transposed term breaks it."""
+    cfg = W.CONFIGS["tiny"].with_(T=24, H=1024, num_experts=32, n_group=4)
+    hq, hs = W.gen_hidden(cfg, 31)
+    wg = W.gen_router_weight(cfg, 31)
+    shape = _proj_shape(cfg.T, cfg.H, cfg.num_experts)
+    got = oracle_lib.router_logits(shape, hq.numpy(), hs.numpy(), wg.numpy()).astype(np.float64)
+    x = (hq.view(torch.float8_e4m3fn).double() * hs.double().repeat_interleave(128, 1)).numpy()
+    w = wg.double().numpy()
+    exact = x @ w.T
+    mag = np.abs(x) @ np.abs(w).T
+    u = 2.0 ** -24
+    bound = (128 + cfg.H // 128 + 1) * u * mag
+    err = np.abs(got - exact)
+    assert (err <= bound).all()
+    assert np.abs(exact).std() > 0.5   # logits of about unit size, as the recipe says
+    assert (err > 0).mean() > 0.3       # rounding is real on such data
+
+
+def test_router_logits_exact_on_integers(oracle_lib):
+    """Integer-valued codes, small integer weights and power-of-two block scales
+    keep every partial sum exact in fp32: the logits equal an int64 product."""
+    rng = np.random.default_rng(32)
+    T, H, E = 6, 768, 16
+    codes = {v: _code(v) for v in range(-16, 17)}
+    xv = rng.integers(-16, 17, (T, H))
+    wv = rng.integers(-8, 9, (E, H))
+    xq = np.vectorize(codes.get)(xv).astype(np.uint8)
+    se = rng.integers(-4, 3, (T, H // 128))
+    xs = np.exp2(se).astype(np.float32)
+    got = oracle_lib.router_logits(_proj_shape(T, H, E), xq, xs, wv.astype(np.float32))
+    ref = np.einsum("tbi,ebi->te", (xv * 1.0).reshape(T, H // 128, 128) * xs[:, :, None],
+                    (wv * 1.0).reshape(E, H // 128, 128))
+    assert (got.astype(np.float64) == ref).all()
+
+
+def test_router_logits_fixed_sequence(oracle_lib):
+    """Worked example of the fixed order.  In one block, 2^24 followed by 126 ones
+    and then -2^24: each 1 added to 2^24 rounds back to 2^24 (a tie, to even), so
+    the ascending fused multiply-add chain ends at 0, not at the exact 126.
+    Across blocks the same happens with the block sums and the scales."""
+    H, E = 256, 2
+    one = _code(1.0)
+    xq = np.full((1, H), one, np.uint8)
+    w = np.ones((E, H), np.float32)
+    w[0, 0], w[0, 127] = 2.0 ** 24, -(2.0 ** 24)      # expert 0: absorption in block 0
+    w[1, :128] = 0.0                                   # expert 1: block 0 sums to 0
+    xs = np.ones((1, 2), np.float32)
+    got = oracle_lib.router_logits(_proj_shape(1, H, E, G=1, K=1), xq, xs, w)
+    assert got[0, 0] == 128.0       # block 0 -> 0, block 1 -> 128
+    assert got[0, 1] == 128.0
+    # outer chain: block sums 2^24 (scale 1) then 1 (scale 1) -> 2^24, exact would be 2^24+1
+    H = 384
+    xq = np.zeros((1, H), np.uint8)
+    xq[0, 0] = _code(2.0 ** 8)
+    xq[0, 128] = one
+    w = np.zeros((2, H), np.float32)
+    w[0, 0] = 2.0 ** 16
+    w[0, 128] = 1.0
+    xq[0, 256] = one
+    w[0, 256] = -(2.0 ** 24)
+    xs = np.ones((1, 3), np.float32)
+    got = oracle_lib.router_logits(_proj_shape(1, H, 2, G=1, K=1), xq, xs, w)
+    assert got[0, 0] == 0.0         # (2^24 + 1) -> 2^24, minus 2^24
+
+
+def test_router_logits_scale_and_zero(oracle_lib):
+    """Zero rows give zero logits; doubling every block scale doubles every logit
+    exactly (powers of two commute with each rounding)."""
+    cfg = W.CONFIGS["tiny"].with_(T=5, H=512, num_experts=16)
+    hq, hs = W.gen_hidden(cfg, 33)
+    wg = W.gen_router_weight(cfg, 33).numpy()
+    shape = _proj_shape(cfg.T, cfg.H, cfg.num_experts)
+    a = oracle_lib.router_logits(shape, hq.numpy(), hs.numpy(), wg)
+    b = oracle_lib.router_logits(shape, hq.numpy(), (hs * 2).numpy(), wg)
+    assert (b == 2 * a).all()
+    z = oracle_lib.router_logits(shape, np.zeros_like(hq.numpy()), hs.numpy(), wg)
+    assert (z == 0).all()

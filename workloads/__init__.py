@@ -17,6 +17,9 @@ regenerated alone):
                    with fp32 scale = amax / 448                       [T, H]
   * w13 (gate rows [0,I), up rows [I,2I)), w2: N(0, 0.02) quantised   id 4, 5
     per 128x128 block, fp32 scale = amax / 448
+  * router weight  fp32 N(0, 1/H) [E_g, H] (for the router projection:  id 7
+    with N(0, 1) hidden rows the projected logits are about N(0, 1),
+    the distribution of the logits drawn directly)
 Input quantisation uses torch's own float8_e4m3fn conversion (round to nearest
 even) after clamping to +-448; an all-zero block gets scale 1.
 """
@@ -108,7 +111,7 @@ def all_configs() -> dict[str, MoEConfig]:
 # ---------------------------------------------------------------------------
 # seeded sub-streams
 # ---------------------------------------------------------------------------
-TID_LOGITS, TID_BIAS, TID_HIDDEN, TID_W13, TID_W2, TID_HOT = 1, 2, 3, 4, 5, 6
+TID_LOGITS, TID_BIAS, TID_HIDDEN, TID_W13, TID_W2, TID_HOT, TID_ROUTER_W = 1, 2, 3, 4, 5, 6, 7
 
 
 def substream_seed(seed: int, tid: int, expert: int = 0) -> int:
@@ -145,6 +148,12 @@ def gen_router(cfg: MoEConfig, seed: int, device="cpu"):
         hot = torch.randperm(cfg.num_experts, generator=g)[: cfg.hot_experts]
         bias[hot.to(device)] += cfg.hot_bias
     return logits, bias, hot
+
+
+def gen_router_weight(cfg: MoEConfig, seed: int, device="cpu"):
+    """Router projection weight fp32 [E_g, H], N(0, 1/H)."""
+    return torch.randn(cfg.num_experts, cfg.H, generator=_gen(device, seed, TID_ROUTER_W),
+                       device=device, dtype=torch.float32) * (1.0 / cfg.H) ** 0.5
 
 
 def gen_hidden(cfg: MoEConfig, seed: int, device="cpu"):
