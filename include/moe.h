@@ -83,7 +83,7 @@ typedef struct {
   int32_t *pair_row;
 } moe_route_out_t;
 
-/* Bytes of device workspace that moe_route / moe_fused_fp8 need for `s`
+/* Bytes of device workspace that every entry point below needs for `s`
  * (a worst case: every pair resident).  Returns 0 for an invalid shape.
  * The workspace needs no initialisation and is not read across calls. */
 size_t moe_workspace_size(const moe_shape_t *s);
@@ -98,6 +98,24 @@ size_t moe_workspace_size(const moe_shape_t *s);
 moe_status_t moe_route(const moe_shape_t *s, const float *router_logits,
                        const float *routing_bias, const moe_route_out_t *out,
                        void *workspace, size_t ws_bytes, void *stream);
+
+/* moe_route with the router projection of stage (1) (Section 3.1.1: the
+ * routing scores start from a linear projection of the hidden state) done on
+ * the device instead of taking logits:
+ *  hidden        [T, H] e4m3      hidden_scale [T, H/128] float
+ *  router_weight [E_g, H] float   routing_bias [E_g] float
+ * logit[t, e] follows one fixed fp32 sequence (the expert choice depends on
+ * it bit for bit): for each 128-element block kb, p = fused multiply-add
+ * chain over the block's elements in ascending order, starting from 0, of
+ * decode(hidden[t, h]) * router_weight[e, h]; then logit = fused multiply-add
+ * chain over the blocks in ascending order, starting from 0, of
+ * hidden_scale[t, kb] * p.  The logits are not written anywhere.  Outputs,
+ * T = 0 handling and determinism as moe_route; the workspace is the same
+ * (moe_workspace_size). */
+moe_status_t moe_route_hidden(const moe_shape_t *s, const uint8_t *hidden,
+                              const float *hidden_scale, const float *router_weight,
+                              const float *routing_bias, const moe_route_out_t *out,
+                              void *workspace, size_t ws_bytes, void *stream);
 
 /* The whole layer, stages (1)-(4) of Section 3.1.1.
  *  hidden        [T, H] e4m3      hidden_scale [T, H/128] float
@@ -122,6 +140,19 @@ moe_status_t moe_fused_fp8(const moe_shape_t *s, const uint8_t *hidden,
                            const float *w2_scale, uint16_t *out,
                            const moe_route_out_t *route_out, void *workspace,
                            size_t ws_bytes, void *stream);
+
+/* moe_fused_fp8 with the router projection of stage (1) on the device:
+ * router_weight [E_g, H] float replaces router_logits; the logits are those
+ * defined under moe_route_hidden.  Everything else as moe_fused_fp8 (the
+ * projection runs inside the "route" stage). */
+moe_status_t moe_fused_fp8_router(const moe_shape_t *s, const uint8_t *hidden,
+                                  const float *hidden_scale,
+                                  const float *router_weight,
+                                  const float *routing_bias, const uint8_t *w13,
+                                  const float *w13_scale, const uint8_t *w2,
+                                  const float *w2_scale, uint16_t *out,
+                                  const moe_route_out_t *route_out, void *workspace,
+                                  size_t ws_bytes, void *stream);
 
 /* Same as moe_fused_fp8; additionally records `stage_events[i]` (hipEvent_t
  * handles created by the caller) on `stream` before stage i and

@@ -32,6 +32,15 @@ moe_status_t moe_debug_e4m3_encode(const float *x, uint8_t *q, int64_t n, void *
 moe_status_t moe_debug_mfma_block(const uint8_t *a, const uint8_t *b, float *d, int64_t n,
                                   void *stream);
 
+/* logits [T, E_g] float = the router projection of stage (1) (paper Section
+ * 3.1.1) exactly as moe_route_hidden forms it (the fixed fp32 sequence
+ * stated there), from hidden [T, H] e4m3, hidden_scale [T, H/128] float and
+ * router_weight [E_g, H] float.  Uses the workspace of `s`. */
+moe_status_t moe_debug_router_logits(const moe_shape_t *s, const uint8_t *hidden,
+                                     const float *hidden_scale, const float *router_weight,
+                                     float *logits, void *workspace, size_t ws_bytes,
+                                     void *stream);
+
 /* Device addresses, inside a workspace used by moe_fused_fp8 for shape `s`,
  * of the re-quantised intermediate activation: act [P, I] e4m3 in permuted
  * row order and act_scale [P, I/128] float.  Valid after the call completes,

@@ -25,9 +25,10 @@ LIB_PATH = os.path.join(_HERE, "libmoe.so")
 
 MOE_OK, MOE_ERR_INVALID_ARG, MOE_ERR_UNSUPPORTED, MOE_ERR_WORKSPACE_TOO_SMALL, MOE_ERR_HIP = range(5)
 
-EXPORTED = ("moe_workspace_size", "moe_route", "moe_fused_fp8", "moe_fused_fp8_staged",
-            "moe_num_stages", "moe_stage_name", "moe_status_string", "moe_debug_sigmoid",
-            "moe_debug_e4m3_encode", "moe_debug_act_views", "moe_debug_mfma_block")
+EXPORTED = ("moe_workspace_size", "moe_route", "moe_route_hidden", "moe_fused_fp8",
+            "moe_fused_fp8_router", "moe_fused_fp8_staged", "moe_num_stages", "moe_stage_name",
+            "moe_status_string", "moe_debug_sigmoid", "moe_debug_e4m3_encode",
+            "moe_debug_act_views", "moe_debug_mfma_block", "moe_debug_router_logits")
 
 
 class MoEError(RuntimeError):
@@ -92,6 +93,12 @@ def lib() -> ctypes.CDLL:
         L.moe_route.restype = ctypes.c_int
         L.moe_fused_fp8.argtypes = [S, P, P, P, P, P, P, P, P, P, R, P, Z, P]
         L.moe_fused_fp8.restype = ctypes.c_int
+        L.moe_route_hidden.argtypes = [S, P, P, P, P, R, P, Z, P]
+        L.moe_route_hidden.restype = ctypes.c_int
+        L.moe_fused_fp8_router.argtypes = [S, P, P, P, P, P, P, P, P, P, R, P, Z, P]
+        L.moe_fused_fp8_router.restype = ctypes.c_int
+        L.moe_debug_router_logits.argtypes = [S, P, P, P, P, P, Z, P]
+        L.moe_debug_router_logits.restype = ctypes.c_int
         L.moe_fused_fp8_staged.argtypes = [S, P, P, P, P, P, P, P, P, P, R, P, Z, P,
                                            ctypes.POINTER(P), ctypes.c_int]
         L.moe_fused_fp8_staged.restype = ctypes.c_int
@@ -180,6 +187,39 @@ def route(shape: Shape, logits: torch.Tensor, bias: torch.Tensor, route_out: dic
     return ro
 
 
+def route_hidden(shape: Shape, hidden, hidden_scale, router_weight, bias,
+                 route_out: dict | None = None, workspace: torch.Tensor | None = None,
+                 stream=None) -> dict:
+    """Stage (1) with the router projection on the device (fp32 router weight
+    [E_g, H]), then the permutation of stage (2); returns the route-out tensors."""
+    ro = route_out if route_out is not None else alloc_route_out(shape, hidden.device)
+    ws = workspace if workspace is not None else alloc_workspace(shape, hidden.device)
+    cro = _route_struct(ro)
+    rc = lib().moe_route_hidden(ctypes.byref(shape.c()), _dev(hidden, torch.uint8, "hidden"),
+                                _dev(hidden_scale, torch.float32, "hidden_scale"),
+                                _dev(router_weight, torch.float32, "router_weight"),
+                                _dev(bias, torch.float32, "bias"), ctypes.byref(cro),
+                                _dev(ws, torch.uint8, "workspace"), ws.numel(), _stream(stream))
+    _check("moe_route_hidden", rc)
+    return ro
+
+
+def debug_router_logits(shape: Shape, hidden, hidden_scale, router_weight,
+                        workspace: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+    """The fp32 logits [T, E_g] that moe_route_hidden forms (test hook)."""
+    ws = workspace if workspace is not None else alloc_workspace(shape, hidden.device)
+    out = torch.empty(max(shape.T, 1), shape.num_experts, dtype=torch.float32,
+                      device=hidden.device)[: shape.T]
+    rc = lib().moe_debug_router_logits(ctypes.byref(shape.c()), _dev(hidden, torch.uint8, "hidden"),
+                                       _dev(hidden_scale, torch.float32, "hidden_scale"),
+                                       _dev(router_weight, torch.float32, "router_weight"),
+                                       _dev(out, torch.float32, "logits"),
+                                       _dev(ws, torch.uint8, "workspace"), ws.numel(),
+                                       _stream(stream))
+    _check("moe_debug_router_logits", rc)
+    return out
+
+
 def _fused_args(shape, hidden, hidden_scale, logits, bias, w13, w13_scale, w2, w2_scale, out,
                 route_out, workspace):
     return [ctypes.byref(shape.c()),
@@ -203,6 +243,22 @@ def fused_fp8(shape: Shape, hidden, hidden_scale, logits, bias, w13, w13_scale, 
     args = _fused_args(shape, hidden, hidden_scale, logits, bias, w13, w13_scale, w2, w2_scale,
                        out, route_out, workspace)
     _check("moe_fused_fp8", lib().moe_fused_fp8(*args, _stream(stream)))
+    return out
+
+
+def fused_fp8_router(shape: Shape, hidden, hidden_scale, router_weight, bias, w13, w13_scale,
+                     w2, w2_scale, out: torch.Tensor | None = None,
+                     route_out: dict | None = None, workspace: torch.Tensor | None = None,
+                     stream=None) -> torch.Tensor:
+    """The whole layer with the router projection on the device; returns out
+    [T, H] bf16."""
+    if out is None:
+        out = torch.empty(shape.T, shape.H, dtype=torch.bfloat16, device=hidden.device)
+    if workspace is None:
+        workspace = alloc_workspace(shape, hidden.device)
+    args = _fused_args(shape, hidden, hidden_scale, router_weight, bias, w13, w13_scale, w2,
+                       w2_scale, out, route_out, workspace)
+    _check("moe_fused_fp8_router", lib().moe_fused_fp8_router(*args, _stream(stream)))
     return out
 
 

@@ -3,8 +3,9 @@
     python -m paper_2608_14560_amd.build
 
 Every HIP source is compiled without packed fp32 instructions; the routing
-kernel also without floating-point contraction (its fp32 sequence is a
-specification whose integer decisions must be reproducible).
+and router projection kernels also without floating-point contraction (their
+fp32 sequences are specifications whose integer decisions must be
+reproducible).
 """
 from __future__ import annotations
 
@@ -26,6 +27,7 @@ COMMON = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}", "-Wall",
           "-I", os.path.join(ROOT, "include")]
 SOURCES = {
     "route.hip": ["-ffp-contract=off"],
+    "router.hip": ["-ffp-contract=off"],
     "permute.hip": [],
     "gemm.hip": [],
     "gemm_tile.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"],

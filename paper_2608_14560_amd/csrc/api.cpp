@@ -61,7 +61,7 @@ struct Plan {
   bool tile;     // large-tile kernels (BM >= 64)
   int64_t P_max;
   size_t off_ids, off_w, off_offsets, off_perm_token, off_perm_pair, off_pair_row, off_chunk_counts,
-      off_tile_base, off_n_items, off_act, off_act_scale, off_abuf, off_Y, total;
+      off_tile_base, off_n_items, off_act, off_act_scale, off_abuf, off_Y, off_partials, total;
 };
 
 Plan make_plan(const moe_shape_t *s) {
@@ -107,7 +107,12 @@ Plan make_plan(const moe_shape_t *s) {
   p.off_act = take((size_t)p.P_max * s->I);
   p.off_act_scale = take(sizeof(float) * (size_t)p.P_max * (s->I / 128));
   p.off_abuf = take(p.narrow1 ? sizeof(float) * (size_t)p.P_max * s->I : 0);
-  p.off_Y = take(sizeof(float) * (size_t)p.S2 * p.P_max * s->H);
+  // the router projection's block sums [T, H/128, E_g] live where GEMM2 later
+  // writes Y: the routing kernel consumes them before GEMM2 runs
+  const size_t y_bytes = sizeof(float) * (size_t)p.S2 * p.P_max * s->H;
+  const size_t part_bytes = sizeof(float) * (size_t)(s->T > 0 ? s->T : 1) * (s->H / 128) * s->num_experts;
+  p.off_Y = take(y_bytes > part_bytes ? y_bytes : part_bytes);
+  p.off_partials = p.off_Y;
   p.total = o;
   return p;
 }
@@ -148,15 +153,44 @@ moe_status_t check_route_out(const moe_route_out_t *ro) {
     if ((expr) != hipSuccess) return MOE_ERR_HIP; \
   } while (0)
 
-moe_status_t enqueue_route(const moe_shape_t *s, const Plan &pl, const float *logits,
+// Router input: either the logits, or the hidden rows with the router weight
+// (the projection then runs first and the routing kernel forms the logits
+// from its block sums).
+struct RouterIn {
+  const float *logits;
+  const uint8_t *hidden;
+  const float *hidden_scale;
+  const float *weight;
+};
+
+RouteParams route_params(const moe_shape_t *s, const Plan &pl, const RouterIn &in,
+                         const float *bias, const Ptrs &r, void *ws) {
+  RouteParams rp{in.logits, bias, r.ids, r.w, s->T, s->num_experts, s->n_group, s->topk_group,
+                 s->top_k, s->routed_scaling_factor};
+  if (in.weight) {
+    rp.partials = at<float>(ws, pl.off_partials);
+    rp.pscale = in.hidden_scale;
+    rp.KB = s->H / 128;
+  }
+  return rp;
+}
+
+hipError_t enqueue_projection(const moe_shape_t *s, const Plan &pl, const RouterIn &in, void *ws,
+                              hipStream_t st) {
+  if (!in.weight) return hipSuccess;
+  RouterParams q{in.hidden, in.weight, at<float>(ws, pl.off_partials), s->T, s->H,
+                 s->num_experts};
+  return launch_router_partials(q, st);
+}
+
+moe_status_t enqueue_route(const moe_shape_t *s, const Plan &pl, const RouterIn &in,
                            const float *bias, const Ptrs &r, void *ws, hipStream_t st,
                            void *const *ev, int &stage) {
   auto mark = [&]() {
     if (ev) (void)hipEventRecord(static_cast<hipEvent_t>(ev[stage]), st);
     ++stage;
   };
-  RouteParams rp{logits, bias, r.ids, r.w, s->T, s->num_experts, s->n_group, s->topk_group,
-                 s->top_k, s->routed_scaling_factor};
+  const RouteParams rp = route_params(s, pl, in, bias, r, ws);
   PermuteParams pp{};
   pp.topk_ids = r.ids;
   pp.chunk_counts = at<int32_t>(ws, pl.off_chunk_counts);
@@ -175,6 +209,7 @@ moe_status_t enqueue_route(const moe_shape_t *s, const Plan &pl, const float *lo
   pp.items_per_tile1 = pl.NB1 * pl.S1;
   pp.items_per_tile2 = pl.NB2 * pl.S2;
   mark();
+  MOE_TRY_HIP(enqueue_projection(s, pl, in, ws, st));
   MOE_TRY_HIP(launch_route(rp, st));
   mark();
   MOE_TRY_HIP(launch_permute_count(pp, st));
@@ -184,15 +219,16 @@ moe_status_t enqueue_route(const moe_shape_t *s, const Plan &pl, const float *lo
 }
 
 moe_status_t fused_impl(const moe_shape_t *s, const uint8_t *hidden, const float *hidden_scale,
-                        const float *logits, const float *bias, const uint8_t *w13,
-                        const float *w13_scale, const uint8_t *w2, const float *w2_scale,
-                        uint16_t *out, const moe_route_out_t *ro, void *ws, size_t ws_bytes,
-                        void *stream, void *const *ev, int n_ev) {
+                        const float *logits, const float *router_weight, const float *bias,
+                        const uint8_t *w13, const float *w13_scale, const uint8_t *w2,
+                        const float *w2_scale, uint16_t *out, const moe_route_out_t *ro, void *ws,
+                        size_t ws_bytes, void *stream, void *const *ev, int n_ev) {
   moe_status_t rc = check_shape(s);
   if (rc != MOE_OK) return rc;
   if (ev && n_ev != kStages + 1) return MOE_ERR_INVALID_ARG;
   if (s->T == 0) return MOE_OK;
-  const void *ptrs[] = {hidden, hidden_scale, logits, bias, w13, w13_scale, w2, w2_scale, out};
+  const float *router_in = logits ? logits : router_weight;
+  const void *ptrs[] = {hidden, hidden_scale, router_in, bias, w13, w13_scale, w2, w2_scale, out};
   for (const void *q : ptrs)
     if (!q || !aligned(q, 16)) return MOE_ERR_INVALID_ARG;
   if ((rc = check_route_out(ro)) != MOE_OK) return rc;
@@ -203,7 +239,8 @@ moe_status_t fused_impl(const moe_shape_t *s, const uint8_t *hidden, const float
 
   const Ptrs r = route_ptrs(pl, ws, ro);
   int stage = 0;
-  if ((rc = enqueue_route(s, pl, logits, bias, r, ws, st, ev, stage)) != MOE_OK) return rc;
+  const RouterIn rin{logits, hidden, hidden_scale, router_weight};
+  if ((rc = enqueue_route(s, pl, rin, bias, r, ws, st, ev, stage)) != MOE_OK) return rc;
   auto mark = [&]() {
     if (ev) (void)hipEventRecord(static_cast<hipEvent_t>(ev[stage]), st);
     ++stage;
@@ -302,8 +339,35 @@ moe_status_t moe_route(const moe_shape_t *s, const float *router_logits,
   if (ws_bytes < pl.total) return MOE_ERR_WORKSPACE_TOO_SMALL;
   const Ptrs r = route_ptrs(pl, workspace, out);
   int stage = 0;
-  return enqueue_route(s, pl, router_logits, routing_bias, r, workspace,
-                       static_cast<hipStream_t>(stream), nullptr, stage);
+  const RouterIn rin{router_logits, nullptr, nullptr, nullptr};
+  return enqueue_route(s, pl, rin, routing_bias, r, workspace, static_cast<hipStream_t>(stream),
+                       nullptr, stage);
+}
+
+moe_status_t moe_route_hidden(const moe_shape_t *s, const uint8_t *hidden,
+                              const float *hidden_scale, const float *router_weight,
+                              const float *routing_bias, const moe_route_out_t *out,
+                              void *workspace, size_t ws_bytes, void *stream) {
+  moe_status_t rc = check_shape(s);
+  if (rc != MOE_OK) return rc;
+  if (!out) return MOE_ERR_INVALID_ARG;
+  if (s->T == 0) {
+    if (!out->expert_offsets || !aligned(out->expert_offsets, 16) || !out->perm_token)
+      return MOE_ERR_INVALID_ARG;
+  } else {
+    const void *ptrs[] = {hidden, hidden_scale, router_weight, routing_bias};
+    for (const void *q : ptrs)
+      if (!q || !aligned(q, 16)) return MOE_ERR_INVALID_ARG;
+    if ((rc = check_route_out(out)) != MOE_OK) return rc;
+  }
+  const Plan pl = make_plan(s);
+  if (!workspace || !aligned(workspace, kAlign)) return MOE_ERR_INVALID_ARG;
+  if (ws_bytes < pl.total) return MOE_ERR_WORKSPACE_TOO_SMALL;
+  const Ptrs r = route_ptrs(pl, workspace, out);
+  int stage = 0;
+  const RouterIn rin{nullptr, hidden, hidden_scale, router_weight};
+  return enqueue_route(s, pl, rin, routing_bias, r, workspace, static_cast<hipStream_t>(stream),
+                       nullptr, stage);
 }
 
 moe_status_t moe_fused_fp8(const moe_shape_t *s, const uint8_t *hidden, const float *hidden_scale,
@@ -311,8 +375,18 @@ moe_status_t moe_fused_fp8(const moe_shape_t *s, const uint8_t *hidden, const fl
                            const uint8_t *w13, const float *w13_scale, const uint8_t *w2,
                            const float *w2_scale, uint16_t *out, const moe_route_out_t *route_out,
                            void *workspace, size_t ws_bytes, void *stream) {
-  return fused_impl(s, hidden, hidden_scale, router_logits, routing_bias, w13, w13_scale, w2,
-                    w2_scale, out, route_out, workspace, ws_bytes, stream, nullptr, 0);
+  return fused_impl(s, hidden, hidden_scale, router_logits, nullptr, routing_bias, w13, w13_scale,
+                    w2, w2_scale, out, route_out, workspace, ws_bytes, stream, nullptr, 0);
+}
+
+moe_status_t moe_fused_fp8_router(const moe_shape_t *s, const uint8_t *hidden,
+                                  const float *hidden_scale, const float *router_weight,
+                                  const float *routing_bias, const uint8_t *w13,
+                                  const float *w13_scale, const uint8_t *w2, const float *w2_scale,
+                                  uint16_t *out, const moe_route_out_t *route_out, void *workspace,
+                                  size_t ws_bytes, void *stream) {
+  return fused_impl(s, hidden, hidden_scale, nullptr, router_weight, routing_bias, w13, w13_scale,
+                    w2, w2_scale, out, route_out, workspace, ws_bytes, stream, nullptr, 0);
 }
 
 moe_status_t moe_fused_fp8_staged(const moe_shape_t *s, const uint8_t *hidden,
@@ -325,8 +399,9 @@ moe_status_t moe_fused_fp8_staged(const moe_shape_t *s, const uint8_t *hidden,
   if (!stage_events) return MOE_ERR_INVALID_ARG;
   for (int i = 0; i < n_events; ++i)
     if (!stage_events[i]) return MOE_ERR_INVALID_ARG;
-  return fused_impl(s, hidden, hidden_scale, router_logits, routing_bias, w13, w13_scale, w2,
-                    w2_scale, out, route_out, workspace, ws_bytes, stream, stage_events, n_events);
+  return fused_impl(s, hidden, hidden_scale, router_logits, nullptr, routing_bias, w13, w13_scale,
+                    w2, w2_scale, out, route_out, workspace, ws_bytes, stream, stage_events,
+                    n_events);
 }
 
 int moe_num_stages(void) { return kStages; }
@@ -365,6 +440,26 @@ moe_status_t moe_debug_mfma_block(const uint8_t *a, const uint8_t *b, float *d, 
   return launch_debug_mfma_block(a, b, d, n, static_cast<hipStream_t>(stream)) == hipSuccess
              ? MOE_OK
              : MOE_ERR_HIP;
+}
+
+moe_status_t moe_debug_router_logits(const moe_shape_t *s, const uint8_t *hidden,
+                                     const float *hidden_scale, const float *router_weight,
+                                     float *logits, void *workspace, size_t ws_bytes,
+                                     void *stream) {
+  if (check_shape(s) != MOE_OK) return MOE_ERR_INVALID_ARG;
+  if (s->T == 0) return MOE_OK;
+  const void *ptrs[] = {hidden, hidden_scale, router_weight, logits};
+  for (const void *q : ptrs)
+    if (!q || !aligned(q, 16)) return MOE_ERR_INVALID_ARG;
+  const Plan pl = make_plan(s);
+  if (!workspace || !aligned(workspace, kAlign)) return MOE_ERR_INVALID_ARG;
+  if (ws_bytes < pl.total) return MOE_ERR_WORKSPACE_TOO_SMALL;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const RouterIn rin{nullptr, hidden, hidden_scale, router_weight};
+  const Ptrs r{};
+  const RouteParams rp = route_params(s, pl, rin, nullptr, r, workspace);
+  if (enqueue_projection(s, pl, rin, workspace, st) != hipSuccess) return MOE_ERR_HIP;
+  return launch_router_logits(rp, logits, st) == hipSuccess ? MOE_OK : MOE_ERR_HIP;
 }
 
 moe_status_t moe_debug_act_views(const moe_shape_t *s, void *workspace, uint8_t **act,

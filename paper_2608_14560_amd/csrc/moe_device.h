@@ -79,12 +79,40 @@ __device__ __forceinline__ bool beats(float va, int ia, float vb, int ib) {
 // ---------------------------------------------------------------- launch blocks
 
 struct RouteParams {
-  const float *logits;   // [T, E]
+  const float *logits;   // [T, E] (unused when `partials` is set)
   const float *bias;     // [E]
   int32_t *topk_ids;     // [T, K]
   float *topk_w;         // [T, K]
   int T, E, G, TG, K;
   float rsf;
+  // Router projection path: the projection's per-block sums [T, KB, E] and
+  // the hidden rows' block scales [T, KB]; the logits are formed from them.
+  const float *partials;
+  const float *pscale;
+  int KB;
+};
+
+// Logit of expert e for token t.  Given the router projection's block sums
+// p_kb, the logit is the fused multiply-add chain over the blocks, ascending,
+// from 0: acc = fmaf(scale[kb], p_kb, acc) -- the second half of the
+// projection's fixed fp32 sequence (the first half, the chain inside a
+// block, runs in the projection kernel).
+__device__ __forceinline__ float route_logit(const RouteParams &p, int t, int e) {
+  if (!p.partials) return p.logits[(size_t)t * p.E + e];
+  const float *pp = p.partials + (size_t)t * p.KB * p.E + e;
+  const float *sc = p.pscale + (size_t)t * p.KB;
+  float acc = 0.0f;
+  for (int kb = 0; kb < p.KB; ++kb) acc = __builtin_fmaf(sc[kb], pp[(size_t)kb * p.E], acc);
+  return acc;
+}
+
+// Router projection: block sums of the dequantised-code rows against the
+// fp32 router weight rows.
+struct RouterParams {
+  const uint8_t *hidden;       // [T, H] e4m3fn
+  const float *weight;         // [E, H] fp32
+  float *partials;             // [T, H/128, E] fp32
+  int T, H, E;
 };
 
 struct PermuteParams {
@@ -139,6 +167,8 @@ struct FinalizeParams {
 // ---------------------------------------------------------------- launchers
 // (defined in the .hip files, called by the C-ABI layer)
 hipError_t launch_route(const RouteParams &p, hipStream_t st);
+hipError_t launch_router_partials(const RouterParams &p, hipStream_t st);
+hipError_t launch_router_logits(const RouteParams &p, float *logits, hipStream_t st);
 hipError_t launch_permute(const PermuteParams &p, hipStream_t st);
 hipError_t launch_gemm1(const GemmParams &p, int BM, int grid, hipStream_t st);
 hipError_t launch_gemm1_narrow(const GemmParams &p, int grid, hipStream_t st);

@@ -70,14 +70,13 @@ __global__ __launch_bounds__(256) void route_kernel(RouteParams p) {
   if (t >= p.T) return;  // whole wave leaves; the kernel has no block barrier
 
   const int gsz = p.E / G;
-  const float *lrow = p.logits + (size_t)t * p.E;
 
   float sc[EPL], key[EPL];
 #pragma unroll
   for (int q = 0; q < EPL; ++q) {
     const int e = q * kWave + lane;
     if (e < p.E) {
-      sc[q] = sigmoid_spec(lrow[e]);
+      sc[q] = sigmoid_spec(route_logit(p, t, e));
       key[q] = sc[q] + p.bias[e];
     } else {
       sc[q] = 0.0f;
@@ -248,7 +247,6 @@ __device__ __forceinline__ float key_value(uint32_t h) {
 template <int EPL, int S>
 __device__ __forceinline__ void route_token_seg(const RouteParams &p, int t) {
   const int lane = threadIdx.x & (kWave - 1);
-  const float *lrow = p.logits + (size_t)t * p.E;
   const int seg_lane = lane & (S - 1);
 
   float sc[EPL], key[EPL];
@@ -257,7 +255,7 @@ __device__ __forceinline__ void route_token_seg(const RouteParams &p, int t) {
   for (int q = 0; q < EPL; ++q) {
     const int e = q * kWave + lane;
     const bool v = e < p.E;
-    sc[q] = v ? sigmoid_spec(lrow[e]) : 0.0f;
+    sc[q] = v ? sigmoid_spec(route_logit(p, t, e)) : 0.0f;
     key[q] = v ? sc[q] + p.bias[e] : -INFINITY;
     k2[q].ah = v ? ordered_bits(key[q]) : 0u;
     k2[q].al = ~(uint32_t)e;
@@ -388,6 +386,22 @@ hipError_t launch_route(const RouteParams &p, hipStream_t st) {
     launch_route_epl<8>(p, grid, block, st);
   else
     launch_route_epl<16>(p, grid, block, st);
+  return hipGetLastError();
+}
+
+// Test hook: the logits the routing kernels form (from the router
+// projection's block sums, or as given).
+namespace {
+__global__ void logits_kernel(RouteParams p, float *logits) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < (int64_t)p.T * p.E) logits[i] = route_logit(p, (int)(i / p.E), (int)(i % p.E));
+}
+}  // namespace
+
+hipError_t launch_router_logits(const RouteParams &p, float *logits, hipStream_t st) {
+  const int64_t n = (int64_t)p.T * p.E;
+  if (n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(logits_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, p, logits);
   return hipGetLastError();
 }
 

@@ -129,6 +129,40 @@ def test_route_rejects_bad_arguments(M):
                        None) == M.MOE_ERR_WORKSPACE_TOO_SMALL
 
 
+def test_router_entry_points_reject_bad_arguments(M):
+    s = _shape()
+    L = M.lib()
+    ws_bytes = M.workspace_size(s)
+    ro = M.CRouteOut(*[p.value for p in _fake_ptrs(5)])
+    hid, hsc, wg, bs = _fake_ptrs(4)
+    ws = ctypes.c_void_p(0x7000000)
+    sc = ctypes.byref(s.c())
+    # moe_route_hidden: each input null or misaligned, no route_out, small workspace
+    args = [hid, hsc, wg, bs]
+    for i in range(4):
+        bad = list(args)
+        bad[i] = None
+        assert L.moe_route_hidden(sc, *bad, ctypes.byref(ro), ws, ws_bytes, None) == M.MOE_ERR_INVALID_ARG
+        bad[i] = ctypes.c_void_p(args[i].value + 4)
+        assert L.moe_route_hidden(sc, *bad, ctypes.byref(ro), ws, ws_bytes, None) == M.MOE_ERR_INVALID_ARG
+    assert L.moe_route_hidden(sc, *args, None, ws, ws_bytes, None) == M.MOE_ERR_INVALID_ARG
+    assert L.moe_route_hidden(sc, *args, ctypes.byref(ro), ws, 16, None) == M.MOE_ERR_WORKSPACE_TOO_SMALL
+    # moe_fused_fp8_router: the router weight is required; a null logits pointer
+    # is refused by moe_fused_fp8
+    ptrs = _fake_ptrs(9)
+    bad = list(ptrs)
+    bad[2] = None
+    assert L.moe_fused_fp8_router(sc, *bad, None, ws, ws_bytes, None) == M.MOE_ERR_INVALID_ARG
+    assert L.moe_fused_fp8(sc, *bad, None, ws, ws_bytes, None) == M.MOE_ERR_INVALID_ARG
+    assert L.moe_fused_fp8_router(sc, *ptrs, None, ws, 16, None) == M.MOE_ERR_WORKSPACE_TOO_SMALL
+    # debug logits: null output
+    assert L.moe_debug_router_logits(sc, hid, hsc, wg, None, ws, ws_bytes, None) == M.MOE_ERR_INVALID_ARG
+    # empty batch: a no-op for the projection entry points too
+    s0 = _shape(T=0)
+    ro0 = M.CRouteOut(None, None, _fake_ptrs(1)[0].value, _fake_ptrs(1)[0].value, None)
+    assert L.moe_fused_fp8_router(ctypes.byref(s0.c()), *ptrs, None, None, 0, None) == M.MOE_OK
+
+
 def test_workspace_grows_with_batch(M):
     sizes = [M.workspace_size(_shape(T=t)) for t in (1, 16, 256, 4096)]
     assert sizes == sorted(sizes) and sizes[0] > 0
