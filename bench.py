@@ -11,6 +11,10 @@ synchronisations; each kernel is bracketed by HIP events recorded on the
 library's stream (moe_fused_fp8_staged), which gives the per-kernel durations
 behind the roofline figure.  Prints one JSON line.
 
+The line also carries `router_projection`: the same batches routed from the
+hidden rows with the router projection on the device (moe_route_hidden)
+against routing from given logits (moe_route), both timed back to back.
+
 --cold additionally times calls after a 512 MiB write that evicts L2 and the
 256 MB Infinity Cache (reported separately, never as `value`).
 --copy-calibration runs only a plain 1 GiB device copy, the reference
@@ -37,6 +41,9 @@ import workloads as W  # noqa: E402
 METRIC = "fused FP8 MoE µs/call + effective TFLOP/s (% FP8 MFMA peak), T=16..8192"
 HBM_PEAK_GBS = 8000.0
 FP8_PEAK_TFLOPS = 5000.0
+# fp32 fused multiply-adds without packed instructions (the kernels are built
+# with packed fp32 disabled): 256 CUs x 4 SIMDs x 16 lanes x 2 FLOP x 2.4 GHz
+FP32_FMA_PEAK_TFLOPS = 78.6
 PROFILE_TRAFFIC = os.path.join(ROOT, "profiles", "gemm1_traffic_{cfg}.txt")
 
 
@@ -150,6 +157,74 @@ def cpu_baseline(cfg, batches, weights_dev, max_tokens: int):
             "kind": "oracle", "sample": sample, "wall_s": round(total_s, 2)}
 
 
+def router_projection_leg(cfg, shape, batches, weights, out, ws, stream, K, prefill):
+    """µs per call of routing from the hidden rows (projection on the device)
+    and from given logits, on the same batches, each K calls back to back.
+    The projection's own cost is the difference; its roofline uses the
+    projection's algorithmic work: the router weight, the hidden rows and
+    scales read once, the block sums written and read once, and T*E*H fused
+    multiply-adds."""
+    wg = W.gen_router_weight(cfg, 0, device="cuda")
+    ros = [M.alloc_route_out(shape) for _ in batches]
+
+    def timed(fn):
+        for i in range(3):
+            fn(i)
+        torch.cuda.synchronize()
+        h0 = time.perf_counter()
+        for i in range(K):
+            fn(i)
+        host_ms = (time.perf_counter() - h0) * 1e3
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        prefill(host_ms)
+        a.record(stream)
+        for i in range(K):
+            fn(i)
+        b.record(stream)
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) * 1e3 / K
+
+    nb = len(batches)
+    us_hidden = timed(lambda i: M.route_hidden(shape, batches[i % nb]["hidden"], batches[i % nb]["hidden_scale"],
+                                               wg, batches[i % nb]["bias"], route_out=ros[i % nb],
+                                               workspace=ws, stream=stream))
+    us_logits = timed(lambda i: M.route(shape, batches[i % nb]["logits"], batches[i % nb]["bias"],
+                                        route_out=ros[i % nb], workspace=ws, stream=stream))
+    # context: the same projection unfused, as a caller without it would run
+    # it (dequantise in torch, fp32 GEMM, then routing from the logits)
+    wgt = wg.t().contiguous()
+
+    def unfused(i):
+        b = batches[i % nb]
+        x = b["hidden"].view(torch.float8_e4m3fn).float() * b["hidden_scale"].repeat_interleave(128, dim=1)
+        M.route(shape, x @ wgt, b["bias"], route_out=ros[i % nb], workspace=ws, stream=stream)
+
+    us_unfused = timed(unfused)
+    layer = [M.FusedCall(shape, b["hidden"], b["hidden_scale"], wg, b["bias"], *weights, out, ws,
+                         stream=stream, router=True) for b in batches]
+    us_layer = timed(lambda i: layer[i % nb]())
+    T, E, H = cfg.T, cfg.num_experts, cfg.H
+    KB = H // 128
+    nbytes = 4 * E * H + T * H + 4 * T * KB + 2 * 4 * T * KB * E
+    flop = 2.0 * T * E * H
+    proj_us = max(us_hidden - us_logits, 1e-3)
+    if nbytes / (HBM_PEAK_GBS * 1e9) >= flop / (FP32_FMA_PEAK_TFLOPS * 1e12):
+        ach = nbytes / (proj_us * 1e-6) / 1e9
+        roof = {"bound": "hbm", "achieved": round(ach, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": round(ach / HBM_PEAK_GBS, 4)}
+    else:
+        ach = flop / (proj_us * 1e-6) / 1e12
+        roof = {"bound": "alu", "achieved": round(ach, 2), "peak": FP32_FMA_PEAK_TFLOPS,
+                "unit": "TFLOP/s", "frac": round(ach / FP32_FMA_PEAK_TFLOPS, 4)}
+    roof["algorithmic_bytes"] = int(nbytes)
+    roof["flop"] = int(flop)
+    return {"route_from_hidden_us": round(us_hidden, 2), "route_from_logits_us": round(us_logits, 2),
+            "projection_us": round(proj_us, 2), "layer_with_projection_us": round(us_layer, 2),
+            "unfused_torch_projection_then_route_us": round(us_unfused, 2),
+            "roofline": roof}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -230,8 +305,9 @@ def main():
     host_ms = (time.perf_counter() - h0) * 1e3
     torch.cuda.synchronize()
 
-    def prefill():
-        torch.cuda._sleep(int((2.0 * host_ms + 2.0) * cycles_per_ms))
+    def prefill(enqueue_ms=None):
+        ms = host_ms if enqueue_ms is None else enqueue_ms
+        torch.cuda._sleep(int((2.0 * ms + 2.0) * cycles_per_ms))
 
     # timed region 1: plain calls -> value
     t_start = torch.cuda.Event(enable_timing=True)
@@ -304,6 +380,8 @@ def main():
             times.append(e0.elapsed_time(e1))
         cold = round(float(np.median(times)) * 1e3, 2)
 
+    router = router_projection_leg(cfg, shape, batches, weights, out, ws, stream, K, prefill)
+
     cpu = None
     if not args.no_cpu_baseline:
         cpu = cpu_baseline(cfg, batches, weights, args.cpu_max_tokens)
@@ -334,6 +412,7 @@ def main():
         "stage_us": {n: round(float(v) * 1e3, 2) for n, v in zip(names, stage_avg)},
         "roofline": roof,
         "cpu_baseline": cpu,
+        "router_projection": router,
         "us_per_call_cold": cold,
         "host_enqueue_us_per_call": round(host_ms * 1e3 / K, 1),
         "prefill_covered_enqueue": bool(enq_ms < 2.0 * host_ms + 2.0),

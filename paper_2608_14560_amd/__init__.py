@@ -269,7 +269,10 @@ class FusedCall:
     contents may change between calls."""
 
     def __init__(self, shape: Shape, hidden, hidden_scale, logits, bias, w13, w13_scale, w2,
-                 w2_scale, out, workspace, route_out: dict | None = None, stream=None):
+                 w2_scale, out, workspace, route_out: dict | None = None, stream=None,
+                 router: bool = False):
+        """router=True: `logits` is the fp32 router weight [E_g, H] and each call
+        runs moe_fused_fp8_router (no staged variant)."""
         self._keep = (shape.c(), route_out and _route_struct(route_out))
         args = _fused_args(shape, hidden, hidden_scale, logits, bias, w13, w13_scale, w2,
                            w2_scale, out, route_out, workspace)
@@ -277,8 +280,8 @@ class FusedCall:
         if route_out is not None:
             args[10] = ctypes.byref(self._keep[1])
         self._args = (*args, _stream(stream))
-        self._fn = lib().moe_fused_fp8
-        self._staged = lib().moe_fused_fp8_staged
+        self._fn = lib().moe_fused_fp8_router if router else lib().moe_fused_fp8
+        self._staged = None if router else lib().moe_fused_fp8_staged
         self.out = out
 
     def __call__(self):

@@ -92,18 +92,53 @@ struct RouteParams {
   int KB;
 };
 
-// Logit of expert e for token t.  Given the router projection's block sums
-// p_kb, the logit is the fused multiply-add chain over the blocks, ascending,
-// from 0: acc = fmaf(scale[kb], p_kb, acc) -- the second half of the
-// projection's fixed fp32 sequence (the first half, the chain inside a
-// block, runs in the projection kernel).
-__device__ __forceinline__ float route_logit(const RouteParams &p, int t, int e) {
-  if (!p.partials) return p.logits[(size_t)t * p.E + e];
-  const float *pp = p.partials + (size_t)t * p.KB * p.E + e;
+// Logits of the lane's experts e = q * 64 + lane (q < EPL) for token t.
+// Given the router projection's block sums p_kb, each logit is the fused
+// multiply-add chain over the blocks, ascending, from 0:
+// acc = fmaf(scale[kb], p_kb, acc) -- the second half of the projection's
+// fixed fp32 sequence (the chain inside a block runs in the projection
+// kernel).  The block sums are fetched 32 blocks at a time for all slots
+// before the chains consume them (fewer blocks per batch for wide routers), so
+// the loads overlap.  Experts past E get 0.
+template <int EPL>
+__device__ __forceinline__ void route_logits(const RouteParams &p, int t, int lane,
+                                             float (&lg)[EPL]) {
+  // every load is in bounds (clamped indices) and unconditional; values past
+  // E or KB are replaced by 0 afterwards
+  if (!p.partials) {
+#pragma unroll
+    for (int q = 0; q < EPL; ++q) {
+      const int e = q * kWave + lane;
+      const float x = p.logits[(size_t)t * p.E + min(e, p.E - 1)];
+      lg[q] = e < p.E ? x : 0.0f;
+    }
+    return;
+  }
+  constexpr int kChunk = EPL >= 8 ? 64 / EPL : 32;
+  const float *pp = p.partials + (size_t)t * p.KB * p.E;
   const float *sc = p.pscale + (size_t)t * p.KB;
-  float acc = 0.0f;
-  for (int kb = 0; kb < p.KB; ++kb) acc = __builtin_fmaf(sc[kb], pp[(size_t)kb * p.E], acc);
-  return acc;
+#pragma unroll
+  for (int q = 0; q < EPL; ++q) lg[q] = 0.0f;
+  for (int kb0 = 0; kb0 < p.KB; kb0 += kChunk) {
+    float v[kChunk][EPL], s[kChunk];
+#pragma unroll
+    for (int j = 0; j < kChunk; ++j) {
+      const int kb = min(kb0 + j, p.KB - 1);
+      s[j] = sc[kb];
+#pragma unroll
+      for (int q = 0; q < EPL; ++q) {
+        const int e = q * kWave + lane;
+        const float x = pp[(size_t)kb * p.E + min(e, p.E - 1)];
+        v[j][q] = e < p.E ? x : 0.0f;
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < kChunk; ++j)
+      if (kb0 + j < p.KB) {
+#pragma unroll
+        for (int q = 0; q < EPL; ++q) lg[q] = __builtin_fmaf(s[j], v[j][q], lg[q]);
+      }
+  }
 }
 
 // Router projection: block sums of the dequantised-code rows against the

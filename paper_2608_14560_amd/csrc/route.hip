@@ -66,17 +66,20 @@ __global__ __launch_bounds__(256) void route_kernel(RouteParams p) {
   constexpr int GMAX = GC > 0 ? GC : 64;
   const int G = GC > 0 ? GC : p.G;
   const int lane = threadIdx.x & (kWave - 1);
-  const int t = blockIdx.x * (blockDim.x / kWave) + (threadIdx.x / kWave);
+  // the token is uniform over the wave: readfirstlane lets its row addresses
+  // (scales, logits) live in scalar registers
+  const int t = __builtin_amdgcn_readfirstlane(blockIdx.x * (blockDim.x / kWave) + (threadIdx.x / kWave));
   if (t >= p.T) return;  // whole wave leaves; the kernel has no block barrier
 
   const int gsz = p.E / G;
 
-  float sc[EPL], key[EPL];
+  float sc[EPL], key[EPL], lg[EPL];
+  route_logits<EPL>(p, t, lane, lg);
 #pragma unroll
   for (int q = 0; q < EPL; ++q) {
     const int e = q * kWave + lane;
     if (e < p.E) {
-      sc[q] = sigmoid_spec(route_logit(p, t, e));
+      sc[q] = sigmoid_spec(lg[q]);
       key[q] = sc[q] + p.bias[e];
     } else {
       sc[q] = 0.0f;
@@ -249,13 +252,14 @@ __device__ __forceinline__ void route_token_seg(const RouteParams &p, int t) {
   const int lane = threadIdx.x & (kWave - 1);
   const int seg_lane = lane & (S - 1);
 
-  float sc[EPL], key[EPL];
+  float sc[EPL], key[EPL], lg[EPL];
   Key2 k2[EPL];
+  route_logits<EPL>(p, t, lane, lg);
 #pragma unroll
   for (int q = 0; q < EPL; ++q) {
     const int e = q * kWave + lane;
     const bool v = e < p.E;
-    sc[q] = v ? sigmoid_spec(route_logit(p, t, e)) : 0.0f;
+    sc[q] = v ? sigmoid_spec(lg[q]) : 0.0f;
     key[q] = v ? sc[q] + p.bias[e] : -INFINITY;
     k2[q].ah = v ? ordered_bits(key[q]) : 0u;
     k2[q].al = ~(uint32_t)e;
@@ -340,7 +344,7 @@ __device__ __forceinline__ void route_token_seg(const RouteParams &p, int t) {
 
 template <int EPL, int S>
 __global__ __launch_bounds__(256) void route_seg_kernel(RouteParams p) {
-  const int t = blockIdx.x * (blockDim.x / kWave) + (threadIdx.x / kWave);
+  const int t = __builtin_amdgcn_readfirstlane(blockIdx.x * (blockDim.x / kWave) + (threadIdx.x / kWave));
   if (t >= p.T) return;
   route_token_seg<EPL, S>(p, t);
 }
@@ -392,16 +396,33 @@ hipError_t launch_route(const RouteParams &p, hipStream_t st) {
 // Test hook: the logits the routing kernels form (from the router
 // projection's block sums, or as given).
 namespace {
-__global__ void logits_kernel(RouteParams p, float *logits) {
-  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i < (int64_t)p.T * p.E) logits[i] = route_logit(p, (int)(i / p.E), (int)(i % p.E));
+template <int EPL>
+__global__ __launch_bounds__(256) void logits_kernel(RouteParams p, float *logits) {
+  // one wave per token, as in the routing kernels
+  const int t = __builtin_amdgcn_readfirstlane(blockIdx.x * (blockDim.x / kWave) + threadIdx.x / kWave);
+  const int lane = threadIdx.x & (kWave - 1);
+  if (t >= p.T) return;
+  float lg[EPL];
+  route_logits<EPL>(p, t, lane, lg);
+#pragma unroll
+  for (int q = 0; q < EPL; ++q)
+    if (q * kWave + lane < p.E) logits[(size_t)t * p.E + q * kWave + lane] = lg[q];
 }
 }  // namespace
 
 hipError_t launch_router_logits(const RouteParams &p, float *logits, hipStream_t st) {
-  const int64_t n = (int64_t)p.T * p.E;
-  if (n <= 0) return hipSuccess;
-  hipLaunchKernelGGL(logits_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, p, logits);
+  if (p.T <= 0) return hipSuccess;
+  const dim3 grid((p.T + 3) / 4), block(256);
+  if (p.E <= 64)
+    hipLaunchKernelGGL(logits_kernel<1>, grid, block, 0, st, p, logits);
+  else if (p.E <= 128)
+    hipLaunchKernelGGL(logits_kernel<2>, grid, block, 0, st, p, logits);
+  else if (p.E <= 256)
+    hipLaunchKernelGGL(logits_kernel<4>, grid, block, 0, st, p, logits);
+  else if (p.E <= 512)
+    hipLaunchKernelGGL(logits_kernel<8>, grid, block, 0, st, p, logits);
+  else
+    hipLaunchKernelGGL(logits_kernel<16>, grid, block, 0, st, p, logits);
   return hipGetLastError();
 }
 

@@ -35,25 +35,40 @@ __global__ __launch_bounds__(256) void router_partials_kernel(RouterParams p) {
   const int wave = tid / kWave;
   const int KB = p.H / 128;
 
-  // weight tile: 64 rows x 128 fp32 of block kb (rows past E read as zero)
-  for (int i = tid; i < kProjExperts * 32; i += 256) {
-    const int r = i >> 5, c4 = i & 31;
-    float4 v = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+  // weight tile: 64 rows x 128 fp32 of block kb (rows past E read as zero),
+  // and hidden tile: 16 rows x 128 codes, decoded exactly to fp32.  Every
+  // load is issued before the first LDS store, so they overlap.
+  constexpr int kWLoads = kProjExperts * 32 / 256;
+  float4 wv[kWLoads];
+#pragma unroll
+  for (int j = 0; j < kWLoads; ++j) {
+    const int i = tid + 256 * j, r = i >> 5, c4 = i & 31;
+    wv[j] = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
     if (e0 + r < p.E)
-      v = *reinterpret_cast<const float4 *>(p.weight + (size_t)(e0 + r) * p.H + kb * 128 + c4 * 4);
-    *reinterpret_cast<float4 *>(&w_l[r * kWStride + c4 * 4]) = v;
+      wv[j] = *reinterpret_cast<const float4 *>(p.weight + (size_t)(e0 + r) * p.H + kb * 128 + c4 * 4);
   }
-  // hidden tile: 16 rows x 128 codes of block kb, decoded exactly to fp32
-  for (int i = tid; i < kProjTokens * 32; i += 256) {
-    const int r = i >> 5, c4 = i & 31;
-    int q = 0;
+  constexpr int kXLoads = kProjTokens * 32 / 256;
+  int xq[kXLoads];
+#pragma unroll
+  for (int j = 0; j < kXLoads; ++j) {
+    const int i = tid + 256 * j, r = i >> 5, c4 = i & 31;
+    xq[j] = 0;
     if (t0 + r < p.T)
-      q = *reinterpret_cast<const int *>(p.hidden + (size_t)(t0 + r) * p.H + kb * 128 + c4 * 4);
+      xq[j] = *reinterpret_cast<const int *>(p.hidden + (size_t)(t0 + r) * p.H + kb * 128 + c4 * 4);
+  }
+#pragma unroll
+  for (int j = 0; j < kWLoads; ++j) {
+    const int i = tid + 256 * j, r = i >> 5, c4 = i & 31;
+    *reinterpret_cast<float4 *>(&w_l[r * kWStride + c4 * 4]) = wv[j];
+  }
+#pragma unroll
+  for (int j = 0; j < kXLoads; ++j) {
+    const int i = tid + 256 * j, r = i >> 5, c4 = i & 31;
     float4 v;
-    v.x = __builtin_amdgcn_cvt_f32_fp8(q, 0);
-    v.y = __builtin_amdgcn_cvt_f32_fp8(q, 1);
-    v.z = __builtin_amdgcn_cvt_f32_fp8(q, 2);
-    v.w = __builtin_amdgcn_cvt_f32_fp8(q, 3);
+    v.x = __builtin_amdgcn_cvt_f32_fp8(xq[j], 0);
+    v.y = __builtin_amdgcn_cvt_f32_fp8(xq[j], 1);
+    v.z = __builtin_amdgcn_cvt_f32_fp8(xq[j], 2);
+    v.w = __builtin_amdgcn_cvt_f32_fp8(xq[j], 3);
     *reinterpret_cast<float4 *>(&x_l[r * 128 + c4 * 4]) = v;
   }
   __syncthreads();
