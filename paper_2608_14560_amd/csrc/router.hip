@@ -8,7 +8,7 @@
 // chain over the blocks, acc = fmaf(scale, block sum, acc).
 //
 // This kernel computes the block sums only, split over (block, 64 experts,
-// 16 tokens) workgroups, so a decode-sized batch spreads the 7 MB weight
+// 16 or 32 tokens) workgroups, so a decode-sized batch spreads the 7 MB weight
 // stream over the whole chip; the routing kernel forms each logit from the
 // block sums while it routes, so the logits never go to memory.
 //
@@ -18,13 +18,17 @@
 namespace moe {
 namespace {
 
-constexpr int kProjTokens = 16;   // tokens per workgroup (4 per wave)
 constexpr int kProjExperts = 64;  // experts per workgroup (one per lane)
 // LDS row stride of the weight tile in floats: 128 + 4 keeps the lanes'
 // 16-byte row reads on distinct banks
 constexpr int kWStride = 132;
 
+// TPW tokens per wave, 4 waves: 4 TPW tokens per workgroup.  Large batches
+// take 8 (the weight tile is then reused by 32 tokens), small ones 4 (more
+// workgroups to spread the weight stream).
+template <int TPW>
 __global__ __launch_bounds__(256) void router_partials_kernel(RouterParams p) {
+  constexpr int kProjTokens = 4 * TPW;
   __shared__ __attribute__((aligned(16))) float w_l[kProjExperts * kWStride];
   __shared__ __attribute__((aligned(16))) float x_l[kProjTokens * 128];
   const int kb = blockIdx.x;
@@ -73,16 +77,18 @@ __global__ __launch_bounds__(256) void router_partials_kernel(RouterParams p) {
   }
   __syncthreads();
 
-  // lane = expert e0 + lane, wave = tokens 4 wave .. 4 wave + 3: four
-  // independent chains, each ascending over the block's 128 elements
-  float acc[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+  // lane = expert e0 + lane, wave = tokens TPW wave .. TPW wave + TPW - 1:
+  // TPW independent chains, each ascending over the block's 128 elements
+  float acc[TPW];
+#pragma unroll
+  for (int j = 0; j < TPW; ++j) acc[j] = 0.0f;
   const float *wr = &w_l[lane * kWStride];
-  const float *xr = &x_l[wave * 4 * 128];
+  const float *xr = &x_l[wave * TPW * 128];
 #pragma unroll 8
   for (int h = 0; h < 128; h += 4) {
     const float4 w4 = *reinterpret_cast<const float4 *>(wr + h);
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
+    for (int j = 0; j < TPW; ++j) {
       const float4 x4 = *reinterpret_cast<const float4 *>(xr + j * 128 + h);
       acc[j] = __builtin_fmaf(x4.x, w4.x, acc[j]);
       acc[j] = __builtin_fmaf(x4.y, w4.y, acc[j]);
@@ -93,8 +99,8 @@ __global__ __launch_bounds__(256) void router_partials_kernel(RouterParams p) {
   const int e = e0 + lane;
   if (e < p.E) {
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int t = t0 + wave * 4 + j;
+    for (int j = 0; j < TPW; ++j) {
+      const int t = t0 + wave * TPW + j;
       if (t < p.T) p.partials[((size_t)t * KB + kb) * p.E + e] = acc[j];
     }
   }
@@ -104,9 +110,12 @@ __global__ __launch_bounds__(256) void router_partials_kernel(RouterParams p) {
 
 hipError_t launch_router_partials(const RouterParams &p, hipStream_t st) {
   if (p.T == 0) return hipSuccess;
-  dim3 grid(p.H / 128, (p.E + kProjExperts - 1) / kProjExperts,
-            (p.T + kProjTokens - 1) / kProjTokens);
-  hipLaunchKernelGGL(router_partials_kernel, grid, dim3(256), 0, st, p);
+  const int tpw = p.T >= 512 ? 8 : 4;
+  dim3 grid(p.H / 128, (p.E + kProjExperts - 1) / kProjExperts, (p.T + 4 * tpw - 1) / (4 * tpw));
+  if (tpw == 8)
+    hipLaunchKernelGGL(router_partials_kernel<8>, grid, dim3(256), 0, st, p);
+  else
+    hipLaunchKernelGGL(router_partials_kernel<4>, grid, dim3(256), 0, st, p);
   return hipGetLastError();
 }
 

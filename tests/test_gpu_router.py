@@ -49,13 +49,14 @@ def _assert_bits(got, ref, what):
 
 
 LOGIT_CASES = [("tiny", 8), ("small_ragged", 77), ("small_g6", 50), ("small_many", 300),
-               ("decode", 1), ("decode", 16), ("decode", 33), ("decode", 256)]
+               ("decode", 1), ("decode", 16), ("decode", 33), ("decode", 256), ("decode", 600)]
 
 
 @pytest.mark.parametrize("name,T", LOGIT_CASES)
 def test_router_logits_bitexact(M, name, T):
-    """Token counts around the projection's 16-token tiles (1, 16, 33), expert
-    counts below and across its 64-expert tiles (16, 32, 64, 96, 256)."""
+    """Token counts around the projection's 16-token tiles (1, 16, 33) and its
+    32-token tiles for large batches (600: a ragged last tile), expert counts
+    below and across its 64-expert tiles (16, 32, 64, 96, 256)."""
     cfg = W.all_configs()[name].with_(T=T)
     log(f"router logits {name} T={T}")
     hq, hs, wg, _ = _router_inputs(cfg, 3)
