@@ -42,6 +42,11 @@ class OracleShape(ctypes.Structure):
                 ("routed_scaling_factor", ctypes.c_float)]
 
 
+class OracleDsaShape(ctypes.Structure):
+    _fields_ = [("B", ctypes.c_int32), ("NH", ctypes.c_int32), ("D", ctypes.c_int32),
+                ("PS", ctypes.c_int32), ("topk", ctypes.c_int32), ("max_pages", ctypes.c_int32)]
+
+
 _lib = None
 
 
@@ -81,6 +86,10 @@ def lib():
         L.oracle_forward.argtypes = ([ctypes.POINTER(OracleShape)] + [P] * 8
                                      + [P, ctypes.c_int32, P, P, P])
         L.oracle_forward.restype = ctypes.c_int
+        L.oracle_dsa_scores.argtypes = [ctypes.POINTER(OracleDsaShape)] + [P] * 6 + [ctypes.c_int32, P]
+        L.oracle_dsa_scores.restype = ctypes.c_int
+        L.oracle_dsa_topk.argtypes = [ctypes.POINTER(OracleDsaShape)] + [P] * 7
+        L.oracle_dsa_topk.restype = ctypes.c_int
         L.oracle_num_threads.argtypes = []
         L.oracle_num_threads.restype = ctypes.c_int
         _lib = L
@@ -267,3 +276,37 @@ def num_threads() -> int:
 def bf16_bits_to_float(bits: np.ndarray) -> np.ndarray:
     """Reads bf16 bit patterns as fp32 values (a reinterpretation, no arithmetic)."""
     return (np.asarray(bits, dtype=np.uint16).astype(np.uint32) << 16).view(np.float32)
+
+
+# ---------------------------------------------------------------- DSA TopK indexer
+def _dsa_args(q, w, kc, ks, block_table, seq_lens, topk):
+    q = np.ascontiguousarray(q, dtype=np.uint8)
+    w = np.ascontiguousarray(w, dtype=np.float32)
+    kc = np.ascontiguousarray(kc, dtype=np.uint8)
+    ks = np.ascontiguousarray(ks, dtype=np.float32)
+    bt = np.ascontiguousarray(block_table, dtype=np.int32)
+    sl = np.ascontiguousarray(seq_lens, dtype=np.int32)
+    B, NH, D = q.shape
+    shape = OracleDsaShape(B, NH, D, kc.shape[1], topk, bt.shape[1])
+    return shape, (q, w, kc, ks, bt, sl)
+
+
+def dsa_scores(q, w, kc, ks, block_table, seq_lens, b: int) -> np.ndarray:
+    """DSA TopK Indexer scores (paper Section 3.1.3) of sequence b, fp32 [seq_len]."""
+    shape, arrs = _dsa_args(q, w, kc, ks, block_table, seq_lens, 1)
+    out = np.empty(max(int(arrs[5][b]), 1), np.float32)
+    rc = lib().oracle_dsa_scores(ctypes.byref(shape), *[_ptr(a) for a in arrs], int(b), _ptr(out))
+    if rc:
+        raise ValueError(f"oracle_dsa_scores: bad argument ({rc})")
+    return out[: int(arrs[5][b])]
+
+
+def dsa_topk(q, w, kc, ks, block_table, seq_lens, topk: int = 2048) -> np.ndarray:
+    """DSA TopK Indexer: int32 [B, topk] physical cache indices of the topk best
+    tokens of each sequence, in ascending position order, padded with -1."""
+    shape, arrs = _dsa_args(q, w, kc, ks, block_table, seq_lens, topk)
+    out = np.empty((shape.B, topk), np.int32)
+    rc = lib().oracle_dsa_topk(ctypes.byref(shape), *[_ptr(a) for a in arrs], _ptr(out))
+    if rc:
+        raise ValueError(f"oracle_dsa_topk: bad argument ({rc})")
+    return out

@@ -24,6 +24,9 @@
  * FP8 block arithmetic with fp32 promotion (they decide the re-quantised
  * FP8 codes).
  *
+ * The file also holds the oracle of the paper's DSA TopK Indexer (Section
+ * 3.1.3), at its end.
+ *
  * Build: gcc -O2 -fopenmp -ffp-contract=off -fno-fast-math -shared -fPIC
  * (contraction must stay off: the fp32 routing sequence is a specification).
  */
@@ -553,4 +556,112 @@ int oracle_num_threads(void) {
 #else
   return 1;
 #endif
+}
+
+/* ======================================================================== */
+/* DSA TopK Indexer (paper Section 3.1.3): for each batch element b, score   */
+/* every cached token j < seq_len[b] of the sequence against the query's    */
+/* 64 heads and return the TopK highest-scoring tokens.                     */
+/*   score(j) = sum over heads h of ReLU(q_h . k_j) * w_h                    */
+/* Layouts: q [B, NH, D] e4m3; weights [B, NH] fp32; the key cache is paged: */
+/* kc [num_pages, PS, D] e4m3 with per-token fp32 scales ks [num_pages, PS]; */
+/* token j of sequence b is slot j % PS of page block_table[b][j / PS].     */
+/* The scores decide which indices are returned, so they follow one fixed    */
+/* fp32 sequence (the paper's kernel also keeps a scalar fp32 dot product    */
+/* for bit-exactness):                                                        */
+/*   kd[d]   = dec(kc[page, slot, d]) * ks[page, slot]      (one rounding)   */
+/*   dot_h   = fused multiply-add chain over d ascending from 0 of          */
+/*             dec(q[b, h, d]) * kd[d]                                        */
+/*   score   = fused multiply-add chain over h ascending from 0 of          */
+/*             max(dot_h, 0) * w[b, h]                                        */
+/* Selection: the TopK tokens by score, larger first, equal scores to the    */
+/* lower position; returned in ascending position order as physical cache   */
+/* indices page * PS + slot, the rest of the TopK row padded with -1 (a      */
+/* sequence of at most TopK tokens returns all of them).                     */
+/* ======================================================================== */
+typedef struct {
+  int32_t B, NH, D, PS, topk, max_pages;
+} oracle_dsa_shape;
+
+int oracle_dsa_scores(const oracle_dsa_shape *s, const uint8_t *q, const float *w,
+                      const uint8_t *kc, const float *ks, const int32_t *block_table,
+                      const int32_t *seq_lens, int32_t b, float *scores) {
+  int32_t L, j;
+  if (!s || s->NH <= 0 || s->D <= 0 || s->PS <= 0 || b < 0 || b >= s->B) return ORACLE_BAD_ARG;
+  L = seq_lens[b];
+  if (L < 0 || L > s->max_pages * s->PS) return ORACLE_BAD_ARG;
+#pragma omp parallel for schedule(static)
+  for (j = 0; j < L; ++j) {
+    int64_t page = block_table[(int64_t)b * s->max_pages + j / s->PS];
+    int slot = j % s->PS, h, d;
+    const uint8_t *krow = kc + (page * s->PS + slot) * s->D;
+    float scale = ks[page * s->PS + slot];
+    float acc = 0.0f;
+    for (h = 0; h < s->NH; ++h) {
+      const uint8_t *qrow = q + ((int64_t)b * s->NH + h) * s->D;
+      float dot = 0.0f, r;
+      for (d = 0; d < s->D; ++d) {
+        float kd = (float)oracle_e4m3_decode(krow[d]) * scale;
+        dot = fmaf((float)oracle_e4m3_decode(qrow[d]), kd, dot);
+      }
+      r = dot > 0.0f ? dot : 0.0f;
+      acc = fmaf(r, w[(int64_t)b * s->NH + h], acc);
+    }
+    scores[j] = acc;
+  }
+  return ORACLE_OK;
+}
+
+typedef struct {
+  float v;
+  int32_t j;
+} dsa_item;
+
+static int dsa_by_score(const void *a, const void *b) {
+  const dsa_item *x = (const dsa_item *)a, *y = (const dsa_item *)b;
+  if (x->v > y->v) return -1;
+  if (x->v < y->v) return 1;
+  return x->j < y->j ? -1 : (x->j > y->j);
+}
+
+static int dsa_by_pos(const void *a, const void *b) {
+  const dsa_item *x = (const dsa_item *)a, *y = (const dsa_item *)b;
+  return x->j < y->j ? -1 : (x->j > y->j);
+}
+
+int oracle_dsa_topk(const oracle_dsa_shape *s, const uint8_t *q, const float *w,
+                    const uint8_t *kc, const float *ks, const int32_t *block_table,
+                    const int32_t *seq_lens, int32_t *out) {
+  int32_t b;
+  if (!s || s->B < 0 || s->topk <= 0) return ORACLE_BAD_ARG;
+  for (b = 0; b < s->B; ++b) {
+    int32_t L = seq_lens[b], n, i, rc;
+    float *sc;
+    dsa_item *it;
+    int32_t *o = out + (int64_t)b * s->topk;
+    if (L < 0 || L > s->max_pages * s->PS) return ORACLE_BAD_ARG;
+    sc = (float *)malloc(sizeof(float) * (L > 0 ? L : 1));
+    it = (dsa_item *)malloc(sizeof(dsa_item) * (L > 0 ? L : 1));
+    if (!sc || !it) return ORACLE_NO_MEM;
+    rc = oracle_dsa_scores(s, q, w, kc, ks, block_table, seq_lens, b, sc);
+    if (rc) return rc;
+    for (i = 0; i < L; ++i) {
+      it[i].v = sc[i];
+      it[i].j = i;
+    }
+    qsort(it, L, sizeof(dsa_item), dsa_by_score);
+    n = L < s->topk ? L : s->topk;
+    qsort(it, n, sizeof(dsa_item), dsa_by_pos);
+    for (i = 0; i < s->topk; ++i) {
+      if (i < n) {
+        int32_t j = it[i].j;
+        o[i] = block_table[(int64_t)b * s->max_pages + j / s->PS] * s->PS + j % s->PS;
+      } else {
+        o[i] = -1;
+      }
+    }
+    free(sc);
+    free(it);
+  }
+  return ORACLE_OK;
 }

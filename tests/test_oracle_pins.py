@@ -649,3 +649,93 @@ def test_router_logits_scale_and_zero(oracle_lib):
     assert (b == 2 * a).all()
     z = oracle_lib.router_logits(shape, np.zeros_like(hq.numpy()), hs.numpy(), wg)
     assert (z == 0).all()
+
+
+# ------------------------------------------------------ DSA TopK indexer
+def _dsa_np(x):
+    return (x.q.numpy(), x.weights.numpy(), x.k_cache.numpy(), x.k_scale.numpy(),
+            x.block_table.numpy(), x.seq_lens.numpy())
+
+
+def _dsa_exact(x, b):
+    """fp64 score of every token of sequence b, and sum_h |w_h| sum_d |q k| (bound scale)."""
+    q, w, kc, ks, bt, sl = _dsa_np(x)
+    PS = kc.shape[1]
+    L = int(sl[b])
+    j = np.arange(L)
+    pages = bt[b, j // PS]
+    kd = torch.from_numpy(kc[pages, j % PS]).view(torch.float8_e4m3fn).double().numpy() * ks[pages, j % PS][:, None]
+    qd = torch.from_numpy(q[b]).view(torch.float8_e4m3fn).double().numpy()
+    dots = kd @ qd.T                                  # [L, NH]
+    exact = np.maximum(dots, 0) @ w[b].astype(np.float64)
+    mag = (np.abs(kd) @ np.abs(qd).T) @ np.abs(w[b]).astype(np.float64)
+    return exact, mag
+
+
+def test_dsa_scores_error_bound(oracle_lib):
+    """The fixed fp32 sequence against the fp64 definition: within the bound of its
+    roundings ((D + NH + 2) u times the magnitudes; the ReLU only shrinks
+    differences); a dropped head, a wrong page or a transposed operand breaks it."""
+    cfg = W.IndexerConfig("pin", (700, 130), topk=64)
+    x = W.generate_indexer(cfg, 5)
+    u = 2.0 ** -24
+    for b in range(cfg.B):
+        got = oracle_lib.dsa_scores(*_dsa_np(x), b).astype(np.float64)
+        exact, mag = _dsa_exact(x, b)
+        assert (np.abs(got - exact) <= (cfg.head_dim + cfg.num_heads + 2) * u * mag).all()
+        assert np.abs(exact).std() > 0.1 and (np.abs(got - exact) > 0).mean() > 0.3
+
+
+def test_dsa_scores_exact_on_integers(oracle_lib):
+    """Integer codes, power-of-two token scales and weights: every step is exact."""
+    rng = np.random.default_rng(41)
+    B, NH, D, PS, pages = 2, 64, 128, 64, 6
+    codes = {v: _code(v) for v in range(-8, 9)}
+    qv = rng.integers(-8, 9, (B, NH, D))
+    kv = rng.integers(-8, 9, (pages, PS, D))
+    q = np.vectorize(codes.get)(qv).astype(np.uint8)
+    kc = np.vectorize(codes.get)(kv).astype(np.uint8)
+    ks = np.exp2(rng.integers(-3, 3, (pages, PS))).astype(np.float32)
+    w = np.exp2(rng.integers(-4, 2, (B, NH))).astype(np.float32)
+    bt = np.array([[4, 1, 0], [2, 5, 3]], np.int32)
+    sl = np.array([150, 190], np.int32)
+    for b in range(B):
+        got = oracle_lib.dsa_scores(q, w, kc, ks, bt, sl, b)
+        j = np.arange(sl[b])
+        pg = bt[b, j // PS]
+        dots = (kv[pg, j % PS] * ks[pg, j % PS][:, None].astype(np.float64)) @ qv[b].T
+        ref = np.maximum(dots, 0) @ w[b].astype(np.float64)
+        assert (got.astype(np.float64) == ref).all()
+
+
+def test_dsa_topk_selection_brute_force(oracle_lib):
+    """The selection against a plain sort of the oracle's own scores: the topk
+    positions by (score descending, position ascending), returned in ascending
+    position order through the block table, padded with -1."""
+    cfg = W.IndexerConfig("pin", (300, 16, 17, 0, 129), topk=16)
+    x = W.generate_indexer(cfg, 6)
+    got = oracle_lib.dsa_topk(*_dsa_np(x), cfg.topk)
+    bt = x.block_table.numpy()
+    for b, L in enumerate(cfg.seq_lens):
+        sc = oracle_lib.dsa_scores(*_dsa_np(x), b) if L else np.zeros(0, np.float32)
+        order = sorted(range(L), key=lambda j: (-float(sc[j]), j))[: cfg.topk]
+        pos = sorted(order)
+        ref = [int(bt[b, j // 64]) * 64 + j % 64 for j in pos] + [-1] * (cfg.topk - len(pos))
+        assert got[b].tolist() == ref, b
+
+
+def test_dsa_topk_ties_and_relu(oracle_lib):
+    """Queries opposite to every key make every head's dot negative: ReLU zeroes
+    them, all scores are 0, and the tie rule returns the first topk positions."""
+    cfg = W.IndexerConfig("pin", (500,), topk=32)
+    x = W.generate_indexer(cfg, 7)
+    kc = x.k_cache.numpy().copy()
+    kc[:] = _code(1.0)
+    q = x.q.numpy().copy()
+    q[:] = _code(-1.0)
+    w = np.abs(x.weights.numpy()) + 0.1
+    args = (q, w, kc, x.k_scale.numpy(), x.block_table.numpy(), x.seq_lens.numpy())
+    assert (oracle_lib.dsa_scores(*args, 0) == 0).all()
+    got = oracle_lib.dsa_topk(*args, cfg.topk)
+    bt = x.block_table.numpy()
+    assert got[0].tolist() == [int(bt[0, j // 64]) * 64 + j % 64 for j in range(cfg.topk)]

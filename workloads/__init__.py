@@ -231,3 +231,90 @@ def host_arrays(inp: MoEInputs, experts=None) -> dict:
                 logits=inp.logits.cpu().numpy(), bias=inp.bias.cpu().numpy(),
                 w13=per_expert(inp.w13), w13_scale=per_expert(inp.w13_scale),
                 w2=per_expert(inp.w2), w2_scale=per_expert(inp.w2_scale))
+
+
+# ---------------------------------------------------------------------------
+# DSA TopK Indexer (paper Section 3.1.3): FP8 queries with 64 heads of 128,
+# a paged FP8 key cache (64 tokens per page) with per-token fp32 scales,
+# per-head weights, sequence lengths and block tables.  The paper's contest
+# workloads are not available; these seeded inputs stand in for them:
+#   q        N(0,1) per (b, head) row, quantised to e4m3 with scale amax/448;
+#            the row scale is folded into the head weight (the operator has
+#            no query scale)                                            id 21
+#   weights  N(0,1) * row scale / sqrt(64 * 128)                        id 22
+#   K cache  N(0,1) per token, quantised to e4m3 with scale amax/448    id 23
+#   block tables: each sequence's pages drawn without replacement from
+#            the cache (a random permutation)                           id 24
+# ---------------------------------------------------------------------------
+TID_DSA_Q, TID_DSA_W, TID_DSA_K, TID_DSA_BT = 21, 22, 23, 24
+
+
+@dataclass(frozen=True)
+class IndexerConfig:
+    name: str
+    seq_lens: tuple
+    num_heads: int = 64
+    head_dim: int = 128
+    page_size: int = 64
+    topk: int = 2048
+
+    @property
+    def B(self) -> int:
+        return len(self.seq_lens)
+
+    @property
+    def max_pages(self) -> int:
+        return max(1, max((s + self.page_size - 1) // self.page_size for s in self.seq_lens))
+
+    @property
+    def num_pages(self) -> int:
+        # every sequence's pages are distinct; a few spare pages
+        return sum((s + self.page_size - 1) // self.page_size for s in self.seq_lens) + 8
+
+
+INDEXER_CONFIGS: dict[str, IndexerConfig] = {
+    # the paper's long-regime representative (appendix profile): bs 4,
+    # max 36 pages; one sequence above TopK
+    "dsa_paper_long": IndexerConfig("dsa_paper_long", (98, 91, 2241, 100)),
+    # all sequences at or below TopK: the index-remap path only
+    "dsa_short": IndexerConfig("dsa_short", (64, 1, 2048, 1984, 0, 700)),
+    # long sequences, several far above TopK
+    "dsa_long": IndexerConfig("dsa_long", (65536, 32768, 8192, 2049, 40000, 16384, 2048, 100)),
+    # small parity cases around page and TopK edges (TopK 256 keeps the
+    # oracle quick while the selection still has to cut)
+    "dsa_small": IndexerConfig("dsa_small", (257, 256, 255, 1000, 63, 640, 2500), topk=256),
+}
+
+
+@dataclass
+class IndexerInputs:
+    cfg: IndexerConfig
+    q: torch.Tensor            # [B, NH, D] uint8 (e4m3 codes)
+    weights: torch.Tensor      # [B, NH] fp32
+    k_cache: torch.Tensor      # [num_pages, PS, D] uint8
+    k_scale: torch.Tensor      # [num_pages, PS] fp32
+    block_table: torch.Tensor  # [B, max_pages] int32
+    seq_lens: torch.Tensor     # [B] int32
+
+
+def generate_indexer(cfg: IndexerConfig, seed: int = 0, device="cpu") -> IndexerInputs:
+    B, NH, D, PS = cfg.B, cfg.num_heads, cfg.head_dim, cfg.page_size
+    qf = torch.randn(B * NH, D, generator=_gen(device, seed, TID_DSA_Q), device=device)
+    q, qs = quantize_blocks(qf, 1, D)
+    w = torch.randn(B, NH, generator=_gen(device, seed, TID_DSA_W), device=device)
+    w = (w * qs.reshape(B, NH) / (NH * D) ** 0.5).contiguous()
+    kf = torch.randn(cfg.num_pages * PS, D, generator=_gen(device, seed, TID_DSA_K), device=device)
+    kc, ksc = quantize_blocks(kf, 1, D)
+    g = torch.Generator(device="cpu")
+    g.manual_seed(substream_seed(seed, TID_DSA_BT))
+    perm = torch.randperm(cfg.num_pages, generator=g).to(torch.int32)
+    bt = torch.zeros(B, cfg.max_pages, dtype=torch.int32)
+    at = 0
+    for b, s in enumerate(cfg.seq_lens):
+        n = (s + PS - 1) // PS
+        bt[b, :n] = perm[at:at + n]
+        at += n
+    return IndexerInputs(cfg, q.reshape(B, NH, D).contiguous(), w,
+                         kc.reshape(cfg.num_pages, PS, D).contiguous(),
+                         ksc.reshape(cfg.num_pages, PS).contiguous(), bt.to(device),
+                         torch.tensor(cfg.seq_lens, dtype=torch.int32, device=device))
