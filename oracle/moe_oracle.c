@@ -587,27 +587,36 @@ int oracle_dsa_scores(const oracle_dsa_shape *s, const uint8_t *q, const float *
                       const uint8_t *kc, const float *ks, const int32_t *block_table,
                       const int32_t *seq_lens, int32_t b, float *scores) {
   int32_t L, j;
-  if (!s || s->NH <= 0 || s->D <= 0 || s->PS <= 0 || b < 0 || b >= s->B) return ORACLE_BAD_ARG;
+  if (!s || s->NH <= 0 || s->D <= 0 || s->D > 1024 || s->PS <= 0 || b < 0 || b >= s->B)
+    return ORACLE_BAD_ARG;
   L = seq_lens[b];
   if (L < 0 || L > s->max_pages * s->PS) return ORACLE_BAD_ARG;
+  {
+    /* the query's codes decoded once (exact in fp32) */
+    float *qd = (float *)malloc(sizeof(float) * (size_t)s->NH * s->D);
+    int i;
+    if (!qd) return ORACLE_NO_MEM;
+    for (i = 0; i < s->NH * s->D; ++i)
+      qd[i] = (float)oracle_e4m3_decode(q[(int64_t)b * s->NH * s->D + i]);
 #pragma omp parallel for schedule(static)
-  for (j = 0; j < L; ++j) {
-    int64_t page = block_table[(int64_t)b * s->max_pages + j / s->PS];
-    int slot = j % s->PS, h, d;
-    const uint8_t *krow = kc + (page * s->PS + slot) * s->D;
-    float scale = ks[page * s->PS + slot];
-    float acc = 0.0f;
-    for (h = 0; h < s->NH; ++h) {
-      const uint8_t *qrow = q + ((int64_t)b * s->NH + h) * s->D;
-      float dot = 0.0f, r;
-      for (d = 0; d < s->D; ++d) {
-        float kd = (float)oracle_e4m3_decode(krow[d]) * scale;
-        dot = fmaf((float)oracle_e4m3_decode(qrow[d]), kd, dot);
+    for (j = 0; j < L; ++j) {
+      int64_t page = block_table[(int64_t)b * s->max_pages + j / s->PS];
+      int slot = j % s->PS, h, d;
+      const uint8_t *krow = kc + (page * s->PS + slot) * s->D;
+      float scale = ks[page * s->PS + slot];
+      float kd[1024];
+      float acc = 0.0f;
+      for (d = 0; d < s->D; ++d) kd[d] = (float)oracle_e4m3_decode(krow[d]) * scale;
+      for (h = 0; h < s->NH; ++h) {
+        const float *qh = qd + (int64_t)h * s->D;
+        float dot = 0.0f, r;
+        for (d = 0; d < s->D; ++d) dot = fmaf(qh[d], kd[d], dot);
+        r = dot > 0.0f ? dot : 0.0f;
+        acc = fmaf(r, w[(int64_t)b * s->NH + h], acc);
       }
-      r = dot > 0.0f ? dot : 0.0f;
-      acc = fmaf(r, w[(int64_t)b * s->NH + h], acc);
+      scores[j] = acc;
     }
-    scores[j] = acc;
+    free(qd);
   }
   return ORACLE_OK;
 }

@@ -28,7 +28,8 @@ MOE_OK, MOE_ERR_INVALID_ARG, MOE_ERR_UNSUPPORTED, MOE_ERR_WORKSPACE_TOO_SMALL, M
 EXPORTED = ("moe_workspace_size", "moe_route", "moe_route_hidden", "moe_fused_fp8",
             "moe_fused_fp8_router", "moe_fused_fp8_staged", "moe_num_stages", "moe_stage_name",
             "moe_status_string", "moe_debug_sigmoid", "moe_debug_e4m3_encode",
-            "moe_debug_act_views", "moe_debug_mfma_block", "moe_debug_router_logits")
+            "moe_debug_act_views", "moe_debug_mfma_block", "moe_debug_router_logits",
+            "dsa_workspace_size", "dsa_topk_indexer", "dsa_debug_scores")
 
 
 class MoEError(RuntimeError):
@@ -99,6 +100,13 @@ def lib() -> ctypes.CDLL:
         L.moe_fused_fp8_router.restype = ctypes.c_int
         L.moe_debug_router_logits.argtypes = [S, P, P, P, P, P, Z, P]
         L.moe_debug_router_logits.restype = ctypes.c_int
+        DS = ctypes.POINTER(CDsaShape)
+        L.dsa_workspace_size.argtypes = [DS]
+        L.dsa_workspace_size.restype = ctypes.c_size_t
+        L.dsa_topk_indexer.argtypes = [DS, P, P, P, P, P, P, P, P, Z, P]
+        L.dsa_topk_indexer.restype = ctypes.c_int
+        L.dsa_debug_scores.argtypes = [DS, P, P, P, P, P, P, P, P]
+        L.dsa_debug_scores.restype = ctypes.c_int
         L.moe_fused_fp8_staged.argtypes = [S, P, P, P, P, P, P, P, P, P, R, P, Z, P,
                                            ctypes.POINTER(P), ctypes.c_int]
         L.moe_fused_fp8_staged.restype = ctypes.c_int
@@ -369,3 +377,57 @@ def debug_act_views(shape: Shape, workspace: torch.Tensor):
     act = workspace[a.value - base: a.value - base + P * shape.I].view(P, shape.I)
     sc = workspace[s.value - base: s.value - base + P * (shape.I // 128) * 4]
     return act, sc.view(torch.float32).view(P, shape.I // 128)
+
+
+# ---------------------------------------------------------------- DSA TopK indexer
+class CDsaShape(ctypes.Structure):
+    _fields_ = [("B", ctypes.c_int32), ("num_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32),
+                ("page_size", ctypes.c_int32), ("topk", ctypes.c_int32), ("max_pages", ctypes.c_int32),
+                ("num_pages", ctypes.c_int32)]
+
+
+def dsa_shape(q: torch.Tensor, k_cache: torch.Tensor, block_table: torch.Tensor, topk: int) -> CDsaShape:
+    B, NH, D = q.shape
+    return CDsaShape(B, NH, D, k_cache.shape[1], topk, block_table.shape[1], k_cache.shape[0])
+
+
+def dsa_workspace_size(shape: CDsaShape) -> int:
+    return int(lib().dsa_workspace_size(ctypes.byref(shape)))
+
+
+def _dsa_ptrs(q, weights, k_cache, k_scale, block_table, seq_lens):
+    return [_dev(q, torch.uint8, "q"), _dev(weights, torch.float32, "weights"),
+            _dev(k_cache, torch.uint8, "k_cache"), _dev(k_scale, torch.float32, "k_scale"),
+            _dev(block_table, torch.int32, "block_table"), _dev(seq_lens, torch.int32, "seq_lens")]
+
+
+def dsa_topk_indexer(q, weights, k_cache, k_scale, block_table, seq_lens, topk: int = 2048,
+                     out: torch.Tensor | None = None, workspace: torch.Tensor | None = None,
+                     stream=None) -> torch.Tensor:
+    """DSA TopK Indexer (paper Section 3.1.3): int32 [B, topk] physical cache
+    indices of each sequence's topk best tokens, ascending position order,
+    padded with -1."""
+    shape = dsa_shape(q, k_cache, block_table, topk)
+    if out is None:
+        out = torch.empty(max(shape.B, 1), topk, dtype=torch.int32, device=q.device)[: shape.B]
+    if workspace is None:
+        workspace = torch.empty(max(dsa_workspace_size(shape), 256), dtype=torch.uint8, device=q.device)
+    rc = lib().dsa_topk_indexer(ctypes.byref(shape), *_dsa_ptrs(q, weights, k_cache, k_scale, block_table,
+                                                                seq_lens),
+                                _dev(out, torch.int32, "out"), _dev(workspace, torch.uint8, "workspace"),
+                                workspace.numel(), _stream(stream))
+    _check("dsa_topk_indexer", rc)
+    return out
+
+
+def dsa_debug_scores(q, weights, k_cache, k_scale, block_table, seq_lens, stream=None) -> torch.Tensor:
+    """Scores [B, max_pages * page_size] of every token (test hook); entries past a
+    sequence's length are left as allocated (NaN here)."""
+    shape = dsa_shape(q, k_cache, block_table, 1)
+    scores = torch.full((max(shape.B, 1), shape.max_pages * shape.page_size), float("nan"),
+                        dtype=torch.float32, device=q.device)[: shape.B]
+    rc = lib().dsa_debug_scores(ctypes.byref(shape), *_dsa_ptrs(q, weights, k_cache, k_scale, block_table,
+                                                                seq_lens),
+                                _dev(scores, torch.float32, "scores"), _stream(stream))
+    _check("dsa_debug_scores", rc)
+    return scores

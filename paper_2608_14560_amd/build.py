@@ -3,7 +3,7 @@
     python -m paper_2608_14560_amd.build
 
 Every HIP source is compiled without packed fp32 instructions; the routing
-and router projection kernels also without floating-point contraction (their
+router projection and indexer kernels also without floating-point contraction (their
 fp32 sequences are specifications whose integer decisions must be
 reproducible).
 """
@@ -28,6 +28,7 @@ COMMON = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}", "-Wall",
 SOURCES = {
     "route.hip": ["-ffp-contract=off"],
     "router.hip": ["-ffp-contract=off"],
+    "indexer.hip": ["-ffp-contract=off"],
     "permute.hip": [],
     "gemm.hip": [],
     "gemm_tile.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"],

@@ -1,0 +1,251 @@
+// indexer.hip -- the DSA TopK Indexer (paper Section 3.1.3): for each
+// sequence, score every cached token against the query's 64 heads,
+//   score(j) = sum over heads h of ReLU(q_h . k_j) * w_h,
+// and return the TopK best tokens.  The key cache is paged (PS tokens per
+// page) in FP8 e4m3 with one fp32 scale per token; q is FP8 e4m3.
+//
+// The returned indices must be exactly the reference's, so the scores follow
+// one fixed fp32 sequence (scalar fused multiply-adds, as the paper's kernel
+// keeps a scalar fp32 dot product for the same reason):
+//   kd[d]  = decode(k[d]) * scale                       (one rounding)
+//   dot_h  = fmaf chain over d ascending from 0 of decode(q[h][d]) * kd[d]
+//   score  = fmaf chain over h ascending from 0 of (dot_h > 0 ? dot_h : 0) * w_h
+// Selection: larger score first, equal scores to the lower position; the
+// selected tokens come back in ascending position order as physical cache
+// indices page * PS + slot, the row padded with -1.  A sequence of at most
+// TopK tokens returns all of them without scoring (the device reads
+// seq_lens and takes that path itself, no host round trip).
+//
+// Two kernels: dsa_scores_kernel (one thread per token; the token's 128 key
+// values live in registers, the 64 query rows in LDS, read as broadcasts) and
+// dsa_select_kernel (one 1024-thread workgroup per sequence: a four-pass
+// 8-bit radix select of the TopK-th key, then an ordered compaction).
+//
+// Built with -ffp-contract=off: only the explicit fmaf calls fuse.
+#include "moe_device.h"
+
+namespace moe {
+namespace {
+
+constexpr int kNH = 64;    // query heads
+constexpr int kD = 128;    // head dimension
+constexpr int kScoreThreads = 256;
+constexpr int kSelThreads = 1024;
+constexpr int kSelWaves = kSelThreads / kWave;
+
+// Device-side inputs are clamped into range (a sequence length into
+// [0, max_pages * PS], a page id into [0, num_pages)), so bad values give
+// wrong indices, never an out-of-bounds access.
+__device__ __forceinline__ int seq_len_of(const DsaParams &p, int b) {
+  return min(max(p.seq_lens[b], 0), p.max_len);
+}
+__device__ __forceinline__ int page_of(const DsaParams &p, int page) {
+  return min(max(page, 0), p.num_pages - 1);
+}
+
+__global__ __launch_bounds__(kScoreThreads) void dsa_scores_kernel(DsaParams p, int force) {
+  __shared__ __attribute__((aligned(16))) float q_l[kNH * kD];
+  __shared__ float w_l[kNH];
+  const int b = blockIdx.y;
+  const int L = seq_len_of(p, b);
+  const int j0 = blockIdx.x * kScoreThreads;
+  if (j0 >= L || (!force && L <= p.topk)) return;  // whole workgroup
+  const int tid = threadIdx.x;
+
+  // the query's 64 x 128 codes, decoded exactly to fp32 (32 per thread)
+  {
+    const uint8_t *qb = p.q + (size_t)b * kNH * kD;
+    const u32x4 a = *reinterpret_cast<const u32x4 *>(qb + tid * 32);
+    const u32x4 c = *reinterpret_cast<const u32x4 *>(qb + tid * 32 + 16);
+    float *dst = &q_l[tid * 32];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int wa = (int)a[i], wc = (int)c[i];
+      dst[4 * i + 0] = __builtin_amdgcn_cvt_f32_fp8(wa, 0);
+      dst[4 * i + 1] = __builtin_amdgcn_cvt_f32_fp8(wa, 1);
+      dst[4 * i + 2] = __builtin_amdgcn_cvt_f32_fp8(wa, 2);
+      dst[4 * i + 3] = __builtin_amdgcn_cvt_f32_fp8(wa, 3);
+      dst[16 + 4 * i + 0] = __builtin_amdgcn_cvt_f32_fp8(wc, 0);
+      dst[16 + 4 * i + 1] = __builtin_amdgcn_cvt_f32_fp8(wc, 1);
+      dst[16 + 4 * i + 2] = __builtin_amdgcn_cvt_f32_fp8(wc, 2);
+      dst[16 + 4 * i + 3] = __builtin_amdgcn_cvt_f32_fp8(wc, 3);
+    }
+    if (tid < kNH) w_l[tid] = p.weights[(size_t)b * kNH + tid];
+  }
+
+  // this thread's token: its 128 dequantised key values in registers
+  const int j = min(j0 + tid, L - 1);  // past the end: a repeat, not stored
+  const int page = page_of(p, p.block_table[(size_t)b * p.max_pages + j / p.PS]);
+  const size_t tok = (size_t)page * p.PS + (j % p.PS);
+  const uint8_t *krow = p.k_cache + tok * kD;
+  const float scale = p.k_scale[tok];
+  float kd[kD];
+#pragma unroll
+  for (int c = 0; c < kD / 16; ++c) {
+    const u32x4 v = *reinterpret_cast<const u32x4 *>(krow + 16 * c);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int wv = (int)v[i];
+      kd[16 * c + 4 * i + 0] = __builtin_amdgcn_cvt_f32_fp8(wv, 0) * scale;
+      kd[16 * c + 4 * i + 1] = __builtin_amdgcn_cvt_f32_fp8(wv, 1) * scale;
+      kd[16 * c + 4 * i + 2] = __builtin_amdgcn_cvt_f32_fp8(wv, 2) * scale;
+      kd[16 * c + 4 * i + 3] = __builtin_amdgcn_cvt_f32_fp8(wv, 3) * scale;
+    }
+  }
+  __syncthreads();
+
+  float acc = 0.0f;
+  for (int h = 0; h < kNH; ++h) {
+    const float *qh = &q_l[h * kD];
+    float dot = 0.0f;
+#pragma unroll
+    for (int d = 0; d < kD; d += 4) {
+      const float4 q4 = *reinterpret_cast<const float4 *>(qh + d);
+      dot = __builtin_fmaf(q4.x, kd[d + 0], dot);
+      dot = __builtin_fmaf(q4.y, kd[d + 1], dot);
+      dot = __builtin_fmaf(q4.z, kd[d + 2], dot);
+      dot = __builtin_fmaf(q4.w, kd[d + 3], dot);
+    }
+    const float r = dot > 0.0f ? dot : 0.0f;
+    acc = __builtin_fmaf(r, w_l[h], acc);
+  }
+  if (j0 + tid < L) p.scores[(size_t)b * p.max_len + j0 + tid] = acc;
+}
+
+// fp32 -> an unsigned key with the same order (-0 taken as +0, so equal
+// scores get equal keys)
+__device__ __forceinline__ uint32_t score_key(float v) {
+  uint32_t u = __float_as_uint(v);
+  if (u == 0x80000000u) u = 0u;
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
+// Block-wide exclusive prefix count of `flag` over the workgroup's threads in
+// order; returns the prefix and writes the total to *total.  Uses one LDS
+// word per wave.
+__device__ __forceinline__ int block_excl_count(bool flag, int *wave_cnt, int *total) {
+  const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
+  const uint64_t m = __ballot(flag);
+  const int in_wave = __popcll(m & ((1ull << lane) - 1ull));
+  __syncthreads();  // previous users of wave_cnt are done
+  if (lane == 0) wave_cnt[wave] = __popcll(m);
+  __syncthreads();
+  int before = 0, all = 0;
+  for (int w = 0; w < kSelWaves; ++w) {
+    const int c = wave_cnt[w];
+    before += (w < wave) ? c : 0;
+    all += c;
+  }
+  *total = all;
+  return before + in_wave;
+}
+
+__global__ __launch_bounds__(kSelThreads) void dsa_select_kernel(DsaParams p) {
+  __shared__ int hist[kSelWaves][256];
+  __shared__ int wave_cnt[kSelWaves];
+  __shared__ uint32_t sh_prefix, sh_mask;
+  __shared__ int sh_left;
+  const int b = blockIdx.x;
+  const int L = seq_len_of(p, b);
+  const int tid = threadIdx.x;
+  const int lane = tid & (kWave - 1), wave = tid / kWave;
+  int32_t *out = p.out + (size_t)b * p.topk;
+  const int32_t *bt = p.block_table + (size_t)b * p.max_pages;
+
+  if (L <= p.topk) {  // every token, in position order, then -1
+    for (int i = tid; i < p.topk; i += kSelThreads)
+      out[i] = i < L ? page_of(p, bt[i / p.PS]) * p.PS + i % p.PS : -1;
+    return;
+  }
+  const float *sc = p.scores + (size_t)b * p.max_len;
+
+  // radix select of the topk-th largest key, 8 bits per pass from the top:
+  // `prefix` holds the bits fixed so far (under `mask`), `left` how many of
+  // the keys matching them are still to be taken
+  if (tid == 0) {
+    sh_prefix = 0u;
+    sh_mask = 0u;
+    sh_left = p.topk;
+  }
+  for (int pass = 0; pass < 4; ++pass) {
+    const int shift = 24 - 8 * pass;
+    for (int i = tid; i < kSelWaves * 256; i += kSelThreads) (&hist[0][0])[i] = 0;
+    __syncthreads();
+    const uint32_t prefix = sh_prefix, mask = sh_mask;
+    for (int j = tid; j < L; j += kSelThreads) {
+      const uint32_t k = score_key(sc[j]);
+      if ((k & mask) == prefix) atomicAdd(&hist[wave][(k >> shift) & 255u], 1);
+    }
+    __syncthreads();
+    // wave 0: bins summed over the waves, lane l holding bins 4l .. 4l+3;
+    // the suffix counts pick the bin that holds the left-th largest key
+    if (wave == 0) {
+      int c[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        int s = 0;
+        for (int w = 0; w < kSelWaves; ++w) s += hist[w][4 * lane + i];
+        c[i] = s;
+      }
+      const int mine = c[0] + c[1] + c[2] + c[3];
+      int suffix = mine;  // sum over lanes >= lane
+#pragma unroll
+      for (int off = 1; off < kWave; off <<= 1) {
+        const int o = __shfl_down(suffix, off);
+        suffix += (lane + off < kWave) ? o : 0;
+      }
+      const int above = suffix - mine;  // keys in bins of higher lanes
+      const int left = sh_left;
+      if (above < left && suffix >= left) {  // exactly one lane
+        int acc = above, bin = 4 * lane;
+        for (int i = 3; i >= 0; --i) {
+          if (acc + c[i] >= left) {
+            bin = 4 * lane + i;
+            break;
+          }
+          acc += c[i];
+        }
+        sh_prefix = prefix | ((uint32_t)bin << shift);
+        sh_mask = mask | (255u << shift);
+        sh_left = left - acc;
+      }
+    }
+    __syncthreads();
+  }
+  const uint32_t thr = sh_prefix;   // the topk-th largest key
+  const int need = sh_left;         // keys equal to it that are taken
+
+  // ordered compaction: position j is taken if its key beats the threshold,
+  // or equals it and fewer than `need` equal keys come before it
+  int eq_before = 0, sel_before = 0;
+  for (int base = 0; base < L; base += kSelThreads) {
+    const int j = base + tid;
+    const uint32_t k = j < L ? score_key(sc[j]) : 0u;
+    const bool eq = j < L && k == thr;
+    const bool gt = j < L && k > thr;
+    int eq_total, sel_total;
+    const int eq_rank = eq_before + block_excl_count(eq, wave_cnt, &eq_total);
+    const bool sel = gt || (eq && eq_rank < need);
+    const int pos = sel_before + block_excl_count(sel, wave_cnt, &sel_total);
+    if (sel) out[pos] = page_of(p, bt[j / p.PS]) * p.PS + j % p.PS;
+    eq_before += eq_total;
+    sel_before += sel_total;
+  }
+}
+
+}  // namespace
+
+hipError_t launch_dsa_scores(const DsaParams &p, int max_len, bool force, hipStream_t st) {
+  if (p.B == 0 || max_len == 0) return hipSuccess;
+  dim3 grid((max_len + kScoreThreads - 1) / kScoreThreads, p.B);
+  hipLaunchKernelGGL(dsa_scores_kernel, grid, dim3(kScoreThreads), 0, st, p, force ? 1 : 0);
+  return hipGetLastError();
+}
+
+hipError_t launch_dsa_select(const DsaParams &p, hipStream_t st) {
+  if (p.B == 0) return hipSuccess;
+  hipLaunchKernelGGL(dsa_select_kernel, dim3(p.B), dim3(kSelThreads), 0, st, p);
+  return hipGetLastError();
+}
+
+}  // namespace moe

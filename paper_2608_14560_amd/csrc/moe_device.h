@@ -199,10 +199,25 @@ struct FinalizeParams {
   int T, H, K, S, P_max;
 };
 
+// DSA TopK indexer: 64 heads of 128, a paged key cache of PS tokens per page
+struct DsaParams {
+  const uint8_t *q;            // [B, 64, 128] e4m3
+  const float *weights;        // [B, 64]
+  const uint8_t *k_cache;      // [num_pages, PS, 128] e4m3
+  const float *k_scale;        // [num_pages, PS]
+  const int32_t *block_table;  // [B, max_pages]
+  const int32_t *seq_lens;     // [B]
+  float *scores;               // [B, max_len] workspace
+  int32_t *out;                // [B, topk]
+  int B, PS, topk, max_pages, max_len, num_pages;
+};
+
 // ---------------------------------------------------------------- launchers
 // (defined in the .hip files, called by the C-ABI layer)
 hipError_t launch_route(const RouteParams &p, hipStream_t st);
 hipError_t launch_router_partials(const RouterParams &p, hipStream_t st);
+hipError_t launch_dsa_scores(const DsaParams &p, int max_len, bool force, hipStream_t st);
+hipError_t launch_dsa_select(const DsaParams &p, hipStream_t st);
 hipError_t launch_router_logits(const RouteParams &p, float *logits, hipStream_t st);
 hipError_t launch_permute(const PermuteParams &p, hipStream_t st);
 hipError_t launch_gemm1(const GemmParams &p, int BM, int grid, hipStream_t st);

@@ -14,10 +14,12 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 
 def _declared_functions():
     names = []
-    for h in ("moe.h", "moe_debug.h"):
+    for h in sorted(os.listdir(os.path.join(ROOT, "include"))):
+        if not h.endswith(".h"):
+            continue
         src = open(os.path.join(ROOT, "include", h)).read()
         src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
-        names += re.findall(r"\b(moe_[a-z0-9_]+)\s*\(", src)
+        names += re.findall(r"\b((?:moe|dsa)_[a-z0-9_]+)\s*\(", src)
     return sorted(set(names))
 
 
@@ -161,6 +163,33 @@ def test_router_entry_points_reject_bad_arguments(M):
     s0 = _shape(T=0)
     ro0 = M.CRouteOut(None, None, _fake_ptrs(1)[0].value, _fake_ptrs(1)[0].value, None)
     assert L.moe_fused_fp8_router(ctypes.byref(s0.c()), *ptrs, None, None, 0, None) == M.MOE_OK
+
+
+def test_dsa_indexer_rejects_bad_arguments(M):
+    L = M.lib()
+    good = M.CDsaShape(4, 64, 128, 64, 2048, 36, 300)
+    assert M.dsa_workspace_size(good) >= 4 * 36 * 64 * 4
+    for bad, code in [(M.CDsaShape(4, 32, 128, 64, 2048, 36, 300), M.MOE_ERR_UNSUPPORTED),
+                      (M.CDsaShape(4, 64, 64, 64, 2048, 36, 300), M.MOE_ERR_UNSUPPORTED),
+                      (M.CDsaShape(-1, 64, 128, 64, 2048, 36, 300), M.MOE_ERR_INVALID_ARG),
+                      (M.CDsaShape(4, 64, 128, 0, 2048, 36, 300), M.MOE_ERR_INVALID_ARG),
+                      (M.CDsaShape(4, 64, 128, 64, 0, 36, 300), M.MOE_ERR_INVALID_ARG),
+                      (M.CDsaShape(4, 64, 128, 64, 2048, 36, 0), M.MOE_ERR_INVALID_ARG)]:
+        assert M.dsa_workspace_size(bad) == 0
+        assert L.dsa_topk_indexer(ctypes.byref(bad), *_fake_ptrs(7), ctypes.c_void_p(0x7000000), 1 << 30,
+                                  None) == code
+    ptrs = _fake_ptrs(7)
+    ws = ctypes.c_void_p(0x7000000)
+    nbytes = M.dsa_workspace_size(good)
+    for i in range(7):
+        bad = list(ptrs)
+        bad[i] = None
+        assert L.dsa_topk_indexer(ctypes.byref(good), *bad, ws, nbytes, None) == M.MOE_ERR_INVALID_ARG
+        bad[i] = ctypes.c_void_p(ptrs[i].value + 4)
+        assert L.dsa_topk_indexer(ctypes.byref(good), *bad, ws, nbytes, None) == M.MOE_ERR_INVALID_ARG
+    assert L.dsa_topk_indexer(ctypes.byref(good), *ptrs, ws, nbytes - 1, None) == M.MOE_ERR_WORKSPACE_TOO_SMALL
+    empty = M.CDsaShape(0, 64, 128, 64, 2048, 36, 300)
+    assert L.dsa_topk_indexer(ctypes.byref(empty), *([None] * 7), None, 0, None) == M.MOE_OK
 
 
 def test_workspace_grows_with_batch(M):
