@@ -11,6 +11,10 @@ synchronisations; each kernel is bracketed by HIP events recorded on the
 library's stream (moe_fused_fp8_staged), which gives the per-kernel durations
 behind the roofline figure.  Prints one JSON line.
 
+The line also carries `dsa_topk_indexer`: the paper's third operator (DSA
+TopK indexer) on seeded inputs of its long-regime representative and of a
+long-sequence batch, µs per call and the score kernel's roofline.
+
 The line also carries `router_projection`: the same batches routed from the
 hidden rows with the router projection on the device (moe_route_hidden)
 against routing from given logits (moe_route), both timed back to back.
@@ -23,6 +27,7 @@ kernel for scaling the HBM byte counters of rocprofv3.
 from __future__ import annotations
 
 import argparse
+import ctypes
 import hashlib
 import json
 import os
@@ -225,6 +230,67 @@ def router_projection_leg(cfg, shape, batches, weights, out, ws, stream, K, pref
             "roofline": roof}
 
 
+def indexer_leg(K, prefill, with_cpu: bool):
+    """µs per call of the DSA TopK indexer on two workloads, each K calls back to
+    back; the score kernel alone (every sequence scored, dsa_debug_scores) gives
+    the roofline: 2*64*128 FLOP per scored token (plain fp32 fused multiply-adds,
+    the fixed sequence) and its key row (128 B + a 4-byte scale) read once."""
+    res = {}
+    for name in ("dsa_paper_long", "dsa_long"):
+        cfg = W.INDEXER_CONFIGS[name]
+        x = W.generate_indexer(cfg, 0, device="cuda")
+        args = (x.q, x.weights, x.k_cache, x.k_scale, x.block_table, x.seq_lens)
+        shape = M.dsa_shape(x.q, x.k_cache, x.block_table, cfg.topk)
+        ws = torch.empty(max(M.dsa_workspace_size(shape), 256), dtype=torch.uint8, device="cuda")
+        out = torch.empty(cfg.B, cfg.topk, dtype=torch.int32, device="cuda")
+        scores = torch.empty(cfg.B, cfg.max_pages * cfg.page_size, dtype=torch.float32, device="cuda")
+
+        def timed(fn):
+            for _ in range(3):
+                fn()
+            torch.cuda.synchronize()
+            h0 = time.perf_counter()
+            for _ in range(K):
+                fn()
+            host_ms = (time.perf_counter() - h0) * 1e3
+            torch.cuda.synchronize()
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            prefill(host_ms)
+            a.record()
+            for _ in range(K):
+                fn()
+            b.record()
+            torch.cuda.synchronize()
+            return a.elapsed_time(b) * 1e3 / K
+
+        call_us = timed(lambda: M.dsa_topk_indexer(*args, topk=cfg.topk, out=out, workspace=ws))
+        sc_shape = M.dsa_shape(x.q, x.k_cache, x.block_table, 1)
+        ptrs = M._dsa_ptrs(*args)
+        sc_ptr = scores.data_ptr()
+        L = M.lib()
+        scores_us = timed(lambda: L.dsa_debug_scores(ctypes.byref(sc_shape), *ptrs, sc_ptr, None))
+        tokens = sum(cfg.seq_lens)
+        flop = 2.0 * cfg.num_heads * cfg.head_dim * tokens
+        nbytes = tokens * (cfg.head_dim + 4) + x.q.numel() + 4 * x.weights.numel() + 4 * tokens
+        ach = flop / (scores_us * 1e-6) / 1e12
+        rec = {"workload": f"{name}: B={cfg.B}, seq_lens={list(cfg.seq_lens)}, 64 heads x 128, "
+                           f"page {cfg.page_size}, topk {cfg.topk}",
+               "us_per_call": round(call_us, 2), "score_kernel_all_tokens_us": round(scores_us, 2),
+               "roofline_score_kernel": {"bound": "alu", "achieved": round(ach, 2),
+                                         "peak": FP32_FMA_PEAK_TFLOPS, "unit": "TFLOP/s",
+                                         "frac": round(ach / FP32_FMA_PEAK_TFLOPS, 4),
+                                         "flop": int(flop), "algorithmic_bytes": int(nbytes)}}
+        if with_cpu:
+            import oracle as O  # the CPU baseline: the oracle timed beside the GPU figure
+            h = [t.cpu().numpy() for t in args]
+            t0 = time.perf_counter()
+            O.dsa_topk(*h, cfg.topk)
+            rec["cpu_oracle_us"] = round((time.perf_counter() - t0) * 1e6, 1)
+            rec["cpu_oracle_threads"] = int(O.lib().oracle_num_threads())
+        res[name] = rec
+    return res
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -381,6 +447,7 @@ def main():
         cold = round(float(np.median(times)) * 1e3, 2)
 
     router = router_projection_leg(cfg, shape, batches, weights, out, ws, stream, K, prefill)
+    indexer = indexer_leg(K, prefill, not args.no_cpu_baseline)
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -413,6 +480,7 @@ def main():
         "roofline": roof,
         "cpu_baseline": cpu,
         "router_projection": router,
+        "dsa_topk_indexer": indexer,
         "us_per_call_cold": cold,
         "host_enqueue_us_per_call": round(host_ms * 1e3 / K, 1),
         "prefill_covered_enqueue": bool(enq_ms < 2.0 * host_ms + 2.0),

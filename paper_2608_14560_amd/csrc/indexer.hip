@@ -16,8 +16,9 @@
 // TopK tokens returns all of them without scoring (the device reads
 // seq_lens and takes that path itself, no host round trip).
 //
-// Two kernels: dsa_scores_kernel (one thread per token; the token's 128 key
-// values live in registers, the 64 query rows in LDS, read as broadcasts) and
+// Two kernels: dsa_scores_kernel (four threads per token, 16 heads each; the
+// token's 128 key values live in registers, the 64 query rows in LDS, read as
+// broadcasts) and
 // dsa_select_kernel (one 1024-thread workgroup per sequence: a four-pass
 // 8-bit radix select of the TopK-th key, then an ordered compaction).
 //
@@ -43,14 +44,25 @@ __device__ __forceinline__ int page_of(const DsaParams &p, int page) {
   return min(max(page, 0), p.num_pages - 1);
 }
 
+// Four threads per token, each the dot products of 16 heads (16 independent
+// chains, interleaved four at a time); the ReLU'd dots go through LDS and the
+// token's first thread runs the head chain in order.  64 tokens per
+// workgroup, so a sequence of a few thousand tokens still spreads over tens
+// of CUs.
+constexpr int kTokPerWG = kScoreThreads / 4;
+constexpr int kHeadsPerThread = kNH / 4;
+
 __global__ __launch_bounds__(kScoreThreads) void dsa_scores_kernel(DsaParams p, int force) {
   __shared__ __attribute__((aligned(16))) float q_l[kNH * kD];
   __shared__ float w_l[kNH];
+  __shared__ float r_l[kTokPerWG][kNH + 1];
   const int b = blockIdx.y;
   const int L = seq_len_of(p, b);
-  const int j0 = blockIdx.x * kScoreThreads;
+  const int j0 = blockIdx.x * kTokPerWG;
   if (j0 >= L || (!force && L <= p.topk)) return;  // whole workgroup
   const int tid = threadIdx.x;
+  const int tl = tid & (kTokPerWG - 1);  // token of the workgroup
+  const int qq = tid / kTokPerWG;        // head quarter
 
   // the query's 64 x 128 codes, decoded exactly to fp32 (32 per thread)
   {
@@ -74,7 +86,7 @@ __global__ __launch_bounds__(kScoreThreads) void dsa_scores_kernel(DsaParams p, 
   }
 
   // this thread's token: its 128 dequantised key values in registers
-  const int j = min(j0 + tid, L - 1);  // past the end: a repeat, not stored
+  const int j = min(j0 + tl, L - 1);  // past the end: a repeat, not stored
   const int page = page_of(p, p.block_table[(size_t)b * p.max_pages + j / p.PS]);
   const size_t tok = (size_t)page * p.PS + (j % p.PS);
   const uint8_t *krow = p.k_cache + tok * kD;
@@ -94,22 +106,34 @@ __global__ __launch_bounds__(kScoreThreads) void dsa_scores_kernel(DsaParams p, 
   }
   __syncthreads();
 
-  float acc = 0.0f;
-  for (int h = 0; h < kNH; ++h) {
-    const float *qh = &q_l[h * kD];
-    float dot = 0.0f;
+  // each head's dot: its own fused multiply-add chain over d ascending
+  constexpr int kHG = 4;
+  for (int h0 = qq * kHeadsPerThread; h0 < (qq + 1) * kHeadsPerThread; h0 += kHG) {
+    float dot[kHG];
+#pragma unroll
+    for (int g = 0; g < kHG; ++g) dot[g] = 0.0f;
 #pragma unroll
     for (int d = 0; d < kD; d += 4) {
-      const float4 q4 = *reinterpret_cast<const float4 *>(qh + d);
-      dot = __builtin_fmaf(q4.x, kd[d + 0], dot);
-      dot = __builtin_fmaf(q4.y, kd[d + 1], dot);
-      dot = __builtin_fmaf(q4.z, kd[d + 2], dot);
-      dot = __builtin_fmaf(q4.w, kd[d + 3], dot);
+#pragma unroll
+      for (int g = 0; g < kHG; ++g) {
+        const float4 q4 = *reinterpret_cast<const float4 *>(&q_l[(h0 + g) * kD + d]);
+        dot[g] = __builtin_fmaf(q4.x, kd[d + 0], dot[g]);
+        dot[g] = __builtin_fmaf(q4.y, kd[d + 1], dot[g]);
+        dot[g] = __builtin_fmaf(q4.z, kd[d + 2], dot[g]);
+        dot[g] = __builtin_fmaf(q4.w, kd[d + 3], dot[g]);
+      }
     }
-    const float r = dot > 0.0f ? dot : 0.0f;
-    acc = __builtin_fmaf(r, w_l[h], acc);
+#pragma unroll
+    for (int g = 0; g < kHG; ++g) r_l[tl][h0 + g] = dot[g] > 0.0f ? dot[g] : 0.0f;
   }
-  if (j0 + tid < L) p.scores[(size_t)b * p.max_len + j0 + tid] = acc;
+  __syncthreads();
+  // the head chain, in order
+  if (qq == 0 && j0 + tl < L) {
+    float acc = 0.0f;
+#pragma unroll 8
+    for (int h = 0; h < kNH; ++h) acc = __builtin_fmaf(r_l[tl][h], w_l[h], acc);
+    p.scores[(size_t)b * p.max_len + j0 + tl] = acc;
+  }
 }
 
 // fp32 -> an unsigned key with the same order (-0 taken as +0, so equal
@@ -120,24 +144,28 @@ __device__ __forceinline__ uint32_t score_key(float v) {
   return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
 }
 
-// Block-wide exclusive prefix count of `flag` over the workgroup's threads in
+// Block-wide exclusive prefix sum of `v` over the workgroup's threads in
 // order; returns the prefix and writes the total to *total.  Uses one LDS
 // word per wave.
-__device__ __forceinline__ int block_excl_count(bool flag, int *wave_cnt, int *total) {
+__device__ __forceinline__ int block_excl_sum(int v, int *wave_sum, int *total) {
   const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
-  const uint64_t m = __ballot(flag);
-  const int in_wave = __popcll(m & ((1ull << lane) - 1ull));
-  __syncthreads();  // previous users of wave_cnt are done
-  if (lane == 0) wave_cnt[wave] = __popcll(m);
+  int incl = v;  // inclusive scan inside the wave
+#pragma unroll
+  for (int off = 1; off < kWave; off <<= 1) {
+    const int o = __shfl_up(incl, off);
+    incl += (lane >= off) ? o : 0;
+  }
+  __syncthreads();  // previous users of wave_sum are done
+  if (lane == kWave - 1) wave_sum[wave] = incl;
   __syncthreads();
   int before = 0, all = 0;
   for (int w = 0; w < kSelWaves; ++w) {
-    const int c = wave_cnt[w];
+    const int c = wave_sum[w];
     before += (w < wave) ? c : 0;
     all += c;
   }
   *total = all;
-  return before + in_wave;
+  return before + incl - v;
 }
 
 __global__ __launch_bounds__(kSelThreads) void dsa_select_kernel(DsaParams p) {
@@ -172,9 +200,17 @@ __global__ __launch_bounds__(kSelThreads) void dsa_select_kernel(DsaParams p) {
     for (int i = tid; i < kSelWaves * 256; i += kSelThreads) (&hist[0][0])[i] = 0;
     __syncthreads();
     const uint32_t prefix = sh_prefix, mask = sh_mask;
-    for (int j = tid; j < L; j += kSelThreads) {
-      const uint32_t k = score_key(sc[j]);
-      if ((k & mask) == prefix) atomicAdd(&hist[wave][(k >> shift) & 255u], 1);
+    for (int j4 = tid; j4 < L; j4 += 4 * kSelThreads) {
+      uint32_t k[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int j = j4 + i * kSelThreads;
+        k[i] = j < L ? score_key(sc[j]) : 0u;
+      }
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        if (j4 + i * kSelThreads < L && (k[i] & mask) == prefix)
+          atomicAdd(&hist[wave][(k[i] >> shift) & 255u], 1);
     }
     __syncthreads();
     // wave 0: bins summed over the waves, lane l holding bins 4l .. 4l+3;
@@ -216,18 +252,40 @@ __global__ __launch_bounds__(kSelThreads) void dsa_select_kernel(DsaParams p) {
   const int need = sh_left;         // keys equal to it that are taken
 
   // ordered compaction: position j is taken if its key beats the threshold,
-  // or equals it and fewer than `need` equal keys come before it
+  // or equals it and fewer than `need` equal keys come before it.  Each
+  // thread owns kPer consecutive positions of a chunk; two block scans per
+  // chunk give the equal-key ranks and the output slots.
+  constexpr int kPer = 16;
   int eq_before = 0, sel_before = 0;
-  for (int base = 0; base < L; base += kSelThreads) {
-    const int j = base + tid;
-    const uint32_t k = j < L ? score_key(sc[j]) : 0u;
-    const bool eq = j < L && k == thr;
-    const bool gt = j < L && k > thr;
+  for (int base = 0; base < L; base += kSelThreads * kPer) {
+    const int j0 = base + tid * kPer;
+    uint32_t k[kPer];
+    int neq = 0;
+#pragma unroll
+    for (int i = 0; i < kPer; ++i) {
+      const int j = j0 + i;
+      k[i] = j < L ? score_key(sc[j]) : 0u;
+      neq += (j < L && k[i] == thr) ? 1 : 0;
+    }
     int eq_total, sel_total;
-    const int eq_rank = eq_before + block_excl_count(eq, wave_cnt, &eq_total);
-    const bool sel = gt || (eq && eq_rank < need);
-    const int pos = sel_before + block_excl_count(sel, wave_cnt, &sel_total);
-    if (sel) out[pos] = page_of(p, bt[j / p.PS]) * p.PS + j % p.PS;
+    int eq_rank = eq_before + block_excl_sum(neq, wave_cnt, &eq_total);
+    uint32_t selm = 0u;
+#pragma unroll
+    for (int i = 0; i < kPer; ++i) {
+      const bool in = j0 + i < L;
+      const bool eq = in && k[i] == thr;
+      const bool sel = (in && k[i] > thr) || (eq && eq_rank < need);
+      eq_rank += eq ? 1 : 0;
+      selm |= sel ? (1u << i) : 0u;
+    }
+    int pos = sel_before + block_excl_sum(__popc(selm), wave_cnt, &sel_total);
+#pragma unroll
+    for (int i = 0; i < kPer; ++i) {
+      if (selm & (1u << i)) {
+        const int j = j0 + i;
+        out[pos++] = page_of(p, bt[j / p.PS]) * p.PS + j % p.PS;
+      }
+    }
     eq_before += eq_total;
     sel_before += sel_total;
   }
@@ -237,7 +295,7 @@ __global__ __launch_bounds__(kSelThreads) void dsa_select_kernel(DsaParams p) {
 
 hipError_t launch_dsa_scores(const DsaParams &p, int max_len, bool force, hipStream_t st) {
   if (p.B == 0 || max_len == 0) return hipSuccess;
-  dim3 grid((max_len + kScoreThreads - 1) / kScoreThreads, p.B);
+  dim3 grid((max_len + kTokPerWG - 1) / kTokPerWG, p.B);
   hipLaunchKernelGGL(dsa_scores_kernel, grid, dim3(kScoreThreads), 0, st, p, force ? 1 : 0);
   return hipGetLastError();
 }
