@@ -492,10 +492,14 @@ moe_status_t dsa_check_ptrs(const void *const *ptrs, int n) {
   return MOE_OK;
 }
 
+size_t dsa_scores_bytes(const dsa_shape_t *s) {
+  return align_up(sizeof(float) * (size_t)(s->B > 0 ? s->B : 1) * s->max_pages * s->page_size);
+}
+
 DsaParams dsa_params(const dsa_shape_t *s, const uint8_t *q, const float *weights,
                      const uint8_t *k_cache, const float *k_scale, const int32_t *block_table,
-                     const int32_t *seq_lens, float *scores, int32_t *out) {
-  DsaParams p{q, weights, k_cache, k_scale, block_table, seq_lens, scores, out, s->B,
+                     const int32_t *seq_lens, float *scores, int *hist, int32_t *out) {
+  DsaParams p{q, weights, k_cache, k_scale, block_table, seq_lens, scores, hist, out, s->B,
               s->page_size, s->topk, s->max_pages, s->max_pages * s->page_size, s->num_pages};
   return p;
 }
@@ -504,7 +508,12 @@ DsaParams dsa_params(const dsa_shape_t *s, const uint8_t *q, const float *weight
 
 size_t dsa_workspace_size(const dsa_shape_t *s) {
   if (dsa_check(s) != MOE_OK) return 0;
-  return align_up(sizeof(float) * (size_t)(s->B > 0 ? s->B : 1) * s->max_pages * s->page_size);
+  // the scores, then (batches that may hold long sequences) the radix
+  // histograms [4, B, 256]
+  const size_t hist = dsa_wide_select(s->max_pages * s->page_size)
+                          ? align_up(sizeof(int) * 4 * 256 * (size_t)(s->B > 0 ? s->B : 1))
+                          : 0;
+  return dsa_scores_bytes(s) + hist;
 }
 
 moe_status_t dsa_topk_indexer(const dsa_shape_t *s, const uint8_t *q, const float *weights,
@@ -518,8 +527,11 @@ moe_status_t dsa_topk_indexer(const dsa_shape_t *s, const uint8_t *q, const floa
   if ((rc = dsa_check_ptrs(ptrs, 8)) != MOE_OK) return rc;
   if (ws_bytes < dsa_workspace_size(s)) return MOE_ERR_WORKSPACE_TOO_SMALL;
   hipStream_t st = static_cast<hipStream_t>(stream);
+  int *hist = dsa_wide_select(s->max_pages * s->page_size)
+                  ? at<int>(workspace, dsa_scores_bytes(s))
+                  : nullptr;
   const DsaParams p = dsa_params(s, q, weights, k_cache, k_scale, block_table, seq_lens,
-                                 static_cast<float *>(workspace), out);
+                                 static_cast<float *>(workspace), hist, out);
   MOE_TRY_HIP(launch_dsa_scores(p, p.max_len, false, st));
   MOE_TRY_HIP(launch_dsa_select(p, st));
   return MOE_OK;
@@ -535,7 +547,7 @@ moe_status_t dsa_debug_scores(const dsa_shape_t *s, const uint8_t *q, const floa
   const void *ptrs[] = {q, weights, k_cache, k_scale, block_table, seq_lens, scores};
   if ((rc = dsa_check_ptrs(ptrs, 7)) != MOE_OK) return rc;
   const DsaParams p = dsa_params(s, q, weights, k_cache, k_scale, block_table, seq_lens, scores,
-                                 nullptr);
+                                 nullptr, nullptr);
   return launch_dsa_scores(p, p.max_len, true, static_cast<hipStream_t>(stream)) == hipSuccess
              ? MOE_OK
              : MOE_ERR_HIP;

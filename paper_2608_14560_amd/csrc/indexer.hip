@@ -20,7 +20,10 @@
 // token's 128 key values live in registers, the 64 query rows in LDS, read as
 // broadcasts) and
 // dsa_select_kernel (one 1024-thread workgroup per sequence: a four-pass
-// 8-bit radix select of the TopK-th key, then an ordered compaction).
+// 8-bit radix select of the TopK-th key, then an ordered compaction).  For
+// batches that may hold long sequences, the four histogram passes are spread
+// over many workgroups per sequence (dsa_hist_kernel, global histograms
+// cleared by the score kernel) and the select kernel only replays them.
 //
 // Built with -ffp-contract=off: only the explicit fmaf calls fuse.
 #include "moe_device.h"
@@ -59,6 +62,10 @@ __global__ __launch_bounds__(kScoreThreads) void dsa_scores_kernel(DsaParams p, 
   const int b = blockIdx.y;
   const int L = seq_len_of(p, b);
   const int j0 = blockIdx.x * kTokPerWG;
+  if (blockIdx.x == 0 && p.hist) {  // the radix histograms of this sequence start at zero
+    for (int i = threadIdx.x; i < 4 * 256; i += kScoreThreads)
+      p.hist[((size_t)(i / 256) * p.B + b) * 256 + (i % 256)] = 0;
+  }
   if (j0 >= L || (!force && L <= p.topk)) return;  // whole workgroup
   const int tid = threadIdx.x;
   const int tl = tid & (kTokPerWG - 1);  // token of the workgroup
@@ -168,15 +175,118 @@ __device__ __forceinline__ int block_excl_sum(int v, int *wave_sum, int *total) 
   return before + incl - v;
 }
 
+// One radix-select step, run by one wave: given the 256 bin counts of the
+// keys matching `prefix` under `mask` (summed over `nsub` sub-histograms
+// `stride` ints apart) and the `left`-th largest of them sought, fix the
+// next 8 bits (at `shift`) and the count still sought inside that bin.  Lane
+// l holds bins 4l .. 4l+3; suffix sums over the lanes pick the bin.
+struct SelState {
+  uint32_t prefix, mask;
+  int left;
+};
+
+__device__ __forceinline__ void resolve_bin(const int *bins, int nsub, int stride, int shift,
+                                            SelState *st) {
+  const int lane = threadIdx.x & (kWave - 1);
+  int c[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    int s = 0;
+    for (int w = 0; w < nsub; ++w) s += bins[w * stride + 4 * lane + i];
+    c[i] = s;
+  }
+  const int mine = c[0] + c[1] + c[2] + c[3];
+  int suffix = mine;  // sum over lanes >= lane
+#pragma unroll
+  for (int off = 1; off < kWave; off <<= 1) {
+    const int o = __shfl_down(suffix, off);
+    suffix += (lane + off < kWave) ? o : 0;
+  }
+  const int above = suffix - mine;  // keys in bins of higher lanes
+  const int left = st->left;
+  const uint32_t prefix = st->prefix, mask = st->mask;
+  __builtin_amdgcn_wave_barrier();
+  if (above < left && suffix >= left) {  // exactly one lane
+    int acc = above, bin = 4 * lane;
+    for (int i = 3; i >= 0; --i) {
+      if (acc + c[i] >= left) {
+        bin = 4 * lane + i;
+        break;
+      }
+      acc += c[i];
+    }
+    st->prefix = prefix | ((uint32_t)bin << shift);
+    st->mask = mask | (255u << shift);
+    st->left = left - acc;
+  }
+}
+
+// Keys of positions [j_begin, j_end) matching the state, counted into the
+// per-wave LDS histograms by byte `shift`.
+__device__ __forceinline__ void count_keys(const float *sc, int j_begin, int j_end, int nthreads,
+                                           const SelState &st, int shift, int *my_hist) {
+  for (int j4 = j_begin + (int)threadIdx.x; j4 < j_end; j4 += 4 * nthreads) {
+    uint32_t k[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int j = j4 + i * nthreads;
+      k[i] = j < j_end ? score_key(sc[j]) : 0u;
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      if (j4 + i * nthreads < j_end && (k[i] & st.mask) == st.prefix)
+        atomicAdd(&my_hist[(k[i] >> shift) & 255u], 1);
+  }
+}
+
+// Long sequences, pass `pass` of the radix select spread over the grid's x
+// dimension: each workgroup first replays the earlier passes from their
+// global histograms (every workgroup reaches the same state), then counts
+// its slice of positions and adds its bins to the pass's global histogram.
+// Sequences of at most topk tokens return at once.
+constexpr int kHistThreads = 256;
+
+__global__ __launch_bounds__(kHistThreads) void dsa_hist_kernel(DsaParams p, int pass) {
+  __shared__ int hist[kHistThreads / kWave][256];
+  __shared__ SelState st;
+  const int b = blockIdx.y;
+  const int L = seq_len_of(p, b);
+  if (L <= p.topk) return;
+  const int tid = threadIdx.x, wave = tid / kWave;
+  const int per = (L + gridDim.x - 1) / gridDim.x;
+  const int j_begin = blockIdx.x * per;
+  const int j_end = min(L, j_begin + per);
+  if (j_begin >= j_end) return;
+  if (tid == 0) st = SelState{0u, 0u, p.topk};
+  for (int i = tid; i < (kHistThreads / kWave) * 256; i += kHistThreads) (&hist[0][0])[i] = 0;
+  __syncthreads();
+  for (int q = 0; q < pass; ++q) {
+    if (wave == 0) resolve_bin(p.hist + ((size_t)q * p.B + b) * 256, 1, 0, 24 - 8 * q, &st);
+    __syncthreads();
+  }
+  const SelState s0 = st;
+  count_keys(p.scores + (size_t)b * p.max_len, j_begin, j_end, kHistThreads, s0, 24 - 8 * pass,
+             hist[wave]);
+  __syncthreads();
+  int *g = p.hist + ((size_t)pass * p.B + b) * 256;
+  for (int i = tid; i < 256; i += kHistThreads) {
+    int c = 0;
+    for (int w = 0; w < kHistThreads / kWave; ++w) c += hist[w][i];
+    if (c) atomicAdd(&g[i], c);
+  }
+}
+
+// GLOBAL: the four histograms come from dsa_hist_kernel; otherwise this
+// workgroup counts every position itself.
+template <bool GLOBAL>
 __global__ __launch_bounds__(kSelThreads) void dsa_select_kernel(DsaParams p) {
   __shared__ int hist[kSelWaves][256];
   __shared__ int wave_cnt[kSelWaves];
-  __shared__ uint32_t sh_prefix, sh_mask;
-  __shared__ int sh_left;
+  __shared__ SelState st;
   const int b = blockIdx.x;
   const int L = seq_len_of(p, b);
   const int tid = threadIdx.x;
-  const int lane = tid & (kWave - 1), wave = tid / kWave;
+  const int wave = tid / kWave;
   int32_t *out = p.out + (size_t)b * p.topk;
   const int32_t *bt = p.block_table + (size_t)b * p.max_pages;
 
@@ -190,66 +300,24 @@ __global__ __launch_bounds__(kSelThreads) void dsa_select_kernel(DsaParams p) {
   // radix select of the topk-th largest key, 8 bits per pass from the top:
   // `prefix` holds the bits fixed so far (under `mask`), `left` how many of
   // the keys matching them are still to be taken
-  if (tid == 0) {
-    sh_prefix = 0u;
-    sh_mask = 0u;
-    sh_left = p.topk;
-  }
+  if (tid == 0) st = SelState{0u, 0u, p.topk};
+  __syncthreads();
   for (int pass = 0; pass < 4; ++pass) {
     const int shift = 24 - 8 * pass;
-    for (int i = tid; i < kSelWaves * 256; i += kSelThreads) (&hist[0][0])[i] = 0;
-    __syncthreads();
-    const uint32_t prefix = sh_prefix, mask = sh_mask;
-    for (int j4 = tid; j4 < L; j4 += 4 * kSelThreads) {
-      uint32_t k[4];
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int j = j4 + i * kSelThreads;
-        k[i] = j < L ? score_key(sc[j]) : 0u;
-      }
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-        if (j4 + i * kSelThreads < L && (k[i] & mask) == prefix)
-          atomicAdd(&hist[wave][(k[i] >> shift) & 255u], 1);
-    }
-    __syncthreads();
-    // wave 0: bins summed over the waves, lane l holding bins 4l .. 4l+3;
-    // the suffix counts pick the bin that holds the left-th largest key
-    if (wave == 0) {
-      int c[4];
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        int s = 0;
-        for (int w = 0; w < kSelWaves; ++w) s += hist[w][4 * lane + i];
-        c[i] = s;
-      }
-      const int mine = c[0] + c[1] + c[2] + c[3];
-      int suffix = mine;  // sum over lanes >= lane
-#pragma unroll
-      for (int off = 1; off < kWave; off <<= 1) {
-        const int o = __shfl_down(suffix, off);
-        suffix += (lane + off < kWave) ? o : 0;
-      }
-      const int above = suffix - mine;  // keys in bins of higher lanes
-      const int left = sh_left;
-      if (above < left && suffix >= left) {  // exactly one lane
-        int acc = above, bin = 4 * lane;
-        for (int i = 3; i >= 0; --i) {
-          if (acc + c[i] >= left) {
-            bin = 4 * lane + i;
-            break;
-          }
-          acc += c[i];
-        }
-        sh_prefix = prefix | ((uint32_t)bin << shift);
-        sh_mask = mask | (255u << shift);
-        sh_left = left - acc;
-      }
+    if (GLOBAL) {
+      if (wave == 0) resolve_bin(p.hist + ((size_t)pass * p.B + b) * 256, 1, 0, shift, &st);
+    } else {
+      for (int i = tid; i < kSelWaves * 256; i += kSelThreads) (&hist[0][0])[i] = 0;
+      __syncthreads();
+      const SelState s0 = st;
+      count_keys(sc, 0, L, kSelThreads, s0, shift, hist[wave]);
+      __syncthreads();
+      if (wave == 0) resolve_bin(&hist[0][0], kSelWaves, 256, shift, &st);
     }
     __syncthreads();
   }
-  const uint32_t thr = sh_prefix;   // the topk-th largest key
-  const int need = sh_left;         // keys equal to it that are taken
+  const uint32_t thr = st.prefix;   // the topk-th largest key
+  const int need = st.left;         // keys equal to it that are taken
 
   // ordered compaction: position j is taken if its key beats the threshold,
   // or equals it and fewer than `need` equal keys come before it.  Each
@@ -300,10 +368,24 @@ hipError_t launch_dsa_scores(const DsaParams &p, int max_len, bool force, hipStr
   return hipGetLastError();
 }
 
+// Batches whose longest possible sequence reaches this many tokens count
+// the radix histograms with many workgroups per sequence.
+constexpr int kWideSelectLen = 16384;
+constexpr int kWideTokensPerWG = 2048;
+
 hipError_t launch_dsa_select(const DsaParams &p, hipStream_t st) {
   if (p.B == 0) return hipSuccess;
-  hipLaunchKernelGGL(dsa_select_kernel, dim3(p.B), dim3(kSelThreads), 0, st, p);
+  if (p.max_len >= kWideSelectLen && p.hist) {
+    const dim3 grid((p.max_len + kWideTokensPerWG - 1) / kWideTokensPerWG, p.B);
+    for (int pass = 0; pass < 4; ++pass)
+      hipLaunchKernelGGL(dsa_hist_kernel, grid, dim3(kHistThreads), 0, st, p, pass);
+    hipLaunchKernelGGL(dsa_select_kernel<true>, dim3(p.B), dim3(kSelThreads), 0, st, p);
+  } else {
+    hipLaunchKernelGGL(dsa_select_kernel<false>, dim3(p.B), dim3(kSelThreads), 0, st, p);
+  }
   return hipGetLastError();
 }
+
+bool dsa_wide_select(int max_len) { return max_len >= kWideSelectLen; }
 
 }  // namespace moe

@@ -208,6 +208,7 @@ struct DsaParams {
   const int32_t *block_table;  // [B, max_pages]
   const int32_t *seq_lens;     // [B]
   float *scores;               // [B, max_len] workspace
+  int *hist;                   // [4, B, 256] radix histograms (workspace; long batches)
   int32_t *out;                // [B, topk]
   int B, PS, topk, max_pages, max_len, num_pages;
 };
@@ -218,6 +219,7 @@ hipError_t launch_route(const RouteParams &p, hipStream_t st);
 hipError_t launch_router_partials(const RouterParams &p, hipStream_t st);
 hipError_t launch_dsa_scores(const DsaParams &p, int max_len, bool force, hipStream_t st);
 hipError_t launch_dsa_select(const DsaParams &p, hipStream_t st);
+bool dsa_wide_select(int max_len);
 hipError_t launch_router_logits(const RouteParams &p, float *logits, hipStream_t st);
 hipError_t launch_permute(const PermuteParams &p, hipStream_t st);
 hipError_t launch_gemm1(const GemmParams &p, int BM, int grid, hipStream_t st);
