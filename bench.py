@@ -83,12 +83,18 @@ def layer_bytes(cfg, P: int, touched: int) -> int:
     return w + cfg.T * per_tok + 4 * cfg.num_experts
 
 
+# The sources that decide the grouped GEMMs' kernels, their launch plan and
+# their work-item order (the other operators' files are left out).
+GEMM_SOURCES = ("api.cpp", "gemm.hip", "gemm_tile.hip", "moe_device.h", "permute.hip",
+                "scatter_device.h")
+
+
 def source_digest() -> str:
-    """Digest of the kernel sources (every file of the library's csrc): a
-    traffic measurement is reported only while it matches."""
+    """Digest of the GEMM kernel sources: a traffic measurement is reported
+    only while it matches."""
     h = hashlib.sha256()
     d = os.path.join(ROOT, "paper_2608_14560_amd", "csrc")
-    for f in sorted(os.listdir(d)):
+    for f in GEMM_SOURCES:
         with open(os.path.join(d, f), "rb") as fh:
             h.update(f.encode())
             h.update(fh.read())
@@ -302,6 +308,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-max-tokens", type=int, default=16)
     ap.add_argument("--copy-calibration", action="store_true")
+    ap.add_argument("--layer-only", action="store_true",
+                    help="skip the router-projection and DSA-indexer legs (counter passes)")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
@@ -446,8 +454,10 @@ def main():
             times.append(e0.elapsed_time(e1))
         cold = round(float(np.median(times)) * 1e3, 2)
 
-    router = router_projection_leg(cfg, shape, batches, weights, out, ws, stream, K, prefill)
-    indexer = indexer_leg(K, prefill, not args.no_cpu_baseline)
+    router = indexer = None
+    if not args.layer_only:
+        router = router_projection_leg(cfg, shape, batches, weights, out, ws, stream, K, prefill)
+        indexer = indexer_leg(K, prefill, not args.no_cpu_baseline)
 
     cpu = None
     if not args.no_cpu_baseline:
