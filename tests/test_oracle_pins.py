@@ -739,3 +739,80 @@ def test_dsa_topk_ties_and_relu(oracle_lib):
     got = oracle_lib.dsa_topk(*args, cfg.topk)
     bt = x.block_table.numpy()
     assert got[0].tolist() == [int(bt[0, j // 64]) * 64 + j % 64 for j in range(cfg.topk)]
+
+
+# ------------------------------------------------------ DSA sparse attention
+def _att_np(x):
+    b = lambda t: t.contiguous().view(torch.int16).numpy().view(np.uint16)
+    return b(x.q_nope), b(x.q_pe), b(x.ckv), b(x.kpe), x.indices.numpy()
+
+
+def test_attention_uniform_and_single():
+    """q = 0 makes every logit 0: the output is the plain mean of the gathered Kc
+    rows and the LSE is log2 of their count.  A single valid index returns that
+    row exactly, with the LSE equal to its own base-2 logit."""
+    from oracle import dsa_attention as A
+    cfg = W.AttentionConfig("pin", (300, 40), topk=64)
+    x = W.generate_attention(cfg, 3)
+    qn, qp, kc, kp, idx = _att_np(x)
+    z = np.zeros_like(qn), np.zeros_like(qp)
+    out, lse = A.sparse_attention(z[0], z[1], kc, kp, idx, x.sm_scale)
+    for t in range(cfg.T):
+        valid = idx[t][idx[t] >= 0]
+        rows = A.bf16_to_f64(kc.reshape(-1, cfg.dc)[valid])
+        assert np.allclose(out[t], rows.mean(0)[None, :], rtol=0, atol=1e-12)
+        assert (lse[t] == np.log2(len(valid))).all()
+    one = np.full_like(idx, -1)
+    one[:, 5] = idx[:, 0]
+    out, lse = A.sparse_attention(qn, qp, kc, kp, one, x.sm_scale)
+    for t in range(cfg.T):
+        j = idx[t, 0]
+        krow = A.bf16_to_f64(kc.reshape(-1, cfg.dc)[j])
+        assert (out[t] == krow[None, :]).all()
+        s = (A.bf16_to_f64(qn[t]) @ krow + A.bf16_to_f64(qp[t]) @ A.bf16_to_f64(kp.reshape(-1, cfg.dp)[j])) \
+            * x.sm_scale * A.LOG2E
+        assert np.allclose(lse[t], s, rtol=1e-13, atol=1e-12)
+
+
+def test_attention_brute_force_and_invariances():
+    """Against a plain per-entry loop (no max shift, Python floats) on a tiny case;
+    the index order and -1 padding do not change the result; the weights
+    2^(s - lse) sum to 1."""
+    import math
+    from oracle import dsa_attention as A
+    cfg = W.AttentionConfig("pin", (90,), num_heads=2, topk=32)
+    x = W.generate_attention(cfg, 4)
+    qn, qp, kc, kp, idx = _att_np(x)
+    out, lse = A.sparse_attention(qn, qp, kc, kp, idx, x.sm_scale)
+    kcf, kpf = A.bf16_to_f64(kc.reshape(-1, cfg.dc)), A.bf16_to_f64(kp.reshape(-1, cfg.dp))
+    for h in range(cfg.num_heads):
+        q1, q2 = A.bf16_to_f64(qn[0, h]), A.bf16_to_f64(qp[0, h])
+        ss = [(sum(q1 * kcf[j]) + sum(q2 * kpf[j])) * x.sm_scale * A.LOG2E for j in idx[0] if j >= 0]
+        tot = math.fsum(2.0 ** v for v in ss)
+        assert math.isclose(lse[0, h], math.log2(tot), rel_tol=1e-12)
+        ref = sum((2.0 ** v / tot) * kcf[j] for v, j in zip(ss, [j for j in idx[0] if j >= 0]))
+        assert np.allclose(out[0, h], ref, rtol=1e-10, atol=1e-12)
+        assert math.isclose(math.fsum(2.0 ** (v - lse[0, h]) for v in ss), 1.0, rel_tol=1e-12)
+    perm = idx[:, ::-1].copy()
+    out2, lse2 = A.sparse_attention(qn, qp, kc, kp, perm, x.sm_scale)
+    assert np.allclose(out2, out, rtol=0, atol=1e-12) and np.allclose(lse2, lse, rtol=0, atol=1e-12)
+    # a short sequence: -1 entries moved among the valid ones change nothing
+    cfg = W.AttentionConfig("pin", (20,), num_heads=2, topk=32)
+    x = W.generate_attention(cfg, 6)
+    qn, qp, kc, kp, idx = _att_np(x)
+    out, lse = A.sparse_attention(qn, qp, kc, kp, idx, x.sm_scale)
+    mixed = np.full_like(idx, -1)
+    mixed[0, 1::2][:10] = idx[0, :10]
+    mixed[0, 25:] = idx[0, 10:17]
+    mixed[0, 22:25] = idx[0, 17:20]
+    out2, lse2 = A.sparse_attention(qn, qp, kc, kp, mixed, x.sm_scale)
+    assert np.allclose(out2, out, rtol=0, atol=1e-12) and np.allclose(lse2, lse, rtol=0, atol=1e-12)
+
+
+def test_attention_no_valid_index():
+    from oracle import dsa_attention as A
+    cfg = W.AttentionConfig("pin", (10,), topk=16)
+    x = W.generate_attention(cfg, 5)
+    qn, qp, kc, kp, idx = _att_np(x)
+    out, lse = A.sparse_attention(qn, qp, kc, kp, np.full_like(idx, -1), x.sm_scale)
+    assert (out == 0).all() and np.isneginf(lse).all()

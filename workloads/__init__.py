@@ -318,3 +318,80 @@ def generate_indexer(cfg: IndexerConfig, seed: int = 0, device="cpu") -> Indexer
                          kc.reshape(cfg.num_pages, PS, D).contiguous(),
                          ksc.reshape(cfg.num_pages, PS).contiguous(), bt.to(device),
                          torch.tensor(cfg.seq_lens, dtype=torch.int32, device=device))
+
+
+# ---------------------------------------------------------------------------
+# DSA Sparse Attention (paper Section 3.1.2): per query token, 16 heads of
+# q_nope (512) and q_pe (64) against a paged KV cache of 512-wide Kc and
+# 64-wide Kp entries, through a list of TopK sparse indices.  The contest
+# workloads are not available; seeded inputs of the same shapes stand in:
+#   q_nope, q_pe, Kc, Kp   N(0,1) rounded to bf16                 ids 31-34
+#   indices  TopK distinct cache positions of the token's sequence (a
+#            sequence of seq_len tokens over randomly permuted pages),
+#            -1 past a short sequence's length                     id 35
+#   sm_scale 1/sqrt(192) (DeepSeek-V3's 128 + 64 query head width)
+# ---------------------------------------------------------------------------
+TID_ATT_QN, TID_ATT_QP, TID_ATT_KC, TID_ATT_KP, TID_ATT_IDX = 31, 32, 33, 34, 35
+
+
+@dataclass(frozen=True)
+class AttentionConfig:
+    name: str
+    seq_lens: tuple            # one per query token
+    num_heads: int = 16
+    dc: int = 512
+    dp: int = 64
+    page_size: int = 64
+    topk: int = 2048
+    num_pages: int = 0         # 0: just enough for the sequences
+
+    @property
+    def T(self) -> int:
+        return len(self.seq_lens)
+
+    @property
+    def pages(self) -> int:
+        need = sum((s + self.page_size - 1) // self.page_size for s in self.seq_lens)
+        return max(self.num_pages, need, 1)
+
+
+ATTENTION_CONFIGS: dict[str, AttentionConfig] = {
+    # the paper's long-regime representative: 8 tokens, 8462 cache pages
+    "attn_long": AttentionConfig("attn_long", (60000,) * 8, num_pages=8462),
+    # the single-token and two-token regimes of its dispatch table
+    "attn_one": AttentionConfig("attn_one", (30000,)),
+    "attn_two": AttentionConfig("attn_two", (9000, 5000)),
+    # parity cases: short sequences (padding), TopK 256 and 2048
+    "attn_small": AttentionConfig("attn_small", (100, 3000, 257, 1), topk=256),
+    "attn_pad": AttentionConfig("attn_pad", (700, 2048, 1500, 4000)),
+}
+
+
+@dataclass
+class AttentionInputs:
+    cfg: AttentionConfig
+    q_nope: torch.Tensor   # [T, H, 512] bf16
+    q_pe: torch.Tensor     # [T, H, 64] bf16
+    ckv: torch.Tensor      # [pages, PS, 512] bf16
+    kpe: torch.Tensor      # [pages, PS, 64] bf16
+    indices: torch.Tensor  # [T, topk] int32
+    sm_scale: float
+
+
+def generate_attention(cfg: AttentionConfig, seed: int = 0, device="cpu") -> AttentionInputs:
+    T, H, PS = cfg.T, cfg.num_heads, cfg.page_size
+    qn = torch.randn(T, H, cfg.dc, generator=_gen(device, seed, TID_ATT_QN), device=device).to(torch.bfloat16)
+    qp = torch.randn(T, H, cfg.dp, generator=_gen(device, seed, TID_ATT_QP), device=device).to(torch.bfloat16)
+    kc = torch.randn(cfg.pages, PS, cfg.dc, generator=_gen(device, seed, TID_ATT_KC), device=device).to(torch.bfloat16)
+    kp = torch.randn(cfg.pages, PS, cfg.dp, generator=_gen(device, seed, TID_ATT_KP), device=device).to(torch.bfloat16)
+    g = torch.Generator(device="cpu")
+    g.manual_seed(substream_seed(seed, TID_ATT_IDX))
+    perm = torch.randperm(cfg.pages, generator=g)
+    idx = torch.full((T, cfg.topk), -1, dtype=torch.int32)
+    for t, s in enumerate(cfg.seq_lens):
+        n = (s + PS - 1) // PS
+        pages = perm[torch.randint(0, cfg.pages - n + 1, (1,), generator=g).item():][:n]
+        k = min(s, cfg.topk)
+        pos = torch.randperm(s, generator=g)[:k]
+        idx[t, :k] = (pages[pos // PS] * PS + pos % PS).to(torch.int32)
+    return AttentionInputs(cfg, qn, qp, kc, kp, idx.to(device), 1.0 / 192 ** 0.5)
