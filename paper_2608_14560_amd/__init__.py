@@ -29,7 +29,8 @@ EXPORTED = ("moe_workspace_size", "moe_route", "moe_route_hidden", "moe_fused_fp
             "moe_fused_fp8_router", "moe_fused_fp8_staged", "moe_num_stages", "moe_stage_name",
             "moe_status_string", "moe_debug_sigmoid", "moe_debug_e4m3_encode",
             "moe_debug_act_views", "moe_debug_mfma_block", "moe_debug_router_logits",
-            "dsa_workspace_size", "dsa_topk_indexer", "dsa_debug_scores")
+            "dsa_workspace_size", "dsa_topk_indexer", "dsa_debug_scores",
+            "dsa_attention_workspace_size", "dsa_sparse_attention")
 
 
 class MoEError(RuntimeError):
@@ -107,6 +108,11 @@ def lib() -> ctypes.CDLL:
         L.dsa_topk_indexer.restype = ctypes.c_int
         L.dsa_debug_scores.argtypes = [DS, P, P, P, P, P, P, P, P]
         L.dsa_debug_scores.restype = ctypes.c_int
+        AS = ctypes.POINTER(CAttnShape)
+        L.dsa_attention_workspace_size.argtypes = [AS]
+        L.dsa_attention_workspace_size.restype = ctypes.c_size_t
+        L.dsa_sparse_attention.argtypes = [AS, P, P, P, P, P, P, P, P, Z, P]
+        L.dsa_sparse_attention.restype = ctypes.c_int
         L.moe_fused_fp8_staged.argtypes = [S, P, P, P, P, P, P, P, P, P, R, P, Z, P,
                                            ctypes.POINTER(P), ctypes.c_int]
         L.moe_fused_fp8_staged.restype = ctypes.c_int
@@ -431,3 +437,49 @@ def dsa_debug_scores(q, weights, k_cache, k_scale, block_table, seq_lens, stream
                                 _dev(scores, torch.float32, "scores"), _stream(stream))
     _check("dsa_debug_scores", rc)
     return scores
+
+
+# ---------------------------------------------------------------- DSA sparse attention
+class CAttnShape(ctypes.Structure):
+    _fields_ = [("T", ctypes.c_int32), ("num_heads", ctypes.c_int32), ("topk", ctypes.c_int32),
+                ("num_rows", ctypes.c_int32), ("sm_scale", ctypes.c_float)]
+
+
+def attention_shape(q_nope: torch.Tensor, ckv: torch.Tensor, indices: torch.Tensor, sm_scale: float) -> CAttnShape:
+    T, H, _ = q_nope.shape
+    rows = ckv.numel() // ckv.shape[-1]
+    return CAttnShape(T, H, indices.shape[1], rows, float(sm_scale))
+
+
+def dsa_attention_workspace_size(shape: CAttnShape) -> int:
+    return int(lib().dsa_attention_workspace_size(ctypes.byref(shape)))
+
+
+def dsa_sparse_attention(q_nope, q_pe, ckv, kpe, indices, sm_scale: float, out=None, lse=None,
+                         workspace=None, stream=None):
+    """DSA sparse attention (paper Section 3.1.2): (out bf16 [T, H, 512],
+    lse float32 [T, H], base 2)."""
+    if q_nope.dim() != 3 or q_nope.shape[2] != 512 or ckv.shape[-1] != 512 or indices.dim() != 2:
+        raise ValueError("q_nope must be [T, H, 512], ckv [..., 512] and indices [T, topk]")
+    shape = attention_shape(q_nope, ckv, indices, sm_scale)
+    T, H = shape.T, shape.num_heads
+    if tuple(q_pe.shape) != (T, H, 64) or kpe.numel() != shape.num_rows * 64 or kpe.shape[-1] != 64 \
+            or indices.shape[0] != T:
+        raise ValueError("q_pe must be [T, H, 64], kpe [rows, 64] over the rows of ckv and indices [T, topk]")
+    if (out is not None and tuple(out.shape) != (T, H, 512)) or (lse is not None and tuple(lse.shape) != (T, H)):
+        raise ValueError("out must be [T, H, 512] and lse [T, H]")
+    if out is None:
+        out = torch.empty(max(T, 1), H, 512, dtype=torch.bfloat16, device=q_nope.device)[:T]
+    if lse is None:
+        lse = torch.empty(max(T, 1), H, dtype=torch.float32, device=q_nope.device)[:T]
+    if workspace is None:
+        workspace = torch.empty(max(dsa_attention_workspace_size(shape), 256), dtype=torch.uint8,
+                                device=q_nope.device)
+    rc = lib().dsa_sparse_attention(ctypes.byref(shape), _dev(q_nope, torch.bfloat16, "q_nope"),
+                                    _dev(q_pe, torch.bfloat16, "q_pe"), _dev(ckv, torch.bfloat16, "ckv"),
+                                    _dev(kpe, torch.bfloat16, "kpe"), _dev(indices, torch.int32, "indices"),
+                                    _dev(out, torch.bfloat16, "out"), _dev(lse, torch.float32, "lse"),
+                                    _dev(workspace, torch.uint8, "workspace"), workspace.numel(),
+                                    _stream(stream))
+    _check("dsa_sparse_attention", rc)
+    return out, lse

@@ -33,6 +33,8 @@ SOURCES = {
     "gemm.hip": [],
     "gemm_tile.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"],
     "api.cpp": ["-x", "hip"],
+    "attention.hip": [],
+    "attention_api.cpp": ["-x", "hip"],
 }
 
 

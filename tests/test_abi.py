@@ -192,6 +192,33 @@ def test_dsa_indexer_rejects_bad_arguments(M):
     assert L.dsa_topk_indexer(ctypes.byref(empty), *([None] * 7), None, 0, None) == M.MOE_OK
 
 
+def test_dsa_attention_rejects_bad_arguments(M):
+    L = M.lib()
+    good = M.CAttnShape(8, 16, 2048, 8462 * 64, 0.072)
+    nbytes = M.dsa_attention_workspace_size(good)
+    assert nbytes >= 8 * 32 * 16 * 512 * 4
+    for bad, code in [(M.CAttnShape(8, 8, 2048, 100, 0.1), M.MOE_ERR_UNSUPPORTED),
+                      (M.CAttnShape(8, 16, 70000, 100, 0.1), M.MOE_ERR_UNSUPPORTED),
+                      (M.CAttnShape(-1, 16, 2048, 100, 0.1), M.MOE_ERR_INVALID_ARG),
+                      (M.CAttnShape(8, 16, 0, 100, 0.1), M.MOE_ERR_INVALID_ARG),
+                      (M.CAttnShape(8, 16, 2048, 0, 0.1), M.MOE_ERR_INVALID_ARG),
+                      (M.CAttnShape(8, 16, 2048, 100, float("nan")), M.MOE_ERR_INVALID_ARG)]:
+        assert M.dsa_attention_workspace_size(bad) == 0
+        assert L.dsa_sparse_attention(ctypes.byref(bad), *_fake_ptrs(7), ctypes.c_void_p(0x7000000), 1 << 30,
+                                      None) == code
+    ptrs = _fake_ptrs(7)
+    ws = ctypes.c_void_p(0x7000000)
+    for i in range(7):
+        bad = list(ptrs)
+        bad[i] = None
+        assert L.dsa_sparse_attention(ctypes.byref(good), *bad, ws, nbytes, None) == M.MOE_ERR_INVALID_ARG
+        bad[i] = ctypes.c_void_p(ptrs[i].value + 4)
+        assert L.dsa_sparse_attention(ctypes.byref(good), *bad, ws, nbytes, None) == M.MOE_ERR_INVALID_ARG
+    assert L.dsa_sparse_attention(ctypes.byref(good), *ptrs, ws, nbytes - 1, None) == M.MOE_ERR_WORKSPACE_TOO_SMALL
+    assert L.dsa_sparse_attention(ctypes.byref(M.CAttnShape(0, 16, 2048, 100, 0.1)), *([None] * 7), None, 0,
+                                  None) == M.MOE_OK
+
+
 def test_workspace_grows_with_batch(M):
     sizes = [M.workspace_size(_shape(T=t)) for t in (1, 16, 256, 4096)]
     assert sizes == sorted(sizes) and sizes[0] > 0
