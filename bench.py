@@ -297,6 +297,68 @@ def indexer_leg(K, prefill, with_cpu: bool):
     return res
 
 
+def attention_leg(K, prefill, with_cpu: bool):
+    """µs per call of the DSA sparse attention (both launches: the split kernel
+    and the merge) on the paper's regimes, each K calls back to back.  Roofline
+    over the whole call: 2*(576 + 512) FLOP per (token, head, valid entry), plain
+    fp32 fused multiply-adds; algorithmic bytes = each valid entry's gathered
+    row (1152 B) and its index once per token, the query rows, the bf16 output
+    and the LSE."""
+    res = {}
+    for name in ("attn_long", "attn_two", "attn_one"):
+        cfg = W.ATTENTION_CONFIGS[name]
+        x = W.generate_attention(cfg, 0, device="cuda")
+        args = (x.q_nope, x.q_pe, x.ckv, x.kpe, x.indices, x.sm_scale)
+        shape = M.attention_shape(x.q_nope, x.ckv, x.indices, x.sm_scale)
+        ws = torch.empty(max(M.dsa_attention_workspace_size(shape), 256), dtype=torch.uint8, device="cuda")
+        out = torch.empty(cfg.T, cfg.num_heads, cfg.dc, dtype=torch.bfloat16, device="cuda")
+        lse = torch.empty(cfg.T, cfg.num_heads, dtype=torch.float32, device="cuda")
+
+        def fn():
+            M.dsa_sparse_attention(*args, out=out, lse=lse, workspace=ws)
+
+        for _ in range(3):
+            fn()
+        torch.cuda.synchronize()
+        h0 = time.perf_counter()
+        for _ in range(K):
+            fn()
+        host_ms = (time.perf_counter() - h0) * 1e3
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        prefill(host_ms)
+        a.record()
+        for _ in range(K):
+            fn()
+        b.record()
+        torch.cuda.synchronize()
+        call_us = a.elapsed_time(b) * 1e3 / K
+        valid = int((x.indices >= 0).sum().item())
+        H = cfg.num_heads
+        flop = 2.0 * (cfg.dc + cfg.dp) * H * valid + 2.0 * cfg.dc * H * valid
+        nbytes = valid * 2 * (cfg.dc + cfg.dp) + 4 * x.indices.numel() + 2 * (x.q_nope.numel() + x.q_pe.numel()) \
+            + 2 * out.numel() + 4 * lse.numel()
+        ach = flop / (call_us * 1e-6) / 1e12
+        rec = {"workload": f"{name}: {cfg.T} tokens x {H} heads, topk {cfg.topk}, seq_lens "
+                           f"{sorted(set(cfg.seq_lens))}, {cfg.pages} pages of {cfg.page_size}",
+               "us_per_call": round(call_us, 2),
+               "roofline_call": {"bound": "alu", "achieved": round(ach, 3), "peak": FP32_FMA_PEAK_TFLOPS,
+                                 "unit": "TFLOP/s", "frac": round(ach / FP32_FMA_PEAK_TFLOPS, 4),
+                                 "flop": int(flop), "algorithmic_bytes": int(nbytes),
+                                 "hbm_gbps": round(nbytes / (call_us * 1e-6) / 1e9, 1)}}
+        if with_cpu:
+            from oracle import dsa_attention as A  # the CPU baseline: the oracle timed beside the GPU figure
+            h = [t.contiguous().cpu().view(torch.int16).numpy().view(np.uint16)
+                 for t in (x.q_nope, x.q_pe, x.ckv, x.kpe)]
+            idx = x.indices.cpu().numpy()
+            t0 = time.perf_counter()
+            A.sparse_attention(*h, idx, x.sm_scale)
+            rec["cpu_oracle_us"] = round((time.perf_counter() - t0) * 1e6, 1)
+            rec["cpu_oracle_threads"] = torch.get_num_threads()
+        res[name] = rec
+    return res
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -309,7 +371,7 @@ def main():
     ap.add_argument("--cpu-max-tokens", type=int, default=16)
     ap.add_argument("--copy-calibration", action="store_true")
     ap.add_argument("--layer-only", action="store_true",
-                    help="skip the router-projection and DSA-indexer legs (counter passes)")
+                    help="skip the router-projection, DSA-indexer and sparse-attention legs (counter passes)")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
@@ -454,10 +516,11 @@ def main():
             times.append(e0.elapsed_time(e1))
         cold = round(float(np.median(times)) * 1e3, 2)
 
-    router = indexer = None
+    router = indexer = attention = None
     if not args.layer_only:
         router = router_projection_leg(cfg, shape, batches, weights, out, ws, stream, K, prefill)
         indexer = indexer_leg(K, prefill, not args.no_cpu_baseline)
+        attention = attention_leg(K, prefill, not args.no_cpu_baseline)
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -491,6 +554,7 @@ def main():
         "cpu_baseline": cpu,
         "router_projection": router,
         "dsa_topk_indexer": indexer,
+        "dsa_sparse_attention": attention,
         "us_per_call_cold": cold,
         "host_enqueue_us_per_call": round(host_ms * 1e3 / K, 1),
         "prefill_covered_enqueue": bool(enq_ms < 2.0 * host_ms + 2.0),

@@ -29,7 +29,7 @@ moe_status_t attn_check(const dsa_attn_shape_t *s) {
 int splits(const dsa_attn_shape_t *s) { return (s->topk + kAttnEntries - 1) / kAttnEntries; }
 
 size_t part_o_bytes(const dsa_attn_shape_t *s) {
-  return align_up(sizeof(float) * (size_t)(s->T > 0 ? s->T : 1) * splits(s) * s->num_heads * kAttnDC);
+  return align_up(sizeof(uint16_t) * (size_t)(s->T > 0 ? s->T : 1) * splits(s) * s->num_heads * kAttnDC);
 }
 
 }  // namespace
@@ -59,7 +59,7 @@ moe_status_t dsa_sparse_attention(const dsa_attn_shape_t *s, const uint16_t *q_n
   p.ckv = ckv;
   p.kpe = kpe;
   p.indices = indices;
-  p.part_o = static_cast<float *>(workspace);
+  p.part_o = static_cast<uint16_t *>(workspace);
   p.part_ml = reinterpret_cast<float *>(static_cast<uint8_t *>(workspace) + part_o_bytes(s));
   p.out = out;
   p.lse = lse;
