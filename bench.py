@@ -49,6 +49,7 @@ FP8_PEAK_TFLOPS = 5000.0
 # fp32 fused multiply-adds without packed instructions (the kernels are built
 # with packed fp32 disabled): 256 CUs x 4 SIMDs x 16 lanes x 2 FLOP x 2.4 GHz
 FP32_FMA_PEAK_TFLOPS = 78.6
+BF16_PEAK_TFLOPS = 2500.0  # dense bf16 MFMA
 PROFILE_TRAFFIC = os.path.join(ROOT, "profiles", "gemm1_traffic_{cfg}.txt")
 
 
@@ -300,10 +301,11 @@ def indexer_leg(K, prefill, with_cpu: bool):
 def attention_leg(K, prefill, with_cpu: bool):
     """µs per call of the DSA sparse attention (both launches: the split kernel
     and the merge) on the paper's regimes, each K calls back to back.  Roofline
-    over the whole call: 2*(576 + 512) FLOP per (token, head, valid entry), plain
-    fp32 fused multiply-adds; algorithmic bytes = each valid entry's gathered
-    row (1152 B) and its index once per token, the query rows, the bf16 output
-    and the LSE."""
+    over the whole call against HBM (the products run on the bf16 matrix cores,
+    where 2*(576 + 512) FLOP per (token, head, valid entry) take a tenth of the
+    time the bytes need at peak): algorithmic bytes = each valid entry's
+    gathered row (1152 B) and its index once per token, the query rows, the
+    bf16 output and the LSE."""
     res = {}
     for name in ("attn_long", "attn_two", "attn_one"):
         cfg = W.ATTENTION_CONFIGS[name]
@@ -338,14 +340,15 @@ def attention_leg(K, prefill, with_cpu: bool):
         flop = 2.0 * (cfg.dc + cfg.dp) * H * valid + 2.0 * cfg.dc * H * valid
         nbytes = valid * 2 * (cfg.dc + cfg.dp) + 4 * x.indices.numel() + 2 * (x.q_nope.numel() + x.q_pe.numel()) \
             + 2 * out.numel() + 4 * lse.numel()
-        ach = flop / (call_us * 1e-6) / 1e12
+        gbs = nbytes / (call_us * 1e-6) / 1e9
+        tf = flop / (call_us * 1e-6) / 1e12
         rec = {"workload": f"{name}: {cfg.T} tokens x {H} heads, topk {cfg.topk}, seq_lens "
                            f"{sorted(set(cfg.seq_lens))}, {cfg.pages} pages of {cfg.page_size}",
                "us_per_call": round(call_us, 2),
-               "roofline_call": {"bound": "alu", "achieved": round(ach, 3), "peak": FP32_FMA_PEAK_TFLOPS,
-                                 "unit": "TFLOP/s", "frac": round(ach / FP32_FMA_PEAK_TFLOPS, 4),
-                                 "flop": int(flop), "algorithmic_bytes": int(nbytes),
-                                 "hbm_gbps": round(nbytes / (call_us * 1e-6) / 1e9, 1)}}
+               "roofline_call": {"bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                                 "frac": round(gbs / HBM_PEAK_GBS, 4), "algorithmic_bytes": int(nbytes),
+                                 "flop": int(flop), "tflops": round(tf, 2),
+                                 "pct_bf16_mfma_peak": round(100 * tf / BF16_PEAK_TFLOPS, 3)}}
         if with_cpu:
             from oracle import dsa_attention as A  # the CPU baseline: the oracle timed beside the GPU figure
             h = [t.contiguous().cpu().view(torch.int16).numpy().view(np.uint16)

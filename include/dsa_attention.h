@@ -47,8 +47,12 @@ size_t dsa_attention_workspace_size(const dsa_attn_shape_t *s);
  *  indices  [T, topk] int32 cache rows; entries outside [0, num_rows) (-1
  *           for padding) are absent
  *  out      [T, H, 512] bf16      lse  [T, H] float (base 2)
- * fp32 accumulation; the softmax is split over groups of 64 index entries
- * and merged with the split maxima (flash decoding); deterministic. */
+ * Arithmetic: both products on the bf16 matrix cores with fp32 accumulation
+ * (the logits from the bf16 inputs as given; the weighted sum from the
+ * softmax weights rounded to bf16); the softmax is split over groups of 64
+ * index entries, each group's output normalised by its own fp32 sum and kept
+ * in bf16, and the groups merged with their maxima and sums (flash decoding).
+ * The LSE comes from the fp32 sums.  Deterministic (no atomics). */
 moe_status_t dsa_sparse_attention(const dsa_attn_shape_t *s, const uint16_t *q_nope,
                                   const uint16_t *q_pe, const uint16_t *ckv, const uint16_t *kpe,
                                   const int32_t *indices, uint16_t *out, float *lse,

@@ -196,7 +196,7 @@ def test_dsa_attention_rejects_bad_arguments(M):
     L = M.lib()
     good = M.CAttnShape(8, 16, 2048, 8462 * 64, 0.072)
     nbytes = M.dsa_attention_workspace_size(good)
-    assert nbytes >= 8 * 32 * 16 * 512 * 4
+    assert nbytes >= 8 * 32 * 16 * (512 * 2 + 2 * 4)  # bf16 split outputs, fp32 (max, sum)
     for bad, code in [(M.CAttnShape(8, 8, 2048, 100, 0.1), M.MOE_ERR_UNSUPPORTED),
                       (M.CAttnShape(8, 16, 70000, 100, 0.1), M.MOE_ERR_UNSUPPORTED),
                       (M.CAttnShape(-1, 16, 2048, 100, 0.1), M.MOE_ERR_INVALID_ARG),
