@@ -58,6 +58,149 @@ __device__ __forceinline__ float key_of(const float (&v)[EPL], int e) {
   return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, x), src));
 }
 
+// Top-K experts among the candidates, in selection order: key descending, the
+// lower expert id first among equal keys (the order of K successive wave
+// arg-maxes, without their K dependent reduction chains).  A bitwise radix
+// select over the ordered key bits finds the K-th largest key: per bit, one
+// ballot per slot counts the candidates that match the prefix so far with that
+// bit set.  Every candidate above the threshold wins, and those equal to it
+// win in ascending id order until K are taken.  The winners go to LDS in id
+// order, each ranks itself among them, and lane j < K returns winner j.
+// K <= 16 (validated on the host); the wave works alone (no block barrier).
+constexpr int kRouteWaves = 4;   // waves per routing workgroup
+constexpr int kMaxTopK = 16;
+
+__device__ __forceinline__ int lanes_below(uint64_t m) {
+  return (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+}
+
+__device__ __forceinline__ void wave_lds_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+//
+// With a lower bound (bh, bl) on the K-th largest packed key (value bits, then
+// the complemented id) known, only the candidates at or above it can win; when
+// at most 64 of them are, each takes a lane and counts the others that beat it
+// (LDS broadcast reads): its rank is its output slot, and nothing else runs.
+template <int EPL>
+__device__ __forceinline__ void select_topk(const float (&key)[EPL], const float (&sc)[EPL],
+                                            const bool (&cand)[EPL], int K, int lane, int &my_id,
+                                            float &my_s, bool bounded = false, uint32_t bh = 0u,
+                                            uint32_t bl = 0u) {
+  __shared__ uint32_t sel_hi[kRouteWaves][kWave];
+  __shared__ int sel_e[kRouteWaves][kWave];
+  __shared__ float sel_s[kRouteWaves][kWave];
+  __shared__ int out_e[kRouteWaves][kMaxTopK];
+  __shared__ float out_s[kRouteWaves][kMaxTopK];
+  const int wave = threadIdx.x / kWave;
+
+  uint32_t hi[EPL];
+#pragma unroll
+  for (int q = 0; q < EPL; ++q) hi[q] = ordered_bits(key[q]);
+
+  if (bounded) {
+    bool f[EPL];
+    int n = 0;
+#pragma unroll
+    for (int q = 0; q < EPL; ++q) {
+      const uint32_t lo = ~(uint32_t)(q * kWave + lane);
+      f[q] = cand[q] && (hi[q] > bh || (hi[q] == bh && lo >= bl));
+      n += __popcll(__ballot(f[q]));
+    }
+    if (n <= kWave) {
+      int pos_base = 0;
+#pragma unroll
+      for (int q = 0; q < EPL; ++q) {
+        const uint64_t fm = __ballot(f[q]);
+        const int pos = pos_base + lanes_below(fm);
+        if (f[q]) {  // pos < n <= 64
+          sel_hi[wave][pos] = hi[q];
+          sel_e[wave][pos] = q * kWave + lane;
+          sel_s[wave][pos] = sc[q];
+        }
+        pos_base += __popcll(fm);
+      }
+      wave_lds_sync();
+      if (lane < n) {
+        const uint32_t h = sel_hi[wave][lane];
+        int rank = 0;
+        for (int i = 0; i < n; ++i) {
+          const uint32_t hi_i = sel_hi[wave][i];
+          rank += (hi_i > h || (hi_i == h && i < lane)) ? 1 : 0;
+        }
+        if (rank < K) {
+          out_e[wave][rank] = sel_e[wave][lane];
+          out_s[wave][rank] = sel_s[wave][lane];
+        }
+      }
+      wave_lds_sync();
+      if (lane < K) {
+        my_id = out_e[wave][lane];
+        my_s = out_s[wave][lane];
+      }
+      return;
+    }
+  }
+
+  uint32_t thr = 0;
+  int need = K;
+  for (int b = 31; b >= 0; --b) {
+    const uint32_t target = (thr >> b) | 1u;
+    int c = 0;
+#pragma unroll
+    for (int q = 0; q < EPL; ++q) c += __popcll(__ballot(cand[q] && (hi[q] >> b) == target));
+    if (c >= need)
+      thr |= 1u << b;
+    else
+      need -= c;
+  }
+  // winners, then their slots in id order (slot-major: id = q * 64 + lane)
+  int tie_base = 0, pos_base = 0;
+#pragma unroll
+  for (int q = 0; q < EPL; ++q) {
+    const bool eq = cand[q] && hi[q] == thr;
+    const uint64_t em = __ballot(eq);
+    const bool win = cand[q] && (hi[q] > thr || (eq && tie_base + lanes_below(em) < need));
+    tie_base += __popcll(em);
+    const uint64_t wm = __ballot(win);
+    const int pos = pos_base + lanes_below(wm);
+    if (win && pos < kMaxTopK) {  // exactly K winners; the bound only guards the array
+      sel_hi[wave][pos] = hi[q];
+      sel_e[wave][pos] = q * kWave + lane;
+      sel_s[wave][pos] = sc[q];
+    }
+    pos_base += __popcll(wm);
+  }
+  wave_lds_sync();
+  if (lane < K) {
+    const uint32_t h = sel_hi[wave][lane];
+    int rank = 0;
+    for (int i = 0; i < K; ++i) {
+      const uint32_t hi_i = sel_hi[wave][i];
+      rank += (hi_i > h || (hi_i == h && i < lane)) ? 1 : 0;
+    }
+    out_e[wave][rank] = sel_e[wave][lane];
+    out_s[wave][rank] = sel_s[wave][lane];
+  }
+  wave_lds_sync();
+  if (lane < K) {
+    my_id = out_e[wave][lane];
+    my_s = out_s[wave][lane];
+  }
+}
+
+// The bias of the lane's experts, loaded unconditionally (clamped index) so the
+// loads go out with the logits' and the sigmoids below run without branches:
+// per-slot branches around a load serialise one round trip per slot.
+template <int EPL>
+__device__ __forceinline__ void load_bias(const RouteParams &p, int lane, float (&bs)[EPL]) {
+#pragma unroll
+  for (int q = 0; q < EPL; ++q) bs[q] = p.bias[min(q * kWave + lane, p.E - 1)];
+}
+
 // EPL = experts held per lane (expert e lives in lane e % 64, slot e / 64).
 // GC = number of groups when known at compile time (its group reductions are
 // then independent chains the compiler interleaves), 0 for a runtime count.
@@ -73,18 +216,15 @@ __global__ __launch_bounds__(256) void route_kernel(RouteParams p) {
 
   const int gsz = p.E / G;
 
-  float sc[EPL], key[EPL], lg[EPL];
+  float sc[EPL], key[EPL], lg[EPL], bs[EPL];
+  load_bias<EPL>(p, lane, bs);
   route_logits<EPL>(p, t, lane, lg);
 #pragma unroll
   for (int q = 0; q < EPL; ++q) {
     const int e = q * kWave + lane;
-    if (e < p.E) {
-      sc[q] = sigmoid_spec(lg[q]);
-      key[q] = sc[q] + p.bias[e];
-    } else {
-      sc[q] = 0.0f;
-      key[q] = -INFINITY;
-    }
+    const float s = sigmoid_spec(lg[q]);
+    sc[q] = e < p.E ? s : 0.0f;
+    key[q] = e < p.E ? s + bs[q] : -INFINITY;
   }
 
   // group score = sum of the two largest keys of the group
@@ -167,27 +307,7 @@ __global__ __launch_bounds__(256) void route_kernel(RouteParams p) {
   // top-k experts among the kept groups, in selection order
   int my_id = 0;
   float my_s = 0.0f;
-  for (int j = 0; j < p.K; ++j) {
-    float bv = -INFINITY;
-    int bi = kNoIdx;
-#pragma unroll
-    for (int q = 0; q < EPL; ++q) {
-      const int e = q * kWave + lane;
-      if (cand[q] && beats(key[q], e, bv, bi)) {
-        bv = key[q];
-        bi = e;
-      }
-    }
-    const int win = wave_argmax(bv, bi);
-#pragma unroll
-    for (int q = 0; q < EPL; ++q)
-      if (q * kWave + lane == win) cand[q] = false;
-    const float ws = key_of(sc, win);
-    if (lane == j) {
-      my_id = win;
-      my_s = ws;
-    }
-  }
+  select_topk<EPL>(key, sc, cand, p.K, lane, my_id, my_s);
 
   // weights: unbiased scores normalised over the k selections (summed in
   // selection order), times the routed scaling factor
@@ -252,15 +372,17 @@ __device__ __forceinline__ void route_token_seg(const RouteParams &p, int t) {
   const int lane = threadIdx.x & (kWave - 1);
   const int seg_lane = lane & (S - 1);
 
-  float sc[EPL], key[EPL], lg[EPL];
+  float sc[EPL], key[EPL], lg[EPL], bs[EPL];
   Key2 k2[EPL];
+  load_bias<EPL>(p, lane, bs);
   route_logits<EPL>(p, t, lane, lg);
 #pragma unroll
   for (int q = 0; q < EPL; ++q) {
     const int e = q * kWave + lane;
     const bool v = e < p.E;
-    sc[q] = v ? sigmoid_spec(lg[q]) : 0.0f;
-    key[q] = v ? sc[q] + p.bias[e] : -INFINITY;
+    const float s = sigmoid_spec(lg[q]);
+    sc[q] = v ? s : 0.0f;
+    key[q] = v ? s + bs[q] : -INFINITY;
     k2[q].ah = v ? ordered_bits(key[q]) : 0u;
     k2[q].al = ~(uint32_t)e;
     k2[q].bh = 0u;
@@ -312,26 +434,28 @@ __device__ __forceinline__ void route_token_seg(const RouteParams &p, int t) {
     cand[q] = (e < p.E) && ((kept >> (e / S)) & 1ull);
   }
 
-  // top-k experts among the kept groups, in selection order
+  // top-k experts among the kept groups, in selection order.  When K <= 2 *
+  // topk_group the K-th largest key is at least the smallest runner-up of the
+  // kept groups (their bests and runner-ups are 2 * topk_group candidates).
+  uint32_t bh = 0xffffffffu, bl = 0xffffffffu;
+#pragma unroll
+  for (int q = 0; q < EPL; ++q) {
+#pragma unroll
+    for (int sg = 0; sg < SEGS; ++sg) {
+      const int g = q * SEGS + sg;
+      if (g < G && ((kept >> g) & 1ull)) {
+        const uint32_t h = (uint32_t)__builtin_amdgcn_readlane((int)k2[q].bh, sg * S + S - 1);
+        const uint32_t l = (uint32_t)__builtin_amdgcn_readlane((int)k2[q].bl, sg * S + S - 1);
+        if (key_gt(bh, bl, h, l)) {
+          bh = h;
+          bl = l;
+        }
+      }
+    }
+  }
   int my_id = 0;
   float my_s = 0.0f;
-  for (int j = 0; j < p.K; ++j) {
-    float bv = -INFINITY;
-    int bi = kNoIdx;
-#pragma unroll
-    for (int q = 0; q < EPL; ++q) {
-      const int e = q * kWave + lane;
-      const bool take = cand[q] && beats(key[q], e, bv, bi);
-      bv = take ? key[q] : bv;
-      bi = take ? e : bi;
-    }
-    const int win = wave_argmax(bv, bi);
-#pragma unroll
-    for (int q = 0; q < EPL; ++q) cand[q] = cand[q] && (q * kWave + lane != win);
-    const float ws = key_of(sc, win);
-    my_id = (lane == j) ? win : my_id;
-    my_s = (lane == j) ? ws : my_s;
-  }
+  select_topk<EPL>(key, sc, cand, p.K, lane, my_id, my_s, p.K <= 2 * p.TG, bh, bl);
 
   float sum = 0.0f;
   for (int j = 0; j < p.K; ++j)
@@ -378,7 +502,7 @@ void launch_route_epl(const RouteParams &p, dim3 grid, dim3 block, hipStream_t s
 
 hipError_t launch_route(const RouteParams &p, hipStream_t st) {
   if (p.T == 0) return hipSuccess;
-  const int waves_per_block = 4;
+  const int waves_per_block = kRouteWaves;
   dim3 grid((p.T + waves_per_block - 1) / waves_per_block), block(waves_per_block * kWave);
   if (p.E <= 64)
     launch_route_epl<1>(p, grid, block, st);
