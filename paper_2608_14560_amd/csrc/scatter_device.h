@@ -9,6 +9,7 @@ namespace moe {
 
 constexpr int kPermMaxEl = 1024;
 constexpr int kPermTokenWaves = kChunkTokens / kWave;  // waves that hold a chunk's tokens
+constexpr int kPermMaxK = 16;                           // top_k limit of the shape check
 
 // LDS of one scatter workgroup of NT threads.  SINGLE: the batch is one chunk
 // and the workgroup counts its own pairs.
@@ -17,58 +18,92 @@ struct ScatterLds {
   int base[kPermMaxEl];
   int hist[SINGLE ? kPermMaxEl : 1];
   unsigned long long bits[kPermTokenWaves][kPermMaxEl];
-  int wsum[NT / kWave];
+  int wsum[NT / kWave][2];
 };
 
-// Exclusive scan of v over the NT threads (one value per thread); returns the
-// exclusive prefix and writes the total to *total.  Every thread must call it.
+// Inclusive scan over the wave with DPP: a window of four lanes (row_shr 1, 2,
+// 3 of the original values), then row_shr 4 and 8 into the upper lanes of each
+// 16-lane row, then row_bcast 15 and 31 across rows.
+template <int kCtrl, int kRows, int kBanks>
+__device__ __forceinline__ int scan_dpp(int v) {
+  return __builtin_amdgcn_update_dpp(0, v, kCtrl, kRows, kBanks, false);
+}
+__device__ __forceinline__ int wave_incl_scan(int v) {
+  int x = v + scan_dpp<0x111, 0xf, 0xf>(v);
+  x += scan_dpp<0x112, 0xf, 0xf>(v);
+  x += scan_dpp<0x113, 0xf, 0xf>(v);
+  x += scan_dpp<0x114, 0xf, 0xe>(x);
+  x += scan_dpp<0x118, 0xf, 0xc>(x);
+  x += scan_dpp<0x142, 0xa, 0xf>(x);
+  x += scan_dpp<0x143, 0xc, 0xf>(x);
+  return x;
+}
+
+// Exclusive scans of two values over the NT threads (one pair per thread):
+// the prefixes and the totals.  Every thread must call it.
 template <int NT>
-__device__ int scatter_block_scan(int v, int *wsum, int *total) {
+__device__ void scatter_block_scan2(int a, int b, int (*wsum)[2], int &pa, int &pb, int &ta, int &tb) {
   constexpr int NW = NT / kWave;
   const int lane = threadIdx.x & (kWave - 1);
   const int w = threadIdx.x / kWave;
-  int x = v;
+  const int xa = wave_incl_scan(a), xb = wave_incl_scan(b);
+  if (lane == kWave - 1) {
+    wsum[w][0] = xa;
+    wsum[w][1] = xb;
+  }
+  __syncthreads();
+  int ba = 0, bb = 0, aa = 0, ab = 0;
 #pragma unroll
-  for (int off = 1; off < kWave; off <<= 1) {
-    const int y = __shfl_up(x, off);
-    if (lane >= off) x += y;
-  }
-  if (lane == kWave - 1) wsum[w] = x;
-  __syncthreads();
-  int before = 0, all = 0;
   for (int i = 0; i < NW; ++i) {
-    if (i < w) before += wsum[i];
-    all += wsum[i];
+    const int va = wsum[i][0], vb = wsum[i][1];
+    ba += i < w ? va : 0;
+    bb += i < w ? vb : 0;
+    aa += va;
+    ab += vb;
   }
-  __syncthreads();
-  *total = all;
-  return before + x - v;
+  pa = ba + xa - a;
+  pb = bb + xb - b;
+  ta = aa;
+  tb = ab;
 }
 
 // Scatter of chunk `chunk` (tokens [256 chunk, 256 chunk + 256)); thread t of
-// the first 256 holds token 256 chunk + t.  `ids` is the [T, K] routing
-// output (global or LDS).  Workgroup 0 also writes expert_offsets, the M-tile
-// prefix of every expert and the GEMM work-item counts.  Every thread of the
-// workgroup must call it (it contains barriers).
+// the first 256 holds token 256 chunk + t and keeps its K expert ids in
+// registers for the three passes (count, mark, rank).  `ids` is the [T, K]
+// routing output.  Workgroup 0 also writes expert_offsets, the M-tile prefix
+// of every expert and the GEMM work-item counts (one combined scan of the
+// per-expert pair counts and tile counts).  Every thread of the workgroup must
+// call it (it contains barriers).
 template <int NT, bool SINGLE>
 __device__ void scatter_chunk(const PermuteParams &p, int chunk, const int32_t *ids,
                               ScatterLds<NT, SINGLE> &sh) {
   static_assert(NT >= kChunkTokens, "a thread per token of the chunk");
   const int lane = threadIdx.x & (kWave - 1);
   const int w = threadIdx.x / kWave;
+  const int t = chunk * kChunkTokens + threadIdx.x;
+  const bool live = threadIdx.x < kChunkTokens && t < p.T;
+
+  // the token's local expert ids (-1: not resident, or past K); the loads are
+  // unconditional (clamped indices) so they all go out at once
+  int le[kPermMaxK];
+  {
+    const int tc = min(t, p.T - 1);
+#pragma unroll
+    for (int j = 0; j < kPermMaxK; ++j) {
+      const int x = ids[(size_t)tc * p.K + min(j, p.K - 1)] - p.offset;
+      le[j] = (live && j < p.K && x >= 0 && x < p.El) ? x : -1;
+    }
+  }
 
   for (int e = threadIdx.x; e < p.El; e += NT) {
     for (int i = 0; i < kPermTokenWaves; ++i) sh.bits[i][e] = 0ull;
     if (SINGLE) sh.hist[e] = 0;
   }
+  __syncthreads();
   if (SINGLE) {
-    __syncthreads();
-    const int t = threadIdx.x;
-    if (t < p.T && t < kChunkTokens)
-      for (int j = 0; j < p.K; ++j) {
-        const int le = ids[(size_t)t * p.K + j] - p.offset;
-        if (le >= 0 && le < p.El) atomicAdd(&sh.hist[le], 1);
-      }
+#pragma unroll
+    for (int j = 0; j < kPermMaxK; ++j)
+      if (le[j] >= 0) atomicAdd(&sh.hist[le[j]], 1);
     __syncthreads();
   }
   // count of local expert e in chunk c
@@ -76,11 +111,11 @@ __device__ void scatter_chunk(const PermuteParams &p, int chunk, const int32_t *
     return SINGLE ? sh.hist[e] : p.chunk_counts[(size_t)c * p.El + e];
   };
 
-  // expert offsets: exclusive scan of the per-expert totals over all chunks.
-  // Each thread owns a contiguous run of experts.
+  // per-expert totals over all chunks.  Each thread owns a contiguous run of
+  // experts: its pair and tile totals enter one block scan.
   const int per = (p.El + NT - 1) / NT;
   const int e0 = threadIdx.x * per;
-  int tot_run = 0;
+  int tot_run = 0, tiles_run = 0;
   for (int e = e0; e < e0 + per && e < p.El; ++e) {
     int tot = 0, before = 0;
     for (int c = 0; c < p.nchunks; ++c) {
@@ -90,70 +125,53 @@ __device__ void scatter_chunk(const PermuteParams &p, int chunk, const int32_t *
     }
     sh.base[e] = before;  // chunk-local part; the expert offset is added below
     tot_run += tot;
-  }
-  int P = 0;
-  const int run_start = scatter_block_scan<NT>(tot_run, sh.wsum, &P);
-  // walk the run again to turn totals into offsets
-  int acc = run_start;
-  for (int e = e0; e < e0 + per && e < p.El; ++e) {
-    int tot = 0;
-    for (int c = 0; c < p.nchunks; ++c) tot += cnt(c, e);
-    if (chunk == 0) p.expert_offsets[e] = acc;
-    sh.base[e] += acc;
-    acc += tot;
-  }
-  if (chunk == 0 && threadIdx.x == 0) p.expert_offsets[p.El] = P;
-  __syncthreads();
-
-  // rank the chunk's pairs: bit `lane` of bits[w][e] marks that the lane's
-  // token holds local expert e
-  const int t = chunk * kChunkTokens + threadIdx.x;
-  const bool live = threadIdx.x < kChunkTokens && t < p.T;
-  if (live) {
-    for (int j = 0; j < p.K; ++j) {
-      const int le = ids[(size_t)t * p.K + j] - p.offset;
-      if (le >= 0 && le < p.El) atomicOr(&sh.bits[w][le], 1ull << lane);
-    }
-  }
-  __syncthreads();
-  if (live) {
-    const unsigned long long below = (lane == 0) ? 0ull : (~0ull >> (kWave - lane));
-    for (int j = 0; j < p.K; ++j) {
-      const int le = ids[(size_t)t * p.K + j] - p.offset;
-      int row = -1;
-      if (le >= 0 && le < p.El) {
-        row = sh.base[le];
-        for (int i = 0; i < w; ++i) row += __popcll(sh.bits[i][le]);
-        row += __popcll(sh.bits[w][le] & below);
-        p.perm_token[row] = t;
-        p.perm_pair[row] = t * p.K + j;
-      }
-      p.pair_row[(size_t)t * p.K + j] = row;
-    }
-  }
-
-  if (chunk != 0) return;  // uniform over the workgroup
-
-  // M-tile prefix per expert and the GEMM work-item counts
-  __syncthreads();
-  int tiles_run = 0;
-  for (int e = e0; e < e0 + per && e < p.El; ++e) {
-    int tot = 0;
-    for (int c = 0; c < p.nchunks; ++c) tot += cnt(c, e);
     tiles_run += (tot + p.BM - 1) / p.BM;
   }
-  int n_tiles = 0;
-  int tacc = scatter_block_scan<NT>(tiles_run, sh.wsum, &n_tiles);
+  int run_start, tile_start, P, n_tiles;
+  scatter_block_scan2<NT>(tot_run, tiles_run, sh.wsum, run_start, tile_start, P, n_tiles);
+  // walk the run again: expert offsets, M-tile prefix
+  int acc = run_start, tacc = tile_start;
   for (int e = e0; e < e0 + per && e < p.El; ++e) {
     int tot = 0;
     for (int c = 0; c < p.nchunks; ++c) tot += cnt(c, e);
-    p.tile_base[e] = tacc;
+    if (chunk == 0) {
+      p.expert_offsets[e] = acc;
+      p.tile_base[e] = tacc;
+    }
+    sh.base[e] += acc;
+    acc += tot;
     tacc += (tot + p.BM - 1) / p.BM;
   }
-  if (threadIdx.x == 0) {
+  if (chunk == 0 && threadIdx.x == 0) {
+    p.expert_offsets[p.El] = P;
     p.tile_base[p.El] = n_tiles;
     p.n_items[0] = n_tiles * p.items_per_tile1;
     p.n_items[1] = n_tiles * p.items_per_tile2;
+  }
+
+  // rank the chunk's pairs: bit `lane` of bits[w][e] marks that the lane's
+  // token holds local expert e
+#pragma unroll
+  for (int j = 0; j < kPermMaxK; ++j)
+    if (le[j] >= 0) atomicOr(&sh.bits[w][le[j]], 1ull << lane);
+  __syncthreads();
+  if (live) {
+    const unsigned long long below = (lane == 0) ? 0ull : (~0ull >> (kWave - lane));
+#pragma unroll
+    for (int j = 0; j < kPermMaxK; ++j) {
+      if (j < p.K) {
+        int row = -1;
+        const int e = le[j];
+        if (e >= 0) {
+          row = sh.base[e];
+          for (int i = 0; i < w; ++i) row += __popcll(sh.bits[i][e]);
+          row += __popcll(sh.bits[w][e] & below);
+          p.perm_token[row] = t;
+          p.perm_pair[row] = t * p.K + j;
+        }
+        p.pair_row[(size_t)t * p.K + j] = row;
+      }
+    }
   }
 }
 
