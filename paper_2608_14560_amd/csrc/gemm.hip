@@ -576,29 +576,57 @@ __global__ __launch_bounds__(256) void requant_kernel(GemmParams p) {
   if (c0 == 0) p.act_scale[(size_t)row * IB + blk] = scale;
 }
 
+// The combine: out[t] = bf16(sum over the token's resident slots, in slot
+// order, of w_j * Y[pair_row[t, j]]).  All K pair rows and weights are loaded
+// first, then the Y rows of the resident slots, so a token costs two
+// dependent round trips, not 2K.
+// KM >= K slots (4, 8 or 16).
+template <int KM>
 __global__ __launch_bounds__(256) void finalize_kernel(FinalizeParams p) {
   const int t = blockIdx.x;
   const int n0 = (blockIdx.y * 256 + threadIdx.x) * 8;
   if (n0 >= p.H) return;
+  int pr[KM];
+  float w[KM];
+#pragma unroll
+  for (int j = 0; j < KM; ++j) {
+    const int jj = min(j, p.K - 1);
+    pr[j] = p.pair_row[(size_t)t * p.K + jj];
+    w[j] = p.topk_w[(size_t)t * p.K + jj];
+  }
+  // the token is the workgroup's, so pr[j] is uniform: absent slots branch
+  // around their loads without splitting the wave
+  float4 ya[KM], yb[KM];
+#pragma unroll
+  for (int j = 0; j < KM; ++j) {
+    ya[j] = yb[j] = float4{0.f, 0.f, 0.f, 0.f};
+    if (pr[j] >= 0) {
+      const float *src = p.Y + (size_t)pr[j] * p.H + n0;
+      ya[j] = *reinterpret_cast<const float4 *>(src);
+      yb[j] = *reinterpret_cast<const float4 *>(src + 4);
+    }
+  }
+  for (int q = 1; q < p.S; ++q) {  // K-split planes of Y, summed first
+#pragma unroll
+    for (int j = 0; j < KM; ++j) {
+      if (pr[j] < 0) continue;
+      const float *src = p.Y + ((size_t)q * p.P_max + pr[j]) * p.H + n0;
+      const float4 a = *reinterpret_cast<const float4 *>(src);
+      const float4 b = *reinterpret_cast<const float4 *>(src + 4);
+      ya[j].x += a.x; ya[j].y += a.y; ya[j].z += a.z; ya[j].w += a.w;
+      yb[j].x += b.x; yb[j].y += b.y; yb[j].z += b.z; yb[j].w += b.w;
+    }
+  }
   float acc[8];
 #pragma unroll
   for (int c = 0; c < 8; ++c) acc[c] = 0.0f;
-  for (int j = 0; j < p.K; ++j) {
-    const int pr = p.pair_row[(size_t)t * p.K + j];
-    if (pr < 0) continue;
-    const float w = p.topk_w[(size_t)t * p.K + j];
-    float y[8];
 #pragma unroll
-    for (int c = 0; c < 8; ++c) y[c] = 0.0f;
-    for (int q = 0; q < p.S; ++q) {
-      const float *src = p.Y + ((size_t)q * p.P_max + pr) * p.H + n0;
-      const float4 v0 = *reinterpret_cast<const float4 *>(src);
-      const float4 v1 = *reinterpret_cast<const float4 *>(src + 4);
-      y[0] += v0.x; y[1] += v0.y; y[2] += v0.z; y[3] += v0.w;
-      y[4] += v1.x; y[5] += v1.y; y[6] += v1.z; y[7] += v1.w;
+  for (int j = 0; j < KM; ++j) {
+    if (j < p.K && pr[j] >= 0) {
+      const float y[8] = {ya[j].x, ya[j].y, ya[j].z, ya[j].w, yb[j].x, yb[j].y, yb[j].z, yb[j].w};
+#pragma unroll
+      for (int c = 0; c < 8; ++c) acc[c] = __builtin_fmaf(w[j], y[c], acc[c]);
     }
-#pragma unroll
-    for (int c = 0; c < 8; ++c) acc[c] = __builtin_fmaf(w, y[c], acc[c]);
   }
   uint4 o;
   o.x = (uint32_t)f32_to_bf16_rne(acc[0]) | ((uint32_t)f32_to_bf16_rne(acc[1]) << 16);
@@ -706,7 +734,12 @@ hipError_t launch_gemm2(const GemmParams &p, int BM, int grid, hipStream_t st) {
 hipError_t launch_finalize(const FinalizeParams &p, hipStream_t st) {
   if (p.T == 0) return hipSuccess;
   dim3 grid(p.T, (p.H + 2047) / 2048);
-  hipLaunchKernelGGL(finalize_kernel, grid, dim3(256), 0, st, p);
+  if (p.K <= 4)
+    hipLaunchKernelGGL(finalize_kernel<4>, grid, dim3(256), 0, st, p);
+  else if (p.K <= 8)
+    hipLaunchKernelGGL(finalize_kernel<8>, grid, dim3(256), 0, st, p);
+  else
+    hipLaunchKernelGGL(finalize_kernel<16>, grid, dim3(256), 0, st, p);
   return hipGetLastError();
 }
 
