@@ -16,7 +16,7 @@
 // TopK tokens returns all of them without scoring (the device reads
 // seq_lens and takes that path itself, no host round trip).
 //
-// Two kernels: dsa_scores_kernel (four threads per token, 16 heads each; the
+// Two kernels: dsa_scores_kernel (4 or 16 threads per token, 16 or 4 heads each; the
 // token's 128 key values live in registers, the 64 query rows in LDS, read as
 // broadcasts) and
 // dsa_select_kernel (one 1024-thread workgroup per sequence: a four-pass
@@ -47,15 +47,18 @@ __device__ __forceinline__ int page_of(const DsaParams &p, int page) {
   return min(max(page, 0), p.num_pages - 1);
 }
 
-// Four threads per token, each the dot products of 16 heads (16 independent
-// chains, interleaved four at a time); the ReLU'd dots go through LDS and the
-// token's first thread runs the head chain in order.  64 tokens per
-// workgroup, so a sequence of a few thousand tokens still spreads over tens
-// of CUs.
-constexpr int kTokPerWG = kScoreThreads / 4;
-constexpr int kHeadsPerThread = kNH / 4;
-
+// TPW tokens per workgroup, 256 / TPW threads per token, each the dot
+// products of its share of the heads (independent chains, interleaved four at
+// a time); the ReLU'd dots go through LDS and the token's first thread runs
+// the head chain in order.  64 tokens per workgroup for batches with long
+// sequences; 16 when the batch is short, so that a sequence of a few
+// thousand tokens still spreads over a hundred CUs and more.  The arithmetic
+// per token is the same either way.
+template <int TPW>
 __global__ __launch_bounds__(kScoreThreads) void dsa_scores_kernel(DsaParams p, int force) {
+  constexpr int kTokPerWG = TPW;
+  constexpr int kHeadsPerThread = kNH / (kScoreThreads / TPW);
+  static_assert(kHeadsPerThread % 4 == 0, "heads in groups of four");
   __shared__ __attribute__((aligned(16))) float q_l[kNH * kD];
   __shared__ float w_l[kNH];
   __shared__ float r_l[kTokPerWG][kNH + 1];
@@ -363,8 +366,15 @@ __global__ __launch_bounds__(kSelThreads) void dsa_select_kernel(DsaParams p) {
 
 hipError_t launch_dsa_scores(const DsaParams &p, int max_len, bool force, hipStream_t st) {
   if (p.B == 0 || max_len == 0) return hipSuccess;
-  dim3 grid((max_len + kTokPerWG - 1) / kTokPerWG, p.B);
-  hipLaunchKernelGGL(dsa_scores_kernel, grid, dim3(kScoreThreads), 0, st, p, force ? 1 : 0);
+  // a batch that would give fewer than two 64-token workgroups per CU takes
+  // 16-token workgroups
+  if ((int64_t)((max_len + 63) / 64) * p.B < 512) {
+    const dim3 grid((max_len + 15) / 16, p.B);
+    hipLaunchKernelGGL(dsa_scores_kernel<16>, grid, dim3(kScoreThreads), 0, st, p, force ? 1 : 0);
+  } else {
+    const dim3 grid((max_len + 63) / 64, p.B);
+    hipLaunchKernelGGL(dsa_scores_kernel<64>, grid, dim3(kScoreThreads), 0, st, p, force ? 1 : 0);
+  }
   return hipGetLastError();
 }
 
