@@ -36,6 +36,7 @@ constexpr int kD = 128;    // head dimension
 constexpr int kScoreThreads = 256;
 constexpr int kSelThreads = 1024;
 constexpr int kSelWaves = kSelThreads / kWave;
+constexpr int kSelPer = 16;  // positions per select thread per chunk
 
 // Device-side inputs are clamped into range (a sequence length into
 // [0, max_pages * PS], a page id into [0, num_pages)), so bad values give
@@ -154,28 +155,49 @@ __device__ __forceinline__ uint32_t score_key(float v) {
   return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
 }
 
-// Block-wide exclusive prefix sum of `v` over the workgroup's threads in
-// order; returns the prefix and writes the total to *total.  Uses one LDS
-// word per wave.
-__device__ __forceinline__ int block_excl_sum(int v, int *wave_sum, int *total) {
+// Inclusive scan over the wave with DPP: a window of four lanes (row_shr 1,
+// 2, 3 of the original values), row_shr 4 and 8 into the upper lanes of each
+// 16-lane row, then row_bcast 15 and 31 across rows.
+template <int kCtrl, int kRows, int kBanks>
+__device__ __forceinline__ int sel_dpp(int v) {
+  return __builtin_amdgcn_update_dpp(0, v, kCtrl, kRows, kBanks, false);
+}
+__device__ __forceinline__ int wave_scan_incl(int v) {
+  int x = v + sel_dpp<0x111, 0xf, 0xf>(v);
+  x += sel_dpp<0x112, 0xf, 0xf>(v);
+  x += sel_dpp<0x113, 0xf, 0xf>(v);
+  x += sel_dpp<0x114, 0xf, 0xe>(x);
+  x += sel_dpp<0x118, 0xf, 0xc>(x);
+  x += sel_dpp<0x142, 0xa, 0xf>(x);
+  x += sel_dpp<0x143, 0xc, 0xf>(x);
+  return x;
+}
+
+// Block-wide exclusive prefix sums of two values over the workgroup's
+// threads in order: the prefixes and the totals.  Every thread must call it.
+__device__ __forceinline__ void block_excl_sum2(int a, int b, int (*wave_sum)[2], int &pa, int &pb,
+                                                int &ta, int &tb) {
   const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
-  int incl = v;  // inclusive scan inside the wave
-#pragma unroll
-  for (int off = 1; off < kWave; off <<= 1) {
-    const int o = __shfl_up(incl, off);
-    incl += (lane >= off) ? o : 0;
-  }
+  const int xa = wave_scan_incl(a), xb = wave_scan_incl(b);
   __syncthreads();  // previous users of wave_sum are done
-  if (lane == kWave - 1) wave_sum[wave] = incl;
-  __syncthreads();
-  int before = 0, all = 0;
-  for (int w = 0; w < kSelWaves; ++w) {
-    const int c = wave_sum[w];
-    before += (w < wave) ? c : 0;
-    all += c;
+  if (lane == kWave - 1) {
+    wave_sum[wave][0] = xa;
+    wave_sum[wave][1] = xb;
   }
-  *total = all;
-  return before + incl - v;
+  __syncthreads();
+  int ba = 0, bb = 0, aa = 0, ab = 0;
+#pragma unroll
+  for (int w = 0; w < kSelWaves; ++w) {
+    const int ca = wave_sum[w][0], cb = wave_sum[w][1];
+    ba += (w < wave) ? ca : 0;
+    bb += (w < wave) ? cb : 0;
+    aa += ca;
+    ab += cb;
+  }
+  pa = ba + xa - a;
+  pb = bb + xb - b;
+  ta = aa;
+  tb = ab;
 }
 
 // One radix-select step, run by one wave: given the 256 bin counts of the
@@ -199,12 +221,8 @@ __device__ __forceinline__ void resolve_bin(const int *bins, int nsub, int strid
     c[i] = s;
   }
   const int mine = c[0] + c[1] + c[2] + c[3];
-  int suffix = mine;  // sum over lanes >= lane
-#pragma unroll
-  for (int off = 1; off < kWave; off <<= 1) {
-    const int o = __shfl_down(suffix, off);
-    suffix += (lane + off < kWave) ? o : 0;
-  }
+  const int incl = wave_scan_incl(mine);
+  const int suffix = __builtin_amdgcn_readlane(incl, kWave - 1) - incl + mine;  // lanes >= lane
   const int above = suffix - mine;  // keys in bins of higher lanes
   const int left = st->left;
   const uint32_t prefix = st->prefix, mask = st->mask;
@@ -283,8 +301,9 @@ __global__ __launch_bounds__(kHistThreads) void dsa_hist_kernel(DsaParams p, int
 // workgroup counts every position itself.
 template <bool GLOBAL>
 __global__ __launch_bounds__(kSelThreads) void dsa_select_kernel(DsaParams p) {
-  __shared__ int hist[kSelWaves][256];
-  __shared__ int wave_cnt[kSelWaves];
+  constexpr int kPer = kSelPer;
+  __shared__ int hist[GLOBAL ? 1 : 2][kSelWaves][256];
+  __shared__ int wave_cnt[kSelWaves][2];
   __shared__ SelState st;
   const int b = blockIdx.x;
   const int L = seq_len_of(p, b);
@@ -300,9 +319,26 @@ __global__ __launch_bounds__(kSelThreads) void dsa_select_kernel(DsaParams p) {
   }
   const float *sc = p.scores + (size_t)b * p.max_len;
 
+  // keys of positions tid * kPer + i (the only chunk when the histograms are
+  // counted here: such batches hold fewer than kSelThreads * kPer tokens);
+  // positions past L get key 0 and are never counted
+  uint32_t kr[kPer];
+  auto load_keys = [&](int j0) {
+#pragma unroll
+    for (int i = 0; i < kPer; ++i) {
+      const int j = j0 + i;
+      kr[i] = j < L ? score_key(sc[j]) : 0u;
+    }
+  };
+  if (!GLOBAL) {
+    load_keys(tid * kPer);
+    for (int i = tid; i < kSelWaves * 256; i += kSelThreads) (&hist[0][0][0])[i] = 0;
+  }
+
   // radix select of the topk-th largest key, 8 bits per pass from the top:
   // `prefix` holds the bits fixed so far (under `mask`), `left` how many of
-  // the keys matching them are still to be taken
+  // the keys matching them are still to be taken.  Local histograms are
+  // double-buffered: the next pass's buffer is cleared while this one counts.
   if (tid == 0) st = SelState{0u, 0u, p.topk};
   __syncthreads();
   for (int pass = 0; pass < 4; ++pass) {
@@ -310,12 +346,15 @@ __global__ __launch_bounds__(kSelThreads) void dsa_select_kernel(DsaParams p) {
     if (GLOBAL) {
       if (wave == 0) resolve_bin(p.hist + ((size_t)pass * p.B + b) * 256, 1, 0, shift, &st);
     } else {
-      for (int i = tid; i < kSelWaves * 256; i += kSelThreads) (&hist[0][0])[i] = 0;
-      __syncthreads();
       const SelState s0 = st;
-      count_keys(sc, 0, L, kSelThreads, s0, shift, hist[wave]);
+      int *h = &hist[pass & 1][wave][0];
+#pragma unroll
+      for (int i = 0; i < kPer; ++i)
+        if (tid * kPer + i < L && (kr[i] & s0.mask) == s0.prefix) atomicAdd(&h[(kr[i] >> shift) & 255u], 1);
+      if (pass < 3)
+        for (int i = tid; i < kSelWaves * 256; i += kSelThreads) (&hist[(pass + 1) & 1][0][0])[i] = 0;
       __syncthreads();
-      if (wave == 0) resolve_bin(&hist[0][0], kSelWaves, 256, shift, &st);
+      if (wave == 0) resolve_bin(&hist[pass & 1][0][0], kSelWaves, 256, shift, &st);
     }
     __syncthreads();
   }
@@ -323,42 +362,54 @@ __global__ __launch_bounds__(kSelThreads) void dsa_select_kernel(DsaParams p) {
   const int need = st.left;         // keys equal to it that are taken
 
   // ordered compaction: position j is taken if its key beats the threshold,
-  // or equals it and fewer than `need` equal keys come before it.  Each
-  // thread owns kPer consecutive positions of a chunk; two block scans per
-  // chunk give the equal-key ranks and the output slots.
-  constexpr int kPer = 16;
-  int eq_before = 0, sel_before = 0;
+  // or equals it and fewer than `need` equal keys come before it; its output
+  // slot is (keys above the threshold before j) + min(equal keys before j,
+  // need), from one block scan of the two counts per chunk
+  int gt_all = 0, eq_all = 0;
   for (int base = 0; base < L; base += kSelThreads * kPer) {
     const int j0 = base + tid * kPer;
-    uint32_t k[kPer];
-    int neq = 0;
-#pragma unroll
-    for (int i = 0; i < kPer; ++i) {
-      const int j = j0 + i;
-      k[i] = j < L ? score_key(sc[j]) : 0u;
-      neq += (j < L && k[i] == thr) ? 1 : 0;
-    }
-    int eq_total, sel_total;
-    int eq_rank = eq_before + block_excl_sum(neq, wave_cnt, &eq_total);
-    uint32_t selm = 0u;
+    if (GLOBAL) load_keys(j0);
+    int ngt = 0, neq = 0;
 #pragma unroll
     for (int i = 0; i < kPer; ++i) {
       const bool in = j0 + i < L;
-      const bool eq = in && k[i] == thr;
-      const bool sel = (in && k[i] > thr) || (eq && eq_rank < need);
-      eq_rank += eq ? 1 : 0;
-      selm |= sel ? (1u << i) : 0u;
+      ngt += (in && kr[i] > thr) ? 1 : 0;
+      neq += (in && kr[i] == thr) ? 1 : 0;
     }
-    int pos = sel_before + block_excl_sum(__popc(selm), wave_cnt, &sel_total);
+    // the cache index of each position: the positions are consecutive, so one
+    // division gives the first (page, slot); with pages of at least kPer
+    // tokens they span at most two pages, whose block-table entries are
+    // loaded ahead of the scan
+    const int q0 = j0 / p.PS, r0 = j0 - q0 * p.PS;
+    const bool two_pages = p.PS >= kPer;
+    int pg0 = 0, pg1 = 0;
+    if (two_pages) {
+      pg0 = page_of(p, bt[min(q0, p.max_pages - 1)]);
+      pg1 = page_of(p, bt[min(q0 + 1, p.max_pages - 1)]);
+    }
+    int gtb, eqb, gt_total, eq_total;
+    block_excl_sum2(ngt, neq, wave_cnt, gtb, eqb, gt_total, eq_total);
+    gtb += gt_all;
+    eqb += eq_all;
+    int q = q0, r = r0;
 #pragma unroll
     for (int i = 0; i < kPer; ++i) {
-      if (selm & (1u << i)) {
-        const int j = j0 + i;
-        out[pos++] = page_of(p, bt[j / p.PS]) * p.PS + j % p.PS;
+      const bool in = j0 + i < L;
+      const bool gt = in && kr[i] > thr;
+      const bool eq = in && kr[i] == thr;
+      if (gt || (eq && eqb < need)) {
+        const int page = two_pages ? (q == q0 ? pg0 : pg1) : page_of(p, bt[min(q, p.max_pages - 1)]);
+        out[gtb + min(eqb, need)] = page * p.PS + r;
+      }
+      gtb += gt ? 1 : 0;
+      eqb += eq ? 1 : 0;
+      if (++r == p.PS) {
+        r = 0;
+        ++q;
       }
     }
-    eq_before += eq_total;
-    sel_before += sel_total;
+    gt_all += gt_total;
+    eq_all += eq_total;
   }
 }
 
@@ -383,9 +434,13 @@ hipError_t launch_dsa_scores(const DsaParams &p, int max_len, bool force, hipStr
 constexpr int kWideSelectLen = 16384;
 constexpr int kWideTokensPerWG = 2048;
 
+// the select kernel holds a whole sequence's keys in registers below this length
+static_assert(kSelThreads * kSelPer >= kWideSelectLen, "local select covers every shorter sequence");
+
 hipError_t launch_dsa_select(const DsaParams &p, hipStream_t st) {
   if (p.B == 0) return hipSuccess;
-  if (p.max_len >= kWideSelectLen && p.hist) {
+  if (p.max_len >= kWideSelectLen && !p.hist) return hipErrorInvalidValue;  // needs the histograms
+  if (p.max_len >= kWideSelectLen) {
     const dim3 grid((p.max_len + kWideTokensPerWG - 1) / kWideTokensPerWG, p.B);
     for (int pass = 0; pass < 4; ++pass)
       hipLaunchKernelGGL(dsa_hist_kernel, grid, dim3(kHistThreads), 0, st, p, pass);

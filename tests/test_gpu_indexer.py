@@ -60,6 +60,19 @@ def test_dsa_topk_exact(M, name, seed):
         assert (got[b] == ref[b]).all(), f"b={b} (seq_len {cfg.seq_lens[b]}): {(got[b] != ref[b]).sum()} differ"
 
 
+@pytest.mark.parametrize("ps", [8, 16, 1])
+def test_dsa_topk_page_sizes(M, ps):
+    """Pages smaller than, equal to and far below a select thread's 16
+    consecutive positions (several pages per thread), against the oracle."""
+    cfg = W.IndexerConfig(f"ps{ps}", (700, 300, 2000, 5000), page_size=ps, topk=512)
+    log(f"dsa topk page size {ps}")
+    x = W.generate_indexer(cfg, 6, device="cuda")
+    got = M.dsa_topk_indexer(*_dev(x), topk=cfg.topk).cpu().numpy()
+    ref = oracle.dsa_topk(*_host(x), cfg.topk)
+    for b in range(cfg.B):
+        assert (got[b] == ref[b]).all(), f"b={b}: {(got[b] != ref[b]).sum()} differ"
+
+
 def test_dsa_topk_ties(M):
     """Keys and queries from a handful of values with equal weights: many exactly
     equal scores straddle the TopK threshold, and the lower positions must win."""
