@@ -35,8 +35,8 @@ constexpr int kNH = 64;    // query heads
 constexpr int kD = 128;    // head dimension
 constexpr int kScoreThreads = 256;
 constexpr int kSelThreads = 1024;
-constexpr int kSelWaves = kSelThreads / kWave;
 constexpr int kSelPer = 16;  // positions per select thread per chunk
+constexpr int kSmallSelThreads = 256;  // select workgroup for block tables of at most 4,096 tokens
 
 // Device-side inputs are clamped into range (a sequence length into
 // [0, max_pages * PS], a page id into [0, num_pages)), so bad values give
@@ -175,6 +175,7 @@ __device__ __forceinline__ int wave_scan_incl(int v) {
 
 // Block-wide exclusive prefix sums of two values over the workgroup's
 // threads in order: the prefixes and the totals.  Every thread must call it.
+template <int NW>
 __device__ __forceinline__ void block_excl_sum2(int a, int b, int (*wave_sum)[2], int &pa, int &pb,
                                                 int &ta, int &tb) {
   const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
@@ -187,7 +188,7 @@ __device__ __forceinline__ void block_excl_sum2(int a, int b, int (*wave_sum)[2]
   __syncthreads();
   int ba = 0, bb = 0, aa = 0, ab = 0;
 #pragma unroll
-  for (int w = 0; w < kSelWaves; ++w) {
+  for (int w = 0; w < NW; ++w) {
     const int ca = wave_sum[w][0], cb = wave_sum[w][1];
     ba += (w < wave) ? ca : 0;
     bb += (w < wave) ? cb : 0;
@@ -299,11 +300,12 @@ __global__ __launch_bounds__(kHistThreads) void dsa_hist_kernel(DsaParams p, int
 
 // GLOBAL: the four histograms come from dsa_hist_kernel; otherwise this
 // workgroup counts every position itself.
-template <bool GLOBAL>
-__global__ __launch_bounds__(kSelThreads) void dsa_select_kernel(DsaParams p) {
+template <bool GLOBAL, int NT>
+__global__ __launch_bounds__(NT) void dsa_select_kernel(DsaParams p) {
   constexpr int kPer = kSelPer;
-  __shared__ int hist[GLOBAL ? 1 : 2][kSelWaves][256];
-  __shared__ int wave_cnt[kSelWaves][2];
+  constexpr int NW = NT / kWave;
+  __shared__ int hist[GLOBAL ? 1 : 2][NW][256];
+  __shared__ int wave_cnt[NW][2];
   __shared__ SelState st;
   const int b = blockIdx.x;
   const int L = seq_len_of(p, b);
@@ -313,14 +315,14 @@ __global__ __launch_bounds__(kSelThreads) void dsa_select_kernel(DsaParams p) {
   const int32_t *bt = p.block_table + (size_t)b * p.max_pages;
 
   if (L <= p.topk) {  // every token, in position order, then -1
-    for (int i = tid; i < p.topk; i += kSelThreads)
+    for (int i = tid; i < p.topk; i += NT)
       out[i] = i < L ? page_of(p, bt[i / p.PS]) * p.PS + i % p.PS : -1;
     return;
   }
   const float *sc = p.scores + (size_t)b * p.max_len;
 
   // keys of positions tid * kPer + i (the only chunk when the histograms are
-  // counted here: such batches hold fewer than kSelThreads * kPer tokens);
+  // counted here: such batches hold fewer than NT * kPer tokens);
   // positions past L get key 0 and are never counted
   uint32_t kr[kPer];
   auto load_keys = [&](int j0) {
@@ -332,7 +334,7 @@ __global__ __launch_bounds__(kSelThreads) void dsa_select_kernel(DsaParams p) {
   };
   if (!GLOBAL) {
     load_keys(tid * kPer);
-    for (int i = tid; i < kSelWaves * 256; i += kSelThreads) (&hist[0][0][0])[i] = 0;
+    for (int i = tid; i < NW * 256; i += NT) (&hist[0][0][0])[i] = 0;
   }
 
   // radix select of the topk-th largest key, 8 bits per pass from the top:
@@ -352,9 +354,9 @@ __global__ __launch_bounds__(kSelThreads) void dsa_select_kernel(DsaParams p) {
       for (int i = 0; i < kPer; ++i)
         if (tid * kPer + i < L && (kr[i] & s0.mask) == s0.prefix) atomicAdd(&h[(kr[i] >> shift) & 255u], 1);
       if (pass < 3)
-        for (int i = tid; i < kSelWaves * 256; i += kSelThreads) (&hist[(pass + 1) & 1][0][0])[i] = 0;
+        for (int i = tid; i < NW * 256; i += NT) (&hist[(pass + 1) & 1][0][0])[i] = 0;
       __syncthreads();
-      if (wave == 0) resolve_bin(&hist[pass & 1][0][0], kSelWaves, 256, shift, &st);
+      if (wave == 0) resolve_bin(&hist[pass & 1][0][0], NW, 256, shift, &st);
     }
     __syncthreads();
   }
@@ -366,7 +368,7 @@ __global__ __launch_bounds__(kSelThreads) void dsa_select_kernel(DsaParams p) {
   // slot is (keys above the threshold before j) + min(equal keys before j,
   // need), from one block scan of the two counts per chunk
   int gt_all = 0, eq_all = 0;
-  for (int base = 0; base < L; base += kSelThreads * kPer) {
+  for (int base = 0; base < L; base += NT * kPer) {
     const int j0 = base + tid * kPer;
     if (GLOBAL) load_keys(j0);
     int ngt = 0, neq = 0;
@@ -388,7 +390,7 @@ __global__ __launch_bounds__(kSelThreads) void dsa_select_kernel(DsaParams p) {
       pg1 = page_of(p, bt[min(q0 + 1, p.max_pages - 1)]);
     }
     int gtb, eqb, gt_total, eq_total;
-    block_excl_sum2(ngt, neq, wave_cnt, gtb, eqb, gt_total, eq_total);
+    block_excl_sum2<NW>(ngt, neq, wave_cnt, gtb, eqb, gt_total, eq_total);
     gtb += gt_all;
     eqb += eq_all;
     int q = q0, r = r0;
@@ -444,9 +446,11 @@ hipError_t launch_dsa_select(const DsaParams &p, hipStream_t st) {
     const dim3 grid((p.max_len + kWideTokensPerWG - 1) / kWideTokensPerWG, p.B);
     for (int pass = 0; pass < 4; ++pass)
       hipLaunchKernelGGL(dsa_hist_kernel, grid, dim3(kHistThreads), 0, st, p, pass);
-    hipLaunchKernelGGL(dsa_select_kernel<true>, dim3(p.B), dim3(kSelThreads), 0, st, p);
+    hipLaunchKernelGGL((dsa_select_kernel<true, kSelThreads>), dim3(p.B), dim3(kSelThreads), 0, st, p);
+  } else if (p.max_len <= kSmallSelThreads * kSelPer) {  // a short block table: 4 waves hold it all
+    hipLaunchKernelGGL((dsa_select_kernel<false, kSmallSelThreads>), dim3(p.B), dim3(kSmallSelThreads), 0, st, p);
   } else {
-    hipLaunchKernelGGL(dsa_select_kernel<false>, dim3(p.B), dim3(kSelThreads), 0, st, p);
+    hipLaunchKernelGGL((dsa_select_kernel<false, kSelThreads>), dim3(p.B), dim3(kSelThreads), 0, st, p);
   }
   return hipGetLastError();
 }
