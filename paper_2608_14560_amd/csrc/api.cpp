@@ -59,6 +59,7 @@ moe_status_t check_shape(const moe_shape_t *s) {
 struct Plan {
   int BM, S1, S2, NB1, NB2, nchunks, max_tiles;
   bool narrow1;  // GEMM1 split over 32-column groups (small batches)
+  bool gu1;      // ... and over gate and up rows (the fewest rows per expert)
   bool tile;     // large-tile kernels (BM >= 64)
   int64_t P_max;
   size_t off_ids, off_w, off_offsets, off_perm_token, off_perm_pair, off_pair_row, off_chunk_counts,
@@ -82,7 +83,11 @@ Plan make_plan(const moe_shape_t *s) {
   // 16-row tiles: GEMM1 split over 32-column groups, so that a batch with few
   // rows per expert still gives every CU work items (it streams weights)
   p.narrow1 = p.BM == 16;
-  p.NB1 = p.narrow1 ? s->I / gemm1_narrow_cols() : s->I / 128;
+  // at most ~2 rows per expert (decode): 16-column items with the gate and up
+  // rows on separate waves, twice the streaming waves; above that the doubled
+  // re-reads of each activation tile cost more than the waves gain (measured)
+  p.gu1 = p.narrow1 && avg <= 2.0;
+  p.NB1 = p.narrow1 ? s->I / gemm1_narrow_cols(p.gu1) : s->I / 128;
   // GEMM2 column blocks: 128 wide for the small-tile kernel, 256 otherwise
   p.NB2 = p.BM == 16 ? s->H / 128 : (s->H + 255) / 256;
   p.nchunks = (int)((s->T + kChunkTokens - 1) / kChunkTokens);
@@ -275,7 +280,7 @@ moe_status_t fused_impl(const moe_shape_t *s, const uint8_t *hidden, const float
   mark();
   const int grid1 = round8((int64_t)pl.max_tiles * pl.NB1 * pl.S1);
   if (pl.narrow1)
-    MOE_TRY_HIP(launch_gemm1_narrow(g1, grid1, st));
+    MOE_TRY_HIP(launch_gemm1_narrow(g1, grid1, pl.gu1, st));
   else if (pl.tile)
     MOE_TRY_HIP(launch_gemm_tile(g1, true, pl.BM, grid1, st));
   else

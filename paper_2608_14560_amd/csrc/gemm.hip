@@ -434,16 +434,19 @@ __global__ __launch_bounds__(kStreamWaves * kWave) void gemm2_stream_kernel(Gemm
 // codes).  2 waves: wave w streams the gate rows [32j + 16w, +16) and the
 // matching up rows against one A fragment (the tile's 16 gathered rows), two
 // MFMAs per 128-K step with a D-stage register prefetch ring (unconditional,
-// so loads stay in flight); SwiGLU pairs then sit in the same lane.  The
+// so loads stay in flight); SwiGLU pairs then sit in the same lane.
+// GU (the fewest rows per expert): items of 16 columns, wave 0 the gate rows
+// and wave 1 the up rows, so twice as many waves stream (the chip's streaming
+// rate needs many waves per CU); the up half meets the gate half in LDS.  The
 // SwiGLU output goes to a_buf [P, I] fp32 and requant_kernel (the next launch)
 // re-quantises it: no cross-workgroup synchronisation.  Values and codes are
 // bit-identical to the single-item epilogue.
-constexpr int kNarrowCols = 32;
-constexpr int kNarrowWaves = kNarrowCols / 16;
+constexpr int kNarrowWaves = 2;
 
-template <int D>
+template <int D, bool GU>
 __global__ __launch_bounds__(kNarrowWaves * kWave) void gemm1_narrow_kernel(GemmParams p) {
   constexpr int NT = kNarrowWaves * kWave;
+  constexpr int kCols = GU ? 16 : 32;  // intermediate columns per item
   __shared__ int tb[1028];
   extern __shared__ __attribute__((aligned(16))) float scales[];  // sa[16][KB], sb[2][KB]
 
@@ -473,7 +476,7 @@ __global__ __launch_bounds__(kNarrowWaves * kWave) void gemm1_narrow_kernel(Gemm
   const int local = item - tb[e] * X;
   const int mt_idx = local % nt_e;
   const int j = local / nt_e;          // 32-column group
-  const int blk = j * kNarrowCols / 128;  // its 128-column block
+  const int blk = j * kCols / 128;  // its 128-column block
   const int seg0 = p.expert_offsets[e];
   const int seg1 = p.expert_offsets[e + 1];
   const int row0 = seg0 + mt_idx * 16;
@@ -497,7 +500,62 @@ __global__ __launch_bounds__(kNarrowWaves * kWave) void gemm1_narrow_kernel(Gemm
     }
   }
 
-  const int col = j * kNarrowCols + 16 * wave + r16;  // this lane's weight row (gate)
+  if (GU) {
+    // wave 0 streams the 16 gate rows, wave 1 the matching 16 up rows; the up
+    // accumulators meet the gate ones in LDS for the SwiGLU
+    __shared__ float up_l[4][kWave];
+    const int col = j * kCols + r16;
+    const int asrc = p.perm_token[row0 + min(r16, nrows - 1)];
+    const uint8_t *a_ptr = p.A + (size_t)asrc * K + frag_off;
+    const uint8_t *b_ptr = p.B + (size_t)e * p.N_total * K + ((size_t)col + (wave ? p.I : 0)) * K + frag_off;
+    const float *sbw = sb_l + (wave ? KB : 0);
+
+    v8i ra[D], rb[D];
+#pragma unroll
+    for (int d = 0; d < D; ++d) {
+      const size_t o = (size_t)min(d, KB - 1) * 128;
+      ra[d] = *reinterpret_cast<const v8i *>(a_ptr + o);
+      rb[d] = *reinterpret_cast<const v8i *>(b_ptr + o);
+    }
+    __syncthreads();  // scales staged
+
+    v4f acc = {0.f, 0.f, 0.f, 0.f};
+    const int srow = 4 * (lane >> 4);
+    for (int base = 0; base < KB; base += D) {
+#pragma unroll
+      for (int d = 0; d < D; ++d) {
+        const int kb = base + d;
+        if (kb < KB) {
+          const v4f z = {0.f, 0.f, 0.f, 0.f};
+          const v4f t = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(ra[d], rb[d], z, 0, 0, 0, 0, 0, 0);
+          const float sw = sbw[kb];
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const float sa = sa_l[(srow + i) * KB + kb];
+            acc[i] = __builtin_fmaf(t[i], sa * sw, acc[i]);
+          }
+        }
+        const size_t o = (size_t)min(kb + D, KB - 1) * 128;
+        ra[d] = *reinterpret_cast<const v8i *>(a_ptr + o);
+        rb[d] = *reinterpret_cast<const v8i *>(b_ptr + o);
+      }
+    }
+    if (wave == 1) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) up_l[i][lane] = acc[i];
+    }
+    __syncthreads();
+    if (wave == 0) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int r = srow + i;
+        if (r < nrows) p.abuf[(size_t)(row0 + r) * p.I + col] = swiglu_spec(acc[i], up_l[i][lane]);
+      }
+    }
+    return;
+  }
+
+  const int col = j * kCols + 16 * wave + r16;  // this lane's weight row (gate)
   const int asrc = p.perm_token[row0 + min(r16, nrows - 1)];
   const uint8_t *a_ptr = p.A + (size_t)asrc * K + frag_off;
   const uint8_t *bg_ptr = p.B + (size_t)e * p.N_total * K + (size_t)col * K + frag_off;
@@ -708,13 +766,16 @@ hipError_t launch_gemm1(const GemmParams &p, int BM, int grid, hipStream_t st) {
   if (grid <= 0) return hipSuccess;
   return BM == 32 ? launch_gemm_bm<32, true>(p, grid, st) : hipErrorInvalidValue;
 }
-hipError_t launch_gemm1_narrow(const GemmParams &p, int grid, hipStream_t st) {
+hipError_t launch_gemm1_narrow(const GemmParams &p, int grid, bool gate_up_split, hipStream_t st) {
   if (grid <= 0) return hipSuccess;
   const size_t lds = sizeof(float) * 18 * (size_t)p.KB;
-  hipLaunchKernelGGL(gemm1_narrow_kernel<kStreamDepth>, dim3(grid), dim3(kNarrowWaves * kWave), lds, st, p);
+  if (gate_up_split)
+    hipLaunchKernelGGL((gemm1_narrow_kernel<kStreamDepth, true>), dim3(grid), dim3(kNarrowWaves * kWave), lds, st, p);
+  else
+    hipLaunchKernelGGL((gemm1_narrow_kernel<kStreamDepth, false>), dim3(grid), dim3(kNarrowWaves * kWave), lds, st, p);
   return hipGetLastError();
 }
-int gemm1_narrow_cols() { return kNarrowCols; }
+int gemm1_narrow_cols(bool gate_up_split) { return gate_up_split ? 16 : 32; }
 hipError_t launch_requant(const GemmParams &p, int P_max, hipStream_t st) {
   const int pairs = P_max * (p.I / 128);
   if (pairs <= 0) return hipSuccess;

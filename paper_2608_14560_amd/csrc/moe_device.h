@@ -223,8 +223,8 @@ bool dsa_wide_select(int max_len);
 hipError_t launch_router_logits(const RouteParams &p, float *logits, hipStream_t st);
 hipError_t launch_permute(const PermuteParams &p, hipStream_t st);
 hipError_t launch_gemm1(const GemmParams &p, int BM, int grid, hipStream_t st);
-hipError_t launch_gemm1_narrow(const GemmParams &p, int grid, hipStream_t st);
-int gemm1_narrow_cols();
+hipError_t launch_gemm1_narrow(const GemmParams &p, int grid, bool gate_up_split, hipStream_t st);
+int gemm1_narrow_cols(bool gate_up_split);
 hipError_t launch_requant(const GemmParams &p, int P_max, hipStream_t st);
 hipError_t launch_gemm2(const GemmParams &p, int BM, int grid, hipStream_t st);
 // large-tile GEMM1 / GEMM2 (BM = 64 or 128 rows x 256 columns, full K per item)
