@@ -284,11 +284,12 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(GemmParams p) {
 // round trip and no barrier in the K loop.  Prefetches are issued
 // unconditionally (past the end they re-read the last K block) so the
 // compiler can keep D loads in flight instead of draining the queue at every
-// branch.  4 waves; wave w owns output columns [32w, 32w+32) of a 128-wide
-// block.  Activation and weight block scales of the whole K range are staged
-// in LDS once.  The per-element arithmetic (MFMA block products, promotion
+// branch.  8 waves; wave w owns output columns [16w, 16w+16) of a 128-wide
+// block (one weight fragment per step: more waves stream at once, which is
+// what the chip's streaming rate needs).  Activation and weight block scales
+// of the whole K range are staged in LDS once.  The per-element arithmetic (MFMA block products, promotion
 // order) is the same as the other GEMM kernels'.
-constexpr int kStreamWaves = 4;
+constexpr int kStreamWaves = 8;
 
 // ALDS: the item's whole A tile (16 rows x its K range) is staged in LDS once
 // (rows padded by 16 bytes) instead of every wave loading it from L2 at each
@@ -337,9 +338,8 @@ __global__ __launch_bounds__(kStreamWaves * kWave) void gemm2_stream_kernel(Gemm
   const size_t K = (size_t)p.K;
   const int KB = p.KB;
 
-  // B rows of the wave's two sub-tiles (one 128-row scale block)
-  const int brow0 = nb * 128 + 32 * wave + r16;
-  const int brow1 = brow0 + 16;
+  // B rows of the wave's sub-tile (inside one 128-row scale block)
+  const int brow0 = nb * 128 + 16 * wave + r16;
 
   // stage the scales: sa[r][kb] of the tile's rows, sb[0/1][kb] of the blocks
   float *sa_l = scales;
@@ -361,7 +361,6 @@ __global__ __launch_bounds__(kStreamWaves * kWave) void gemm2_stream_kernel(Gemm
   const uint8_t *a_ptr = p.A + (size_t)asrc * K + frag_off;
   const uint8_t *Bexp = p.B + (size_t)e * p.N_total * K;
   const uint8_t *b_ptr0 = Bexp + (size_t)brow0 * K + frag_off;
-  const uint8_t *b_ptr1 = Bexp + (size_t)brow1 * K + frag_off;
 
   // A tile in LDS: row r, K step kb -> a_l + r * astride + (kb - kb0) * 128
   uint8_t *a_l = reinterpret_cast<uint8_t *>(scales) + ((18 * KB * 4 + 15) & ~15);
@@ -378,19 +377,18 @@ __global__ __launch_bounds__(kStreamWaves * kWave) void gemm2_stream_kernel(Gemm
   }
   const uint8_t *a_lds = a_l + r16 * astride + frag_off;
 
-  v8i ra[D], rb0[D], rb1[D];
+  v8i ra[D], rb0[D];
 #define MOE_SLOAD(d, kb)                                                  \
   do {                                                                    \
     if (!ALDS) ra[d] = *reinterpret_cast<const v8i *>(a_ptr + (size_t)(kb) * 128); \
     rb0[d] = *reinterpret_cast<const v8i *>(b_ptr0 + (size_t)(kb) * 128); \
-    rb1[d] = *reinterpret_cast<const v8i *>(b_ptr1 + (size_t)(kb) * 128); \
   } while (0)
 
 #pragma unroll
   for (int d = 0; d < D; ++d) MOE_SLOAD(d, kb0 + min(d, n - 1));
   __syncthreads();  // scales staged
 
-  v4f acc0 = {0.f, 0.f, 0.f, 0.f}, acc1 = {0.f, 0.f, 0.f, 0.f};
+  v4f acc0 = {0.f, 0.f, 0.f, 0.f};
   const int srow = 4 * (lane >> 4);
   for (int base = 0; base < n; base += D) {
 #pragma unroll
@@ -401,13 +399,11 @@ __global__ __launch_bounds__(kStreamWaves * kWave) void gemm2_stream_kernel(Gemm
         const v4f z = {0.f, 0.f, 0.f, 0.f};
         const v8i af = ALDS ? lds_frag(a_lds + it * 128) : ra[d];
         const v4f t0 = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(af, rb0[d], z, 0, 0, 0, 0, 0, 0);
-        const v4f t1 = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(af, rb1[d], z, 0, 0, 0, 0, 0, 0);
         const float s0 = sb_l[kb];
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
           const float sa = sa_l[(srow + i) * KB + kb];
           acc0[i] = __builtin_fmaf(t0[i], sa * s0, acc0[i]);
-          acc1[i] = __builtin_fmaf(t1[i], sa * s0, acc1[i]);
         }
       }
       MOE_SLOAD(d, kb0 + min(it + D, n - 1));
@@ -420,9 +416,8 @@ __global__ __launch_bounds__(kStreamWaves * kWave) void gemm2_stream_kernel(Gemm
   for (int i = 0; i < 4; ++i) {
     const int r = srow + i;
     if (r < nrows) {
-      float *yrow = Ys + (size_t)(row0 + r) * p.H + nb * 128 + 32 * wave + r16;
+      float *yrow = Ys + (size_t)(row0 + r) * p.H + nb * 128 + 16 * wave + r16;
       yrow[0] = acc0[i];
-      yrow[16] = acc1[i];
     }
   }
 }
