@@ -31,6 +31,7 @@ import ctypes
 import hashlib
 import json
 import os
+import re
 import sys
 import time
 
@@ -90,15 +91,23 @@ GEMM_SOURCES = ("api.cpp", "gemm.hip", "gemm_tile.hip", "moe_device.h", "permute
                 "scatter_device.h")
 
 
+def _code_only(text: str) -> str:
+    """Source text without comments and without blank-line or spacing
+    differences: what the digest of the GEMM kernels covers."""
+    text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
+    text = re.sub(r"//[^\n]*", "", text)
+    return "\n".join(" ".join(line.split()) for line in text.splitlines() if line.strip())
+
+
 def source_digest() -> str:
-    """Digest of the GEMM kernel sources: a traffic measurement is reported
-    only while it matches."""
+    """Digest of the GEMM kernel sources (their code, comments aside): a
+    traffic measurement is reported only while it matches."""
     h = hashlib.sha256()
     d = os.path.join(ROOT, "paper_2608_14560_amd", "csrc")
     for f in GEMM_SOURCES:
-        with open(os.path.join(d, f), "rb") as fh:
+        with open(os.path.join(d, f), encoding="utf-8") as fh:
             h.update(f.encode())
-            h.update(fh.read())
+            h.update(_code_only(fh.read()).encode())
     return h.hexdigest()[:16]
 
 

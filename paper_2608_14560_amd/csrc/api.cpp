@@ -58,7 +58,7 @@ moe_status_t check_shape(const moe_shape_t *s) {
 // Host-side plan: tile shape, split factors, grid bounds and the workspace map.
 struct Plan {
   int BM, S1, S2, NB1, NB2, nchunks, max_tiles;
-  bool narrow1;  // GEMM1 split over 32-column groups (small batches)
+  bool narrow1;  // GEMM1 split over 32- (or 16-) column groups (small batches)
   bool gu1;      // ... and over gate and up rows (the fewest rows per expert)
   bool tile;     // large-tile kernels (BM >= 64)
   int64_t P_max;
@@ -80,7 +80,7 @@ Plan make_plan(const moe_shape_t *s) {
   // combine then reads one plane.
   p.S1 = 1;
   p.S2 = 1;
-  // 16-row tiles: GEMM1 split over 32-column groups, so that a batch with few
+  // 16-row tiles: GEMM1 split over column groups, so that a batch with few
   // rows per expert still gives every CU work items (it streams weights)
   p.narrow1 = p.BM == 16;
   // at most ~2 rows per expert (decode): 16-column items with the gate and up

@@ -470,7 +470,7 @@ __global__ __launch_bounds__(kNarrowWaves * kWave) void gemm1_narrow_kernel(Gemm
   const int nt_e = tb[e + 1] - tb[e];
   const int local = item - tb[e] * X;
   const int mt_idx = local % nt_e;
-  const int j = local / nt_e;          // 32-column group
+  const int j = local / nt_e;       // kCols-column group
   const int blk = j * kCols / 128;  // its 128-column block
   const int seg0 = p.expert_offsets[e];
   const int seg1 = p.expert_offsets[e + 1];

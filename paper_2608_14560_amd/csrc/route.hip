@@ -1,7 +1,8 @@
 // route.hip -- stage (1) of the Fused MoE block (paper Section 3.1.1):
 // sigmoid routing scores, group-limited top-k expert selection and the
-// normalised, scaled routing weights.  One wave64 per token; all selections
-// are butterfly reductions over the wave.
+// normalised, scaled routing weights.  One wave64 per token: the group
+// scores by DPP reductions over the wave, the top-k by a bounded rank through
+// LDS (or a ballot radix select); no block barrier.
 //
 // Built with -ffp-contract=off: the fp32 sequence below is a specification
 // (its integer decisions must be reproducible bit for bit), so no
