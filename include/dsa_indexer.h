@@ -37,7 +37,9 @@ typedef struct {
 } dsa_shape_t;
 
 /* Bytes of device workspace dsa_topk_indexer needs for `s` (the scores of
- * every sequence at its longest possible length); 0 for an invalid shape. */
+ * every sequence at its longest possible length; for block tables of 16,384
+ * tokens or more also the long-sequence select's radix histograms, per-slice
+ * counts and final states); 0 for an invalid shape. */
 size_t dsa_workspace_size(const dsa_shape_t *s);
 
 /* The indexer (Section 3.1.3).

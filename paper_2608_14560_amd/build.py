@@ -33,6 +33,7 @@ SOURCES = {
     "gemm.hip": [],
     "gemm_tile.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"],
     "api.cpp": ["-x", "hip"],
+    "dsa_api.cpp": ["-x", "hip"],
     "attention.hip": [],
     "attention_api.cpp": ["-x", "hip"],
 }

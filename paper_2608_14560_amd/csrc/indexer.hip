@@ -298,13 +298,66 @@ __global__ __launch_bounds__(kHistThreads) void dsa_hist_kernel(DsaParams p, int
   }
 }
 
-// GLOBAL: the four histograms come from dsa_hist_kernel; otherwise this
-// workgroup counts every position itself.
-template <bool GLOBAL, int NT>
+// Ordered compaction of a run of kPer consecutive positions per thread
+// (thread t: j0 .. j0 + kPer - 1): position j is taken if its key beats the
+// threshold, or equals it and fewer than `need` equal keys come before it; its
+// output slot is (keys above the threshold before j) + min(equal keys before
+// j, need), from one block scan of the two counts, plus the counts of the
+// positions before the workgroup's run (gt_before, eq_before).  Every thread
+// of the workgroup must call it (it contains barriers).
+template <int NW, int kPer>
+__device__ __forceinline__ void compact_slice(const DsaParams &p, int L, int j0, uint32_t thr, int need,
+                                              int gt_before, int eq_before, const uint32_t (&kr)[kPer],
+                                              int (*wave_cnt)[2], int32_t *out, const int32_t *bt) {
+  int ngt = 0, neq = 0;
+#pragma unroll
+  for (int i = 0; i < kPer; ++i) {
+    const bool in = j0 + i < L;
+    ngt += (in && kr[i] > thr) ? 1 : 0;
+    neq += (in && kr[i] == thr) ? 1 : 0;
+  }
+  // the cache index of each position: the positions are consecutive, so one
+  // division gives the first (page, slot); with pages of at least kPer tokens
+  // they span at most two pages, whose block-table entries are loaded ahead of
+  // the scan
+  const int q0 = j0 / p.PS, r0 = j0 - q0 * p.PS;
+  const bool two_pages = p.PS >= kPer;
+  int pg0 = 0, pg1 = 0;
+  if (two_pages) {
+    pg0 = page_of(p, bt[min(q0, p.max_pages - 1)]);
+    pg1 = page_of(p, bt[min(q0 + 1, p.max_pages - 1)]);
+  }
+  int gtb, eqb, gt_total, eq_total;
+  block_excl_sum2<NW>(ngt, neq, wave_cnt, gtb, eqb, gt_total, eq_total);
+  gtb += gt_before;
+  eqb += eq_before;
+  int q = q0, r = r0;
+#pragma unroll
+  for (int i = 0; i < kPer; ++i) {
+    const bool in = j0 + i < L;
+    const bool gt = in && kr[i] > thr;
+    const bool eq = in && kr[i] == thr;
+    if (gt || (eq && eqb < need)) {
+      const int page = two_pages ? (q == q0 ? pg0 : pg1) : page_of(p, bt[min(q, p.max_pages - 1)]);
+      out[gtb + min(eqb, need)] = page * p.PS + r;
+    }
+    gtb += gt ? 1 : 0;
+    eqb += eq ? 1 : 0;
+    if (++r == p.PS) {
+      r = 0;
+      ++q;
+    }
+  }
+}
+
+// One workgroup per sequence of a batch whose block table holds fewer than
+// kWideSelectLen tokens: the four radix passes over keys held in registers,
+// then the ordered compaction.
+template <int NT>
 __global__ __launch_bounds__(NT) void dsa_select_kernel(DsaParams p) {
   constexpr int kPer = kSelPer;
   constexpr int NW = NT / kWave;
-  __shared__ int hist[GLOBAL ? 1 : 2][NW][256];
+  __shared__ int hist[2][NW][256];
   __shared__ int wave_cnt[NW][2];
   __shared__ SelState st;
   const int b = blockIdx.x;
@@ -321,9 +374,8 @@ __global__ __launch_bounds__(NT) void dsa_select_kernel(DsaParams p) {
   }
   const float *sc = p.scores + (size_t)b * p.max_len;
 
-  // keys of positions tid * kPer + i (the only chunk when the histograms are
-  // counted here: such batches hold fewer than NT * kPer tokens);
-  // positions past L get key 0 and are never counted
+  // keys of positions tid * kPer + i (one chunk: such batches hold fewer than
+  // NT * kPer tokens); positions past L get key 0 and are never counted
   uint32_t kr[kPer];
   auto load_keys = [&](int j0) {
 #pragma unroll
@@ -332,10 +384,8 @@ __global__ __launch_bounds__(NT) void dsa_select_kernel(DsaParams p) {
       kr[i] = j < L ? score_key(sc[j]) : 0u;
     }
   };
-  if (!GLOBAL) {
-    load_keys(tid * kPer);
-    for (int i = tid; i < NW * 256; i += NT) (&hist[0][0][0])[i] = 0;
-  }
+  load_keys(tid * kPer);
+  for (int i = tid; i < NW * 256; i += NT) (&hist[0][0][0])[i] = 0;
 
   // radix select of the topk-th largest key, 8 bits per pass from the top:
   // `prefix` holds the bits fixed so far (under `mask`), `left` how many of
@@ -345,19 +395,15 @@ __global__ __launch_bounds__(NT) void dsa_select_kernel(DsaParams p) {
   __syncthreads();
   for (int pass = 0; pass < 4; ++pass) {
     const int shift = 24 - 8 * pass;
-    if (GLOBAL) {
-      if (wave == 0) resolve_bin(p.hist + ((size_t)pass * p.B + b) * 256, 1, 0, shift, &st);
-    } else {
-      const SelState s0 = st;
-      int *h = &hist[pass & 1][wave][0];
+    const SelState s0 = st;
+    int *h = &hist[pass & 1][wave][0];
 #pragma unroll
-      for (int i = 0; i < kPer; ++i)
-        if (tid * kPer + i < L && (kr[i] & s0.mask) == s0.prefix) atomicAdd(&h[(kr[i] >> shift) & 255u], 1);
-      if (pass < 3)
-        for (int i = tid; i < NW * 256; i += NT) (&hist[(pass + 1) & 1][0][0])[i] = 0;
-      __syncthreads();
-      if (wave == 0) resolve_bin(&hist[pass & 1][0][0], NW, 256, shift, &st);
-    }
+    for (int i = 0; i < kPer; ++i)
+      if (tid * kPer + i < L && (kr[i] & s0.mask) == s0.prefix) atomicAdd(&h[(kr[i] >> shift) & 255u], 1);
+    if (pass < 3)
+      for (int i = tid; i < NW * 256; i += NT) (&hist[(pass + 1) & 1][0][0])[i] = 0;
+    __syncthreads();
+    if (wave == 0) resolve_bin(&hist[pass & 1][0][0], NW, 256, shift, &st);
     __syncthreads();
   }
   const uint32_t thr = st.prefix;   // the topk-th largest key
@@ -366,53 +412,105 @@ __global__ __launch_bounds__(NT) void dsa_select_kernel(DsaParams p) {
   // ordered compaction: position j is taken if its key beats the threshold,
   // or equals it and fewer than `need` equal keys come before it; its output
   // slot is (keys above the threshold before j) + min(equal keys before j,
-  // need), from one block scan of the two counts per chunk
-  int gt_all = 0, eq_all = 0;
-  for (int base = 0; base < L; base += NT * kPer) {
-    const int j0 = base + tid * kPer;
-    if (GLOBAL) load_keys(j0);
-    int ngt = 0, neq = 0;
-#pragma unroll
-    for (int i = 0; i < kPer; ++i) {
-      const bool in = j0 + i < L;
-      ngt += (in && kr[i] > thr) ? 1 : 0;
-      neq += (in && kr[i] == thr) ? 1 : 0;
-    }
-    // the cache index of each position: the positions are consecutive, so one
-    // division gives the first (page, slot); with pages of at least kPer
-    // tokens they span at most two pages, whose block-table entries are
-    // loaded ahead of the scan
-    const int q0 = j0 / p.PS, r0 = j0 - q0 * p.PS;
-    const bool two_pages = p.PS >= kPer;
-    int pg0 = 0, pg1 = 0;
-    if (two_pages) {
-      pg0 = page_of(p, bt[min(q0, p.max_pages - 1)]);
-      pg1 = page_of(p, bt[min(q0 + 1, p.max_pages - 1)]);
-    }
-    int gtb, eqb, gt_total, eq_total;
-    block_excl_sum2<NW>(ngt, neq, wave_cnt, gtb, eqb, gt_total, eq_total);
-    gtb += gt_all;
-    eqb += eq_all;
-    int q = q0, r = r0;
-#pragma unroll
-    for (int i = 0; i < kPer; ++i) {
-      const bool in = j0 + i < L;
-      const bool gt = in && kr[i] > thr;
-      const bool eq = in && kr[i] == thr;
-      if (gt || (eq && eqb < need)) {
-        const int page = two_pages ? (q == q0 ? pg0 : pg1) : page_of(p, bt[min(q, p.max_pages - 1)]);
-        out[gtb + min(eqb, need)] = page * p.PS + r;
-      }
-      gtb += gt ? 1 : 0;
-      eqb += eq ? 1 : 0;
-      if (++r == p.PS) {
-        r = 0;
-        ++q;
-      }
-    }
-    gt_all += gt_total;
-    eq_all += eq_total;
+  // need), from one block scan of the two counts
+  compact_slice<NW, kPer>(p, L, tid * kPer, thr, need, 0, 0, kr, wave_cnt, out, bt);
+}
+
+// Long sequences after the four histogram passes: the radix state replayed
+// from the global histograms, then the positions in slices of kSlice, one
+// workgroup each.  dsa_count_kernel counts each slice's keys above and equal
+// to the threshold (slice 0 also stores the final state); dsa_compact_kernel
+// sums the counts of the slices before its own and compacts its slice.  The
+// counts [B, slices, 2] and the states [B, 2] follow the histograms in the
+// workspace.
+constexpr int kSlice = 2048;
+constexpr int kSliceThreads = 256;
+constexpr int kSlicePer = kSlice / kSliceThreads;
+constexpr int kSliceWaves = kSliceThreads / kWave;
+
+__device__ __forceinline__ int *slice_counts(const DsaParams &p, int b) {
+  const int ns = (p.max_len + kSlice - 1) / kSlice;
+  return p.hist + (size_t)4 * p.B * 256 + (size_t)b * ns * 2;
+}
+__device__ __forceinline__ int *slice_state(const DsaParams &p, int b) {
+  const int ns = (p.max_len + kSlice - 1) / kSlice;
+  return p.hist + (size_t)4 * p.B * 256 + (size_t)p.B * ns * 2 + (size_t)b * 2;
+}
+
+__global__ __launch_bounds__(kSliceThreads) void dsa_count_kernel(DsaParams p) {
+  __shared__ SelState st;
+  __shared__ int wave_cnt[kSliceWaves][2];
+  const int b = blockIdx.y, s = blockIdx.x, tid = threadIdx.x;
+  const int L = seq_len_of(p, b);
+  const int j_begin = s * kSlice;
+  if (L <= p.topk || j_begin >= L) return;  // whole workgroup
+  if (tid == 0) st = SelState{0u, 0u, p.topk};
+  __syncthreads();
+  for (int q = 0; q < 4; ++q) {
+    if (tid < kWave) resolve_bin(p.hist + ((size_t)q * p.B + b) * 256, 1, 0, 24 - 8 * q, &st);
+    __syncthreads();
   }
+  const uint32_t thr = st.prefix;
+  const float *sc = p.scores + (size_t)b * p.max_len;
+  const int j0 = j_begin + tid * kSlicePer;
+  int ngt = 0, neq = 0;
+#pragma unroll
+  for (int i = 0; i < kSlicePer; ++i) {
+    const int j = j0 + i;
+    const uint32_t k = j < L ? score_key(sc[j]) : 0u;
+    ngt += (j < L && k > thr) ? 1 : 0;
+    neq += (j < L && k == thr) ? 1 : 0;
+  }
+  int pa, pb, tg, te;
+  block_excl_sum2<kSliceWaves>(ngt, neq, wave_cnt, pa, pb, tg, te);
+  if (tid == 0) {
+    int *cnt = slice_counts(p, b) + (size_t)s * 2;
+    cnt[0] = tg;
+    cnt[1] = te;
+    if (s == 0) {
+      int *state = slice_state(p, b);
+      state[0] = (int)thr;
+      state[1] = st.left;
+    }
+  }
+}
+
+__global__ __launch_bounds__(kSliceThreads) void dsa_compact_kernel(DsaParams p) {
+  __shared__ int wave_cnt[kSliceWaves][2];
+  const int b = blockIdx.y, s = blockIdx.x, tid = threadIdx.x;
+  const int L = seq_len_of(p, b);
+  int32_t *out = p.out + (size_t)b * p.topk;
+  const int32_t *bt = p.block_table + (size_t)b * p.max_pages;
+  if (L <= p.topk) {  // every token, in position order, then -1
+    for (int i = tid; i < kSlice; i += kSliceThreads) {
+      const int pos = s * kSlice + i;
+      if (pos < p.topk) out[pos] = pos < L ? page_of(p, bt[pos / p.PS]) * p.PS + pos % p.PS : -1;
+    }
+    return;
+  }
+  const int j_begin = s * kSlice;
+  if (j_begin >= L) return;  // whole workgroup
+  const int *state = slice_state(p, b);
+  const uint32_t thr = (uint32_t)state[0];
+  const int need = state[1];
+  // the keys above and equal to the threshold in the slices before this one
+  const int *cnt = slice_counts(p, b);
+  int g = 0, e = 0;
+  for (int t = tid; t < s; t += kSliceThreads) {
+    g += cnt[(size_t)t * 2];
+    e += cnt[(size_t)t * 2 + 1];
+  }
+  int pa, pb, gt_before, eq_before;
+  block_excl_sum2<kSliceWaves>(g, e, wave_cnt, pa, pb, gt_before, eq_before);
+  const float *sc = p.scores + (size_t)b * p.max_len;
+  const int j0 = j_begin + tid * kSlicePer;
+  uint32_t kr[kSlicePer];
+#pragma unroll
+  for (int i = 0; i < kSlicePer; ++i) {
+    const int j = j0 + i;
+    kr[i] = j < L ? score_key(sc[j]) : 0u;
+  }
+  compact_slice<kSliceWaves, kSlicePer>(p, L, j0, thr, need, gt_before, eq_before, kr, wave_cnt, out, bt);
 }
 
 }  // namespace
@@ -443,18 +541,28 @@ hipError_t launch_dsa_select(const DsaParams &p, hipStream_t st) {
   if (p.B == 0) return hipSuccess;
   if (p.max_len >= kWideSelectLen && !p.hist) return hipErrorInvalidValue;  // needs the histograms
   if (p.max_len >= kWideSelectLen) {
-    const dim3 grid((p.max_len + kWideTokensPerWG - 1) / kWideTokensPerWG, p.B);
+    static_assert(kWideTokensPerWG == kSlice, "histogram and compaction slices agree");
+    const dim3 grid((p.max_len + kSlice - 1) / kSlice, p.B);
     for (int pass = 0; pass < 4; ++pass)
       hipLaunchKernelGGL(dsa_hist_kernel, grid, dim3(kHistThreads), 0, st, p, pass);
-    hipLaunchKernelGGL((dsa_select_kernel<true, kSelThreads>), dim3(p.B), dim3(kSelThreads), 0, st, p);
+    hipLaunchKernelGGL(dsa_count_kernel, grid, dim3(kSliceThreads), 0, st, p);
+    const dim3 cgrid((max(p.max_len, p.topk) + kSlice - 1) / kSlice, p.B);
+    hipLaunchKernelGGL(dsa_compact_kernel, cgrid, dim3(kSliceThreads), 0, st, p);
   } else if (p.max_len <= kSmallSelThreads * kSelPer) {  // a short block table: 4 waves hold it all
-    hipLaunchKernelGGL((dsa_select_kernel<false, kSmallSelThreads>), dim3(p.B), dim3(kSmallSelThreads), 0, st, p);
+    hipLaunchKernelGGL(dsa_select_kernel<kSmallSelThreads>, dim3(p.B), dim3(kSmallSelThreads), 0, st, p);
   } else {
-    hipLaunchKernelGGL((dsa_select_kernel<false, kSelThreads>), dim3(p.B), dim3(kSelThreads), 0, st, p);
+    hipLaunchKernelGGL(dsa_select_kernel<kSelThreads>, dim3(p.B), dim3(kSelThreads), 0, st, p);
   }
   return hipGetLastError();
 }
 
 bool dsa_wide_select(int max_len) { return max_len >= kWideSelectLen; }
+
+// ints of the long-sequence select's global state: the four radix histograms
+// [4, B, 256], the slice counts [B, slices, 2] and the final states [B, 2]
+size_t dsa_wide_ints(int B, int max_len) {
+  const size_t ns = (size_t)(max_len + kSlice - 1) / kSlice;
+  return (size_t)4 * 256 * B + (size_t)B * ns * 2 + (size_t)B * 2;
+}
 
 }  // namespace moe

@@ -73,10 +73,14 @@ def test_dsa_topk_page_sizes(M, ps):
         assert (got[b] == ref[b]).all(), f"b={b}: {(got[b] != ref[b]).sum()} differ"
 
 
-def test_dsa_topk_ties(M):
+@pytest.mark.parametrize("cfg", [W.IndexerConfig("ties", (3000, 5000, 300), topk=512),
+                                 # block tables of 16,384+ tokens: the slice-parallel compaction,
+                                 # equal keys spread over many 2,048-position slices
+                                 W.IndexerConfig("ties_wide", (20000, 17000, 300), topk=4096)],
+                         ids=lambda c: c.name)
+def test_dsa_topk_ties(M, cfg):
     """Keys and queries from a handful of values with equal weights: many exactly
     equal scores straddle the TopK threshold, and the lower positions must win."""
-    cfg = W.IndexerConfig("ties", (3000, 5000, 300), topk=512)
     x = W.generate_indexer(cfg, 2, device="cuda")
     g = torch.Generator(device="cpu").manual_seed(3)
     bits = lambda shape: torch.randint(0, 2, shape, generator=g).float().to(torch.float8_e4m3fn).view(torch.uint8)
@@ -93,6 +97,16 @@ def test_dsa_topk_ties(M):
     log(f"ties: {(sc == thr).sum()} scores equal the threshold score")
     assert (sc == thr).sum() > 10
     ref = oracle.dsa_topk(*h, cfg.topk)
+    assert (got == ref).all()
+
+
+def test_dsa_topk_above_every_length_wide(M):
+    """A block table of 16,384 tokens with TopK above every sequence length: every
+    token in position order, then -1 up to TopK (past the block table's length)."""
+    cfg = W.IndexerConfig("wide_short", (16384, 9000, 100, 0), topk=20000)
+    x = W.generate_indexer(cfg, 8, device="cuda")
+    got = M.dsa_topk_indexer(*_dev(x), topk=cfg.topk).cpu().numpy()
+    ref = oracle.dsa_topk(*_host(x), cfg.topk)
     assert (got == ref).all()
 
 
