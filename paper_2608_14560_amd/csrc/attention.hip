@@ -37,6 +37,9 @@ namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef short v4s __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) v4s lds_v4s;
+typedef __attribute__((address_space(3))) uint8_t lds_u8;
 
 constexpr int kThreads = 256;
 constexpr int kD = kAttnDC + kAttnDP;          // 576 bf16 per gathered row
@@ -168,21 +171,26 @@ __global__ __launch_bounds__(kThreads) void attn_partial_kernel(AttnParams p) {
   f32x4 oacc[8];
 #pragma unroll
   for (int nt = 0; nt < 8; ++nt) oacc[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
-  const uint16_t *k16 = reinterpret_cast<const uint16_t *>(k_l);
+  // the Kc^T operand (8 consecutive entries of one column per lane) by the
+  // transposing LDS read: within each 16-lane group, lane s addresses row
+  // e0 + s / 4, columns 4 (s % 4) .. + 3 of the tile, and lane i receives rows
+  // e0 .. e0 + 3 of column i; two reads give the 8 entries
+  lds_u8 *kl3 = (lds_u8 *)smem;  // k_l, as an LDS address
 #pragma unroll
   for (int ks = 0; ks < 2; ++ks) {
     const u32x4 pb = *reinterpret_cast<const u32x4 *>(p_l + n * kPStride + ks * 32 + g * 8);
-    const int eb = ks * 32 + g * 8;
+    const int e0 = ks * 32 + g * 8 + (n >> 2);
 #pragma unroll
     for (int nt = 0; nt < 8; ++nt) {
-      const int col = wave * 128 + nt * 16 + n;
+      const int c0 = wave * 128 + nt * 16 + 4 * (n & 3);
+      lds_u8 *a = kl3 + e0 * kRowStride + c0 * 2;
+      const v4s lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4s *)a);
+      const v4s hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4s *)(a + 4 * kRowStride));
       u32x4 ka;
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const uint32_t lo = k16[(eb + 2 * q) * (kRowStride / 2) + col];
-        const uint32_t hi = k16[(eb + 2 * q + 1) * (kRowStride / 2) + col];
-        ka[q] = lo | (hi << 16);
-      }
+      ka[0] = (uint32_t)(uint16_t)lo[0] | ((uint32_t)(uint16_t)lo[1] << 16);
+      ka[1] = (uint32_t)(uint16_t)lo[2] | ((uint32_t)(uint16_t)lo[3] << 16);
+      ka[2] = (uint32_t)(uint16_t)hi[0] | ((uint32_t)(uint16_t)hi[1] << 16);
+      ka[3] = (uint32_t)(uint16_t)hi[2] | ((uint32_t)(uint16_t)hi[3] << 16);
       oacc[nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(ka), as_bf16x8(pb), oacc[nt], 0, 0, 0);
     }
   }
