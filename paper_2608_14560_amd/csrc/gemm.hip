@@ -426,21 +426,21 @@ __global__ __launch_bounds__(kStreamWaves * kWave) void gemm2_stream_kernel(Gemm
 // M-tile and 32 intermediate columns, so a handful of resident experts still
 // yields several work items per CU (HBM streaming needs all 256 CUs busy;
 // splitting K instead would change the promotion order that decides the FP8
-// codes).  2 waves: wave w streams the gate rows [32j + 16w, +16) and the
-// matching up rows against one A fragment (the tile's 16 gathered rows), two
-// MFMAs per 128-K step with a D-stage register prefetch ring (unconditional,
-// so loads stay in flight); SwiGLU pairs then sit in the same lane.
+// codes).  One wave streams the gate and up rows of both 16-column halves of
+// the item against one A fragment (the tile's 16 gathered rows): four MFMAs
+// per 128-K step with a D-stage register prefetch ring (unconditional, so
+// loads stay in flight); SwiGLU pairs then sit in the same lane.  Four weight
+// fragments per A fragment (fewer A loads per weight byte) measured faster
+// than two waves of two fragments each.
 // GU (the fewest rows per expert): items of 16 columns, wave 0 the gate rows
 // and wave 1 the up rows, so twice as many waves stream (the chip's streaming
 // rate needs many waves per CU); the up half meets the gate half in LDS.  The
 // SwiGLU output goes to a_buf [P, I] fp32 and requant_kernel (the next launch)
 // re-quantises it: no cross-workgroup synchronisation.  Values and codes are
 // bit-identical to the single-item epilogue.
-constexpr int kNarrowWaves = 2;
-
 template <int D, bool GU>
-__global__ __launch_bounds__(kNarrowWaves * kWave) void gemm1_narrow_kernel(GemmParams p) {
-  constexpr int NT = kNarrowWaves * kWave;
+__global__ __launch_bounds__((GU ? 2 : 1) * kWave) void gemm1_narrow_kernel(GemmParams p) {
+  constexpr int NT = (GU ? 2 : 1) * kWave;
   constexpr int kCols = GU ? 16 : 32;  // intermediate columns per item
   __shared__ int tb[1028];
   extern __shared__ __attribute__((aligned(16))) float scales[];  // sa[16][KB], sb[2][KB]
@@ -550,23 +550,30 @@ __global__ __launch_bounds__(kNarrowWaves * kWave) void gemm1_narrow_kernel(Gemm
     return;
   }
 
-  const int col = j * kCols + 16 * wave + r16;  // this lane's weight row (gate)
+  // one wave, the item's two 16-column sub-tiles: four weight fragments (gate
+  // and up of each) against one A fragment per K step
+  const int col0 = j * kCols + r16, col1 = col0 + 16;
   const int asrc = p.perm_token[row0 + min(r16, nrows - 1)];
   const uint8_t *a_ptr = p.A + (size_t)asrc * K + frag_off;
-  const uint8_t *bg_ptr = p.B + (size_t)e * p.N_total * K + (size_t)col * K + frag_off;
-  const uint8_t *bu_ptr = bg_ptr + (size_t)p.I * K;
+  const uint8_t *bexp = p.B + (size_t)e * p.N_total * K;
+  const uint8_t *g0 = bexp + (size_t)col0 * K + frag_off;
+  const uint8_t *g1 = bexp + (size_t)col1 * K + frag_off;
+  const uint8_t *u0 = g0 + (size_t)p.I * K;
+  const uint8_t *u1 = g1 + (size_t)p.I * K;
 
-  v8i ra[D], rg[D], ru[D];
+  v8i ra[D], rg0[D], rg1[D], ru0[D], ru1[D];
 #pragma unroll
   for (int d = 0; d < D; ++d) {
-    const int kb = min(d, KB - 1);
-    ra[d] = *reinterpret_cast<const v8i *>(a_ptr + (size_t)kb * 128);
-    rg[d] = *reinterpret_cast<const v8i *>(bg_ptr + (size_t)kb * 128);
-    ru[d] = *reinterpret_cast<const v8i *>(bu_ptr + (size_t)kb * 128);
+    const size_t o = (size_t)min(d, KB - 1) * 128;
+    ra[d] = *reinterpret_cast<const v8i *>(a_ptr + o);
+    rg0[d] = *reinterpret_cast<const v8i *>(g0 + o);
+    rg1[d] = *reinterpret_cast<const v8i *>(g1 + o);
+    ru0[d] = *reinterpret_cast<const v8i *>(u0 + o);
+    ru1[d] = *reinterpret_cast<const v8i *>(u1 + o);
   }
   __syncthreads();  // scales staged
 
-  v4f accg = {0.f, 0.f, 0.f, 0.f}, accu = {0.f, 0.f, 0.f, 0.f};
+  v4f ag0 = {0.f, 0.f, 0.f, 0.f}, ag1 = ag0, au0 = ag0, au1 = ag0;
   const int srow = 4 * (lane >> 4);
   for (int base = 0; base < KB; base += D) {
 #pragma unroll
@@ -574,28 +581,35 @@ __global__ __launch_bounds__(kNarrowWaves * kWave) void gemm1_narrow_kernel(Gemm
       const int kb = base + d;
       if (kb < KB) {
         const v4f z = {0.f, 0.f, 0.f, 0.f};
-        const v4f tg = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(ra[d], rg[d], z, 0, 0, 0, 0, 0, 0);
-        const v4f tu = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(ra[d], ru[d], z, 0, 0, 0, 0, 0, 0);
+        const v4f tg0 = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(ra[d], rg0[d], z, 0, 0, 0, 0, 0, 0);
+        const v4f tg1 = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(ra[d], rg1[d], z, 0, 0, 0, 0, 0, 0);
+        const v4f tu0 = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(ra[d], ru0[d], z, 0, 0, 0, 0, 0, 0);
+        const v4f tu1 = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(ra[d], ru1[d], z, 0, 0, 0, 0, 0, 0);
         const float sg = sb_l[kb], su = sb_l[KB + kb];
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
           const float sa = sa_l[(srow + i) * KB + kb];
-          accg[i] = __builtin_fmaf(tg[i], sa * sg, accg[i]);
-          accu[i] = __builtin_fmaf(tu[i], sa * su, accu[i]);
+          ag0[i] = __builtin_fmaf(tg0[i], sa * sg, ag0[i]);
+          ag1[i] = __builtin_fmaf(tg1[i], sa * sg, ag1[i]);
+          au0[i] = __builtin_fmaf(tu0[i], sa * su, au0[i]);
+          au1[i] = __builtin_fmaf(tu1[i], sa * su, au1[i]);
         }
       }
-      const int nk = min(kb + D, KB - 1);
-      ra[d] = *reinterpret_cast<const v8i *>(a_ptr + (size_t)nk * 128);
-      rg[d] = *reinterpret_cast<const v8i *>(bg_ptr + (size_t)nk * 128);
-      ru[d] = *reinterpret_cast<const v8i *>(bu_ptr + (size_t)nk * 128);
+      const size_t o = (size_t)min(kb + D, KB - 1) * 128;
+      ra[d] = *reinterpret_cast<const v8i *>(a_ptr + o);
+      rg0[d] = *reinterpret_cast<const v8i *>(g0 + o);
+      rg1[d] = *reinterpret_cast<const v8i *>(g1 + o);
+      ru0[d] = *reinterpret_cast<const v8i *>(u0 + o);
+      ru1[d] = *reinterpret_cast<const v8i *>(u1 + o);
     }
   }
-
-  // accumulator element i of this lane: row srow + i, column `col`
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     const int r = srow + i;
-    if (r < nrows) p.abuf[(size_t)(row0 + r) * p.I + col] = swiglu_spec(accg[i], accu[i]);
+    if (r < nrows) {
+      p.abuf[(size_t)(row0 + r) * p.I + col0] = swiglu_spec(ag0[i], au0[i]);
+      p.abuf[(size_t)(row0 + r) * p.I + col1] = swiglu_spec(ag1[i], au1[i]);
+    }
   }
 }
 
@@ -765,9 +779,9 @@ hipError_t launch_gemm1_narrow(const GemmParams &p, int grid, bool gate_up_split
   if (grid <= 0) return hipSuccess;
   const size_t lds = sizeof(float) * 18 * (size_t)p.KB;
   if (gate_up_split)
-    hipLaunchKernelGGL((gemm1_narrow_kernel<kStreamDepth, true>), dim3(grid), dim3(kNarrowWaves * kWave), lds, st, p);
+    hipLaunchKernelGGL((gemm1_narrow_kernel<kStreamDepth, true>), dim3(grid), dim3(2 * kWave), lds, st, p);
   else
-    hipLaunchKernelGGL((gemm1_narrow_kernel<kStreamDepth, false>), dim3(grid), dim3(kNarrowWaves * kWave), lds, st, p);
+    hipLaunchKernelGGL((gemm1_narrow_kernel<kStreamDepth, false>), dim3(grid), dim3(kWave), lds, st, p);
   return hipGetLastError();
 }
 int gemm1_narrow_cols(bool gate_up_split) { return gate_up_split ? 16 : 32; }
