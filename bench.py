@@ -387,7 +387,7 @@ def main():
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
-        print("bench.py: this build runs on one GPU only (no multi-GPU path); use --gpus 1",
+        print("bench.py: the library runs on one GPU (it has no multi-GPU path); use --gpus 1",
               file=sys.stderr)
         sys.exit(2)
     if not torch.cuda.is_available():
@@ -513,7 +513,7 @@ def main():
     traffic = read_traffic(cfg.name)
     roof["traffic"] = traffic
 
-    cold = None
+    cold = cold_p10 = cold_p90 = None
     if args.cold:
         flush = torch.empty(512 << 20, dtype=torch.uint8, device=dev)
         times = []
@@ -527,6 +527,7 @@ def main():
             torch.cuda.synchronize()
             times.append(e0.elapsed_time(e1))
         cold = round(float(np.median(times)) * 1e3, 2)
+        cold_p10, cold_p90 = (round(float(np.percentile(times, q)) * 1e3, 2) for q in (10, 90))
 
     router = indexer = attention = None
     if not args.layer_only:
@@ -561,6 +562,9 @@ def main():
         "pct_fp8_mfma_peak": round(100 * tflops / FP8_PEAK_TFLOPS, 4),
         "gbps": round(gbs, 1),
         "pct_hbm_peak": round(100 * gbs / HBM_PEAK_GBS, 2),
+        # the layer against its binding roof: max(t_MFMA, t_HBM) / t
+        "binding_roof": "mfma" if tflops / FP8_PEAK_TFLOPS > gbs / HBM_PEAK_GBS else "hbm",
+        "pct_binding_roofline": round(100 * max(tflops / FP8_PEAK_TFLOPS, gbs / HBM_PEAK_GBS), 2),
         "stage_us": {n: round(float(v) * 1e3, 2) for n, v in zip(names, stage_avg)},
         "roofline": roof,
         "cpu_baseline": cpu,
@@ -568,6 +572,8 @@ def main():
         "dsa_topk_indexer": indexer,
         "dsa_sparse_attention": attention,
         "us_per_call_cold": cold,
+        "us_per_call_cold_p10": cold_p10,
+        "us_per_call_cold_p90": cold_p90,
         "host_enqueue_us_per_call": round(host_ms * 1e3 / K, 1),
         "prefill_covered_enqueue": bool(enq_ms < 2.0 * host_ms + 2.0),
         "host_wall_s": round(wall, 3),

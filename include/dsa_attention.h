@@ -26,7 +26,7 @@
 extern "C" {
 #endif
 
-/* Problem shape.  Limits of this build: num_heads a positive multiple of 16;
+/* Problem shape.  Limits of this library: num_heads a positive multiple of 16;
  * 1 <= topk <= 65536; num_rows >= 1; sm_scale finite. */
 typedef struct {
   int32_t T;          /* query tokens                                      */

@@ -24,7 +24,7 @@
 extern "C" {
 #endif
 
-/* Problem shape.  Limits of this build: num_heads 64, head_dim 128 (the
+/* Problem shape.  Limits of this library: num_heads 64, head_dim 128 (the
  * paper's operator); page_size >= 1; 1 <= topk <= 65536; B >= 0. */
 typedef struct {
   int32_t B;          /* batch elements (sequences)                      */

@@ -39,7 +39,7 @@ extern "C" {
 typedef enum {
   MOE_OK = 0,
   MOE_ERR_INVALID_ARG = 1,         /* bad shape, null or misaligned pointer */
-  MOE_ERR_UNSUPPORTED = 2,         /* valid but outside this build's limits */
+  MOE_ERR_UNSUPPORTED = 2,         /* valid but outside the library's limits */
   MOE_ERR_WORKSPACE_TOO_SMALL = 3, /* ws_bytes < moe_workspace_size()        */
   MOE_ERR_HIP = 4                  /* a HIP runtime call or launch failed    */
 } moe_status_t;
@@ -48,7 +48,7 @@ typedef enum {
  * experts [local_expert_offset, local_expert_offset + E_l) have their weights
  * on this GPU; a (token, expert) pair whose expert is elsewhere contributes
  * zero to this GPU's output but still counts in the weight normalisation.
- * Limits of this build: H, I multiples of 128; 2 <= E_g/n_group;
+ * Limits of this library: H, I multiples of 128; 2 <= E_g/n_group;
  * E_g <= 1024; E_l <= 1024; top_k <= 16; T * top_k < 2^31. */
 typedef struct {
   int32_t T;                     /* tokens (0 allowed: no-op)              */

@@ -46,7 +46,7 @@ moe_status_t check_shape(const moe_shape_t *s) {
       (int64_t)s->local_expert_offset + s->num_local_experts > s->num_experts)
     return MOE_ERR_INVALID_ARG;
   if (!std::isfinite(s->routed_scaling_factor)) return MOE_ERR_INVALID_ARG;
-  // limits of this build
+  // limits of this library
   if (s->num_experts > 1024 || s->num_local_experts > 1024 || s->n_group > 64 || s->top_k > 16)
     return MOE_ERR_UNSUPPORTED;
   if ((int64_t)s->T * s->top_k >= (int64_t)1 << 31) return MOE_ERR_UNSUPPORTED;
