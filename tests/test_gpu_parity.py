@@ -124,7 +124,8 @@ def test_mfma_block_rule(M, kind):
 # ------------------------------------------------------------ routing
 ROUTE_CASES = [("tiny", 0), ("tiny", 1), ("small_ragged", 0), ("small_dense", 0), ("small_g6", 0), ("small_many", 0),
                ("small_many", 3), ("decode", 0), ("decode", 1), ("decode", 2), ("mid", 0), ("mid", 1),
-               ("small_t64", 0), ("small_t128", 0), ("small_t256", 0), ("prefill", 0), ("skewed", 0)]
+               ("small_t64", 0), ("small_t128", 0), ("small_t256", 0), ("prefill", 0), ("skewed", 0),
+               ("median", 0), ("long", 0)]
 
 
 @pytest.mark.parametrize("name,seed", ROUTE_CASES)
@@ -175,7 +176,7 @@ def test_route_ties_bitexact(M):
 # ------------------------------------------------------------ whole layer
 FULL_CASES = [("tiny", 0), ("small_ragged", 0), ("small_ragged", 1), ("small_dense", 0), ("small_g6", 0),
               ("small_many", 0), ("small_t64", 0), ("small_t64", 1), ("small_t128", 0), ("small_t128", 2), ("small_t256", 0),
-              ("decode", 0), ("decode", 1), ("mid", 0)]
+              ("decode", 0), ("decode", 1), ("mid", 0), ("median", 0)]
 
 
 @pytest.mark.parametrize("name,seed", FULL_CASES)
@@ -207,7 +208,7 @@ def _sample_tokens(cfg, ref, n, seed=0):
     return np.array(sorted(toks), np.int32)
 
 
-@pytest.mark.parametrize("name,n", [("prefill", 40), ("skewed", 16)])
+@pytest.mark.parametrize("name,n", [("prefill", 40), ("skewed", 16), ("long", 24)])
 def test_fused_sampled_parity(M, name, n):
     cfg = W.CONFIGS[name]
     log(f"fused {name}: generating")

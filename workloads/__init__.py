@@ -68,6 +68,10 @@ CONFIGS: dict[str, MoEConfig] = {
     "prefill": _ds_v3("prefill", 4096),
     # all 256 experts resident, 16 hot experts
     "skewed": _ds_v3("skewed", 8192, num_local_experts=256, hot_experts=16),
+    # context points at the paper's regime representatives: its median regime
+    # (T = 64) and its longest workload (T = 14,107), same recipe as decode
+    "median": _ds_v3("median", 64),
+    "long": _ds_v3("long", 14107),
 }
 
 # Extra parity shapes: several tiles plus ragged tails, still fast on the CPU.
