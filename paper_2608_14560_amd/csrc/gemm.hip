@@ -338,8 +338,15 @@ __global__ __launch_bounds__(kStreamWaves * kWave) void gemm2_stream_kernel(Gemm
   const size_t K = (size_t)p.K;
   const int KB = p.KB;
 
-  // B rows of the wave's sub-tile (inside one 128-row scale block)
+  // B rows of the wave's sub-tile (inside one 128-row scale block).  They
+  // depend on the expert and column block only: the first D weight loads go
+  // out before the item's rows, scales and activation tile are looked up.
   const int brow0 = nb * 128 + 16 * wave + r16;
+  const uint8_t *Bexp = p.B + (size_t)e * p.N_total * K;
+  const uint8_t *b_ptr0 = Bexp + (size_t)brow0 * K + frag_off;
+  v8i ra[D], rb0[D];
+#pragma unroll
+  for (int d = 0; d < D; ++d) rb0[d] = *reinterpret_cast<const v8i *>(b_ptr0 + (size_t)(kb0 + min(d, n - 1)) * 128);
 
   // stage the scales: sa[r][kb] of the tile's rows, sb[0/1][kb] of the blocks
   float *sa_l = scales;
@@ -359,8 +366,6 @@ __global__ __launch_bounds__(kStreamWaves * kWave) void gemm2_stream_kernel(Gemm
   const int arow = min(r16, nrows - 1);
   const int asrc = row0 + arow;
   const uint8_t *a_ptr = p.A + (size_t)asrc * K + frag_off;
-  const uint8_t *Bexp = p.B + (size_t)e * p.N_total * K;
-  const uint8_t *b_ptr0 = Bexp + (size_t)brow0 * K + frag_off;
 
   // A tile in LDS: row r, K step kb -> a_l + r * astride + (kb - kb0) * 128
   uint8_t *a_l = reinterpret_cast<uint8_t *>(scales) + ((18 * KB * 4 + 15) & ~15);
@@ -377,15 +382,16 @@ __global__ __launch_bounds__(kStreamWaves * kWave) void gemm2_stream_kernel(Gemm
   }
   const uint8_t *a_lds = a_l + r16 * astride + frag_off;
 
-  v8i ra[D], rb0[D];
 #define MOE_SLOAD(d, kb)                                                  \
   do {                                                                    \
     if (!ALDS) ra[d] = *reinterpret_cast<const v8i *>(a_ptr + (size_t)(kb) * 128); \
     rb0[d] = *reinterpret_cast<const v8i *>(b_ptr0 + (size_t)(kb) * 128); \
   } while (0)
 
+  if (!ALDS) {
 #pragma unroll
-  for (int d = 0; d < D; ++d) MOE_SLOAD(d, kb0 + min(d, n - 1));
+    for (int d = 0; d < D; ++d) ra[d] = *reinterpret_cast<const v8i *>(a_ptr + (size_t)(kb0 + min(d, n - 1)) * 128);
+  }
   __syncthreads();  // scales staged
 
   v4f acc0 = {0.f, 0.f, 0.f, 0.f};
