@@ -55,12 +55,21 @@ __device__ __forceinline__ int page_of(const DsaParams &p, int page) {
 // sequences; 16 when the batch is short, so that a sequence of a few
 // thousand tokens still spreads over a hundred CUs and more.  The arithmetic
 // per token is the same either way.
+typedef float v2f __attribute__((ext_vector_type(2)));
+
 template <int TPW>
 __global__ __launch_bounds__(kScoreThreads) void dsa_scores_kernel(DsaParams p, int force) {
   constexpr int kTokPerWG = TPW;
   constexpr int kHeadsPerThread = kNH / (kScoreThreads / TPW);
   static_assert(kHeadsPerThread % 4 == 0, "heads in groups of four");
-  __shared__ __attribute__((aligned(16))) float q_l[kNH * kD];
+  // 16-token workgroups: a wave spans 16 head groups, so its query reads are
+  // not broadcasts and LDS bandwidth bounds the loop: the query stays in e4m3
+  // codes there (a quarter of the bytes), decoded exactly where it is used.
+  // 64-token workgroups: a wave is one head group (broadcast reads) and the
+  // loop is bound by the fused multiply-adds: the query is decoded once.
+  constexpr bool kCodes = TPW < kWave;
+  __shared__ __attribute__((aligned(16))) uint8_t q_c[kCodes ? kNH * kD : 16];
+  __shared__ __attribute__((aligned(16))) float q_l[kCodes ? 4 : kNH * kD];
   __shared__ float w_l[kNH];
   __shared__ float r_l[kTokPerWG][kNH + 1];
   const int b = blockIdx.y;
@@ -75,23 +84,29 @@ __global__ __launch_bounds__(kScoreThreads) void dsa_scores_kernel(DsaParams p, 
   const int tl = tid & (kTokPerWG - 1);  // token of the workgroup
   const int qq = tid / kTokPerWG;        // head quarter
 
-  // the query's 64 x 128 codes, decoded exactly to fp32 (32 per thread)
+  // the query's 64 x 128 codes (32 per thread), as codes or decoded exactly
+  // to fp32
   {
     const uint8_t *qb = p.q + (size_t)b * kNH * kD;
     const u32x4 a = *reinterpret_cast<const u32x4 *>(qb + tid * 32);
     const u32x4 c = *reinterpret_cast<const u32x4 *>(qb + tid * 32 + 16);
-    float *dst = &q_l[tid * 32];
+    if (kCodes) {
+      *reinterpret_cast<u32x4 *>(&q_c[tid * 32]) = a;
+      *reinterpret_cast<u32x4 *>(&q_c[tid * 32 + 16]) = c;
+    } else {
+      float *dst = &q_l[tid * 32];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int wa = (int)a[i], wc = (int)c[i];
-      dst[4 * i + 0] = __builtin_amdgcn_cvt_f32_fp8(wa, 0);
-      dst[4 * i + 1] = __builtin_amdgcn_cvt_f32_fp8(wa, 1);
-      dst[4 * i + 2] = __builtin_amdgcn_cvt_f32_fp8(wa, 2);
-      dst[4 * i + 3] = __builtin_amdgcn_cvt_f32_fp8(wa, 3);
-      dst[16 + 4 * i + 0] = __builtin_amdgcn_cvt_f32_fp8(wc, 0);
-      dst[16 + 4 * i + 1] = __builtin_amdgcn_cvt_f32_fp8(wc, 1);
-      dst[16 + 4 * i + 2] = __builtin_amdgcn_cvt_f32_fp8(wc, 2);
-      dst[16 + 4 * i + 3] = __builtin_amdgcn_cvt_f32_fp8(wc, 3);
+      for (int i = 0; i < 4; ++i) {
+        const int wa = (int)a[i], wc = (int)c[i];
+        dst[4 * i + 0] = __builtin_amdgcn_cvt_f32_fp8(wa, 0);
+        dst[4 * i + 1] = __builtin_amdgcn_cvt_f32_fp8(wa, 1);
+        dst[4 * i + 2] = __builtin_amdgcn_cvt_f32_fp8(wa, 2);
+        dst[4 * i + 3] = __builtin_amdgcn_cvt_f32_fp8(wa, 3);
+        dst[16 + 4 * i + 0] = __builtin_amdgcn_cvt_f32_fp8(wc, 0);
+        dst[16 + 4 * i + 1] = __builtin_amdgcn_cvt_f32_fp8(wc, 1);
+        dst[16 + 4 * i + 2] = __builtin_amdgcn_cvt_f32_fp8(wc, 2);
+        dst[16 + 4 * i + 3] = __builtin_amdgcn_cvt_f32_fp8(wc, 3);
+      }
     }
     if (tid < kNH) w_l[tid] = p.weights[(size_t)b * kNH + tid];
   }
@@ -127,7 +142,15 @@ __global__ __launch_bounds__(kScoreThreads) void dsa_scores_kernel(DsaParams p, 
     for (int d = 0; d < kD; d += 4) {
 #pragma unroll
       for (int g = 0; g < kHG; ++g) {
-        const float4 q4 = *reinterpret_cast<const float4 *>(&q_l[(h0 + g) * kD + d]);
+        float4 q4;
+        if (kCodes) {
+          const int c4 = *reinterpret_cast<const int *>(&q_c[(h0 + g) * kD + d]);
+          const v2f lo = __builtin_amdgcn_cvt_pk_f32_fp8(c4, false);  // codes d, d+1
+          const v2f hi = __builtin_amdgcn_cvt_pk_f32_fp8(c4, true);   // codes d+2, d+3
+          q4 = float4{lo[0], lo[1], hi[0], hi[1]};
+        } else {
+          q4 = *reinterpret_cast<const float4 *>(&q_l[(h0 + g) * kD + d]);
+        }
         dot[g] = __builtin_fmaf(q4.x, kd[d + 0], dot[g]);
         dot[g] = __builtin_fmaf(q4.y, kd[d + 1], dot[g]);
         dot[g] = __builtin_fmaf(q4.z, kd[d + 2], dot[g]);
