@@ -19,6 +19,9 @@ The line also carries `router_projection`: the same batches routed from the
 hidden rows with the router projection on the device (moe_route_hidden)
 against routing from given logits (moe_route), both timed back to back.
 
+`us_per_call_weights_rotated`: the same calls alternating between two
+independent sets of expert weights, so that no call reads weights the call
+before it left in the Infinity Cache (reported separately, never as `value`).
 --cold additionally times calls after a 512 MiB write that evicts L2 and the
 256 MB Infinity Cache (reported separately, never as `value`).
 --copy-calibration runs only a plain 1 GiB device copy, the reference
@@ -379,6 +382,8 @@ def main():
     ap.add_argument("--config", default="decode", choices=sorted(W.CONFIGS))
     ap.add_argument("--rotate", type=int, default=4, help="distinct activation batches")
     ap.add_argument("--cold", action="store_true")
+    ap.add_argument("--no-weight-rotation", action="store_true",
+                    help="skip the timing with two alternating sets of expert weights")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-max-tokens", type=int, default=16)
     ap.add_argument("--copy-calibration", action="store_true")
@@ -513,6 +518,32 @@ def main():
     traffic = read_traffic(cfg.name)
     roof["traffic"] = traffic
 
+    # timed region 3: the calls alternating between two independent sets of
+    # expert weights, so that no call finds its weights in the Infinity Cache
+    # left by the call before it (between two calls on one set, the other set
+    # streams more weight bytes than the cache holds): the rate of the weight
+    # streams from HBM, as a model that runs other layers between calls of
+    # this one sees it
+    rotated = None
+    if not args.no_weight_rotation:
+        weights2 = W.gen_weights(cfg, 1, device=dev)
+        calls2 = [M.FusedCall(shape, b["hidden"], b["hidden_scale"], b["logits"], b["bias"], *weights2,
+                              out, ws, stream=stream) for b in batches]
+        sets = (calls, calls2)
+        for i in range(2):
+            sets[i % 2][i % len(calls)]()
+        torch.cuda.synchronize()
+        r0, r1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        prefill()
+        r0.record(stream)
+        for i in range(K):
+            sets[i % 2][i % len(calls)]()
+        r1.record(stream)
+        torch.cuda.synchronize()
+        rotated = round(r0.elapsed_time(r1) / K * 1e3, 2)
+        del calls2, sets, weights2
+        torch.cuda.empty_cache()
+
     cold = cold_p10 = cold_p90 = None
     if args.cold:
         flush = torch.empty(512 << 20, dtype=torch.uint8, device=dev)
@@ -571,6 +602,7 @@ def main():
         "router_projection": router,
         "dsa_topk_indexer": indexer,
         "dsa_sparse_attention": attention,
+        "us_per_call_weights_rotated": rotated,
         "us_per_call_cold": cold,
         "us_per_call_cold_p10": cold_p10,
         "us_per_call_cold_p90": cold_p90,
