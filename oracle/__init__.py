@@ -63,10 +63,6 @@ def lib():
         L.oracle_e4m3_encode.restype = ctypes.c_uint8
         L.oracle_e4m3_encode_array.argtypes = [P, P, ctypes.c_int64]
         L.oracle_e4m3_encode_array.restype = None
-        L.oracle_fp8_block_dot.argtypes = [P, P]
-        L.oracle_fp8_block_dot.restype = ctypes.c_float
-        L.oracle_fp8_block_dot_array.argtypes = [P, P, P, ctypes.c_int64]
-        L.oracle_fp8_block_dot_array.restype = None
         L.oracle_swiglu.argtypes = [ctypes.c_float, ctypes.c_float]
         L.oracle_swiglu.restype = ctypes.c_float
         L.oracle_bf16_from_double.argtypes = [ctypes.c_double]
@@ -83,6 +79,14 @@ def lib():
         L.oracle_permute.restype = ctypes.c_int
         L.oracle_expert_ffn.argtypes = [ctypes.c_int32, ctypes.c_int32] + [P] * 10
         L.oracle_expert_ffn.restype = None
+        L.oracle_expert_admissible.argtypes = [ctypes.c_int32, ctypes.c_int32] + [P] * 11
+        L.oracle_expert_admissible.restype = None
+        L.oracle_admissible_batch.argtypes = ([ctypes.POINTER(OracleShape)] + [P] * 4
+                                              + [ctypes.c_int32] + [P] * 9)
+        L.oracle_admissible_batch.restype = ctypes.c_int
+        L.oracle_combine_from_act.argtypes = ([ctypes.POINTER(OracleShape)] + [P] * 8
+                                              + [ctypes.c_int32, P])
+        L.oracle_combine_from_act.restype = ctypes.c_int
         L.oracle_forward.argtypes = ([ctypes.POINTER(OracleShape)] + [P] * 8
                                      + [P, ctypes.c_int32, P, P, P])
         L.oracle_forward.restype = ctypes.c_int
@@ -142,17 +146,8 @@ def e4m3_encode_array(x: np.ndarray) -> np.ndarray:
     return q
 
 
-def fp8_block_dot(a: np.ndarray, w: np.ndarray) -> np.ndarray:
-    """FP8 block dot products (the GEMM1 block rule) of [..., 128] code arrays."""
-    a = np.ascontiguousarray(a, dtype=np.uint8)
-    w = np.ascontiguousarray(w, dtype=np.uint8)
-    assert a.shape == w.shape and a.shape[-1] == 128
-    d = np.empty(a.shape[:-1], np.float32)
-    lib().oracle_fp8_block_dot_array(_ptr(a), _ptr(w), _ptr(d), d.size)
-    return d
-
-
 def swiglu(g: float, u: float) -> float:
+    """fp32(silu(g) * u) with silu evaluated in double."""
     return lib().oracle_swiglu(g, u)
 
 
@@ -222,6 +217,91 @@ def expert_ffn(hidden_row, hidden_scale_row, w13, w13_scale, w2, w2_scale):
     qs = np.empty(I // 128, np.float32)
     lib().oracle_expert_ffn(H, I, *[_ptr(a) for a in args], _ptr(y), _ptr(g), _ptr(q), _ptr(qs))
     return y, g, q, qs
+
+
+def expert_admissible(hidden_row, hidden_scale_row, w13, w13_scale):
+    """The admissible re-quantised intermediate of one (token, expert) pair
+    (see oracle_expert_admissible in moe_oracle.c for the error model).
+
+    Returns a dict: q [I] and qs [I/128] (the oracle's own codes and scales),
+    v_lo / v_hi [I] (range of admissible code values), s_lo / s_hi [I/128]
+    (range of admissible scales), zero_ok [I/128] (an all-zero block admissible)."""
+    H = hidden_row.shape[0]
+    I = w13.shape[0] // 2
+    args = [np.ascontiguousarray(a) for a in (hidden_row, hidden_scale_row, w13, w13_scale)]
+    o = dict(q=np.empty(I, np.uint8), qs=np.empty(I // 128, np.float32),
+             v_lo=np.empty(I, np.float32), v_hi=np.empty(I, np.float32),
+             s_lo=np.empty(I // 128, np.float32), s_hi=np.empty(I // 128, np.float32),
+             zero_ok=np.empty(I // 128, np.uint8))
+    lib().oracle_expert_admissible(H, I, *[_ptr(a) for a in args], _ptr(o["q"]), _ptr(o["qs"]),
+                                   _ptr(o["v_lo"]), _ptr(o["v_hi"]), _ptr(o["s_lo"]), _ptr(o["s_hi"]),
+                                   _ptr(o["zero_ok"]))
+    return o
+
+
+def _table(ws, El, dtype, keep):
+    arr = (ctypes.c_void_p * El)()
+    for e in range(El):
+        we = ws[e]
+        if we is None:
+            arr[e] = None
+            continue
+        we = np.ascontiguousarray(we, dtype=dtype)
+        keep.append(we)
+        arr[e] = we.ctypes.data
+    return arr
+
+
+def admissible_batch(shape: Shape, hidden, hidden_scale, w13, w13_scale, tokens, experts):
+    """expert_admissible for n (token, local expert) pairs, in parallel.  Arrays
+    of the returned dict have a leading axis of n."""
+    tokens = np.ascontiguousarray(tokens, dtype=np.int32)
+    experts = np.ascontiguousarray(experts, dtype=np.int32)
+    n, I = tokens.shape[0], shape.I
+    keep: list = []
+    t13 = _table(w13, shape.num_local_experts, np.uint8, keep)
+    t13s = _table(w13_scale, shape.num_local_experts, np.float32, keep)
+    hidden = np.ascontiguousarray(hidden, dtype=np.uint8)
+    hidden_scale = np.ascontiguousarray(hidden_scale, dtype=np.float32)
+    m = max(n, 1)
+    o = dict(q=np.empty((m, I), np.uint8), qs=np.empty((m, I // 128), np.float32),
+             v_lo=np.empty((m, I), np.float32), v_hi=np.empty((m, I), np.float32),
+             s_lo=np.empty((m, I // 128), np.float32), s_hi=np.empty((m, I // 128), np.float32),
+             zero_ok=np.empty((m, I // 128), np.uint8))
+    rc = lib().oracle_admissible_batch(ctypes.byref(shape.c()), _ptr(hidden), _ptr(hidden_scale),
+                                       ctypes.cast(t13, ctypes.c_void_p), ctypes.cast(t13s, ctypes.c_void_p),
+                                       n, _ptr(tokens), _ptr(experts), _ptr(o["q"]), _ptr(o["qs"]),
+                                       _ptr(o["v_lo"]), _ptr(o["v_hi"]), _ptr(o["s_lo"]), _ptr(o["s_hi"]),
+                                       _ptr(o["zero_ok"]))
+    if rc:
+        raise ValueError(f"oracle_admissible_batch failed ({rc})")
+    return {k: v[:n] for k, v in o.items()}
+
+
+def combine_from_act(shape: Shape, act, act_scale, w2, w2_scale, expert_offsets, pair_row,
+                     topk_weights, tokens=None):
+    """Stage (3)'s GEMM2 and stage (4)'s combine from a given re-quantised
+    intermediate act [P, I] e4m3 / act_scale [P, I/128] (permuted row order of
+    ``permute``), for the listed tokens.  Returns bf16 bits uint16 [n, H]."""
+    if tokens is None:
+        tokens = np.arange(shape.T, dtype=np.int32)
+    tokens = np.ascontiguousarray(tokens, dtype=np.int32)
+    n = tokens.shape[0]
+    keep: list = []
+    t2 = _table(w2, shape.num_local_experts, np.uint8, keep)
+    t2s = _table(w2_scale, shape.num_local_experts, np.float32, keep)
+    act = np.ascontiguousarray(act, dtype=np.uint8)
+    act_scale = np.ascontiguousarray(act_scale, dtype=np.float32)
+    offs = np.ascontiguousarray(expert_offsets, dtype=np.int32)
+    pr = np.ascontiguousarray(pair_row, dtype=np.int32)
+    w = np.ascontiguousarray(topk_weights, dtype=np.float32)
+    out = np.empty((max(n, 1), shape.H), np.uint16)
+    rc = lib().oracle_combine_from_act(ctypes.byref(shape.c()), _ptr(act), _ptr(act_scale),
+                                       ctypes.cast(t2, ctypes.c_void_p), ctypes.cast(t2s, ctypes.c_void_p),
+                                       _ptr(offs), _ptr(pr), _ptr(w), _ptr(tokens), n, _ptr(out))
+    if rc:
+        raise ValueError(f"oracle_combine_from_act failed ({rc})")
+    return out[:n]
 
 
 def forward(shape: Shape, hidden, hidden_scale, logits, bias, w13, w13_scale, w2, w2_scale,

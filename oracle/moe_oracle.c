@@ -17,12 +17,16 @@
  * reading used here is stated next to the code; all readings are collected in
  * the design notes of the repository.
  *
- * Precision: fp64 wherever floating point decides no integer (GEMM2, the
- * combine, rounded once to bf16).  Where floating point decides an integer,
- * the decision is taken in the precision of the GPU kernel: routing in one
- * fixed fp32 sequence (expert choice), GEMM1 and SwiGLU in the matrix cores'
- * FP8 block arithmetic with fp32 promotion (they decide the re-quantised
- * FP8 codes).
+ * Precision: every GEMM and the combine are their plain definitions summed
+ * in double (GEMM1 rounded once to fp32, SwiGLU's silu in double, the output
+ * rounded once to bf16).  Routing follows one fixed fp32 sequence (the expert
+ * choice is an integer decided by floating point, and the layer fixes the
+ * sequence).  The re-quantised FP8 intermediate is also an integer decided by
+ * floating point, but its inputs come from an FP8 block GEMM whose
+ * accumulation the paper leaves to the matrix units: besides its own codes
+ * the oracle states the set of codes any GEMM1 within a stated error model
+ * admits (oracle_expert_admissible), and a device kernel is checked against
+ * that set.
  *
  * The file also holds the oracle of the paper's DSA TopK Indexer (Section
  * 3.1.3), at its end.
@@ -341,96 +345,79 @@ int oracle_permute(const oracle_shape *s, const int32_t *topk_ids,
 }
 
 /* ------------------------------------------------------------------------ */
-/* FP8 block dot product in the precision of the matrix cores that compute   */
-/* it.  Stage (3) re-quantises GEMM1's output to FP8, so an integer (the     */
-/* code) is decided by floating point; that decision is taken here in the    */
-/* kernel's precision.  The 128 products of one K block are taken in 16      */
-/* groups of 8 consecutive k.  In a group, E = max over its 8 products of    */
-/* (exp(a_k) + exp(w_k)), exp = the unbiased exponent of the code (-6 for    */
-/* exponent field 0); every product is truncated toward zero to a multiple   */
-/* of 2^(E-13) and the truncated products are summed exactly.  The 16 group  */
-/* sums are added in group order into an fp32 value, round to nearest even.  */
-/* (Measured on CDNA4 FP8 matrix cores; see the design notes.)               */
+/* Decoded e4m3 values as a 256-entry table (each entry from the bit-field   */
+/* decoder above), so the GEMM loops below read one double per code.         */
+/* Filled once, before any parallel region, by every entry point using it.   */
 /* ------------------------------------------------------------------------ */
+static double dec_tab[256];
+static int dec_tab_ready = 0;
+
+static void dec_table_init(void) {
+  int c;
+  if (dec_tab_ready) return;
+  for (c = 0; c < 256; ++c) dec_tab[c] = oracle_e4m3_decode((uint8_t)c);
+  dec_tab_ready = 1;
+}
+
+/* Unbiased exponent of an e4m3 code's exponent field (-6 for field 0, the   */
+/* subnormal binade): a code's value is a multiple of 2^(exponent - 3).      */
 static int e4m3_exponent(uint8_t q) {
   int ef = (q >> 3) & 0xF;
   return ef == 0 ? -6 : ef - 7;
 }
 
-float oracle_fp8_block_dot(const uint8_t *a, const uint8_t *w) {
-  float acc = 0.0f;
-  int g, k;
-  for (g = 0; g < 16; ++g) {
-    int E = -1000;
-    double grid, sum = 0.0;
-    for (k = g * 8; k < g * 8 + 8; ++k) {
-      int ek = e4m3_exponent(a[k]) + e4m3_exponent(w[k]);
-      if (ek > E) E = ek;
-    }
-    grid = ldexp(1.0, E - 13);
-    for (k = g * 8; k < g * 8 + 8; ++k) {
-      double prod = oracle_e4m3_decode(a[k]) * oracle_e4m3_decode(w[k]); /* exact */
-      sum += trunc(prod / grid) * grid;                                 /* exact */
-    }
-    acc = (float)((double)acc + sum); /* one rounding: the sum is exact in double */
-  }
-  return acc;
-}
+/* SwiGLU of stage (3) from its definition: silu(g) * u with                 */
+/* silu(z) = z / (1 + e^-z) evaluated in double, the product rounded once    */
+/* to fp32.                                                                  */
+static double silu_d(double z) { return z / (1.0 + exp(-z)); }
 
-void oracle_fp8_block_dot_array(const uint8_t *a, const uint8_t *w, float *d, int64_t n) {
-  int64_t i;
-#pragma omp parallel for schedule(static)
-  for (i = 0; i < n; ++i) d[i] = oracle_fp8_block_dot(a + i * 128, w + i * 128);
-}
+float oracle_swiglu(float g, float u) { return (float)(silu_d((double)g) * (double)u); }
 
-/* SwiGLU of stage (3): silu(g) * u with silu(g) = g * sigmoid(g), in fp32,
- * the sigmoid being the fixed fp32 sequence of the routing stage. */
-float oracle_swiglu(float g, float u) {
-  float silu = g * oracle_sigmoid(g);
-  return silu * u;
-}
-
-/* ------------------------------------------------------------------------ */
-/* Stage (3): the gated MLP of one expert applied to one token row.          */
-/*   GEMM1 (FP8 block GEMM with fp32 block scales; decides the codes below,  */
-/*   so it runs in the kernel's precision): for each 128-block kb of h,      */
-/*     t = fp8_block_dot(hidden[kb], w13[n, kb])                             */
-/*     g[n] = fmaf(t, hidden_scale[kb] * w13_scale[n/128, kb], g[n])         */
-/*   in kb order from g[n] = 0; rows [0,I) gate, [I,2I) up                   */
-/*   a[i]   = swiglu(g[i], g[I+i])                                (fp32)     */
-/*   per 128-block b of a: amax_b = max|a|, scale_b = amax_b / 448 (fp32),   */
-/*     q[i] = e4m3(a[i] / scale_b) (fp32 division, RNE, saturating);         */
-/*     amax_b = 0 gives scale_b = 1 and q = 0                                */
-/*   y[n]   = sum_i dec(q[i]) scale[i/128] dec(w2[n,i]) w2_scale[n/128,i/128] */
-/* Optional outputs: g (fp32, 2I), q (I codes), qscale (I/128).              */
-/* ------------------------------------------------------------------------ */
-void oracle_expert_ffn(int32_t H, int32_t I, const uint8_t *hidden_row,
-                       const float *hidden_scale_row, const uint8_t *w13,
-                       const float *w13_scale, const uint8_t *w2,
-                       const float *w2_scale, double *y, float *g_out,
-                       uint8_t *q_out, float *qscale_out) {
-  int HB = H / 128, IB = I / 128;
-  float *g = (float *)malloc(sizeof(float) * 2 * I);
-  float *a = (float *)malloc(sizeof(float) * I);
-  uint8_t *q = (uint8_t *)malloc(I);
-  float *qs = (float *)malloc(sizeof(float) * IB);
-  double *aq = (double *)malloc(sizeof(double) * I);
-  int n, i, b;
-
-  for (n = 0; n < 2 * I; ++n) {
+/* GEMM1 of one token row against one expert, from its definition: for each  */
+/* output row n, the exact products of the dequantised operands summed in    */
+/* double (x = dec(hidden) * hidden_scale and w = dec(w13) * w13_scale are   */
+/* exact in double).  Optionally also, per n, the two sums the admissible-   */
+/* set bound needs: abs_sum[n] = sum |x w| and blk_sum[n] = sum over blocks  */
+/* kb of |sa sw| 2^(E_kb - 6), E_kb the largest exponent sum                 */
+/* exp(a_k) + exp(w_k) over the block's 128 code pairs.                      */
+static void gemm1_row(int32_t H, int32_t n2, const uint8_t *hidden_row,
+                      const float *hidden_scale_row, const uint8_t *w13,
+                      const float *w13_scale, double *g, double *abs_sum,
+                      double *blk_sum) {
+  int HB = H / 128, n, kb, k;
+  for (n = 0; n < n2; ++n) {
     const uint8_t *wr = w13 + (int64_t)n * H;
     const float *sr = w13_scale + (int64_t)(n / 128) * HB;
-    float acc = 0.0f;
-    int kb;
+    double acc = 0.0, aabs = 0.0, ablk = 0.0;
     for (kb = 0; kb < HB; ++kb) {
-      float t = oracle_fp8_block_dot(hidden_row + kb * 128, wr + kb * 128);
-      float sc = hidden_scale_row[kb] * sr[kb];
-      acc = fmaf(t, sc, acc);
+      double sa = hidden_scale_row[kb], sw = sr[kb];
+      for (k = kb * 128; k < kb * 128 + 128; ++k)
+        acc += (dec_tab[hidden_row[k]] * sa) * (dec_tab[wr[k]] * sw);
+      if (abs_sum) {
+        int E = -1000;
+        double pabs = 0.0;
+        for (k = kb * 128; k < kb * 128 + 128; ++k) {
+          int ek = e4m3_exponent(hidden_row[k]) + e4m3_exponent(wr[k]);
+          if (ek > E) E = ek;
+          pabs += fabs(dec_tab[hidden_row[k]] * dec_tab[wr[k]]);
+        }
+        aabs += fabs(sa * sw) * pabs;
+        ablk += fabs(sa * sw) * ldexp(1.0, E - 6);
+      }
     }
     g[n] = acc;
+    if (abs_sum) abs_sum[n] = aabs;
+    if (blk_sum) blk_sum[n] = ablk;
   }
-  for (i = 0; i < I; ++i) a[i] = oracle_swiglu(g[i], g[I + i]);
-  for (b = 0; b < IB; ++b) {
+}
+
+/* Re-quantisation of one row of SwiGLU outputs, per 1x128 block:           */
+/*   amax = max |a| (fp32); scale = amax / 448 (fp32 division);              */
+/*   q = e4m3(a / scale) (fp32 division, round to nearest even, saturating); */
+/*   an all-zero block gets scale 1 and codes 0.                             */
+static void requant_row(int32_t I, const float *a, uint8_t *q, float *qs) {
+  int b, i;
+  for (b = 0; b < I / 128; ++b) {
     float amax = 0.0f, scale;
     for (i = b * 128; i < (b + 1) * 128; ++i) {
       float m = fabsf(a[i]);
@@ -438,27 +425,285 @@ void oracle_expert_ffn(int32_t H, int32_t I, const uint8_t *hidden_row,
     }
     scale = (amax == 0.0f) ? 1.0f : amax / 448.0f;
     qs[b] = scale;
-    for (i = b * 128; i < (b + 1) * 128; ++i) {
+    for (i = b * 128; i < (b + 1) * 128; ++i)
       q[i] = (amax == 0.0f) ? 0 : oracle_e4m3_encode(a[i] / scale);
-      aq[i] = oracle_e4m3_decode(q[i]) * (double)scale;
-    }
   }
+}
+
+/* ------------------------------------------------------------------------ */
+/* Stage (3): the gated MLP of one expert applied to one token row, from the */
+/* plain definition of each step (double wherever floating point decides no  */
+/* integer):                                                                 */
+/*   g[n] = fp32( sum_h x[h] w13[n,h] )  in double;  rows [0,I) gate,        */
+/*          [I,2I) up                                                         */
+/*   a[i] = fp32( silu(g[i]) * g[I+i] ),  silu in double                     */
+/*   (q, scale) = the 1x128 re-quantisation of a (requant_row above)         */
+/*   y[n] = sum_i dec(q[i]) scale[i/128] dec(w2[n,i]) w2_scale[n/128,i/128]  */
+/*          in double                                                         */
+/* Optional outputs: g (fp32, 2I), q (I codes), qscale (I/128).              */
+/* ------------------------------------------------------------------------ */
+void oracle_expert_ffn(int32_t H, int32_t I, const uint8_t *hidden_row,
+                       const float *hidden_scale_row, const uint8_t *w13,
+                       const float *w13_scale, const uint8_t *w2,
+                       const float *w2_scale, double *y, float *g_out,
+                       uint8_t *q_out, float *qscale_out) {
+  int IB = I / 128;
+  double *gd = (double *)malloc(sizeof(double) * 2 * I);
+  float *g = (float *)malloc(sizeof(float) * 2 * I);
+  float *a = (float *)malloc(sizeof(float) * I);
+  uint8_t *q = (uint8_t *)malloc(I);
+  float *qs = (float *)malloc(sizeof(float) * IB);
+  double *aq = (double *)malloc(sizeof(double) * I);
+  int n, i;
+
+  dec_table_init();
+  gemm1_row(H, 2 * I, hidden_row, hidden_scale_row, w13, w13_scale, gd, NULL, NULL);
+  for (n = 0; n < 2 * I; ++n) g[n] = (float)gd[n];
+  for (i = 0; i < I; ++i) a[i] = oracle_swiglu(g[i], g[I + i]);
+  requant_row(I, a, q, qs);
+  for (i = 0; i < I; ++i) aq[i] = dec_tab[q[i]] * (double)qs[i / 128];
   for (n = 0; n < H; ++n) {
     const uint8_t *wr = w2 + (int64_t)n * I;
     const float *sr = w2_scale + (int64_t)(n / 128) * IB;
     double acc = 0.0;
-    for (i = 0; i < I; ++i)
-      acc += aq[i] * (oracle_e4m3_decode(wr[i]) * (double)sr[i / 128]);
+    for (i = 0; i < I; ++i) acc += aq[i] * (dec_tab[wr[i]] * (double)sr[i / 128]);
     y[n] = acc;
   }
   if (g_out) memcpy(g_out, g, sizeof(float) * 2 * I);
   if (q_out) memcpy(q_out, q, I);
   if (qscale_out) memcpy(qscale_out, qs, sizeof(float) * IB);
+  free(gd);
   free(g);
   free(a);
   free(q);
   free(qs);
   free(aq);
+}
+
+/* ------------------------------------------------------------------------ */
+/* The admissible re-quantised intermediate of one (token, expert) pair.     */
+/* Stage (3) turns GEMM1's output into integers (the FP8 codes), and GEMM1   */
+/* is an FP8 block GEMM whose accumulation precision the paper leaves to the */
+/* matrix units; a device kernel's codes are therefore not compared for      */
+/* equality but checked for membership in the set that every GEMM1 within    */
+/* the following error model produces:                                       */
+/*  (i)  the 128 exact e4m3 products p_k of a K block are accumulated at a   */
+/*       resolution no coarser than 2^(E_kb - 13), E_kb the largest exponent */
+/*       sum exp(a_k) + exp(w_k) of the block (each product is a multiple of */
+/*       2^(exp(a)+exp(w)-6) below 2^(exp(a)+exp(w)+2): 13 fraction bits of */
+/*       the block's leading product exponent), with fp32 rounding of        */
+/*       partial sums:  |t' - t| <= beta_kb = 2^(E_kb-6) + 2^-19 sum|p_k|;   */
+/*  (ii) the block sums are scaled by fp32(sa*sw) and added in fp32, in any  */
+/*       order (a split K included): at most gamma(nb+2) (sum|x w| + sum    */
+/*       |sa sw| beta_kb) more, gamma(m) = m u / (1 - m u), u = 2^-24;       */
+/*  (iii) SwiGLU is evaluated in fp32 with relative error at most 8 u (plus  */
+/*       1e-30 absolute for inputs whose sigmoid underflows);                 */
+/*  (iv) amax, scale = amax/448 and the codes then follow exactly (fp32      */
+/*       division, nearest-even, saturating), the ratio allowed 2 ulps.       */
+/* So g' lies in [g - dg, g + dg], dg = sum|sa sw| beta_kb + (i)'s and (ii)'s */
+/* fp32 terms (+ 2^-50 sum|x w| for the double sum itself); a' in the range  */
+/* of silu(g')u' over that box, widened by (iii); the block's scale in        */
+/* [fp32(amax_lo/448), fp32(amax_hi/448)]; each code's value in               */
+/* [dec(e4m3(r_lo)), dec(e4m3(r_hi))] over the extreme ratios a'/scale'.     */
+/* An all-zero block (scale 1, codes 0) is admissible when amax_lo = 0.      */
+/* Outputs per pair: v_lo/v_hi [I] (admissible code values), s_lo/s_hi [I/128]*/
+/* (admissible scales), zero_ok [I/128], and the nominal codes/scales of     */
+/* oracle_expert_ffn (q [I], qs [I/128]).                                    */
+/* ------------------------------------------------------------------------ */
+static const double kSiluArgMin = -1.2784645427610738; /* root of silu' */
+
+static void silu_range(double lo, double hi, double *mn, double *mx) {
+  double a = silu_d(lo), b = silu_d(hi);
+  *mn = a < b ? a : b;
+  *mx = a > b ? a : b;
+  if (lo <= kSiluArgMin && kSiluArgMin <= hi) {
+    double m = silu_d(kSiluArgMin);
+    if (m < *mn) *mn = m;
+  }
+}
+
+static float next_down(float x, int k) {
+  while (k--) x = nextafterf(x, -INFINITY);
+  return x;
+}
+static float next_up(float x, int k) {
+  while (k--) x = nextafterf(x, INFINITY);
+  return x;
+}
+
+void oracle_expert_admissible(int32_t H, int32_t I, const uint8_t *hidden_row,
+                              const float *hidden_scale_row, const uint8_t *w13,
+                              const float *w13_scale, uint8_t *q, float *qs,
+                              float *v_lo, float *v_hi, float *s_lo, float *s_hi,
+                              uint8_t *zero_ok) {
+  const double u = ldexp(1.0, -24);
+  const int HB = H / 128, IB = I / 128;
+  const double gam = (HB + 2) * u / (1.0 - (HB + 2) * u);
+  double *gd = (double *)malloc(sizeof(double) * 2 * I);
+  double *sabs = (double *)malloc(sizeof(double) * 2 * I);
+  double *sblk = (double *)malloc(sizeof(double) * 2 * I);
+  double *dg = (double *)malloc(sizeof(double) * 2 * I);
+  float *a = (float *)malloc(sizeof(float) * I);
+  double *alo = (double *)malloc(sizeof(double) * I);
+  double *ahi = (double *)malloc(sizeof(double) * I);
+  int n, i, b;
+
+  dec_table_init();
+  gemm1_row(H, 2 * I, hidden_row, hidden_scale_row, w13, w13_scale, gd, sabs, sblk);
+  for (n = 0; n < 2 * I; ++n) {
+    double beta = sblk[n] + ldexp(1.0, -19) * sabs[n]; /* (i), summed over kb */
+    dg[n] = beta + gam * (sabs[n] + beta) + ldexp(1.0, -50) * sabs[n];
+  }
+  /* the nominal intermediate (the oracle's own codes) */
+  for (i = 0; i < I; ++i) a[i] = oracle_swiglu((float)gd[i], (float)gd[I + i]);
+  requant_row(I, a, q, qs);
+  /* (iii): the range of silu(g') u' over the box, widened */
+  for (i = 0; i < I; ++i) {
+    double smn, smx, ulo = gd[I + i] - dg[I + i], uhi = gd[I + i] + dg[I + i];
+    double c[4], lo, hi, m;
+    int k;
+    silu_range(gd[i] - dg[i], gd[i] + dg[i], &smn, &smx);
+    c[0] = smn * ulo;
+    c[1] = smn * uhi;
+    c[2] = smx * ulo;
+    c[3] = smx * uhi;
+    lo = hi = c[0];
+    for (k = 1; k < 4; ++k) {
+      if (c[k] < lo) lo = c[k];
+      if (c[k] > hi) hi = c[k];
+    }
+    m = fabs(lo) > fabs(hi) ? fabs(lo) : fabs(hi);
+    alo[i] = lo - 8 * u * m - 1e-30;
+    ahi[i] = hi + 8 * u * m + 1e-30;
+  }
+  /* (iv) per block: admissible amax and scale, then each code's range */
+  for (b = 0; b < IB; ++b) {
+    double mlo = 0.0, mhi = 0.0;
+    float sl, sh, flo, fhi;
+    for (i = b * 128; i < (b + 1) * 128; ++i) {
+      double mn = (alo[i] <= 0.0 && ahi[i] >= 0.0) ? 0.0
+                  : (fabs(alo[i]) < fabs(ahi[i]) ? fabs(alo[i]) : fabs(ahi[i]));
+      double mx = fabs(alo[i]) > fabs(ahi[i]) ? fabs(alo[i]) : fabs(ahi[i]);
+      if (mn > mlo) mlo = mn;
+      if (mx > mhi) mhi = mx;
+    }
+    /* the kernel's amax is the largest of its fp32 values: an fp32 number   */
+    flo = next_down((float)mlo, 1);
+    if (flo < 0.0f) flo = 0.0f;
+    fhi = next_up((float)mhi, 1);
+    zero_ok[b] = flo == 0.0f;
+    sl = flo / 448.0f;
+    sh = fhi / 448.0f;
+    if (sl == 0.0f) sl = nextafterf(0.0f, 1.0f); /* a nonzero amax's scale */
+    s_lo[b] = sl;
+    s_hi[b] = sh;
+    for (i = b * 128; i < (b + 1) * 128; ++i) {
+      float lo = (float)alo[i], hi = (float)ahi[i], rlo, rhi;
+      lo = next_down(lo, 1);
+      hi = next_up(hi, 1);
+      rlo = lo >= 0.0f ? lo / sh : lo / sl;
+      rhi = hi >= 0.0f ? hi / sl : hi / sh;
+      rlo = next_down(rlo, 2);
+      rhi = next_up(rhi, 2);
+      v_lo[i] = (float)dec_tab[oracle_e4m3_encode(rlo)];
+      v_hi[i] = (float)dec_tab[oracle_e4m3_encode(rhi)];
+      if (zero_ok[b]) {
+        if (v_lo[i] > 0.0f) v_lo[i] = 0.0f;
+        if (v_hi[i] < 0.0f) v_hi[i] = 0.0f;
+      }
+    }
+  }
+  free(gd);
+  free(sabs);
+  free(sblk);
+  free(dg);
+  free(a);
+  free(alo);
+  free(ahi);
+}
+
+/* oracle_expert_admissible for a list of n (token, local expert) pairs, in  */
+/* parallel; outputs are [n, I] and [n, I/128] arrays in list order.         */
+int oracle_admissible_batch(const oracle_shape *s, const uint8_t *hidden,
+                            const float *hidden_scale, const uint8_t *const *w13,
+                            const float *const *w13_scale, int32_t n,
+                            const int32_t *tokens, const int32_t *experts,
+                            uint8_t *q, float *qs, float *v_lo, float *v_hi,
+                            float *s_lo, float *s_hi, uint8_t *zero_ok) {
+  int32_t p;
+  int H = s->H, I = s->I, HB, IB, bad = 0;
+  if (oracle_check_shape(s) || n < 0) return ORACLE_BAD_ARG;
+  HB = H / 128;
+  IB = I / 128;
+  for (p = 0; p < n; ++p) {
+    int e = experts[p];
+    if (tokens[p] < 0 || tokens[p] >= s->T || e < 0 || e >= s->num_local_experts ||
+        !w13[e] || !w13_scale[e])
+      bad = 1;
+  }
+  if (bad) return ORACLE_BAD_ARG;
+  dec_table_init();
+#pragma omp parallel for schedule(dynamic, 1)
+  for (p = 0; p < n; ++p) {
+    int e = experts[p];
+    int64_t t = tokens[p];
+    oracle_expert_admissible(H, I, hidden + t * H, hidden_scale + t * HB, w13[e], w13_scale[e],
+                             q + (int64_t)p * I, qs + (int64_t)p * IB, v_lo + (int64_t)p * I,
+                             v_hi + (int64_t)p * I, s_lo + (int64_t)p * IB,
+                             s_hi + (int64_t)p * IB, zero_ok + (int64_t)p * IB);
+  }
+  return ORACLE_OK;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Stage (3)'s GEMM2 and stage (4)'s combine from a given re-quantised       */
+/* intermediate: act [P, I] e4m3 with act_scale [P, I/128], rows in the      */
+/* permuted order of oracle_permute (expert_offsets, pair_row), for the      */
+/* listed tokens:                                                            */
+/*   out[r, n] = bf16( sum over local slots j of token_list[r], in slot      */
+/*               order, of w_j * y_j[n] ),                                    */
+/*   y_j[n] = sum_i dec(act[row,i]) act_scale[row,i/128] dec(w2[e,n,i])      */
+/*            w2_scale[e,n/128,i/128]   (double), row = pair_row[t,j]         */
+/* ------------------------------------------------------------------------ */
+int oracle_combine_from_act(const oracle_shape *s, const uint8_t *act,
+                            const float *act_scale, const uint8_t *const *w2,
+                            const float *const *w2_scale, const int32_t *expert_offsets,
+                            const int32_t *pair_row, const float *topk_w,
+                            const int32_t *token_list, int32_t n_tokens, uint16_t *out) {
+  int H = s->H, I = s->I, k = s->top_k, IB, El = s->num_local_experts;
+  int32_t r;
+  if (oracle_check_shape(s) || n_tokens < 0) return ORACLE_BAD_ARG;
+  IB = I / 128;
+  for (r = 0; r < n_tokens; ++r)
+    if (token_list[r] < 0 || token_list[r] >= s->T) return ORACLE_BAD_ARG;
+  dec_table_init();
+#pragma omp parallel for schedule(dynamic, 1)
+  for (r = 0; r < n_tokens; ++r) {
+    int64_t t = token_list[r];
+    double *acc = (double *)calloc(H, sizeof(double));
+    double *aq = (double *)malloc(sizeof(double) * I);
+    int j, n, i;
+    for (j = 0; j < k; ++j) {
+      int row = pair_row[t * k + j], e = 0;
+      double wj;
+      if (row < 0) continue;
+      while (e + 1 < El && expert_offsets[e + 1] <= row) ++e;
+      wj = (double)topk_w[t * k + j];
+      for (i = 0; i < I; ++i)
+        aq[i] = dec_tab[act[(int64_t)row * I + i]] * (double)act_scale[(int64_t)row * IB + i / 128];
+      for (n = 0; n < H; ++n) {
+        const uint8_t *wr = w2[e] + (int64_t)n * I;
+        const float *sr = w2_scale[e] + (int64_t)(n / 128) * IB;
+        double y = 0.0;
+        for (i = 0; i < I; ++i) y += aq[i] * (dec_tab[wr[i]] * (double)sr[i / 128]);
+        acc[n] += wj * y;
+      }
+    }
+    for (n = 0; n < H; ++n) out[(int64_t)r * H + n] = oracle_bf16_from_double(acc[n]);
+    free(acc);
+    free(aq);
+  }
+  return ORACLE_OK;
 }
 
 /* ------------------------------------------------------------------------ */
@@ -483,6 +728,7 @@ int oracle_forward(const oracle_shape *s, const uint8_t *hidden,
   int r, j, p, n, bad = 0;
   if (oracle_check_shape(s)) return ORACLE_BAD_ARG;
   if (n_tokens < 0 || (n_tokens > 0 && !token_list)) return ORACLE_BAD_ARG;
+  dec_table_init();
   HB = H / 128;
   ids = (int32_t *)malloc(sizeof(int32_t) * ((size_t)n_tokens * k + 1));
   w = (float *)malloc(sizeof(float) * ((size_t)n_tokens * k + 1));
