@@ -41,6 +41,23 @@ moe_status_t moe_debug_router_logits(const moe_shape_t *s, const uint8_t *hidden
                                      float *logits, void *workspace, size_t ws_bytes,
                                      void *stream);
 
+/* Stage (3)'s GEMM2 and stage (4)'s weighted combine (paper Section 3.1.1)
+ * on a re-quantised intermediate supplied by the caller: the routing and
+ * permutation of moe_route are computed from router_logits / routing_bias
+ * into the workspace, then GEMM2 and the combine run exactly as in
+ * moe_fused_fp8 but read
+ *  act       [T * top_k, I] e4m3, rows in the permuted order of moe_route
+ *            (the first P = expert_offsets[E_l] rows are read)
+ *  act_scale [T * top_k, I/128] float
+ * instead of the intermediate GEMM1 would write.  out [T, H] bf16 is fully
+ * overwritten.  For checking the GEMM2 and combine kernels on an intermediate
+ * that does not come from the device. */
+moe_status_t moe_debug_combine_from_act(const moe_shape_t *s, const float *router_logits,
+                                        const float *routing_bias, const uint8_t *act,
+                                        const float *act_scale, const uint8_t *w2,
+                                        const float *w2_scale, uint16_t *out, void *workspace,
+                                        size_t ws_bytes, void *stream);
+
 /* Device addresses, inside a workspace used by moe_fused_fp8 for shape `s`,
  * of the re-quantised intermediate activation: act [P, I] e4m3 in permuted
  * row order and act_scale [P, I/128] float.  Valid after the call completes,

@@ -29,6 +29,7 @@ EXPORTED = ("moe_workspace_size", "moe_route", "moe_route_hidden", "moe_fused_fp
             "moe_fused_fp8_router", "moe_fused_fp8_staged", "moe_num_stages", "moe_stage_name",
             "moe_status_string", "moe_debug_sigmoid", "moe_debug_e4m3_encode",
             "moe_debug_act_views", "moe_debug_mfma_block", "moe_debug_router_logits",
+            "moe_debug_combine_from_act",
             "dsa_workspace_size", "dsa_topk_indexer", "dsa_debug_scores",
             "dsa_attention_workspace_size", "dsa_sparse_attention")
 
@@ -130,6 +131,8 @@ def lib() -> ctypes.CDLL:
         L.moe_debug_mfma_block.restype = ctypes.c_int
         L.moe_debug_act_views.argtypes = [S, P, ctypes.POINTER(P), ctypes.POINTER(P)]
         L.moe_debug_act_views.restype = ctypes.c_int
+        L.moe_debug_combine_from_act.argtypes = [S, P, P, P, P, P, P, P, P, Z, P]
+        L.moe_debug_combine_from_act.restype = ctypes.c_int
         _lib = L
     return _lib
 
@@ -383,6 +386,29 @@ def debug_act_views(shape: Shape, workspace: torch.Tensor):
     act = workspace[a.value - base: a.value - base + P * shape.I].view(P, shape.I)
     sc = workspace[s.value - base: s.value - base + P * (shape.I // 128) * 4]
     return act, sc.view(torch.float32).view(P, shape.I // 128)
+
+
+def debug_combine_from_act(shape: Shape, logits, bias, act, act_scale, w2, w2_scale,
+                           out: torch.Tensor | None = None, workspace: torch.Tensor | None = None,
+                           stream=None) -> torch.Tensor:
+    """GEMM2 and the weighted combine on a given intermediate act [T*k, I] uint8 /
+    act_scale [T*k, I/128] f32 (permuted row order of ``route``); routing is
+    recomputed from logits/bias.  Returns out [T, H] bf16 (test hook)."""
+    if out is None:
+        out = torch.empty(shape.T, shape.H, dtype=torch.bfloat16, device=logits.device)
+    if workspace is None:
+        workspace = alloc_workspace(shape, logits.device)
+    P = shape.T * shape.top_k
+    if tuple(act.shape) != (P, shape.I) or tuple(act_scale.shape) != (P, shape.I // 128):
+        raise ValueError("act must be [T*top_k, I] and act_scale [T*top_k, I/128]")
+    rc = lib().moe_debug_combine_from_act(
+        ctypes.byref(shape.c()), _dev(logits, torch.float32, "logits"), _dev(bias, torch.float32, "bias"),
+        _dev(act, torch.uint8, "act"), _dev(act_scale, torch.float32, "act_scale"),
+        _dev(w2, torch.uint8, "w2"), _dev(w2_scale, torch.float32, "w2_scale"),
+        _dev(out, torch.bfloat16, "out"), _dev(workspace, torch.uint8, "workspace"),
+        ctypes.c_size_t(workspace.numel()), _stream(stream))
+    _check("moe_debug_combine_from_act", rc)
+    return out
 
 
 # ---------------------------------------------------------------- DSA TopK indexer

@@ -73,9 +73,10 @@ Plan make_plan(const moe_shape_t *s) {
   const double avg = (double)TK / s->num_experts;
   p.BM = avg <= 16 ? 16 : (avg <= 48 ? 32 : (avg <= 96 ? 64 : (avg <= 192 ? 128 : 256)));
   p.tile = p.BM >= 64;
-  // GEMM1 promotes its K blocks in order (its output decides the re-quantised
-  // codes), so it never splits K.  GEMM2 could (S2 > 1 planes of Y, summed by
-  // the combine), but measured at decode the full-K items are faster and the
+  // GEMM1 keeps the whole K range in one item: its epilogue (SwiGLU and the
+  // 1x128 re-quantisation) needs complete sums, and a K split would add a
+  // reduction pass.  GEMM2 could split K (S2 > 1 planes of Y, summed by the
+  // combine), but measured at decode the full-K items are faster and the
   // combine then reads one plane.
   p.S1 = 1;
   p.S2 = 1;
@@ -223,6 +224,48 @@ moe_status_t enqueue_route(const moe_shape_t *s, const Plan &pl, const RouterIn 
   return MOE_OK;
 }
 
+// Stage (3)'s GEMM2 on the permuted intermediate act [P, I] / act_scale
+// [P, I/128] and stage (4)'s weighted combine into `out`, after the routing
+// and permutation have been enqueued into `ws`.
+moe_status_t enqueue_gemm2_combine(const moe_shape_t *s, const Plan &pl, const Ptrs &r,
+                                   const uint8_t *act, const float *act_scale, const uint8_t *w2,
+                                   const float *w2_scale, uint16_t *out, void *ws, hipStream_t st,
+                                   void *const *ev, int &stage) {
+  auto mark = [&]() {
+    if (ev) (void)hipEventRecord(static_cast<hipEvent_t>(ev[stage]), st);
+    ++stage;
+  };
+  GemmParams g2{};
+  g2.expert_offsets = r.offsets;
+  g2.tile_base = at<int32_t>(ws, pl.off_tile_base);
+  g2.perm_token = r.perm_token;
+  g2.Y = at<float>(ws, pl.off_Y);
+  g2.I = s->I;
+  g2.H = s->H;
+  g2.P_max = (int)pl.P_max;
+  g2.El = s->num_local_experts;
+  g2.A = act;
+  g2.A_scale = act_scale;
+  g2.B = w2;
+  g2.B_scale = w2_scale;
+  g2.n_items = at<int32_t>(ws, pl.off_n_items) + 1;
+  g2.K = s->I;
+  g2.KB = s->I / 128;
+  g2.N_total = s->H;
+  g2.NB = pl.NB2;
+  g2.S = pl.S2;
+  mark();
+  const int grid2 = round8((int64_t)pl.max_tiles * pl.NB2 * pl.S2);
+  MOE_TRY_HIP(pl.tile ? launch_gemm_tile(g2, false, pl.BM, grid2, st)
+                      : launch_gemm2(g2, pl.BM, grid2, st));
+
+  // weighted combine in slot order, one bf16 rounding per element
+  FinalizeParams f{g2.Y, r.pair_row, r.w, out, s->T, s->H, s->top_k, pl.S2, (int)pl.P_max};
+  mark();
+  MOE_TRY_HIP(launch_finalize(f, st));
+  return MOE_OK;
+}
+
 moe_status_t fused_impl(const moe_shape_t *s, const uint8_t *hidden, const float *hidden_scale,
                         const float *logits, const float *router_weight, const float *bias,
                         const uint8_t *w13, const float *w13_scale, const uint8_t *w2,
@@ -288,27 +331,10 @@ moe_status_t fused_impl(const moe_shape_t *s, const uint8_t *hidden, const float
   mark();
   if (pl.narrow1) MOE_TRY_HIP(launch_requant(g1, (int)pl.P_max, st));
 
-  // GEMM2: permuted activation rows x W2 -> Y
-  GemmParams g2 = g;
-  g2.A = g.act;
-  g2.A_scale = g.act_scale;
-  g2.B = w2;
-  g2.B_scale = w2_scale;
-  g2.n_items = at<int32_t>(ws, pl.off_n_items) + 1;
-  g2.K = s->I;
-  g2.KB = s->I / 128;
-  g2.N_total = s->H;
-  g2.NB = pl.NB2;
-  g2.S = pl.S2;
-  mark();
-  const int grid2 = round8((int64_t)pl.max_tiles * pl.NB2 * pl.S2);
-  MOE_TRY_HIP(pl.tile ? launch_gemm_tile(g2, false, pl.BM, grid2, st)
-                      : launch_gemm2(g2, pl.BM, grid2, st));
-
-  // weighted combine in slot order, one bf16 rounding per element
-  FinalizeParams f{g.Y, r.pair_row, r.w, out, s->T, s->H, s->top_k, pl.S2, (int)pl.P_max};
-  mark();
-  MOE_TRY_HIP(launch_finalize(f, st));
+  // GEMM2 and the weighted combine on the intermediate GEMM1 just wrote
+  if ((rc = enqueue_gemm2_combine(s, pl, r, g.act, g.act_scale, w2, w2_scale, out, ws, st, ev,
+                                  stage)) != MOE_OK)
+    return rc;
   if (ev) (void)hipEventRecord(static_cast<hipEvent_t>(ev[stage]), st);
   return MOE_OK;
 }
@@ -465,6 +491,30 @@ moe_status_t moe_debug_router_logits(const moe_shape_t *s, const uint8_t *hidden
   const RouteParams rp = route_params(s, pl, rin, nullptr, r, workspace);
   if (enqueue_projection(s, pl, rin, workspace, st) != hipSuccess) return MOE_ERR_HIP;
   return launch_router_logits(rp, logits, st) == hipSuccess ? MOE_OK : MOE_ERR_HIP;
+}
+
+moe_status_t moe_debug_combine_from_act(const moe_shape_t *s, const float *router_logits,
+                                        const float *routing_bias, const uint8_t *act,
+                                        const float *act_scale, const uint8_t *w2,
+                                        const float *w2_scale, uint16_t *out, void *workspace,
+                                        size_t ws_bytes, void *stream) {
+  moe_status_t rc = check_shape(s);
+  if (rc != MOE_OK) return rc;
+  if (s->T == 0) return MOE_OK;
+  const void *ptrs[] = {router_logits, routing_bias, act, act_scale, w2, w2_scale, out};
+  for (const void *q : ptrs)
+    if (!q || !aligned(q, 16)) return MOE_ERR_INVALID_ARG;
+  const Plan pl = make_plan(s);
+  if (!workspace || !aligned(workspace, kAlign)) return MOE_ERR_INVALID_ARG;
+  if (ws_bytes < pl.total) return MOE_ERR_WORKSPACE_TOO_SMALL;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const Ptrs r = route_ptrs(pl, workspace, nullptr);
+  int stage = 0;
+  const RouterIn rin{router_logits, nullptr, nullptr, nullptr};
+  if ((rc = enqueue_route(s, pl, rin, routing_bias, r, workspace, st, nullptr, stage)) != MOE_OK)
+    return rc;
+  return enqueue_gemm2_combine(s, pl, r, act, act_scale, w2, w2_scale, out, workspace, st, nullptr,
+                               stage);
 }
 
 moe_status_t moe_debug_act_views(const moe_shape_t *s, void *workspace, uint8_t **act,
