@@ -1,31 +1,29 @@
 """Benchmark of the fused block-scaled FP8 MoE layer on one MI355X.
 
-    python bench.py [--steps K] [--warmup W] [--config decode|mid|prefill|skewed]
+    python bench.py [--steps K] [--warmup W] [--config decode|mid|prefill|skewed|...]
 
 A step is one call of the whole layer (routing, permutation, GEMM1 + SwiGLU +
 re-quantisation, GEMM2, combine) on one batch of seeded synthetic inputs
-already resident in HBM.  Activation batches rotate over --rotate seeds (the
-resident expert weights are the model's and stay fixed), so consecutive calls
-route to different experts.  K calls run back to back between two stream
-synchronisations; each kernel is bracketed by HIP events recorded on the
-library's stream (moe_fused_fp8_staged), which gives the per-kernel durations
-behind the roofline figure.  Prints one JSON line.
+already resident in HBM.  By default the four DeepSeek-V3-shaped workloads of
+the metric are timed in one run -- decode T=16, mid T=256, prefill T=4096 (32
+of 256 experts resident) and skewed T=8192 (all 256 resident, 16 hot) -- each
+with its own result object under "configs"; the line's `value` is the skewed
+(largest) workload's µs per call over exactly --steps calls.  Activation
+batches rotate over --rotate seeds (the resident expert weights stay fixed).
+Each timed region starts behind a device spin long enough for the host to
+enqueue all calls, so the calls run back to back; HIP events on the library's
+stream give the per-kernel durations behind each roofline object.
 
-The line also carries `dsa_topk_indexer`: the paper's third operator (DSA
-TopK indexer) on seeded inputs of its long-regime representative and of a
-long-sequence batch, µs per call and the score kernel's roofline.
+Per workload also: the cold µs per call (median, p10, p90 of calls each
+preceded, outside the timed interval, by a read-only sweep of 1 GiB that
+evicts L2 and the 256 MB Infinity Cache without leaving dirty lines), P and
+the touched experts, and the CPU oracle on a bounded token sample.  The line
+carries the GPU clock read before and after the timed regions.
 
-The line also carries `router_projection`: the same batches routed from the
-hidden rows with the router projection on the device (moe_route_hidden)
-against routing from given logits (moe_route), both timed back to back.
-
-`us_per_call_weights_rotated`: the same calls alternating between two
-independent sets of expert weights, so that no call reads weights the call
-before it left in the Infinity Cache (reported separately, never as `value`).
---cold additionally times calls after a 512 MiB write that evicts L2 and the
-256 MB Infinity Cache (reported separately, never as `value`).
---copy-calibration runs only a plain 1 GiB device copy, the reference
-kernel for scaling the HBM byte counters of rocprofv3.
+Extra legs (not `value`): `dsa_topk_indexer`, `dsa_sparse_attention` and
+`router_projection` (see their functions).  --copy-calibration runs only a
+plain 1 GiB device copy, the reference kernel for scaling the HBM byte
+counters of rocprofv3.
 """
 from __future__ import annotations
 
@@ -145,20 +143,40 @@ def copy_calibration():
     print(json.dumps({"copy_bytes_read": n, "copy_bytes_written": n, "launches": 3}))
 
 
-def cpu_baseline(cfg, batches, weights_dev, max_tokens: int):
-    """The CPU oracle on this host, on the bench's own batches (all tokens, or a
-    seeded sample of max_tokens per batch), scaled to microseconds per call."""
+def cpu_info() -> dict:
+    model = None
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    try:
+        affinity = len(os.sched_getaffinity(0))
+    except OSError:
+        affinity = None
+    return {"cpu_model": model, "nproc": os.cpu_count(), "cpus_available": affinity}
+
+
+def cpu_baseline(cfg, batch, weights_dev, max_tokens: int, threads: int | None = None):
+    """The CPU oracle on this host on one of the bench's batches (all tokens, or
+    a seeded sample of max_tokens), scaled to microseconds per call by the
+    resident-pair count (the oracle's time is proportional to it)."""
     import oracle
     oracle.build(force=False)
-    shape = oracle.shape_of(cfg)
-    total_s, pairs_done, pairs_all = 0.0, 0, 0
-    for b in batches:
-        logits = b["logits"].cpu().numpy()
-        bias = b["bias"].cpu().numpy()
+    before = oracle.num_threads()
+    if threads:
+        oracle.set_num_threads(threads)
+    try:
+        shape = oracle.shape_of(cfg)
+        logits = batch["logits"].cpu().numpy()
+        bias = batch["bias"].cpu().numpy()
         ids, _ = oracle.route(shape, logits, bias)
         le = ids - cfg.local_expert_offset
         local = (le >= 0) & (le < cfg.num_local_experts)
-        pairs_all += int(local.sum())
+        pairs_all = int(local.sum())
         if cfg.T <= max_tokens:
             toks = np.arange(cfg.T, dtype=np.int32)
         else:
@@ -167,18 +185,36 @@ def cpu_baseline(cfg, batches, weights_dev, max_tokens: int):
         w13, s13, w2, s2 = weights_dev
         host = lambda t: [t[e].cpu().numpy() if e in need else None for e in range(cfg.num_local_experts)]
         hw = dict(w13=host(w13), w13_scale=host(s13), w2=host(w2), w2_scale=host(s2))
+        hidden, hscale = batch["hidden"].cpu().numpy(), batch["hidden_scale"].cpu().numpy()
+        used = oracle.num_threads()
         t0 = time.perf_counter()
-        oracle.forward(shape, b["hidden"].cpu().numpy(), b["hidden_scale"].cpu().numpy(), logits, bias,
-                       **hw, tokens=toks)
-        total_s += time.perf_counter() - t0
-        pairs_done += int(local[toks].sum())
-    # scale the sample to whole calls by the resident-pair count (the oracle's
-    # time is proportional to it)
-    per_call_s = total_s / len(batches) * (pairs_all / max(pairs_done, 1))
-    sample = (f"{len(batches)} batches x {'all' if cfg.T <= max_tokens else max_tokens} of {cfg.T} "
-              f"tokens ({pairs_done} resident pairs), scaled by resident pairs")
-    return {"value": per_call_s * 1e6, "unit": "us/call", "cores": oracle.num_threads(),
-            "kind": "oracle", "sample": sample, "wall_s": round(total_s, 2)}
+        oracle.forward(shape, hidden, hscale, logits, bias, **hw, tokens=toks)
+        wall = time.perf_counter() - t0
+    finally:
+        oracle.set_num_threads(before)
+    done = int(local[toks].sum())
+    per_call_s = wall * (pairs_all / max(done, 1))
+    sample = (f"{'all' if cfg.T <= max_tokens else len(toks)} of {cfg.T} tokens ({done} of {pairs_all} "
+              f"resident pairs), scaled to the call by resident pairs")
+    return {"value": round(per_call_s * 1e6, 1), "unit": "us/call", "cores": used, "kind": "oracle",
+            "sample": sample, "wall_s": round(wall, 3),
+            "extrapolated": bool(cfg.T > max_tokens)}
+
+
+def gpu_clock() -> dict:
+    """The shader clock as the driver reports it (sysfs: the active DPM level)."""
+    res = {}
+    import glob
+    for path in sorted(glob.glob("/sys/class/drm/card*/device/pp_dpm_sclk")):
+        try:
+            with open(path) as f:
+                lines = f.read().split("\n")
+        except OSError:
+            continue
+        cur = [ln for ln in lines if ln.strip().endswith("*")]
+        if cur:
+            res[path.split("/")[4]] = cur[0].split(":", 1)[1].replace("*", "").strip()
+    return res
 
 
 def router_projection_leg(cfg, shape, batches, weights, out, ws, stream, K, prefill):
@@ -374,41 +410,16 @@ def attention_leg(K, prefill, with_cpu: bool):
     return res
 
 
-def main():
-    ap = argparse.ArgumentParser()
-    ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--config", default="decode", choices=sorted(W.CONFIGS))
-    ap.add_argument("--rotate", type=int, default=4, help="distinct activation batches")
-    ap.add_argument("--cold", action="store_true")
-    ap.add_argument("--no-weight-rotation", action="store_true",
-                    help="skip the timing with two alternating sets of expert weights")
-    ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-max-tokens", type=int, default=16)
-    ap.add_argument("--copy-calibration", action="store_true")
-    ap.add_argument("--layer-only", action="store_true",
-                    help="skip the router-projection, DSA-indexer and sparse-attention legs (counter passes)")
-    args = ap.parse_args()
-
-    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
-        print("bench.py: the library runs on one GPU (it has no multi-GPU path); use --gpus 1",
-              file=sys.stderr)
-        sys.exit(2)
-    if not torch.cuda.is_available():
-        print("bench.py: no GPU visible", file=sys.stderr)
-        sys.exit(2)
-    if args.copy_calibration:
-        copy_calibration()
-        return
-
-    cfg = W.CONFIGS[args.config]
+def run_config(cfg, steps: int, warmup: int, rotate: int, cold_calls: int, weights_rotated: bool,
+               cpu_tokens: int, with_cpu: bool):
+    """Times one workload; returns its result object (and the call closure data
+    the extra legs reuse)."""
     shape = M.Shape.of(cfg)
     dev = "cuda"
     weights = W.gen_weights(cfg, 0, device=dev)
     _, bias, _ = W.gen_router(cfg, 0, device=dev)
     batches = []
-    for seed in range(args.rotate):
+    for seed in range(rotate):
         logits, _, _ = W.gen_router(cfg, seed, device=dev)
         hidden, hscale = W.gen_hidden(cfg, seed, device=dev)
         batches.append(dict(logits=logits, bias=bias, hidden=hidden, hidden_scale=hscale))
@@ -435,15 +446,13 @@ def main():
         else:
             c.staged(events, nst + 1)
 
-    for i in range(args.warmup):
+    for i in range(warmup):
         call(i)
     torch.cuda.synchronize()
 
     # The host enqueues a call (ctypes + one launch per kernel) more slowly
-    # than the GPU can run small batches, which would leave the GPU idle
-    # between kernels.  Each timed region therefore starts behind a GPU spin
-    # long enough for the host to enqueue all K calls, so the calls run back to
-    # back; the host's own cost per call is reported separately.
+    # than the GPU runs small batches; each timed region starts behind a GPU
+    # spin long enough for the host to enqueue all calls.
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     e0.record(stream)
     torch.cuda._sleep(10_000_000)
@@ -451,7 +460,7 @@ def main():
     torch.cuda.synchronize()
     cycles_per_ms = 10_000_000 / max(e0.elapsed_time(e1), 1e-3)
 
-    K = args.steps
+    K = steps
     h0 = time.perf_counter()
     for i in range(K):
         call(i)
@@ -462,7 +471,7 @@ def main():
         ms = host_ms if enqueue_ms is None else enqueue_ms
         torch.cuda._sleep(int((2.0 * ms + 2.0) * cycles_per_ms))
 
-    # timed region 1: plain calls -> value
+    # timed region 1: plain calls
     t_start = torch.cuda.Event(enable_timing=True)
     t_end = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
@@ -475,12 +484,11 @@ def main():
     enq_ms = (time.perf_counter() - wall0) * 1e3
     torch.cuda.synchronize()
     wall = time.perf_counter() - wall0
-    ms_total = t_start.elapsed_time(t_end)
-    ms_per_step = ms_total / K
+    ms_per_step = t_start.elapsed_time(t_end) / K
 
     # timed region 2: the same calls with a HIP event around every kernel
     evs = [[torch.cuda.Event(enable_timing=True) for _ in range(nst + 1)] for _ in range(K)]
-    ev_arrays = [M.event_array(row) for row in evs]  # HIP events created before timing
+    ev_arrays = [M.event_array(row) for row in evs]
     torch.cuda.synchronize()
     prefill()
     for i in range(K):
@@ -512,20 +520,16 @@ def main():
         ach = g1_flop / (g1_ms * 1e-3) / 1e12
         roof = {"bound": "mfma", "achieved": round(ach, 2), "peak": FP8_PEAK_TFLOPS, "unit": "TFLOP/s",
                 "frac": round(ach / FP8_PEAK_TFLOPS, 4)}
+    roof["traffic"] = read_traffic(cfg.name)
     roof["kernel"] = "gemm1_swiglu"
     roof["avg_launch_us"] = round(g1_ms * 1e3, 2)
     roof["algorithmic_bytes_per_launch"] = int(g1bytes)
-    traffic = read_traffic(cfg.name)
-    roof["traffic"] = traffic
+    roof["flop_per_launch"] = int(g1_flop)
 
-    # timed region 3: the calls alternating between two independent sets of
-    # expert weights, so that no call finds its weights in the Infinity Cache
-    # left by the call before it (between two calls on one set, the other set
-    # streams more weight bytes than the cache holds): the rate of the weight
-    # streams from HBM, as a model that runs other layers between calls of
-    # this one sees it
+    # the calls alternating between two independent sets of expert weights (no
+    # call finds its weights in the Infinity Cache left by the call before it)
     rotated = None
-    if not args.no_weight_rotation:
+    if weights_rotated:
         weights2 = W.gen_weights(cfg, 1, device=dev)
         calls2 = [M.FusedCall(shape, b["hidden"], b["hidden_scale"], b["logits"], b["bias"], *weights2,
                               out, ws, stream=stream) for b in batches]
@@ -544,71 +548,172 @@ def main():
         del calls2, sets, weights2
         torch.cuda.empty_cache()
 
-    cold = cold_p10 = cold_p90 = None
-    if args.cold:
-        flush = torch.empty(512 << 20, dtype=torch.uint8, device=dev)
+    # cold calls: a read-only sweep of 1 GiB before each (outside the timed
+    # interval) evicts L2 and the Infinity Cache and leaves no dirty lines
+    cold = None
+    if cold_calls > 0:
+        sweep = torch.ones(1 << 28, dtype=torch.float32, device=dev)
         times = []
-        for i in range(min(K, 10)):
-            flush.fill_(i & 0xFF)
-            e0 = torch.cuda.Event(enable_timing=True)
-            e1 = torch.cuda.Event(enable_timing=True)
-            e0.record(stream)
+        for i in range(cold_calls):
+            sweep.sum()
+            a0 = torch.cuda.Event(enable_timing=True)
+            a1 = torch.cuda.Event(enable_timing=True)
+            a0.record(stream)
             call(i)
-            e1.record(stream)
+            a1.record(stream)
             torch.cuda.synchronize()
-            times.append(e0.elapsed_time(e1))
-        cold = round(float(np.median(times)) * 1e3, 2)
-        cold_p10, cold_p90 = (round(float(np.percentile(times, q)) * 1e3, 2) for q in (10, 90))
+            times.append(a0.elapsed_time(a1))
+        cold = {"median": round(float(np.median(times)) * 1e3, 2),
+                "p10": round(float(np.percentile(times, 10)) * 1e3, 2),
+                "p90": round(float(np.percentile(times, 90)) * 1e3, 2), "calls": cold_calls}
+        del sweep
+
+    cpu = None
+    if with_cpu:
+        cpu = cpu_baseline(cfg, batches[0], weights, cpu_tokens)
+
+    rec = {
+        "workload": f"{cfg.name}: T={cfg.T}, H={cfg.H}, I={cfg.I}, {cfg.num_local_experts} of "
+                    f"{cfg.num_experts} experts resident, top-{cfg.top_k} of {cfg.topk_group}/"
+                    f"{cfg.n_group} groups" + (f", {cfg.hot_experts} hot experts (+{cfg.hot_bias} bias)"
+                                               if cfg.hot_experts else ""),
+        "us_per_call": round(us, 2),
+        "ms_per_step": round(ms_per_step, 5),
+        "steps": K,
+        "tflops": round(tflops, 3),
+        "pct_fp8_mfma_peak": round(100 * tflops / FP8_PEAK_TFLOPS, 3),
+        "gbps": round(gbs, 1),
+        "pct_hbm_peak": round(100 * gbs / HBM_PEAK_GBS, 2),
+        "binding_roof": "mfma" if tflops / FP8_PEAK_TFLOPS > gbs / HBM_PEAK_GBS else "hbm",
+        "pct_binding_roofline": round(100 * max(tflops / FP8_PEAK_TFLOPS, gbs / HBM_PEAK_GBS), 2),
+        "resident_pairs_avg": P_avg,
+        "touched_experts_avg": T_avg,
+        "batches": rotate,
+        "stage_us": {n: round(float(v) * 1e3, 2) for n, v in zip(names, stage_avg)},
+        "roofline": roof,
+        "us_per_call_cold": cold,
+        "us_per_call_weights_rotated": rotated,
+        "host_enqueue_us_per_call": round(host_ms * 1e3 / K, 1),
+        "prefill_covered_enqueue": bool(enq_ms < 2.0 * host_ms + 2.0),
+        "host_wall_s": round(wall, 3),
+        "shader_clock_mhz_spin": round(cycles_per_ms / 1e3, 1),
+        "cpu_baseline": cpu,
+    }
+    extras = dict(shape=shape, batches=batches, weights=weights, out=out, ws=ws, stream=stream,
+                  prefill=prefill)
+    return rec, extras
+
+
+# the metric's workloads, in order; the last one is the line's `value`
+METRIC_CONFIGS = ("decode", "mid", "prefill", "skewed")
+# CPU oracle sample per workload: tokens (all threads); single-thread tokens
+CPU_TOKENS = {"tiny": 8, "decode": 16, "mid": 256, "prefill": 1024, "skewed": 384, "median": 64,
+              "long": 1024}
+CPU_TOKENS_1T = {"tiny": 8, "decode": 16, "mid": 16}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--config", default=None, choices=sorted(W.CONFIGS),
+                    help="time one workload only (default: decode, mid, prefill, skewed)")
+    ap.add_argument("--rotate", type=int, default=4, help="distinct activation batches")
+    ap.add_argument("--cold-calls", type=int, default=10)
+    ap.add_argument("--no-weight-rotation", action="store_true",
+                    help="skip the timing with two alternating sets of expert weights (decode)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true")
+    ap.add_argument("--layer-only", action="store_true",
+                    help="skip the router-projection, DSA-indexer and sparse-attention legs")
+    args = ap.parse_args()
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py: this build runs on one GPU only (no multi-GPU path; how the layer would "
+              "shard by expert is described in the design notes); use --gpus 1", file=sys.stderr)
+        sys.exit(2)
+    if not torch.cuda.is_available():
+        print("bench.py: no GPU visible", file=sys.stderr)
+        sys.exit(2)
+    if args.copy_calibration:
+        copy_calibration()
+        return
+
+    names = (args.config,) if args.config else METRIC_CONFIGS
+    clock_before = gpu_clock()
+    configs = {}
+    extras = None
+    for name in names:
+        cfg = W.CONFIGS[name]
+        last = name == names[-1]
+        K = args.steps if last else max(args.steps, 20)
+        print(f"bench: {name} ...", file=sys.stderr, flush=True)
+        rec, ex = run_config(cfg, K, args.warmup, args.rotate, args.cold_calls,
+                             weights_rotated=(name == "decode" and not args.no_weight_rotation),
+                             cpu_tokens=CPU_TOKENS.get(name, 16), with_cpu=not args.no_cpu_baseline)
+        configs[name] = rec
+        if name == "decode" or (extras is None and last):
+            extras = (cfg, ex)
+        else:
+            del ex
+        torch.cuda.empty_cache()
+    clock_after = gpu_clock()
 
     router = indexer = attention = None
     if not args.layer_only:
-        router = router_projection_leg(cfg, shape, batches, weights, out, ws, stream, K, prefill)
-        indexer = indexer_leg(K, prefill, not args.no_cpu_baseline)
-        attention = attention_leg(K, prefill, not args.no_cpu_baseline)
+        cfg0, ex = extras
+        router = router_projection_leg(cfg0, ex["shape"], ex["batches"], ex["weights"], ex["out"], ex["ws"],
+                                       ex["stream"], 20, ex["prefill"])
+        indexer = indexer_leg(20, ex["prefill"], not args.no_cpu_baseline)
+        attention = attention_leg(20, ex["prefill"], not args.no_cpu_baseline)
 
+    head = configs[names[-1]]
     cpu = None
     if not args.no_cpu_baseline:
-        cpu = cpu_baseline(cfg, batches, weights, args.cpu_max_tokens)
+        cpu = dict(head["cpu_baseline"])
+        cpu.update(cpu_info())
+        cpu["per_config_us_per_call"] = {n: (c["cpu_baseline"] or {}).get("value") for n, c in configs.items()}
+        # single-thread oracle on the small workloads (bounded samples)
+        single = {}
+        for n in ("tiny", "decode", "mid"):
+            cfg = W.CONFIGS[n]
+            wts = W.gen_weights(cfg, 0, device="cuda")
+            lg, bs, _ = W.gen_router(cfg, 0, device="cuda")
+            hq, hs = W.gen_hidden(cfg, 0, device="cuda")
+            b = cpu_baseline(cfg, dict(logits=lg, bias=bs, hidden=hq, hidden_scale=hs), wts,
+                             CPU_TOKENS_1T[n], threads=1)
+            single[n] = {k: b[k] for k in ("value", "unit", "cores", "sample", "wall_s", "extrapolated")}
+            del wts
+        cpu["single_thread"] = single
+        torch.cuda.empty_cache()
 
     rec = {
         "metric": METRIC,
-        "value": round(us, 2),
+        "value": head["us_per_call"],
         "unit": "us/call",
         "n_gpus": 1,
-        "steps": K,
+        "steps": head["steps"],
         "warmup": args.warmup,
-        "ms_per_step": round(ms_per_step, 5),
+        "ms_per_step": head["ms_per_step"],
         "higher_is_better": False,
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "fp8e4m3 (fp32 accumulate)",
         "data": "synthetic (seeded; DeepSeek-V3 shapes)",
-        "config": {"workload": f"{cfg.name}: T={cfg.T}, H={cfg.H}, I={cfg.I}, {cfg.num_local_experts} of "
-                               f"{cfg.num_experts} experts resident, top-{cfg.top_k} of {cfg.topk_group}/"
-                               f"{cfg.n_group} groups",
-                   "T": cfg.T, "H": cfg.H, "I": cfg.I, "num_experts": cfg.num_experts,
-                   "num_local_experts": cfg.num_local_experts, "top_k": cfg.top_k,
-                   "batches": args.rotate, "resident_pairs_avg": P_avg, "touched_experts_avg": T_avg},
-        "tflops": round(tflops, 4),
-        "pct_fp8_mfma_peak": round(100 * tflops / FP8_PEAK_TFLOPS, 4),
-        "gbps": round(gbs, 1),
-        "pct_hbm_peak": round(100 * gbs / HBM_PEAK_GBS, 2),
-        # the layer against its binding roof: max(t_MFMA, t_HBM) / t
-        "binding_roof": "mfma" if tflops / FP8_PEAK_TFLOPS > gbs / HBM_PEAK_GBS else "hbm",
-        "pct_binding_roofline": round(100 * max(tflops / FP8_PEAK_TFLOPS, gbs / HBM_PEAK_GBS), 2),
-        "stage_us": {n: round(float(v) * 1e3, 2) for n, v in zip(names, stage_avg)},
-        "roofline": roof,
+        "config": {"workload": head["workload"], "configs_timed": list(names)},
+        "tflops": head["tflops"],
+        "pct_fp8_mfma_peak": head["pct_fp8_mfma_peak"],
+        "gbps": head["gbps"],
+        "pct_hbm_peak": head["pct_hbm_peak"],
+        "roofline": head["roofline"],
         "cpu_baseline": cpu,
+        "configs": configs,
+        "gpu_clock_before": clock_before,
+        "gpu_clock_after": clock_after,
         "router_projection": router,
         "dsa_topk_indexer": indexer,
         "dsa_sparse_attention": attention,
-        "us_per_call_weights_rotated": rotated,
-        "us_per_call_cold": cold,
-        "us_per_call_cold_p10": cold_p10,
-        "us_per_call_cold_p90": cold_p90,
-        "host_enqueue_us_per_call": round(host_ms * 1e3 / K, 1),
-        "prefill_covered_enqueue": bool(enq_ms < 2.0 * host_ms + 2.0),
-        "host_wall_s": round(wall, 3),
     }
     print(json.dumps(rec))
 

@@ -96,6 +96,8 @@ def lib():
         L.oracle_dsa_topk.restype = ctypes.c_int
         L.oracle_num_threads.argtypes = []
         L.oracle_num_threads.restype = ctypes.c_int
+        L.oracle_set_num_threads.argtypes = [ctypes.c_int]
+        L.oracle_set_num_threads.restype = None
         _lib = L
     return _lib
 
@@ -351,6 +353,11 @@ def forward(shape: Shape, hidden, hidden_scale, logits, bias, w13, w13_scale, w2
 
 def num_threads() -> int:
     return lib().oracle_num_threads()
+
+
+def set_num_threads(n: int) -> None:
+    """Threads of the oracle's parallel loops from now on."""
+    lib().oracle_set_num_threads(int(n))
 
 
 def bf16_bits_to_float(bits: np.ndarray) -> np.ndarray:

@@ -804,6 +804,16 @@ int oracle_num_threads(void) {
 #endif
 }
 
+/* Threads of the parallel loops above (n < 1: leave unchanged).  Used to
+ * time the oracle on one core. */
+void oracle_set_num_threads(int n) {
+#ifdef _OPENMP
+  if (n >= 1) omp_set_num_threads(n);
+#else
+  (void)n;
+#endif
+}
+
 /* ======================================================================== */
 /* DSA TopK Indexer (paper Section 3.1.3): for each batch element b, score   */
 /* every cached token j < seq_len[b] of the sequence against the query's    */
