@@ -141,6 +141,28 @@ moe_status_t moe_fused_fp8(const moe_shape_t *s, const uint8_t *hidden,
                            const moe_route_out_t *route_out, void *workspace,
                            size_t ws_bytes, void *stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc):
+ * moe_fused_fp8 without a workspace argument.  The workspace is a 32 MiB
+ * device array inside the library, one per GPU, held until the process ends
+ * (its address is looked up on the first call on each device).  Arguments,
+ * outputs and determinism as moe_fused_fp8; shapes whose workspace
+ * (moe_workspace_size) exceeds 32 MiB return MOE_ERR_UNSUPPORTED before
+ * anything is enqueued (DeepSeek-V3 shapes: up to about 100 tokens).  Every
+ * call on one GPU uses that GPU's array: calls that overlap in time on one
+ * GPU (other streams, other threads) race and must be serialised by the
+ * caller.  The array needs no initialisation; nothing is read across calls.
+ * No hipMalloc, hipFree or allocating library routine is called. */
+moe_status_t moe_fused_fp8_noalloc(const moe_shape_t *s, const uint8_t *hidden,
+                                   const float *hidden_scale,
+                                   const float *router_logits,
+                                   const float *routing_bias,
+                                   const uint8_t *w13, const float *w13_scale,
+                                   const uint8_t *w2, const float *w2_scale,
+                                   uint16_t *out,
+                                   const moe_route_out_t *route_out,
+                                   void *stream);
+
 /* moe_fused_fp8 with the router projection of stage (1) on the device:
  * router_weight [E_g, H] float replaces router_logits; the logits are those
  * defined under moe_route_hidden.  Everything else as moe_fused_fp8 (the

@@ -10,6 +10,7 @@ Entry points (same names as the C-ABI):
   workspace_size(shape)               bytes of scratch the calls need
   route(shape, logits, bias, ...)     stage (1) + stage (2) bookkeeping
   fused_fp8(shape, ...)               the whole layer, bf16 output
+  fused_fp8_noalloc(shape, ...)       the same with the library's own scratch (no allocation)
   fused_fp8_staged(..., events)       same, recording an event before each kernel
 """
 from __future__ import annotations
@@ -26,7 +27,7 @@ LIB_PATH = os.path.join(_HERE, "libmoe.so")
 MOE_OK, MOE_ERR_INVALID_ARG, MOE_ERR_UNSUPPORTED, MOE_ERR_WORKSPACE_TOO_SMALL, MOE_ERR_HIP = range(5)
 
 EXPORTED = ("moe_workspace_size", "moe_route", "moe_route_hidden", "moe_fused_fp8",
-            "moe_fused_fp8_router", "moe_fused_fp8_staged", "moe_num_stages", "moe_stage_name",
+            "moe_fused_fp8_router", "moe_fused_fp8_staged", "moe_fused_fp8_noalloc", "moe_num_stages", "moe_stage_name",
             "moe_status_string", "moe_debug_sigmoid", "moe_debug_e4m3_encode",
             "moe_debug_act_views", "moe_debug_mfma_block", "moe_debug_router_logits",
             "moe_debug_combine_from_act",
@@ -96,6 +97,8 @@ def lib() -> ctypes.CDLL:
         L.moe_route.restype = ctypes.c_int
         L.moe_fused_fp8.argtypes = [S, P, P, P, P, P, P, P, P, P, R, P, Z, P]
         L.moe_fused_fp8.restype = ctypes.c_int
+        L.moe_fused_fp8_noalloc.argtypes = [S, P, P, P, P, P, P, P, P, P, R, P]
+        L.moe_fused_fp8_noalloc.restype = ctypes.c_int
         L.moe_route_hidden.argtypes = [S, P, P, P, P, R, P, Z, P]
         L.moe_route_hidden.restype = ctypes.c_int
         L.moe_fused_fp8_router.argtypes = [S, P, P, P, P, P, P, P, P, P, R, P, Z, P]
@@ -246,7 +249,8 @@ def _fused_args(shape, hidden, hidden_scale, logits, bias, w13, w13_scale, w2, w
             _dev(w2, torch.uint8, "w2"), _dev(w2_scale, torch.float32, "w2_scale"),
             _dev(out, torch.bfloat16, "out"),
             ctypes.byref(_route_struct(route_out)) if route_out is not None else None,
-            _dev(workspace, torch.uint8, "workspace"), ctypes.c_size_t(workspace.numel())]
+            ] + ([] if workspace is None else
+                 [_dev(workspace, torch.uint8, "workspace"), ctypes.c_size_t(workspace.numel())])
 
 
 def fused_fp8(shape: Shape, hidden, hidden_scale, logits, bias, w13, w13_scale, w2, w2_scale,
@@ -260,6 +264,18 @@ def fused_fp8(shape: Shape, hidden, hidden_scale, logits, bias, w13, w13_scale, 
     args = _fused_args(shape, hidden, hidden_scale, logits, bias, w13, w13_scale, w2, w2_scale,
                        out, route_out, workspace)
     _check("moe_fused_fp8", lib().moe_fused_fp8(*args, _stream(stream)))
+    return out
+
+
+def fused_fp8_noalloc(shape: Shape, hidden, hidden_scale, logits, bias, w13, w13_scale, w2,
+                      w2_scale, out: torch.Tensor, route_out: dict | None = None,
+                      stream=None) -> torch.Tensor:
+    """The whole layer with the library's own per-GPU scratch instead of a
+    workspace (moe_fused_fp8_noalloc): for callers that cannot allocate, so
+    `out` [T, H] bf16 is required.  Overlapping calls on one GPU race."""
+    args = _fused_args(shape, hidden, hidden_scale, logits, bias, w13, w13_scale, w2, w2_scale,
+                       out, route_out, None)
+    _check("moe_fused_fp8_noalloc", lib().moe_fused_fp8_noalloc(*args, _stream(stream)))
     return out
 
 

@@ -6,6 +6,7 @@
 
 #include <cmath>
 #include <cstdint>
+#include <mutex>
 
 #include "../../include/moe.h"
 #include "../../include/moe_debug.h"
@@ -339,6 +340,35 @@ moe_status_t fused_impl(const moe_shape_t *s, const uint8_t *hidden, const float
   return MOE_OK;
 }
 
+// ---- the allocation-free entry point's workspace: a file-scope device array
+// (each GPU the library runs on holds its own copy until the process ends).
+// Host code never uses the array's name as an address: its device address is
+// taken once per device with hipGetSymbolAddress, with that device current.
+constexpr size_t kScratchBytes = size_t(32) << 20;
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void *g_scratch_ptr[kMaxDevices];
+
+}  // namespace
+
+static __device__ __align__(256) uint8_t scratch[kScratchBytes];
+
+namespace {
+
+moe_status_t scratch_of_current_device(void **ptr) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess) return MOE_ERR_HIP;
+  if (dev < 0 || dev >= kMaxDevices) return MOE_ERR_UNSUPPORTED;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void *p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return MOE_ERR_HIP;
+    g_scratch_ptr[dev] = p;
+  }
+  *ptr = g_scratch_ptr[dev];
+  return MOE_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -408,6 +438,21 @@ moe_status_t moe_fused_fp8(const moe_shape_t *s, const uint8_t *hidden, const fl
                            void *workspace, size_t ws_bytes, void *stream) {
   return fused_impl(s, hidden, hidden_scale, router_logits, nullptr, routing_bias, w13, w13_scale,
                     w2, w2_scale, out, route_out, workspace, ws_bytes, stream, nullptr, 0);
+}
+
+moe_status_t moe_fused_fp8_noalloc(const moe_shape_t *s, const uint8_t *hidden,
+                                   const float *hidden_scale, const float *router_logits,
+                                   const float *routing_bias, const uint8_t *w13,
+                                   const float *w13_scale, const uint8_t *w2,
+                                   const float *w2_scale, uint16_t *out,
+                                   const moe_route_out_t *route_out, void *stream) {
+  moe_status_t rc = check_shape(s);
+  if (rc != MOE_OK) return rc;
+  if (make_plan(s).total > kScratchBytes) return MOE_ERR_UNSUPPORTED;
+  void *ws = nullptr;
+  if ((rc = scratch_of_current_device(&ws)) != MOE_OK) return rc;
+  return fused_impl(s, hidden, hidden_scale, router_logits, nullptr, routing_bias, w13, w13_scale,
+                    w2, w2_scale, out, route_out, ws, kScratchBytes, stream, nullptr, 0);
 }
 
 moe_status_t moe_fused_fp8_router(const moe_shape_t *s, const uint8_t *hidden,
