@@ -61,6 +61,7 @@ struct Plan {
   bool narrow1;  // GEMM1 split over 32- (or 16-) column groups (small batches)
   bool gu1;      // ... and over gate and up rows (the fewest rows per expert)
   bool tile;     // large-tile kernels (BM >= 64)
+  bool fused_combine;  // GEMM2 with the combine in its epilogue (T <= 16)
   int64_t P_max;
   size_t off_ids, off_w, off_offsets, off_perm_token, off_perm_pair, off_pair_row, off_chunk_counts,
       off_tile_base, off_n_items, off_act, off_act_scale, off_abuf, off_Y, off_partials, total;
@@ -91,6 +92,9 @@ Plan make_plan(const moe_shape_t *s) {
   p.NB1 = p.narrow1 ? s->I / gemm1_narrow_cols(p.gu1) : s->I / 128;
   // GEMM2 column blocks: 128 wide for the small-tile kernel, 256 otherwise
   p.NB2 = p.BM == 16 ? s->H / 128 : (s->H + 255) / 256;
+  // at most 16 tokens: one 16-row tile per expert, and GEMM2 workgroups that
+  // own output columns of every token sum the experts themselves
+  p.fused_combine = p.BM == 16 && s->T <= combine_max_tokens();
   p.nchunks = (int)((s->T + kChunkTokens - 1) / kChunkTokens);
   if (p.nchunks < 1) p.nchunks = 1;
   const int64_t touched = TK < s->num_local_experts ? TK : s->num_local_experts;
@@ -256,6 +260,14 @@ moe_status_t enqueue_gemm2_combine(const moe_shape_t *s, const Plan &pl, const P
   g2.NB = pl.NB2;
   g2.S = pl.S2;
   mark();
+  if (pl.fused_combine) {
+    const int KB = s->I / 128;
+    CombineParams c{at<int32_t>(ws, pl.off_perm_pair), r.w, out, s->T, s->top_k,
+                    KB % 4 == 0 ? 4 : (KB % 2 == 0 ? 2 : 1)};
+    MOE_TRY_HIP(launch_gemm2_combine(g2, c, st));
+    mark();  // the combine stage enqueues nothing of its own
+    return MOE_OK;
+  }
   const int grid2 = round8((int64_t)pl.max_tiles * pl.NB2 * pl.S2);
   MOE_TRY_HIP(pl.tile ? launch_gemm_tile(g2, false, pl.BM, grid2, st)
                       : launch_gemm2(g2, pl.BM, grid2, st));

@@ -748,6 +748,183 @@ __global__ __launch_bounds__(256) void finalize_kernel(FinalizeParams p) {
   *reinterpret_cast<uint4 *>(p.out + (size_t)t * p.H + n0) = o;
 }
 
+// GEMM2 and the weighted combine of stage (4) in one kernel, for batches of at
+// most 16 tokens (every resident expert then has a single 16-row tile).  A
+// workgroup owns 16 output columns of every token.  Each tile's K range is cut
+// into C chunks, and chunk u of the batch goes to wave u % NW: the wave
+// streams the 16 weight rows of its columns against the chunk's activation
+// rows (one MFMA per 128-K block, promoted by the row and block scales, as in
+// the other GEMM kernels) and at the chunk's end adds w_pair * partial into
+// its own LDS accumulator at the pair's token.  The waves' accumulators are
+// then summed in wave order and every output element is rounded to bf16
+// once.  No fp32 Y goes to memory and no combine launch follows; the
+// summation order is fixed, so the output is deterministic.  The chunks keep
+// the waves evenly loaded whatever the number of resident experts.  The
+// activation rows (when all P fit), their scales and the tiles' weight-block
+// scales are staged in LDS once, so the K loop's only global loads are the
+// weight fragments.
+constexpr int kCombineWaves = 8;
+constexpr int kCombineTokens = 16;
+constexpr int kCombineStageBytes = 48 * 1024;  // LDS for the activation rows
+
+struct CombineLayout {
+  int P_max, KB, stage_rows, astride;
+  __host__ __device__ CombineLayout(int P_max_, int I) : P_max(P_max_), KB(I / 128) {
+    astride = I + 16;
+    stage_rows = kCombineStageBytes / astride;
+  }
+  __host__ __device__ int sa() const { return 5 * P_max; }                 // [P_max, KB] f32
+  __host__ __device__ int sw() const { return sa() + P_max * KB; }         // [tiles, KB] f32
+  __host__ __device__ int act() const { return sw() + P_max * KB; }        // rows, in ints
+  __host__ __device__ size_t bytes() const {
+    return sizeof(int) * (size_t)act() + (size_t)stage_rows * astride;
+  }
+};
+
+template <int D>
+__global__ __launch_bounds__(kCombineWaves * kWave) void gemm2_combine_kernel(GemmParams p,
+                                                                             CombineParams c) {
+  constexpr int NW = kCombineWaves;
+  constexpr int NT = NW * kWave;
+  __shared__ int tb[1028];
+  __shared__ float acc_l[NW][kCombineTokens][16];
+  extern __shared__ __attribute__((aligned(16))) int dyn[];
+  const CombineLayout Ly(p.P_max, p.K);
+  int *t_e = dyn;                    // per tile: expert, first row, rows
+  int *t_row0 = dyn + p.P_max;
+  int *t_n = dyn + 2 * p.P_max;
+  int *r_tok = dyn + 3 * p.P_max;    // per permuted row: token, weight
+  float *r_w = reinterpret_cast<float *>(dyn + 4 * p.P_max);
+  float *sa_l = reinterpret_cast<float *>(dyn + Ly.sa());
+  float *sw_l = reinterpret_cast<float *>(dyn + Ly.sw());
+  uint8_t *a_l = reinterpret_cast<uint8_t *>(dyn + Ly.act());
+
+  const int tid = threadIdx.x;
+  const int lane = tid & (kWave - 1);
+  const int wave = tid / kWave;
+  const int r16 = lane & 15;
+  const int srow = 4 * (lane >> 4);
+  const int frag_off = (lane >> 4) * 32;
+  const int col0 = blockIdx.x * 16;
+  const int KB = p.KB;
+  const size_t K = (size_t)p.K;
+
+  for (int i = tid; i <= p.El; i += NT) tb[i] = p.tile_base[i];
+  for (int i = tid; i < NW * kCombineTokens * 16; i += NT) (&acc_l[0][0][0])[i] = 0.0f;
+  __syncthreads();
+  const int n_tiles = tb[p.El];
+  const int P = p.expert_offsets[p.El];
+  for (int q = tid; q < n_tiles; q += NT) {
+    int lo = 0, hi = p.El;
+    while (hi - lo > 1) {
+      const int mid = (lo + hi) >> 1;
+      if (tb[mid] <= q) lo = mid; else hi = mid;
+    }
+    const int row0 = p.expert_offsets[lo] + 16 * (q - tb[lo]);
+    t_e[q] = lo;
+    t_row0[q] = row0;
+    t_n[q] = min(16, p.expert_offsets[lo + 1] - row0);
+  }
+  __syncthreads();
+
+  // this wave's steps: unit j of the wave is chunk u = wave + NW j of the
+  // batch, i.e. tile u / C, K blocks [(u % C) L, (u % C) L + L)
+  const int L = KB / c.C;
+  const int n_units = n_tiles * c.C;
+  const int my_units = n_units > wave ? (n_units - wave + NW - 1) / NW : 0;
+  const int steps = my_units * L;
+  const bool alds = P <= Ly.stage_rows;
+  const uint8_t *wcol = p.B + ((size_t)col0 + r16) * K + frag_off;
+  const size_t w_exp = (size_t)p.N_total * K;
+
+  v8i ra[D], rb[D];
+  // loads of step s (clamped to the last step, so every load is in bounds)
+  auto issue = [&](int d, int s) {
+    s = min(s, steps - 1);
+    const int u = wave + NW * (s / L);
+    const int q = u / c.C;
+    const int kb = (u % c.C) * L + s % L;
+    rb[d] = *reinterpret_cast<const v8i *>(wcol + t_e[q] * w_exp + (size_t)kb * 128);
+    if (!alds) {
+      const int arow = t_row0[q] + min(r16, t_n[q] - 1);
+      ra[d] = *reinterpret_cast<const v8i *>(p.A + (size_t)arow * K + (size_t)kb * 128 + frag_off);
+    }
+  };
+  if (steps > 0) {
+#pragma unroll
+    for (int d = 0; d < D; ++d) issue(d, d);
+  }
+
+  // stage the rows' tokens and weights, the activation scales, the tiles'
+  // weight-block scales and (when they fit) the activation rows
+  for (int r = tid; r < P; r += NT) {
+    const int pp = c.perm_pair[r];
+    r_tok[r] = pp / c.K;
+    r_w[r] = c.topk_w[pp];
+  }
+  for (int i = tid; i < P * KB; i += NT) sa_l[i] = p.A_scale[i];
+  for (int i = tid; i < n_tiles * KB; i += NT) {
+    const int q = i / KB, kb = i % KB;
+    sw_l[i] = p.B_scale[((size_t)t_e[q] * (p.N_total / 128) + col0 / 128) * KB + kb];
+  }
+  if (alds) {
+    const int cpr = p.K / 16;  // 16-byte chunks per row
+    for (int i = tid; i < P * cpr; i += NT) {
+      const int r = i / cpr, off = (i % cpr) * 16;
+      *reinterpret_cast<u32x4 *>(a_l + r * Ly.astride + off) =
+          *reinterpret_cast<const u32x4 *>(p.A + (size_t)r * K + off);
+    }
+  }
+  __syncthreads();
+
+  if (steps > 0) {
+    v4f acc = {0.f, 0.f, 0.f, 0.f};
+    for (int base = 0; base < steps; base += D) {
+#pragma unroll
+      for (int d = 0; d < D; ++d) {
+        const int s = base + d;
+        if (s < steps) {
+          const int u = wave + NW * (s / L);
+          const int q = u / c.C;
+          const int kb = (u % c.C) * L + s % L;
+          const int row0 = t_row0[q], n = t_n[q];
+          const v8i af = alds ? lds_frag(a_l + (row0 + min(r16, n - 1)) * Ly.astride + kb * 128 + frag_off)
+                              : ra[d];
+          const v4f z = {0.f, 0.f, 0.f, 0.f};
+          const v4f t = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(af, rb[d], z, 0, 0, 0, 0, 0, 0);
+          const float sw = sw_l[q * KB + kb];
+#pragma unroll
+          for (int i = 0; i < 4; ++i)
+            acc[i] = __builtin_fmaf(t[i], sa_l[(row0 + min(srow + i, n - 1)) * KB + kb] * sw, acc[i]);
+          if (s % L == L - 1) {
+            // the chunk is complete: weight its rows into their tokens
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+              const int r = srow + i;
+              if (r < n) {
+                float *a = &acc_l[wave][r_tok[row0 + r]][r16];
+                *a = __builtin_fmaf(r_w[row0 + r], acc[i], *a);
+              }
+              acc[i] = 0.0f;
+            }
+          }
+          issue(d, s + D);
+        }
+      }
+    }
+  }
+  __syncthreads();
+  if (tid < kCombineTokens * 16) {
+    const int t = tid >> 4, col = tid & 15;
+    if (t < c.T) {
+      float sum = 0.0f;
+#pragma unroll
+      for (int w = 0; w < NW; ++w) sum += acc_l[w][t][col];
+      c.out[(size_t)t * p.H + col0 + col] = f32_to_bf16_rne(sum);
+    }
+  }
+}
+
 template <int BM, bool G1>
 hipError_t launch_gemm_bm(const GemmParams &p, int grid, hipStream_t st) {
   auto k = gemm_kernel<BM, G1>;
@@ -855,6 +1032,21 @@ hipError_t launch_finalize(const FinalizeParams &p, hipStream_t st) {
     hipLaunchKernelGGL(finalize_kernel<8>, grid, dim3(256), 0, st, p);
   else
     hipLaunchKernelGGL(finalize_kernel<16>, grid, dim3(256), 0, st, p);
+  return hipGetLastError();
+}
+
+int combine_max_tokens() { return kCombineTokens; }
+
+hipError_t launch_gemm2_combine(const GemmParams &p, const CombineParams &c, hipStream_t st) {
+  if (c.T <= 0) return hipSuccess;
+  if (c.T > kCombineTokens || p.KB % c.C || p.H % 16) return hipErrorInvalidValue;
+  auto k = gemm2_combine_kernel<kStreamDepth>;
+  const size_t lds = CombineLayout(p.P_max, p.K).bytes();
+  if (lds > 96 * 1024) return hipErrorInvalidValue;
+  static hipError_t attr = hipFuncSetAttribute(reinterpret_cast<const void *>(k),
+                                               hipFuncAttributeMaxDynamicSharedMemorySize, 96 * 1024);
+  if (attr != hipSuccess) return attr;
+  hipLaunchKernelGGL(k, dim3(p.H / 16), dim3(kCombineWaves * kWave), lds, st, p, c);
   return hipGetLastError();
 }
 

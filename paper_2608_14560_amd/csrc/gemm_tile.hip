@@ -6,8 +6,7 @@
 // K range.  Items of one expert are ordered in groups of four column blocks:
 // all M-tiles of a group, column block fastest, so the items an XCD runs side
 // by side share four weight panels and a few A tiles in that XCD's L2
-// (workgroup b runs item (b % 8) * ceil(n/8) + b / 8, and workgroups are
-// dispatched round-robin over the 8 XCDs).
+// (tile_item below maps workgroups to items).
 //
 // One workgroup of 4 x WM waves per item.  Wave (wm, wn) = (wave / 4,
 // wave % 4) owns rows [16 MT wm, 16 MT (wm+1)) of the tile (BM = 16 MT WM)
@@ -89,6 +88,26 @@ __device__ __forceinline__ float4 tile_f4(const float *__restrict__ q) {
 }
 __device__ __forceinline__ float tile_f1(const float *__restrict__ q) { return *q; }
 
+// Workgroup b -> work item.  Workgroups are dispatched round-robin over the
+// 8 XCDs (b runs on XCD b % 8), and an XCD's 32 CUs each hold one workgroup.
+// Items are taken in chunks of 32 -- in an expert's order, four column blocks
+// of eight M-tiles -- and chunk c runs on XCD c % 8: an XCD's concurrent items
+// share four weight panels and eight A tiles in its L2, and the eight XCDs
+// work on neighbouring chunks (the same expert's panels) at the same time,
+// so the panels one XCD re-reads are those its neighbours have just brought
+// into the Infinity Cache.  The last n mod 256 items go contiguously to the
+// XCDs.  Returns -1 for a workgroup without an item.
+__device__ __forceinline__ int tile_item(int b, int n) {
+  const int x = b & 7, j = b >> 3;
+  const int full = n >> 8;  // complete rounds of 8 chunks
+  if (j < 32 * full) return ((j >> 5) * 8 + x) * 32 + (j & 31);
+  const int rest = n - 256 * full;
+  const int per = (rest + 7) >> 3;
+  const int k = j - 32 * full;
+  const int it = 256 * full + x * per + k;
+  return (k < per && it < n) ? it : -1;
+}
+
 template <bool G1, int MT, int WM, int S>
 __global__ __launch_bounds__(256 * WM) void gemm_tile_kernel(GemmParams p) {
   using L = TileLayout<MT, WM, S>;
@@ -110,10 +129,8 @@ __global__ __launch_bounds__(256 * WM) void gemm_tile_kernel(GemmParams p) {
   const int r16 = lane & 15;
   const int g4 = lane >> 4;
 
-  const int n_items = *p.n_items;
-  const int per_xcd = (n_items + 7) / 8;
-  const int item = (blockIdx.x & 7) * per_xcd + (blockIdx.x >> 3);
-  if ((int)(blockIdx.x >> 3) >= per_xcd || item >= n_items) return;
+  const int item = tile_item(blockIdx.x, *p.n_items);
+  if (item < 0) return;
 
   for (int i = tid; i <= p.El; i += NT) tb[i] = p.tile_base[i];
   __syncthreads();

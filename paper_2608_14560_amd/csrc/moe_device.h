@@ -199,6 +199,15 @@ struct FinalizeParams {
   int T, H, K, S, P_max;
 };
 
+// The weighted combine fused into GEMM2 (batches of at most 16 tokens).
+struct CombineParams {
+  const int32_t *perm_pair;  // [P] t*K + j of each permuted row
+  const float *topk_w;       // [T, K]
+  uint16_t *out;             // [T, H] bf16
+  int T, K;
+  int C;                     // K chunks per tile (divides KB)
+};
+
 // DSA TopK indexer: 64 heads of 128, a paged key cache of PS tokens per page
 struct DsaParams {
   const uint8_t *q;            // [B, 64, 128] e4m3
@@ -231,5 +240,8 @@ hipError_t launch_gemm2(const GemmParams &p, int BM, int grid, hipStream_t st);
 hipError_t launch_gemm_tile(const GemmParams &p, bool g1, int BM, int grid, hipStream_t st);
 int gemm_tile_cols();
 hipError_t launch_finalize(const FinalizeParams &p, hipStream_t st);
+// GEMM2 with the weighted combine in its epilogue (T <= combine_max_tokens())
+hipError_t launch_gemm2_combine(const GemmParams &p, const CombineParams &c, hipStream_t st);
+int combine_max_tokens();
 
 }  // namespace moe
