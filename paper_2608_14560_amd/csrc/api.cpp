@@ -64,7 +64,7 @@ struct Plan {
   bool fused_combine;  // GEMM2 with the combine in its epilogue (T <= 16)
   int64_t P_max;
   size_t off_ids, off_w, off_offsets, off_perm_token, off_perm_pair, off_pair_row, off_chunk_counts,
-      off_tile_base, off_n_items, off_act, off_act_scale, off_abuf, off_Y, off_partials, total;
+      off_tile_base, off_n_items, off_act, off_act_scale, off_abuf, off_Y, off_Ye, off_partials, total;
 };
 
 Plan make_plan(const moe_shape_t *s) {
@@ -118,11 +118,14 @@ Plan make_plan(const moe_shape_t *s) {
   p.off_act = take((size_t)p.P_max * s->I);
   p.off_act_scale = take(sizeof(float) * (size_t)p.P_max * (s->I / 128));
   p.off_abuf = take(p.narrow1 ? sizeof(float) * (size_t)p.P_max * s->I : 0);
-  // the router projection's block sums [T, H/128, E_g] live where GEMM2 later
-  // writes Y: the routing kernel consumes them before GEMM2 runs
-  const size_t y_bytes = sizeof(float) * (size_t)p.S2 * p.P_max * s->H;
+  // Y: fp16 codes [P_max, H] and their chunk exponents [P_max, H/16].  The
+  // router projection's block sums [T, H/128, E_g] live in the same region:
+  // the routing kernel consumes them before GEMM2 writes Y
+  const size_t y_bytes = align_up(sizeof(uint16_t) * (size_t)p.P_max * s->H);
+  const size_t ye_bytes = (size_t)p.P_max * (s->H / kYChunk);
   const size_t part_bytes = sizeof(float) * (size_t)(s->T > 0 ? s->T : 1) * (s->H / 128) * s->num_experts;
-  p.off_Y = take(y_bytes > part_bytes ? y_bytes : part_bytes);
+  p.off_Y = take(y_bytes + ye_bytes > part_bytes ? y_bytes + ye_bytes : part_bytes);
+  p.off_Ye = p.off_Y + y_bytes;
   p.off_partials = p.off_Y;
   p.total = o;
   return p;
@@ -244,7 +247,8 @@ moe_status_t enqueue_gemm2_combine(const moe_shape_t *s, const Plan &pl, const P
   g2.expert_offsets = r.offsets;
   g2.tile_base = at<int32_t>(ws, pl.off_tile_base);
   g2.perm_token = r.perm_token;
-  g2.Y = at<float>(ws, pl.off_Y);
+  g2.Y = at<uint16_t>(ws, pl.off_Y);
+  g2.Ye = at<int8_t>(ws, pl.off_Ye);
   g2.I = s->I;
   g2.H = s->H;
   g2.P_max = (int)pl.P_max;
@@ -273,7 +277,7 @@ moe_status_t enqueue_gemm2_combine(const moe_shape_t *s, const Plan &pl, const P
                       : launch_gemm2(g2, pl.BM, grid2, st));
 
   // weighted combine in slot order, one bf16 rounding per element
-  FinalizeParams f{g2.Y, r.pair_row, r.w, out, s->T, s->H, s->top_k, pl.S2, (int)pl.P_max};
+  FinalizeParams f{g2.Y, g2.Ye, r.pair_row, r.w, out, s->T, s->H, s->top_k};
   mark();
   MOE_TRY_HIP(launch_finalize(f, st));
   return MOE_OK;
@@ -314,7 +318,6 @@ moe_status_t fused_impl(const moe_shape_t *s, const uint8_t *hidden, const float
   g.abuf = at<float>(ws, pl.off_abuf);
   g.act = at<uint8_t>(ws, pl.off_act);
   g.act_scale = at<float>(ws, pl.off_act_scale);
-  g.Y = at<float>(ws, pl.off_Y);
   g.I = s->I;
   g.H = s->H;
   g.P_max = (int)pl.P_max;

@@ -222,16 +222,33 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(GemmParams p) {
   // column r16 of sub-tile nt
   if (!G1) {
     if (nb * kBN + 64 * wave >= p.H) return;  // this wave's columns are past H
-    float *Ys = p.Y + (size_t)s * p.P_max * p.H;
+    // Y as fp16 codes, one exponent per row and 16-column chunk (sub-tile
+    // nt): the chunk's columns are the 16 lanes of the row's lane group
+    const int HC = p.H / kYChunk;
+    const int c0 = nb * kBN + 64 * wave;
 #pragma unroll
     for (int m = 0; m < MT; ++m)
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int r = m * 16 + 4 * (lane >> 4) + i;
-        if (r < nrows) {
-          float *yrow = Ys + (size_t)(row0 + r) * p.H + nb * kBN + 64 * wave + r16;
+        int ex[4];
 #pragma unroll
-          for (int nt = 0; nt < 4; ++nt) yrow[16 * nt] = acc[m][nt][i];
+        for (int nt = 0; nt < 4; ++nt) {
+          float mx = fabsf(acc[m][nt][i]);
+#pragma unroll
+          for (int off = 1; off < 16; off <<= 1) mx = fmaxf(mx, __shfl_xor(mx, off));
+          ex[nt] = y16_exponent(mx);
+        }
+        if (r < nrows) {
+          uint16_t *yrow = p.Y + (size_t)(row0 + r) * p.H + c0 + r16;
+#pragma unroll
+          for (int nt = 0; nt < 4; ++nt) yrow[16 * nt] = y16_code(acc[m][nt][i], ex[nt]);
+          if (r16 < 4) {
+            int eg = ex[0];
+#pragma unroll
+            for (int nt = 1; nt < 4; ++nt) eg = r16 == nt ? ex[nt] : eg;
+            p.Ye[(size_t)(row0 + r) * HC + c0 / kYChunk + r16] = (int8_t)eg;
+          }
         }
       }
     return;
@@ -417,13 +434,19 @@ __global__ __launch_bounds__(kStreamWaves * kWave) void gemm2_stream_kernel(Gemm
   }
 #undef MOE_SLOAD
 
-  float *Ys = p.Y + (size_t)s * p.P_max * p.H;
+  // Y as fp16 codes: the wave's 16 columns of a row are one chunk, held by
+  // the 16 lanes of the row's lane group
+  const int c0 = nb * 128 + 16 * wave;
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     const int r = srow + i;
+    float mx = fabsf(acc0[i]);
+#pragma unroll
+    for (int off = 1; off < 16; off <<= 1) mx = fmaxf(mx, __shfl_xor(mx, off));
+    const int ex = y16_exponent(mx);
     if (r < nrows) {
-      float *yrow = Ys + (size_t)(row0 + r) * p.H + nb * 128 + 16 * wave + r16;
-      yrow[0] = acc0[i];
+      p.Y[(size_t)(row0 + r) * p.H + c0 + r16] = y16_code(acc0[i], ex);
+      if (r16 == 0) p.Ye[(size_t)(row0 + r) * (p.H / kYChunk) + c0 / kYChunk] = (int8_t)ex;
     }
   }
 }
@@ -689,9 +712,10 @@ __global__ __launch_bounds__(256) void requant_kernel(GemmParams p) {
 }
 
 // The combine: out[t] = bf16(sum over the token's resident slots, in slot
-// order, of w_j * Y[pair_row[t, j]]).  All K pair rows and weights are loaded
-// first, then the Y rows of the resident slots, so a token costs two
-// dependent round trips, not 2K.
+// order, of w_j * Y[pair_row[t, j]]), Y read back from its fp16 codes and
+// chunk exponents (exact).  All K pair rows and weights are loaded first,
+// then the Y codes and exponents of the resident slots, so a token costs two
+// dependent round trips, not 2K.  A thread owns 8 columns (half a chunk).
 // KM >= K slots (4, 8 or 16).
 template <int KM>
 __global__ __launch_bounds__(256) void finalize_kernel(FinalizeParams p) {
@@ -708,25 +732,16 @@ __global__ __launch_bounds__(256) void finalize_kernel(FinalizeParams p) {
   }
   // the token is the workgroup's, so pr[j] is uniform: absent slots branch
   // around their loads without splitting the wave
-  float4 ya[KM], yb[KM];
+  const int HC = p.H / kYChunk;
+  uint4 yc[KM];
+  int ye[KM];
 #pragma unroll
   for (int j = 0; j < KM; ++j) {
-    ya[j] = yb[j] = float4{0.f, 0.f, 0.f, 0.f};
+    yc[j] = uint4{0u, 0u, 0u, 0u};
+    ye[j] = 0;
     if (pr[j] >= 0) {
-      const float *src = p.Y + (size_t)pr[j] * p.H + n0;
-      ya[j] = *reinterpret_cast<const float4 *>(src);
-      yb[j] = *reinterpret_cast<const float4 *>(src + 4);
-    }
-  }
-  for (int q = 1; q < p.S; ++q) {  // K-split planes of Y, summed first
-#pragma unroll
-    for (int j = 0; j < KM; ++j) {
-      if (pr[j] < 0) continue;
-      const float *src = p.Y + ((size_t)q * p.P_max + pr[j]) * p.H + n0;
-      const float4 a = *reinterpret_cast<const float4 *>(src);
-      const float4 b = *reinterpret_cast<const float4 *>(src + 4);
-      ya[j].x += a.x; ya[j].y += a.y; ya[j].z += a.z; ya[j].w += a.w;
-      yb[j].x += b.x; yb[j].y += b.y; yb[j].z += b.z; yb[j].w += b.w;
+      yc[j] = *reinterpret_cast<const uint4 *>(p.Y + (size_t)pr[j] * p.H + n0);
+      ye[j] = p.Ye[(size_t)pr[j] * HC + n0 / kYChunk];
     }
   }
   float acc[8];
@@ -735,9 +750,12 @@ __global__ __launch_bounds__(256) void finalize_kernel(FinalizeParams p) {
 #pragma unroll
   for (int j = 0; j < KM; ++j) {
     if (j < p.K && pr[j] >= 0) {
-      const float y[8] = {ya[j].x, ya[j].y, ya[j].z, ya[j].w, yb[j].x, yb[j].y, yb[j].z, yb[j].w};
+      const uint32_t u[4] = {yc[j].x, yc[j].y, yc[j].z, yc[j].w};
 #pragma unroll
-      for (int c = 0; c < 8; ++c) acc[c] = __builtin_fmaf(w[j], y[c], acc[c]);
+      for (int c = 0; c < 8; ++c) {
+        const float y = y16_value((uint16_t)(u[c >> 1] >> (16 * (c & 1))), ye[j]);
+        acc[c] = __builtin_fmaf(w[j], y, acc[c]);
+      }
     }
   }
   uint4 o;
@@ -1016,6 +1034,7 @@ hipError_t launch_requant(const GemmParams &p, int P_max, hipStream_t st) {
 // GEMM2 for 16- and 32-row tiles (64 rows and more: the large-tile kernels)
 hipError_t launch_gemm2(const GemmParams &p, int BM, int grid, hipStream_t st) {
   if (grid <= 0) return hipSuccess;
+  if (p.S != 1) return hipErrorInvalidValue;  // Y holds one K plane
   switch (BM) {
     case 16: return launch_gemm2_stream(p, grid, st);
     case 32: return launch_gemm_bm<32, false>(p, grid, st);

@@ -365,13 +365,36 @@ __global__ __launch_bounds__(256 * WM) void gemm_tile_kernel(GemmParams p) {
   const int wrow = 16 * MT * wm;
   if (!G1) {
     if (wrow0 >= p.N_total) return;  // columns past H (ragged last block)
+    // Y as fp16 codes with one exponent per row and 16-column chunk: the
+    // chunk (sub-tile n) of row r16 is held by the lanes r16 + 16 g4, four
+    // columns each
+    const int HC = p.H / kYChunk;
 #pragma unroll
     for (int m = 0; m < MT; ++m) {
       const int r = wrow + 16 * m + r16;
-      if (r < nrows) {
-        float *yrow = p.Y + (size_t)(row0 + r) * p.H + wrow0 + 4 * g4;
+      int ex[4];
 #pragma unroll
-        for (int n = 0; n < 4; ++n) *reinterpret_cast<v4f *>(yrow + 16 * n) = acc[m][n];
+      for (int n = 0; n < 4; ++n) {
+        float mx = fmaxf(fmaxf(fabsf(acc[m][n][0]), fabsf(acc[m][n][1])),
+                         fmaxf(fabsf(acc[m][n][2]), fabsf(acc[m][n][3])));
+        mx = fmaxf(mx, __shfl_xor(mx, 16));
+        mx = fmaxf(mx, __shfl_xor(mx, 32));
+        ex[n] = y16_exponent(mx);
+      }
+      if (r < nrows) {
+        uint16_t *yrow = p.Y + (size_t)(row0 + r) * p.H + wrow0 + 4 * g4;
+#pragma unroll
+        for (int n = 0; n < 4; ++n) {
+          uint2 c;
+          c.x = (uint32_t)y16_code(acc[m][n][0], ex[n]) | ((uint32_t)y16_code(acc[m][n][1], ex[n]) << 16);
+          c.y = (uint32_t)y16_code(acc[m][n][2], ex[n]) | ((uint32_t)y16_code(acc[m][n][3], ex[n]) << 16);
+          *reinterpret_cast<uint2 *>(yrow + 16 * n) = c;
+        }
+        // lane r16 + 16 g4 stores the exponent of chunk g4
+        int eg = ex[0];
+#pragma unroll
+        for (int n = 1; n < 4; ++n) eg = g4 == n ? ex[n] : eg;
+        p.Ye[(size_t)(row0 + r) * HC + wrow0 / kYChunk + g4] = (int8_t)eg;
       }
     }
     return;
@@ -453,6 +476,7 @@ int gemm_tile_cols() { return kTileCols; }
 
 hipError_t launch_gemm_tile(const GemmParams &p, bool g1, int BM, int grid, hipStream_t st) {
   if (grid <= 0) return hipSuccess;
+  if (p.S != 1) return hipErrorInvalidValue;  // full-K items only
   switch (BM) {
     // 64 / 128 rows: 4 waves, three-stage ring (loads two K-steps ahead)
     case 64: return g1 ? launch_tile<true, 4, 1, 3>(p, grid, st) : launch_tile<false, 4, 1, 3>(p, grid, st);

@@ -33,6 +33,28 @@ __device__ __forceinline__ uint32_t e4m3x2_rne_sat(float a, float b) {
   return (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32(a, b, 0, false) & 0xffffu;
 }
 
+// GEMM2's expert outputs Y go to memory as fp16 with one power-of-two
+// exponent per row and 16-column chunk (kYChunk): the chunk's largest
+// magnitude m 2^x (m in [0.5, 1)) is scaled by 2^-(x - 15) into
+// [2^14, 2^15), every value of the chunk is rounded to fp16 (nearest even)
+// after that exact scaling, and the combine multiplies by 2^e back (exact).
+// The rounding error is at most 2^-12 of the chunk's largest magnitude, half
+// of fp32's bytes.  An all-zero chunk gets exponent 0; a chunk below 2^-113
+// keeps exponent -128 (its scaled values still stay below 2^15).
+constexpr int kYChunk = 16;
+
+__device__ __forceinline__ int y16_exponent(float amax) {
+  if (!(amax > 0.0f)) return 0;
+  return max(__builtin_amdgcn_frexp_expf(amax) - 15, -128);
+}
+__device__ __forceinline__ uint16_t y16_code(float y, int e) {
+  const _Float16 h = (_Float16)__builtin_amdgcn_ldexpf(y, -e);
+  return __builtin_bit_cast(uint16_t, h);
+}
+__device__ __forceinline__ float y16_value(uint16_t c, int e) {
+  return __builtin_amdgcn_ldexpf((float)__builtin_bit_cast(_Float16, c), e);
+}
+
 // fp32 sigmoid with a fixed operation sequence: clamp to [-80, 80],
 // e^z for z = -x by Cody-Waite reduction n = rint(z log2 e),
 // r = z - n ln2 (two-part ln2), degree-7 Taylor polynomial of e^r in Horner
@@ -180,23 +202,25 @@ struct GemmParams {
   float *abuf;               // GEMM1 column-split SwiGLU output [P_max, I] fp32
   uint8_t *act;              // GEMM1 out: [P_max, I] e4m3
   float *act_scale;          // GEMM1 out: [P_max, I/128]
-  float *Y;                  // GEMM2 out: [S, P_max, H] fp32
+  uint16_t *Y;               // GEMM2 out: [P_max, H] fp16 codes (see y16_code)
+  int8_t *Ye;                // their exponents, [P_max, H / kYChunk]
   int K, KB;                 // reduction length and its 128-blocks
   int N_total;               // rows of one expert's weight matrix (2I or H)
   int I;                     // intermediate size (GEMM1 gate/up split)
   int NB;                    // column blocks per M-tile
-  int S;                     // split-K factor
+  int S;                     // split-K factor (GEMM2: always 1)
   int P_max;                 // row capacity of act / abuf / Y
   int H;                     // GEMM2 output width (row stride of Y)
   int El;
 };
 
 struct FinalizeParams {
-  const float *Y;            // [S, P_max, H]
+  const uint16_t *Y;         // [P_max, H] fp16 codes
+  const int8_t *Ye;          // [P_max, H / kYChunk] exponents
   const int32_t *pair_row;   // [T, K]
   const float *topk_w;       // [T, K]
   uint16_t *out;             // [T, H] bf16
-  int T, H, K, S, P_max;
+  int T, H, K;
 };
 
 // The weighted combine fused into GEMM2 (batches of at most 16 tokens).
