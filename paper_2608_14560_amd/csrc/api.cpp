@@ -94,7 +94,7 @@ Plan make_plan(const moe_shape_t *s) {
   p.NB2 = p.BM == 16 ? s->H / 128 : (s->H + 255) / 256;
   // at most 16 tokens: one 16-row tile per expert, and GEMM2 workgroups that
   // own output columns of every token sum the experts themselves
-  p.fused_combine = p.BM == 16 && s->T <= combine_max_tokens();
+  p.fused_combine = p.BM == 16 && s->T <= combine_max_tokens() && combine_fits((int)p.P_max, s->I);
   p.nchunks = (int)((s->T + kChunkTokens - 1) / kChunkTokens);
   if (p.nchunks < 1) p.nchunks = 1;
   const int64_t touched = TK < s->num_local_experts ? TK : s->num_local_experts;

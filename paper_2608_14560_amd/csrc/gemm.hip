@@ -1055,6 +1055,7 @@ hipError_t launch_finalize(const FinalizeParams &p, hipStream_t st) {
 }
 
 int combine_max_tokens() { return kCombineTokens; }
+bool combine_fits(int P_max, int I) { return CombineLayout(P_max, I).bytes() <= 96 * 1024; }
 
 hipError_t launch_gemm2_combine(const GemmParams &p, const CombineParams &c, hipStream_t st) {
   if (c.T <= 0) return hipSuccess;

@@ -267,5 +267,6 @@ hipError_t launch_finalize(const FinalizeParams &p, hipStream_t st);
 // GEMM2 with the weighted combine in its epilogue (T <= combine_max_tokens())
 hipError_t launch_gemm2_combine(const GemmParams &p, const CombineParams &c, hipStream_t st);
 int combine_max_tokens();
+bool combine_fits(int P_max, int I);  // its LDS staging fits the workgroup
 
 }  // namespace moe

@@ -99,6 +99,16 @@ PARITY_CONFIGS: dict[str, MoEConfig] = {
     "small_t128": MoEConfig("small_t128", T=256, H=640, I=384, num_experts=8,
                             num_local_experts=6, local_expert_offset=1, n_group=2,
                             topk_group=2, top_k=4),
+    # 16 tokens, every expert resident: 128 pairs, more than the fused
+    # GEMM2 + combine stages in LDS (its activation rows come from memory)
+    "small_decode_all": MoEConfig("small_decode_all", T=16, H=1024, I=2048, num_experts=64,
+                                  num_local_experts=64, local_expert_offset=0, n_group=8,
+                                  topk_group=4, top_k=8),
+    # 16 tokens with a wide intermediate (I = 8192): the fused GEMM2 + combine
+    # would not fit its workgroup's LDS, so GEMM2 and the combine run apart
+    "small_wide_i": MoEConfig("small_wide_i", T=16, H=256, I=8192, num_experts=16,
+                              num_local_experts=16, local_expert_offset=0, n_group=4,
+                              topk_group=4, top_k=8),
     # ~320 rows per expert: 256-row M-tiles with a ragged second tile
     "small_t256": MoEConfig("small_t256", T=640, H=384, I=256, num_experts=8,
                             num_local_experts=8, local_expert_offset=0, n_group=2,
