@@ -262,21 +262,32 @@ __global__ __launch_bounds__(256 * WM) void gemm_tile_kernel(GemmParams p) {
   // it+S-1), then kPfLoads prefetches (step it+S).  At the end of step `it`
   // stage it+1 must have landed: its group was issued S-2 steps earlier, so
   // the (S-2) later groups and this step's prefetches may be outstanding.
+  // Inside a step the group is spread over the first kSpread of the MT row
+  // blocks' MFMAs, the prefetches after it: issued in one burst, a wave
+  // stalled at issue on the CU's full request queue before its first MFMA
+  // (interleaved: prefill 643 -> 604 us, skewed 3698 -> 3622 us, measured on
+  // one box; the last quarter of the blocks issues no loads, so the group
+  // has the rest of the step to land even with a two-stage ring).
   constexpr int kGroup = JA + JB + 1;
   constexpr int kWait = (S - 2) * (kGroup + kPfLoads) + kPfLoads;
+  constexpr int kSpread = MT / 2;
   static_assert(kWait < 64, "vmcnt holds 6 bits");
   static_assert(S >= 2, "LDS ring depth");
 
 #define TILE_STAGE(st) (smem + (st) * L::STAGE)
-#define TILE_DMA(st, kb)                                                                \
+// load j of the group for stage st, K block kb: the wave's A blocks, then its
+// weight blocks, then the row scales (j is a compile-time constant)
+#define TILE_DMA_J(st, kb, j)                                                           \
   do {                                                                                  \
     uint8_t *d_ = TILE_STAGE(st);                                                       \
     const size_t ko_ = (size_t)(kb) * 128;                                              \
-    _Pragma("unroll") for (int j = 0; j < JA; ++j)                                      \
-        lds_load16(a_src[j] + ko_, d_ + (wave * JA + j) * 1024);                        \
-    _Pragma("unroll") for (int j = 0; j < JB; ++j)                                      \
-        lds_load16(b_src[j] + ko_, d_ + L::A_BYTES + wn * 8192 + (wm * JB + j) * 1024); \
-    lds_load4(s_src + (kb), d_ + L::SCL + wave * 256);                                  \
+    if ((j) < JA)                                                                       \
+      lds_load16(a_src[(j) < JA ? (j) : 0] + ko_, d_ + (wave * JA + (j)) * 1024);       \
+    else if ((j) < JA + JB)                                                             \
+      lds_load16(b_src[(j) >= JA && (j) < JA + JB ? (j) - JA : 0] + ko_,                \
+                 d_ + L::A_BYTES + wn * 8192 + (wm * JB + (j) - JA) * 1024);            \
+    else                                                                                \
+      lds_load4(s_src + (kb), d_ + L::SCL + wave * 256);                                \
   } while (0)
 #define TILE_PREFETCH(kb)                                                               \
   do {                                                                                  \
@@ -292,7 +303,12 @@ __global__ __launch_bounds__(256 * WM) void gemm_tile_kernel(GemmParams p) {
 // (a register-only probe on gfx950: 42 cycles per MFMA with one wave per
 // SIMD, 62 when each block's promotions are pinned behind its MFMAs; 32 is
 // the issue rate).  Two waves per SIMD (8-wave tiles) fill the rest.
-#define TILE_COMPUTE(st, kb)                                                            \
+// Blocks m < kSpread also issue their share of the next group (stage stl,
+// K block kbl) and the last of them the prefetches (K block kbp); the
+// scheduling barrier after them lets everything but vector-memory
+// instructions move across (mask 0x78F), so the loads stay among that
+// block's MFMAs while the math keeps its free order.
+#define TILE_COMPUTE(st, kb, stl, kbl, kbp)                                              \
   do {                                                                                  \
     const uint8_t *as_ = TILE_STAGE(st) + wm * MT * 2048;                               \
     const uint8_t *bs_ = TILE_STAGE(st) + L::A_BYTES + wn * 8192;                       \
@@ -312,6 +328,13 @@ __global__ __launch_bounds__(256 * WM) void gemm_tile_kernel(GemmParams p) {
         tile_frag(bs_ + n * 2048, rd_lo, rd_hi);                                        \
     v8i an_ = tile_frag(as_, rd_lo, rd_hi);                                             \
     _Pragma("unroll") for (int m = 0; m < MT; ++m) {                                    \
+      if (m < kSpread) {                                                                \
+        _Pragma("unroll") for (int j_ = (m * kGroup) / kSpread;                         \
+                               j_ < ((m + 1) * kGroup) / kSpread; ++j_)                 \
+            TILE_DMA_J(stl, kbl, j_);                                                   \
+        if (m == kSpread - 1) TILE_PREFETCH(kbp);                                       \
+        __builtin_amdgcn_sched_barrier(0x78F);                                          \
+      }                                                                                 \
       const v8i af_ = an_;                                                              \
       if (m + 1 < MT) an_ = tile_frag(as_ + (m + 1) * 2048, rd_lo, rd_hi);              \
       const float c_ = sav_[m] * sbv_;                                                  \
@@ -333,7 +356,8 @@ __global__ __launch_bounds__(256 * WM) void gemm_tile_kernel(GemmParams p) {
   // it has the same shape as S-1 loop steps)
 #pragma unroll
   for (int st = 0; st < S - 1; ++st) {
-    TILE_DMA(st, min(st, KB - 1));
+#pragma unroll
+    for (int j = 0; j < kGroup; ++j) TILE_DMA_J(st, min(st, KB - 1), j);
     TILE_PREFETCH(min(st + 1, KB - 1));
     __builtin_amdgcn_sched_barrier(0);
   }
@@ -341,10 +365,7 @@ __global__ __launch_bounds__(256 * WM) void gemm_tile_kernel(GemmParams p) {
 
   int st_rd = 0, st_ld = S - 1;
   for (int it = 0; it < KB; ++it) {
-    TILE_DMA(st_ld, min(it + S - 1, KB - 1));
-    TILE_PREFETCH(min(it + S, KB - 1));
-    __builtin_amdgcn_sched_barrier(0);
-    TILE_COMPUTE(st_rd, it);
+    TILE_COMPUTE(st_rd, it, st_ld, min(it + S - 1, KB - 1), min(it + S, KB - 1));
     __builtin_amdgcn_sched_barrier(0);
     asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(kWait) : "memory");
     st_rd = st_rd + 1 == S ? 0 : st_rd + 1;
@@ -357,7 +378,7 @@ __global__ __launch_bounds__(256 * WM) void gemm_tile_kernel(GemmParams p) {
 
 #undef TILE_COMPUTE
 #undef TILE_PREFETCH
-#undef TILE_DMA
+#undef TILE_DMA_J
 #undef TILE_STAGE
 
   // accumulator element (m, n, i) of this lane: tile row 16 MT wm + 16m + r16,
