@@ -64,7 +64,8 @@ struct Plan {
   bool fused_combine;  // GEMM2 with the combine in its epilogue (T <= 16)
   int64_t P_max;
   size_t off_ids, off_w, off_offsets, off_perm_token, off_perm_pair, off_pair_row, off_chunk_counts,
-      off_tile_base, off_n_items, off_act, off_act_scale, off_abuf, off_Y, off_Ye, off_partials, total;
+      off_tile_base, off_n_items, off_act, off_act_scale, off_act_scale_k, off_hs_k, off_abuf, off_Y,
+      off_Ye, off_partials, total;
 };
 
 Plan make_plan(const moe_shape_t *s) {
@@ -118,6 +119,10 @@ Plan make_plan(const moe_shape_t *s) {
   p.off_act = take((size_t)p.P_max * s->I);
   p.off_act_scale = take(sizeof(float) * (size_t)p.P_max * (s->I / 128));
   p.off_abuf = take(p.narrow1 ? sizeof(float) * (size_t)p.P_max * s->I : 0);
+  // large tiles: K-block-major activation scales, [I/128, P_max] written by
+  // GEMM1 for GEMM2 and [H/128, P_max] gathered from the hidden scales
+  p.off_act_scale_k = take(p.tile ? sizeof(float) * (size_t)p.P_max * (s->I / 128) : 0);
+  p.off_hs_k = take(p.tile ? sizeof(float) * (size_t)p.P_max * (s->H / 128) : 0);
   // Y: fp16 codes [P_max, H] and their chunk exponents [P_max, H/16].  The
   // router projection's block sums [T, H/128, E_g] live in the same region:
   // the routing kernel consumes them before GEMM2 writes Y
@@ -236,7 +241,8 @@ moe_status_t enqueue_route(const moe_shape_t *s, const Plan &pl, const RouterIn 
 // [P, I/128] and stage (4)'s weighted combine into `out`, after the routing
 // and permutation have been enqueued into `ws`.
 moe_status_t enqueue_gemm2_combine(const moe_shape_t *s, const Plan &pl, const Ptrs &r,
-                                   const uint8_t *act, const float *act_scale, const uint8_t *w2,
+                                   const uint8_t *act, const float *act_scale,
+                                   const float *act_scale_k, const uint8_t *w2,
                                    const float *w2_scale, uint16_t *out, void *ws, hipStream_t st,
                                    void *const *ev, int &stage) {
   auto mark = [&]() {
@@ -255,6 +261,10 @@ moe_status_t enqueue_gemm2_combine(const moe_shape_t *s, const Plan &pl, const P
   g2.El = s->num_local_experts;
   g2.A = act;
   g2.A_scale = act_scale;
+  // the large-tile kernel reads the K-block-major copy when GEMM1 wrote one
+  g2.sa_tile = act_scale_k ? act_scale_k : act_scale;
+  g2.sa_row = act_scale_k ? 1 : s->I / 128;
+  g2.sa_kb = act_scale_k ? (int)pl.P_max : 1;
   g2.B = w2;
   g2.B_scale = w2_scale;
   g2.n_items = at<int32_t>(ws, pl.off_n_items) + 1;
@@ -323,10 +333,20 @@ moe_status_t fused_impl(const moe_shape_t *s, const uint8_t *hidden, const float
   g.P_max = (int)pl.P_max;
   g.El = s->num_local_experts;
 
+  // large tiles: the gathered hidden scales, K-block-major (part of the
+  // permutation stage)
+  if (pl.tile)
+    MOE_TRY_HIP(launch_gather_scales(r.offsets, s->num_local_experts, r.perm_token, hidden_scale,
+                                     at<float>(ws, pl.off_hs_k), s->H / 128, (int)pl.P_max, st));
+
   // GEMM1: hidden rows (gathered) x W13, SwiGLU + FP8 re-quantisation
   GemmParams g1 = g;
   g1.A = hidden;
   g1.A_scale = hidden_scale;
+  g1.sa_tile = at<float>(ws, pl.off_hs_k);
+  g1.sa_row = 1;
+  g1.sa_kb = (int)pl.P_max;
+  g1.act_scale_k = pl.tile ? at<float>(ws, pl.off_act_scale_k) : nullptr;
   g1.B = w13;
   g1.B_scale = w13_scale;
   g1.n_items = at<int32_t>(ws, pl.off_n_items);
@@ -348,8 +368,8 @@ moe_status_t fused_impl(const moe_shape_t *s, const uint8_t *hidden, const float
   if (pl.narrow1) MOE_TRY_HIP(launch_requant(g1, (int)pl.P_max, st));
 
   // GEMM2 and the weighted combine on the intermediate GEMM1 just wrote
-  if ((rc = enqueue_gemm2_combine(s, pl, r, g.act, g.act_scale, w2, w2_scale, out, ws, st, ev,
-                                  stage)) != MOE_OK)
+  if ((rc = enqueue_gemm2_combine(s, pl, r, g.act, g.act_scale, g1.act_scale_k, w2, w2_scale, out,
+                                  ws, st, ev, stage)) != MOE_OK)
     return rc;
   if (ev) (void)hipEventRecord(static_cast<hipEvent_t>(ev[stage]), st);
   return MOE_OK;
@@ -573,8 +593,8 @@ moe_status_t moe_debug_combine_from_act(const moe_shape_t *s, const float *route
   const RouterIn rin{router_logits, nullptr, nullptr, nullptr};
   if ((rc = enqueue_route(s, pl, rin, routing_bias, r, workspace, st, nullptr, stage)) != MOE_OK)
     return rc;
-  return enqueue_gemm2_combine(s, pl, r, act, act_scale, w2, w2_scale, out, workspace, st, nullptr,
-                               stage);
+  return enqueue_gemm2_combine(s, pl, r, act, act_scale, nullptr, w2, w2_scale, out, workspace, st,
+                               nullptr, stage);
 }
 
 moe_status_t moe_debug_act_views(const moe_shape_t *s, void *workspace, uint8_t **act,

@@ -239,14 +239,17 @@ __global__ __launch_bounds__(256 * WM) void gemm_tile_kernel(GemmParams p) {
     }
   }
   // row scales: slot s = (row % 16) * MTW + row / 16; lane L of wave w loads
-  // slot 64 w + L (slots >= BM are loaded but never read)
+  // slot 64 w + L (slots >= BM are loaded but never read).  They come from
+  // the K-block-major copy sa_tile (permuted rows): the 64 lanes' rows lie
+  // within one tile, so a K step's scale load touches a few cache lines.
   const float *s_src;
   {
     const int sl = 64 * wave + lane;
     const int r = sl < BM ? 16 * (sl % MTW) + sl / MTW : nrows - 1;
     const int rr = min(r, nrows - 1);
-    s_src = p.A_scale + (size_t)(G1 ? p.perm_token[row0 + rr] : row0 + rr) * KB;
+    s_src = p.sa_tile + (size_t)(row0 + rr) * p.sa_row;
   }
+  const size_t sa_kb = (size_t)p.sa_kb;
   // this lane's two 16-byte pieces of a fragment (rows 16m + r16 of a block)
   const int fr = tile_swz(r16);
   const int rd_lo = r16 * 128 + 16 * ((2 * g4) ^ fr);
@@ -287,7 +290,7 @@ __global__ __launch_bounds__(256 * WM) void gemm_tile_kernel(GemmParams p) {
       lds_load16(b_src[(j) >= JA && (j) < JA + JB ? (j) - JA : 0] + ko_,                \
                  d_ + L::A_BYTES + wn * 8192 + (wm * JB + (j) - JA) * 1024);            \
     else                                                                                \
-      lds_load4(s_src + (kb), d_ + L::SCL + wave * 256);                                \
+      lds_load4(s_src + (kb) * sa_kb, d_ + L::SCL + wave * 256);                        \
   } while (0)
 #define TILE_PREFETCH(kb)                                                               \
   do {                                                                                  \
@@ -472,7 +475,10 @@ __global__ __launch_bounds__(256 * WM) void gemm_tile_kernel(GemmParams p) {
               (e4m3x2_rne_sat(acc[m][n][2] / scale, acc[m][n][3] / scale) << 16);
         *reinterpret_cast<uint32_t *>(arow + 16 * n) = q;
       }
-      if (wn == 0 && g4 == 0) p.act_scale[(size_t)(row0 + r) * IB + nb] = scale;
+      if (wn == 0 && g4 == 0) {
+        p.act_scale[(size_t)(row0 + r) * IB + nb] = scale;
+        if (p.act_scale_k) p.act_scale_k[(size_t)nb * p.P_max + row0 + r] = scale;
+      }
     }
   }
 }

@@ -202,6 +202,12 @@ struct GemmParams {
   float *abuf;               // GEMM1 column-split SwiGLU output [P_max, I] fp32
   uint8_t *act;              // GEMM1 out: [P_max, I] e4m3
   float *act_scale;          // GEMM1 out: [P_max, I/128]
+  float *act_scale_k;        // GEMM1 out (large tiles, optional): [I/128, P_max]
+  // The large-tile kernels' activation scales by permuted row r and K block
+  // kb: sa_tile[r * sa_row + kb * sa_kb] (a K-block-major copy, so that the
+  // scales of one K block of a tile's rows share a few cache lines)
+  const float *sa_tile;
+  int sa_row, sa_kb;
   uint16_t *Y;               // GEMM2 out: [P_max, H] fp16 codes (see y16_code)
   int8_t *Ye;                // their exponents, [P_max, H / kYChunk]
   int K, KB;                 // reduction length and its 128-blocks
@@ -255,6 +261,10 @@ hipError_t launch_dsa_select(const DsaParams &p, hipStream_t st);
 bool dsa_wide_select(int max_len);
 hipError_t launch_router_logits(const RouteParams &p, float *logits, hipStream_t st);
 hipError_t launch_permute(const PermuteParams &p, hipStream_t st);
+// hs_k[kb * P_max + r] = hidden_scale[perm_token[r] * KB + kb] for r < P
+hipError_t launch_gather_scales(const int32_t *expert_offsets, int El, const int32_t *perm_token,
+                                const float *hidden_scale, float *hs_k, int KB, int P_max,
+                                hipStream_t st);
 hipError_t launch_gemm1(const GemmParams &p, int BM, int grid, hipStream_t st);
 hipError_t launch_gemm1_narrow(const GemmParams &p, int grid, bool gate_up_split, hipStream_t st);
 int gemm1_narrow_cols(bool gate_up_split);

@@ -43,7 +43,54 @@ __global__ __launch_bounds__(kThreads) void scatter_kernel(PermuteParams p) {
   scatter_chunk<kThreads, SINGLE>(p, blockIdx.x, p.topk_ids, sh);
 }
 
+// The hidden rows' block scales in permuted order and K-block-major,
+// hs_k[kb][r] = hidden_scale[perm_token[r]][kb], for the large-tile GEMM1
+// (its per-K-step scale loads then cover a tile's rows with a few cache
+// lines instead of one line per row).  Workgroup = 64 permuted rows: their
+// scale rows are read whole (consecutive threads, consecutive K blocks of a
+// row), transposed through LDS, and written 64 rows at a time per K block.
+constexpr int kGatherRows = 64;
+constexpr int kGatherMaxKB = 512;  // H <= 65536
+
+__global__ __launch_bounds__(kThreads) void gather_scales_kernel(const int32_t *expert_offsets, int El,
+                                                                 const int32_t *perm_token,
+                                                                 const float *hidden_scale, float *hs_k,
+                                                                 int KB, int P_max) {
+  __shared__ int tok[kGatherRows];
+  extern __shared__ float tr[];  // [KB][kGatherRows + 1]
+  const int P = expert_offsets[El];
+  const int r0 = blockIdx.x * kGatherRows;
+  if (r0 >= P) return;
+  const int n = min(kGatherRows, P - r0);
+  if (threadIdx.x < kGatherRows) tok[threadIdx.x] = perm_token[r0 + min((int)threadIdx.x, n - 1)];
+  __syncthreads();
+  for (int i = threadIdx.x; i < kGatherRows * KB; i += kThreads) {
+    const int row = i / KB, kb = i % KB;
+    tr[kb * (kGatherRows + 1) + row] = hidden_scale[(size_t)tok[row] * KB + kb];
+  }
+  __syncthreads();
+  for (int i = threadIdx.x; i < kGatherRows * KB; i += kThreads) {
+    const int kb = i / kGatherRows, row = i % kGatherRows;
+    if (row < n) hs_k[(size_t)kb * P_max + r0 + row] = tr[kb * (kGatherRows + 1) + row];
+  }
+}
+
 }  // namespace
+
+hipError_t launch_gather_scales(const int32_t *expert_offsets, int El, const int32_t *perm_token,
+                                const float *hidden_scale, float *hs_k, int KB, int P_max,
+                                hipStream_t st) {
+  if (P_max <= 0 || KB <= 0) return hipSuccess;
+  if (KB > kGatherMaxKB) return hipErrorInvalidValue;
+  const size_t lds = sizeof(float) * (size_t)KB * (kGatherRows + 1);
+  static hipError_t attr = hipFuncSetAttribute(reinterpret_cast<const void *>(gather_scales_kernel),
+                                               hipFuncAttributeMaxDynamicSharedMemorySize,
+                                               (int)(sizeof(float) * kGatherMaxKB * (kGatherRows + 1)));
+  if (attr != hipSuccess) return attr;
+  hipLaunchKernelGGL(gather_scales_kernel, dim3((P_max + kGatherRows - 1) / kGatherRows), dim3(kThreads),
+                     lds, st, expert_offsets, El, perm_token, hidden_scale, hs_k, KB, P_max);
+  return hipGetLastError();
+}
 
 // A batch of one chunk needs no count launch: the scatter counts for itself.
 hipError_t launch_permute_count(const PermuteParams &p, hipStream_t st) {
