@@ -108,6 +108,167 @@ __device__ __forceinline__ int tile_item(int b, int n) {
   return (k < per && it < n) ? it : -1;
 }
 
+// A work item's place: its expert, the expert's M-tile count, the M-tile and
+// column block, the tile's rows, and the wave's first weight row and the two
+// weight-scale blocks of its columns.
+struct TileItem {
+  int e, nt_e, mt_idx, nb, row0, nrows, wrow0, nblk0, nblk1;
+};
+
+template <bool G1, int BM>
+__device__ __forceinline__ TileItem tile_decode(const GemmParams &p, const int *tb, int item, int wn) {
+  TileItem t;
+  const int NB = p.NB;
+  const int qt = item / NB;
+  int lo = 0, hi = p.El;
+  while (hi - lo > 1) {
+    const int mid = (lo + hi) >> 1;
+    if (tb[mid] <= qt) lo = mid; else hi = mid;
+  }
+  t.e = lo;
+  t.nt_e = tb[lo + 1] - tb[lo];
+  const int local = item - tb[lo] * NB;
+  const int G = (NB + kGroupN - 1) / kGroupN;
+  const int grp = min(local / (kGroupN * t.nt_e), G - 1);
+  const int wi = local - grp * kGroupN * t.nt_e;
+  const int gsz = min(kGroupN, NB - kGroupN * grp);
+  t.mt_idx = wi / gsz;
+  t.nb = kGroupN * grp + wi % gsz;
+  t.row0 = p.expert_offsets[lo] + t.mt_idx * BM;
+  t.nrows = min(BM, p.expert_offsets[lo + 1] - t.row0);
+  const int half = wn >> 1;  // GEMM1: 0 gate, 1 up.  GEMM2: 128-column half
+  if (G1) {
+    t.wrow0 = half * p.I + t.nb * 128 + 64 * (wn & 1);
+    t.nblk0 = t.nb;
+    t.nblk1 = p.I / 128 + t.nb;
+  } else {
+    t.wrow0 = t.nb * kTileCols + 64 * wn;
+    t.nblk0 = min(2 * t.nb, p.N_total / 128 - 1);
+    t.nblk1 = min(2 * t.nb + 1, p.N_total / 128 - 1);
+  }
+  // every field is uniform over the wave: keep them in scalar registers
+  t.e = __builtin_amdgcn_readfirstlane(t.e);
+  t.nt_e = __builtin_amdgcn_readfirstlane(t.nt_e);
+  t.mt_idx = __builtin_amdgcn_readfirstlane(t.mt_idx);
+  t.nb = __builtin_amdgcn_readfirstlane(t.nb);
+  t.row0 = __builtin_amdgcn_readfirstlane(t.row0);
+  t.nrows = __builtin_amdgcn_readfirstlane(t.nrows);
+  t.wrow0 = __builtin_amdgcn_readfirstlane(t.wrow0);
+  t.nblk0 = __builtin_amdgcn_readfirstlane(t.nblk0);
+  t.nblk1 = __builtin_amdgcn_readfirstlane(t.nblk1);
+  return t;
+}
+
+// This lane's source addresses of a work item's direct loads (K block 0).
+template <int JA, int JB, int PF>
+struct TileSrc {
+  const uint8_t *a[JA];
+  const uint8_t *b[JB];
+  const uint8_t *pf[PF > 0 ? PF : 1];
+  const float *s;
+};
+
+template <bool G1, int MT, int WM, int JA, int JB, int PF>
+__device__ __forceinline__ void tile_sources(const GemmParams &p, const TileItem &t, int wave, int lane,
+                                             TileSrc<JA, JB, PF> &src) {
+  constexpr int BM = 16 * MT * WM;
+  constexpr int MTW = MT * WM;
+  const int wm = wave >> 2;
+  const size_t K = (size_t)p.K;
+  // A wave-wide 16-byte load fills 1 KB of a stage: lane L writes slot L,
+  // i.e. row 8q + L/8, slot L % 8 of 8-row block q, and so fetches chunk
+  // (L % 8) ^ f(row) of that row (f depends on the row's position in its
+  // 16-row fragment only).
+  const int sw_l = lane >> 3;
+#pragma unroll
+  for (int j = 0; j < JA; ++j) {
+    const int r = 8 * (wave * JA + j) + sw_l;
+    const int rr = min(r, t.nrows - 1);  // ragged tail: repeat the last row
+    const int row = G1 ? p.perm_token[t.row0 + rr] : t.row0 + rr;
+    src.a[j] = p.A + (size_t)row * K + 16 * ((lane & 7) ^ tile_swz(r));
+  }
+  // weight rows: the column wave wn's 64 rows are 8 blocks, loaded JB each by
+  // the WM waves of that column
+  const uint8_t *Bexp = p.B + (size_t)t.e * p.N_total * K;
+#pragma unroll
+  for (int j = 0; j < JB; ++j) {
+    const int r = 8 * (wm * JB + j) + sw_l;
+    const int rg = min(t.wrow0 + r, p.N_total - 1);  // ragged last GEMM2 block
+    src.b[j] = Bexp + (size_t)rg * K + 16 * ((lane & 7) ^ tile_swz(r));
+  }
+  // L2 prefetch one K-step beyond the ring: one dword per 128-byte line,
+  // landing in a junk LDS area that is never read.  Each line is prefetched
+  // by one of the items that share it and run side by side on the XCD (the
+  // others then hit in L2 instead of all waiting on the same miss): the A
+  // rows of an M-tile are split over the kGroupN column blocks of its group,
+  // the weight rows of a column block over MS consecutive M-tiles.  Lanes
+  // past the item's share repeat its first line (one request per load).
+  const int ms = t.nt_e >= 4 ? 4 : (t.nt_e >= 2 ? 2 : 1);
+  const int a_share = BM / kGroupN;
+  const int w_share = 256 / ms;
+  const int a_first = (t.nb % kGroupN) * a_share;
+  const int w_first = (t.mt_idx % ms) * w_share;
+#pragma unroll
+  for (int j = 0; j < PF; ++j) {
+    int line = (wave * PF + j) * kWave + lane;
+    if (line >= a_share + w_share) line = 0;
+    if (line < a_share) {
+      const int rr = min(a_first + line, t.nrows - 1);
+      src.pf[j] = p.A + (size_t)(G1 ? p.perm_token[t.row0 + rr] : t.row0 + rr) * K;
+    } else {
+      const int c = w_first + line - a_share;  // weight row c % 64 of column wave c / 64
+      const int w2 = c >> 6;
+      const int base = G1 ? (w2 >> 1) * p.I + t.nb * 128 + 64 * (w2 & 1) : t.nb * kTileCols + 64 * w2;
+      src.pf[j] = Bexp + (size_t)min(base + (c & 63), p.N_total - 1) * K;
+    }
+  }
+  // row scales: slot s = (row % 16) * MTW + row / 16; lane L of wave w loads
+  // slot 64 w + L (slots >= BM are loaded but never read).  They come from
+  // the K-block-major copy sa_tile (permuted rows): the 64 lanes' rows lie
+  // within one tile, so a K step's scale load touches a few cache lines.
+  const int sl = 64 * wave + lane;
+  const int r = sl < BM ? 16 * (sl % MTW) + sl / MTW : t.nrows - 1;
+  src.s = p.sa_tile + (size_t)(t.row0 + min(r, t.nrows - 1)) * p.sa_row;
+}
+
+// GEMM2's epilogue: the wave's accumulators (rows wrow + 16 m + r16 of the
+// tile, columns wrow0 + 16 n + 4 g4 + i) as fp16 Y codes with one exponent
+// per row and 16-column chunk; the chunk (sub-tile n) of row r16 is held by
+// the lanes r16 + 16 g4, four columns each.
+template <int MT>
+__device__ __forceinline__ void tile_store_y(const GemmParams &p, const v4f (&acc)[MT][4], int row0,
+                                             int nrows, int wrow0, int wrow, int r16, int g4) {
+  const int HC = p.H / kYChunk;
+#pragma unroll
+  for (int m = 0; m < MT; ++m) {
+    const int r = wrow + 16 * m + r16;
+    int ex[4];
+#pragma unroll
+    for (int n = 0; n < 4; ++n) {
+      float mx = fmaxf(fmaxf(fabsf(acc[m][n][0]), fabsf(acc[m][n][1])),
+                       fmaxf(fabsf(acc[m][n][2]), fabsf(acc[m][n][3])));
+      mx = fmaxf(mx, __shfl_xor(mx, 16));
+      mx = fmaxf(mx, __shfl_xor(mx, 32));
+      ex[n] = y16_exponent(mx);
+    }
+    if (r < nrows) {
+      uint16_t *yrow = p.Y + (size_t)(row0 + r) * p.H + wrow0 + 4 * g4;
+#pragma unroll
+      for (int n = 0; n < 4; ++n) {
+        uint2 c;
+        c.x = (uint32_t)y16_code(acc[m][n][0], ex[n]) | ((uint32_t)y16_code(acc[m][n][1], ex[n]) << 16);
+        c.y = (uint32_t)y16_code(acc[m][n][2], ex[n]) | ((uint32_t)y16_code(acc[m][n][3], ex[n]) << 16);
+        *reinterpret_cast<uint2 *>(yrow + 16 * n) = c;
+      }
+      // lane r16 + 16 g4 stores the exponent of chunk g4
+      int eg = ex[0];
+#pragma unroll
+      for (int n = 1; n < 4; ++n) eg = g4 == n ? ex[n] : eg;
+      p.Ye[(size_t)(row0 + r) * HC + wrow0 / kYChunk + g4] = (int8_t)eg;
+    }
+  }
+}
+
 template <bool G1, int MT, int WM, int S>
 __global__ __launch_bounds__(256 * WM) void gemm_tile_kernel(GemmParams p) {
   using L = TileLayout<MT, WM, S>;
@@ -136,47 +297,16 @@ __global__ __launch_bounds__(256 * WM) void gemm_tile_kernel(GemmParams p) {
   __syncthreads();
 
   // ---- decode the work item
-  const int NB = p.NB;
-  const int qt = item / NB;
-  int lo = 0, hi = p.El;
-  while (hi - lo > 1) {
-    const int mid = (lo + hi) >> 1;
-    if (tb[mid] <= qt) lo = mid; else hi = mid;
-  }
-  const int e = lo;
-  const int nt_e = tb[e + 1] - tb[e];
-  const int local = item - tb[e] * NB;
-  const int G = (NB + kGroupN - 1) / kGroupN;
-  const int grp = min(local / (kGroupN * nt_e), G - 1);
-  const int wi = local - grp * kGroupN * nt_e;
-  const int gsz = min(kGroupN, NB - kGroupN * grp);
-  const int mt_idx = wi / gsz;
-  const int nb = kGroupN * grp + wi % gsz;
-  const int seg0 = p.expert_offsets[e];
-  const int seg1 = p.expert_offsets[e + 1];
-  const int row0 = seg0 + mt_idx * BM;
-  const int nrows = min(BM, seg1 - row0);
+  const TileItem ti = tile_decode<G1, BM>(p, tb, item, wn);
+  const int e = ti.e, nb = ti.nb, row0 = ti.row0, nrows = ti.nrows, wrow0 = ti.wrow0;
   const int KB = p.KB;
-  const size_t K = (size_t)p.K;
-
-  // ---- this wave's weight rows and scale blocks
-  const int half = wn >> 1;  // GEMM1: 0 gate, 1 up.  GEMM2: 128-column half
-  int wrow0, nblk0, nblk1;
-  if (G1) {
-    wrow0 = half * p.I + nb * 128 + 64 * (wn & 1);
-    nblk0 = nb;
-    nblk1 = p.I / 128 + nb;
-  } else {
-    wrow0 = nb * kTileCols + 64 * wn;
-    nblk0 = min(2 * nb, p.N_total / 128 - 1);
-    nblk1 = min(2 * nb + 1, p.N_total / 128 - 1);
-  }
+  const int half = wn >> 1;
 
   // weight-block scales of the whole K range: sb_l[0][kb] (wn 0/1), sb_l[1][kb]
   float *sb_l = reinterpret_cast<float *>(smem + (G1 ? L::MAIN : L::RING));
   {
-    const float *s0 = p.B_scale + ((size_t)e * (p.N_total / 128) + nblk0) * KB;
-    const float *s1 = p.B_scale + ((size_t)e * (p.N_total / 128) + nblk1) * KB;
+    const float *s0 = p.B_scale + ((size_t)e * (p.N_total / 128) + ti.nblk0) * KB;
+    const float *s1 = p.B_scale + ((size_t)e * (p.N_total / 128) + ti.nblk1) * KB;
     for (int i = tid; i < KB; i += NT) {
       sb_l[i] = s0[i];
       sb_l[KB + i] = s1[i];
@@ -185,70 +315,12 @@ __global__ __launch_bounds__(256 * WM) void gemm_tile_kernel(GemmParams p) {
   const float *sb_w = sb_l + half * KB;
   __syncthreads();
 
-  // ---- direct-load assignments.  A wave-wide 16-byte load fills 1 KB of a
-  // stage: lane L writes slot L, i.e. row 8q + L/8, slot L % 8 of 8-row block
-  // q, and so fetches chunk (L % 8) ^ f(row) of that row (f depends on the
-  // row's position in its 16-row fragment only).
+  // ---- direct-load sources
   constexpr int JA = BM / 8 / (4 * WM);  // A blocks per wave
   constexpr int JB = 8 / WM;             // weight blocks per wave
-  const int sw_l = lane >> 3;
-  const uint8_t *a_src[JA];
-#pragma unroll
-  for (int j = 0; j < JA; ++j) {
-    const int r = 8 * (wave * JA + j) + sw_l;
-    const int rr = min(r, nrows - 1);  // ragged tail: repeat the last row
-    const int src = G1 ? p.perm_token[row0 + rr] : row0 + rr;
-    a_src[j] = p.A + (size_t)src * K + 16 * ((lane & 7) ^ tile_swz(r));
-  }
-  // weight rows: the column wave wn's 64 rows are 8 blocks, loaded JB each by
-  // the WM waves of that column
-  const uint8_t *Bexp = p.B + (size_t)e * p.N_total * K;
-  const uint8_t *b_src[JB];
-#pragma unroll
-  for (int j = 0; j < JB; ++j) {
-    const int r = 8 * (wm * JB + j) + sw_l;
-    const int rg = min(wrow0 + r, p.N_total - 1);  // ragged last GEMM2 block
-    b_src[j] = Bexp + (size_t)rg * K + 16 * ((lane & 7) ^ tile_swz(r));
-  }
-  // L2 prefetch one K-step beyond the ring: one dword per 128-byte line,
-  // landing in a junk LDS area that is never read.  Each line is prefetched
-  // by one of the items that share it and run side by side on the XCD (the
-  // others then hit in L2 instead of all waiting on the same miss): the A
-  // rows of an M-tile are split over the kGroupN column blocks of its group,
-  // the weight rows of a column block over MS consecutive M-tiles.  Lanes
-  // past the item's share repeat its first line (one request per load).
-  const int ms = nt_e >= 4 ? 4 : (nt_e >= 2 ? 2 : 1);
-  const int a_share = BM / kGroupN;
-  const int w_share = 256 / ms;
-  const int a_first = (nb % kGroupN) * a_share;
-  const int w_first = (mt_idx % ms) * w_share;
   constexpr int kPfLoads = (BM / kGroupN + 256 + 4 * WM * kWave - 1) / (4 * WM * kWave);
-  const uint8_t *pf_src[kPfLoads];
-#pragma unroll
-  for (int j = 0; j < kPfLoads; ++j) {
-    int line = (wave * kPfLoads + j) * kWave + lane;
-    if (line >= a_share + w_share) line = 0;
-    if (line < a_share) {
-      const int rr = min(a_first + line, nrows - 1);
-      pf_src[j] = p.A + (size_t)(G1 ? p.perm_token[row0 + rr] : row0 + rr) * K;
-    } else {
-      const int c = w_first + line - a_share;  // weight row c % 64 of column wave c / 64
-      const int w2 = c >> 6;
-      const int base = G1 ? (w2 >> 1) * p.I + nb * 128 + 64 * (w2 & 1) : nb * kTileCols + 64 * w2;
-      pf_src[j] = Bexp + (size_t)min(base + (c & 63), p.N_total - 1) * K;
-    }
-  }
-  // row scales: slot s = (row % 16) * MTW + row / 16; lane L of wave w loads
-  // slot 64 w + L (slots >= BM are loaded but never read).  They come from
-  // the K-block-major copy sa_tile (permuted rows): the 64 lanes' rows lie
-  // within one tile, so a K step's scale load touches a few cache lines.
-  const float *s_src;
-  {
-    const int sl = 64 * wave + lane;
-    const int r = sl < BM ? 16 * (sl % MTW) + sl / MTW : nrows - 1;
-    const int rr = min(r, nrows - 1);
-    s_src = p.sa_tile + (size_t)(row0 + rr) * p.sa_row;
-  }
+  TileSrc<JA, JB, kPfLoads> src;
+  tile_sources<G1, MT, WM>(p, ti, wave, lane, src);
   const size_t sa_kb = (size_t)p.sa_kb;
   // this lane's two 16-byte pieces of a fragment (rows 16m + r16 of a block)
   const int fr = tile_swz(r16);
@@ -285,17 +357,17 @@ __global__ __launch_bounds__(256 * WM) void gemm_tile_kernel(GemmParams p) {
     uint8_t *d_ = TILE_STAGE(st);                                                       \
     const size_t ko_ = (size_t)(kb) * 128;                                              \
     if ((j) < JA)                                                                       \
-      lds_load16(a_src[(j) < JA ? (j) : 0] + ko_, d_ + (wave * JA + (j)) * 1024);       \
+      lds_load16(src.a[(j) < JA ? (j) : 0] + ko_, d_ + (wave * JA + (j)) * 1024);       \
     else if ((j) < JA + JB)                                                             \
-      lds_load16(b_src[(j) >= JA && (j) < JA + JB ? (j) - JA : 0] + ko_,                \
+      lds_load16(src.b[(j) >= JA && (j) < JA + JB ? (j) - JA : 0] + ko_,                \
                  d_ + L::A_BYTES + wn * 8192 + (wm * JB + (j) - JA) * 1024);            \
     else                                                                                \
-      lds_load4(s_src + (kb) * sa_kb, d_ + L::SCL + wave * 256);                        \
+      lds_load4(src.s + (kb) * sa_kb, d_ + L::SCL + wave * 256);                        \
   } while (0)
 #define TILE_PREFETCH(kb)                                                               \
   do {                                                                                  \
     _Pragma("unroll") for (int j = 0; j < kPfLoads; ++j)                                \
-        lds_load4(pf_src[j] + (size_t)(kb) * 128, smem + S * L::STAGE + wave * 256);    \
+        lds_load4(src.pf[j] + (size_t)(kb) * 128, smem + S * L::STAGE + wave * 256);    \
   } while (0)
 // One K-step of the wave's 16 MT x 64 block: per 16-row block m, four MFMAs
 // (one per 16-column sub-tile), each started from zero and promoted with one
@@ -379,48 +451,12 @@ __global__ __launch_bounds__(256 * WM) void gemm_tile_kernel(GemmParams p) {
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   __syncthreads();
 
-#undef TILE_COMPUTE
-#undef TILE_PREFETCH
-#undef TILE_DMA_J
-#undef TILE_STAGE
 
   // accumulator element (m, n, i) of this lane: tile row 16 MT wm + 16m + r16,
   // column 16n + 4*g4 + i of the wave's 64 columns
   const int wrow = 16 * MT * wm;
   if (!G1) {
-    if (wrow0 >= p.N_total) return;  // columns past H (ragged last block)
-    // Y as fp16 codes with one exponent per row and 16-column chunk: the
-    // chunk (sub-tile n) of row r16 is held by the lanes r16 + 16 g4, four
-    // columns each
-    const int HC = p.H / kYChunk;
-#pragma unroll
-    for (int m = 0; m < MT; ++m) {
-      const int r = wrow + 16 * m + r16;
-      int ex[4];
-#pragma unroll
-      for (int n = 0; n < 4; ++n) {
-        float mx = fmaxf(fmaxf(fabsf(acc[m][n][0]), fabsf(acc[m][n][1])),
-                         fmaxf(fabsf(acc[m][n][2]), fabsf(acc[m][n][3])));
-        mx = fmaxf(mx, __shfl_xor(mx, 16));
-        mx = fmaxf(mx, __shfl_xor(mx, 32));
-        ex[n] = y16_exponent(mx);
-      }
-      if (r < nrows) {
-        uint16_t *yrow = p.Y + (size_t)(row0 + r) * p.H + wrow0 + 4 * g4;
-#pragma unroll
-        for (int n = 0; n < 4; ++n) {
-          uint2 c;
-          c.x = (uint32_t)y16_code(acc[m][n][0], ex[n]) | ((uint32_t)y16_code(acc[m][n][1], ex[n]) << 16);
-          c.y = (uint32_t)y16_code(acc[m][n][2], ex[n]) | ((uint32_t)y16_code(acc[m][n][3], ex[n]) << 16);
-          *reinterpret_cast<uint2 *>(yrow + 16 * n) = c;
-        }
-        // lane r16 + 16 g4 stores the exponent of chunk g4
-        int eg = ex[0];
-#pragma unroll
-        for (int n = 1; n < 4; ++n) eg = g4 == n ? ex[n] : eg;
-        p.Ye[(size_t)(row0 + r) * HC + wrow0 / kYChunk + g4] = (int8_t)eg;
-      }
-    }
+    if (wrow0 < p.N_total) tile_store_y<MT>(p, acc, row0, nrows, wrow0, wrow, r16, g4);
     return;
   }
 
@@ -483,6 +519,143 @@ __global__ __launch_bounds__(256 * WM) void gemm_tile_kernel(GemmParams p) {
   }
 }
 
+// GEMM2 on large tiles as a persistent grid: one workgroup per CU walks the
+// work items tile_item(b), tile_item(b + grid), ... (the grid a multiple of
+// 8, so every item runs on the XCD the one-shot launch would give it, in the
+// same rounds).  The LDS ring runs on across items: the last S-1 K steps of
+// an item load the first stages of the next one, and its weight-block scales
+// into the other half of a double buffer, so the next item's setup and first
+// loads hide behind the current item's math, and the current item's Y
+// stores go out while the next item's loads are in flight.  Needs KB >= S.
+template <int MT, int WM, int S>
+__global__ __launch_bounds__(256 * WM) void gemm2_tile_persist_kernel(GemmParams p) {
+  constexpr bool G1 = false;
+  using L = TileLayout<MT, WM, S>;
+  constexpr int NT = L::THREADS;
+  constexpr int BM = L::BM;
+  constexpr int MTW = MT * WM;
+  static_assert(MT % 4 == 0, "row scales are read four at a time");
+
+  __shared__ int tb[1028];
+  extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & (kWave - 1);
+  const int wave = tid / kWave;
+  const int wn = wave & 3;
+  const int wm = wave >> 2;
+  const int r16 = lane & 15;
+  const int g4 = lane >> 4;
+
+  const int n_items = *p.n_items;
+  int v = blockIdx.x;
+  int item = tile_item(v, n_items);
+  if (item < 0) return;
+
+  for (int i = tid; i <= p.El; i += NT) tb[i] = p.tile_base[i];
+  __syncthreads();
+
+  const int KB = p.KB;
+  const int half = wn >> 1;
+  constexpr int JA = BM / 8 / (4 * WM);
+  constexpr int JB = 8 / WM;
+  constexpr int kPfLoads = (BM / kGroupN + 256 + 4 * WM * kWave - 1) / (4 * WM * kWave);
+  constexpr int kGroup = JA + JB + 1;
+  constexpr int kWait = (S - 2) * (kGroup + kPfLoads) + kPfLoads;
+  constexpr int kSpread = MT / 2;
+  static_assert(kWait < 64, "vmcnt holds 6 bits");
+  static_assert(S >= 2, "LDS ring depth");
+
+  // weight-block scales, double-buffered: buffer q holds sb[0][kb] and
+  // sb[1][kb] of one item at sbufs + q * SBP.  Wave 0 fills it with direct
+  // loads issued before the item's first stage, so the wait for that stage
+  // covers them.
+  const int SBP = (2 * KB + kWave - 1) / kWave * kWave;
+  float *sbufs = reinterpret_cast<float *>(smem + L::RING);
+  auto load_sb = [&](const TileItem &t, int q) {
+    if (wave != 0) return;
+    const float *s0 = p.B_scale + ((size_t)t.e * (p.N_total / 128) + t.nblk0) * KB;
+    const float *s1 = p.B_scale + ((size_t)t.e * (p.N_total / 128) + t.nblk1) * KB;
+    for (int c = 0; c < SBP; c += kWave) {
+      const int i = c + lane;
+      const float *g = i < KB ? s0 + i : s1 + min(i - KB, KB - 1);
+      lds_load4(g, reinterpret_cast<uint8_t *>(sbufs + q * SBP + c));
+    }
+  };
+
+  TileItem ti = tile_decode<false, BM>(p, tb, item, wn);
+  TileSrc<JA, JB, kPfLoads> src;
+  tile_sources<false, MT, WM>(p, ti, wave, lane, src);
+  const size_t sa_kb = (size_t)p.sa_kb;
+  const int fr = tile_swz(r16);
+  const int rd_lo = r16 * 128 + 16 * ((2 * g4) ^ fr);
+  const int rd_hi = r16 * 128 + 16 * ((2 * g4 + 1) ^ fr);
+
+  v4f acc[MT][4];
+#pragma unroll
+  for (int m = 0; m < MT; ++m)
+#pragma unroll
+    for (int n = 0; n < 4; ++n) acc[m][n] = v4f{0.f, 0.f, 0.f, 0.f};
+
+  load_sb(ti, 0);
+#pragma unroll
+  for (int st = 0; st < S - 1; ++st) {
+#pragma unroll
+    for (int j = 0; j < kGroup; ++j) TILE_DMA_J(st, min(st, KB - 1), j);
+    TILE_PREFETCH(min(st + 1, KB - 1));
+    __builtin_amdgcn_sched_barrier(0);
+  }
+  asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(kWait) : "memory");
+
+  int st_rd = 0, st_ld = S - 1;
+  int cur = 0;  // scale buffer of the item being computed
+  int row0 = ti.row0, nrows = ti.nrows, wrow0 = ti.wrow0;
+  bool more = false;
+  const int wrow = 16 * MT * wm;
+  while (true) {
+    const float *sb_w = sbufs + cur * SBP + half * KB;
+    for (int it = 0; it < KB; ++it) {
+      const bool nxt = it >= KB - (S - 1);  // this step loads the next item
+      if (it == KB - (S - 1)) {
+        v += gridDim.x;
+        const int ni = tile_item(v, n_items);
+        more = ni >= 0;
+        if (more) {
+          ti = tile_decode<false, BM>(p, tb, ni, wn);
+          tile_sources<false, MT, WM>(p, ti, wave, lane, src);
+          load_sb(ti, cur ^ 1);
+        }
+      }
+      // K blocks of this step's loads and prefetches (with no next item the
+      // loads repeat the current item's last block: in bounds, never read)
+      const int kbl = !nxt ? it + S - 1 : (more ? it + S - 1 - KB : KB - 1);
+      const int kbp = !nxt ? min(it + S, KB - 1) : (more ? min(it + S - KB, KB - 1) : KB - 1);
+      TILE_COMPUTE(st_rd, it, st_ld, kbl, kbp);
+      __builtin_amdgcn_sched_barrier(0);
+      asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(kWait) : "memory");
+      st_rd = st_rd + 1 == S ? 0 : st_rd + 1;
+      st_ld = st_ld + 1 == S ? 0 : st_ld + 1;
+    }
+    if (wrow0 < p.N_total) tile_store_y<MT>(p, acc, row0, nrows, wrow0, wrow, r16, g4);
+#pragma unroll
+    for (int m = 0; m < MT; ++m)
+#pragma unroll
+      for (int n = 0; n < 4; ++n) acc[m][n] = v4f{0.f, 0.f, 0.f, 0.f};
+    if (!more) break;
+    row0 = ti.row0;
+    nrows = ti.nrows;
+    wrow0 = ti.wrow0;
+    cur ^= 1;
+  }
+  // the last steps' loads may still be landing in the ring
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+}
+
+#undef TILE_COMPUTE
+#undef TILE_PREFETCH
+#undef TILE_DMA_J
+#undef TILE_STAGE
+
 template <bool G1, int MT, int WM, int S>
 hipError_t launch_tile(const GemmParams &p, int grid, hipStream_t st) {
   using L = TileLayout<MT, WM, S>;
@@ -497,6 +670,43 @@ hipError_t launch_tile(const GemmParams &p, int grid, hipStream_t st) {
   return hipGetLastError();
 }
 
+// The persistent GEMM2: as many workgroups as the device has CUs (a
+// multiple of 8, at most the one-shot grid); one fits a CU (its LDS ring).
+// (Its dynamic LDS, the ring and the scale double buffer, must leave room for
+// the kernel's static tile_base copy in the CU's 160 KB; larger K ranges use
+// the one-shot kernel.)
+constexpr int kPersistMaxLds = 160 * 1024 - 1028 * (int)sizeof(int);
+
+template <int MT, int WM, int S>
+hipError_t launch_persist(const GemmParams &p, int grid, hipStream_t st) {
+  using L = TileLayout<MT, WM, S>;
+  auto k = gemm2_tile_persist_kernel<MT, WM, S>;
+  const size_t lds = (size_t)L::RING + sizeof(float) * 2 * (size_t)((2 * p.KB + kWave - 1) / kWave * kWave);
+  if (lds > (size_t)kPersistMaxLds) return launch_tile<false, MT, WM, S>(p, grid, st);
+  static hipError_t attr = hipFuncSetAttribute(reinterpret_cast<const void *>(k),
+                                               hipFuncAttributeMaxDynamicSharedMemorySize, kPersistMaxLds);
+  if (attr != hipSuccess) return attr;
+  int dev = 0, cus = 0;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+    return hipErrorInvalidValue;
+  int g = cus / 8 * 8;
+  if (g < 8) g = 8;
+  if (g > grid) g = grid;
+  hipLaunchKernelGGL(k, dim3(g), dim3(L::THREADS), lds, st, p);
+  return hipGetLastError();
+}
+
+template <bool G1, int MT, int WM, int S>
+hipError_t launch_any(const GemmParams &p, int grid, hipStream_t st) {
+  // (the eight-wave tiles keep the one-shot launch: with two waves per SIMD
+  // the persistent loop's extra state spills registers, measured slower)
+  if constexpr (!G1 && WM == 1) {
+    if (p.KB >= S) return launch_persist<MT, WM, S>(p, grid, st);
+  }
+  return launch_tile<G1, MT, WM, S>(p, grid, st);
+}
+
 }  // namespace
 
 int gemm_tile_cols() { return kTileCols; }
@@ -506,10 +716,10 @@ hipError_t launch_gemm_tile(const GemmParams &p, bool g1, int BM, int grid, hipS
   if (p.S != 1) return hipErrorInvalidValue;  // full-K items only
   switch (BM) {
     // 64 / 128 rows: 4 waves, three-stage ring (loads two K-steps ahead)
-    case 64: return g1 ? launch_tile<true, 4, 1, 3>(p, grid, st) : launch_tile<false, 4, 1, 3>(p, grid, st);
-    case 128: return g1 ? launch_tile<true, 8, 1, 3>(p, grid, st) : launch_tile<false, 8, 1, 3>(p, grid, st);
+    case 64: return g1 ? launch_any<true, 4, 1, 3>(p, grid, st) : launch_any<false, 4, 1, 3>(p, grid, st);
+    case 128: return g1 ? launch_any<true, 8, 1, 3>(p, grid, st) : launch_any<false, 8, 1, 3>(p, grid, st);
     // 256 rows: 8 waves (two per SIMD), two-stage ring
-    case 256: return g1 ? launch_tile<true, 8, 2, 2>(p, grid, st) : launch_tile<false, 8, 2, 2>(p, grid, st);
+    case 256: return g1 ? launch_any<true, 8, 2, 2>(p, grid, st) : launch_any<false, 8, 2, 2>(p, grid, st);
     default: return hipErrorInvalidValue;
   }
 }
