@@ -11,9 +11,10 @@
 // One workgroup of 4 x WM waves per item.  Wave (wm, wn) = (wave / 4,
 // wave % 4) owns rows [16 MT wm, 16 MT (wm+1)) of the tile (BM = 16 MT WM)
 // and 64 columns:
-//   GEMM1: wn = 0/1 own gate columns [0,64) / [64,128) of the 128-wide
-//          intermediate block, wn = 2/3 the matching up columns, so a wave's
-//          columns share one 128x128 weight-scale block;
+//   GEMM1: wn owns gate columns [32 wn, 32 wn + 32) of the 128-wide
+//          intermediate block and the matching up columns (sub-tiles 0-1
+//          gate, 2-3 up: SwiGLU pairs meet in the wave's registers; the
+//          gate and up halves take their own weight-block scale);
 //   GEMM2: wn owns output columns [64 wn, 64 wn + 64) of the 256-wide block.
 // Every K-step's operands -- the A tile (rows gathered through perm_token
 // for GEMM1), its row scales and the 256 weight rows -- go straight from
@@ -51,12 +52,7 @@ struct TileLayout {
   static constexpr int STAGE = SCL + 4 * WM * 256;
   static constexpr int JUNK = 4 * WM * 256;  // landing area of the L2 prefetches
   static constexpr int RING = S * STAGE + JUNK;
-  // GEMM1: the up waves hand their accumulators to the gate waves
-  static constexpr int XCH = 2 * WM * MT * 4 * 4 * kWave * 4;
-  static constexpr int MAIN = RING > XCH ? RING : XCH;
-  static size_t bytes(bool g1, int KB) {
-    return (size_t)(g1 ? MAIN : RING) + sizeof(float) * 2 * (size_t)KB;
-  }
+  static size_t bytes(int KB) { return (size_t)RING + sizeof(float) * 2 * (size_t)KB; }
 };
 
 typedef __attribute__((address_space(3))) void lds_void;
@@ -138,7 +134,10 @@ __device__ __forceinline__ TileItem tile_decode(const GemmParams &p, const int *
   t.nrows = min(BM, p.expert_offsets[lo + 1] - t.row0);
   const int half = wn >> 1;  // GEMM1: 0 gate, 1 up.  GEMM2: 128-column half
   if (G1) {
-    t.wrow0 = half * p.I + t.nb * 128 + 64 * (wn & 1);
+    // the wave's 64 weight rows: gate rows wrow0 .. wrow0+31 and the
+    // matching up rows I + wrow0 .. (so SwiGLU pairs meet in the wave)
+    (void)half;
+    t.wrow0 = t.nb * 128 + 32 * wn;
     t.nblk0 = t.nb;
     t.nblk1 = p.I / 128 + t.nb;
   } else {
@@ -193,7 +192,8 @@ __device__ __forceinline__ void tile_sources(const GemmParams &p, const TileItem
 #pragma unroll
   for (int j = 0; j < JB; ++j) {
     const int r = 8 * (wm * JB + j) + sw_l;
-    const int rg = min(t.wrow0 + r, p.N_total - 1);  // ragged last GEMM2 block
+    const int rg = G1 ? (r < 32 ? t.wrow0 + r : p.I + t.wrow0 + r - 32)
+                      : min(t.wrow0 + r, p.N_total - 1);  // ragged last GEMM2 block
     src.b[j] = Bexp + (size_t)rg * K + 16 * ((lane & 7) ^ tile_swz(r));
   }
   // L2 prefetch one K-step beyond the ring: one dword per 128-byte line,
@@ -217,9 +217,10 @@ __device__ __forceinline__ void tile_sources(const GemmParams &p, const TileItem
       src.pf[j] = p.A + (size_t)(G1 ? p.perm_token[t.row0 + rr] : t.row0 + rr) * K;
     } else {
       const int c = w_first + line - a_share;  // weight row c % 64 of column wave c / 64
-      const int w2 = c >> 6;
-      const int base = G1 ? (w2 >> 1) * p.I + t.nb * 128 + 64 * (w2 & 1) : t.nb * kTileCols + 64 * w2;
-      src.pf[j] = Bexp + (size_t)min(base + (c & 63), p.N_total - 1) * K;
+      const int w2 = c >> 6, rr = c & 63;
+      const int row = G1 ? (rr < 32 ? t.nb * 128 + 32 * w2 + rr : p.I + t.nb * 128 + 32 * w2 + rr - 32)
+                         : t.nb * kTileCols + 64 * w2 + rr;
+      src.pf[j] = Bexp + (size_t)min(row, p.N_total - 1) * K;
     }
   }
   // row scales: slot s = (row % 16) * MTW + row / 16; lane L of wave w loads
@@ -269,6 +270,57 @@ __device__ __forceinline__ void tile_store_y(const GemmParams &p, const v4f (&ac
   }
 }
 
+// GEMM1's epilogue: SwiGLU of the wave's 32 gate / 32 up column pairs (sub-
+// tiles n and n + 2 of the accumulators), the row's amax over the 128-column
+// block (four waves, through amax_l), scale amax / 448 (1 for an all-zero
+// block), e4m3 codes (nearest even, saturating), written with the scales
+// (row-major and, for the large-tile GEMM2, K-block-major).  The barrier
+// waits for LDS only: loads in flight for a next item may stay in flight.
+template <int MT, int BM>
+__device__ __forceinline__ void tile_store_act(const GemmParams &p, const v4f (&acc)[MT][4],
+                                               float (*amax_l)[BM], int row0, int nrows, int nb,
+                                               int wn, int wrow, int r16, int g4) {
+  float a[MT][2][4];
+#pragma unroll
+  for (int m = 0; m < MT; ++m) {
+    float mx = 0.0f;
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        a[m][h][i] = swiglu_spec(acc[m][h][i], acc[m][h + 2][i]);
+        mx = fmaxf(mx, fabsf(a[m][h][i]));
+      }
+    // the row's 32 columns of this wave sit in lanes r16, r16+16, r16+32, r16+48
+    mx = fmaxf(mx, __shfl_xor(mx, 16));
+    mx = fmaxf(mx, __shfl_xor(mx, 32));
+    if (g4 == 0) amax_l[wn][wrow + 16 * m + r16] = mx;
+  }
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+  const int IB = p.I / 128;
+#pragma unroll
+  for (int m = 0; m < MT; ++m) {
+    const int r = wrow + 16 * m + r16;
+    const float amax = fmaxf(fmaxf(amax_l[0][r], amax_l[1][r]), fmaxf(amax_l[2][r], amax_l[3][r]));
+    const float scale = (amax > 0.0f) ? amax / 448.0f : 1.0f;
+    if (r < nrows) {
+      uint8_t *arow = p.act + (size_t)(row0 + r) * p.I + nb * 128 + 32 * wn + 4 * g4;
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        uint32_t q = 0u;
+        if (amax > 0.0f)
+          q = e4m3x2_rne_sat(a[m][h][0] / scale, a[m][h][1] / scale) |
+              (e4m3x2_rne_sat(a[m][h][2] / scale, a[m][h][3] / scale) << 16);
+        *reinterpret_cast<uint32_t *>(arow + 16 * h) = q;
+      }
+      if (wn == 0 && g4 == 0) {
+        p.act_scale[(size_t)(row0 + r) * IB + nb] = scale;
+        if (p.act_scale_k) p.act_scale_k[(size_t)nb * p.P_max + row0 + r] = scale;
+      }
+    }
+  }
+}
+
 template <bool G1, int MT, int WM, int S>
 __global__ __launch_bounds__(256 * WM) void gemm_tile_kernel(GemmParams p) {
   using L = TileLayout<MT, WM, S>;
@@ -279,7 +331,7 @@ __global__ __launch_bounds__(256 * WM) void gemm_tile_kernel(GemmParams p) {
   static_assert(MT % 4 == 0, "row scales are read four at a time");
 
   __shared__ int tb[1028];
-  __shared__ float amax_l[2][BM];
+  __shared__ float amax_l[4][BM];
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
 
   const int tid = threadIdx.x;
@@ -303,7 +355,7 @@ __global__ __launch_bounds__(256 * WM) void gemm_tile_kernel(GemmParams p) {
   const int half = wn >> 1;
 
   // weight-block scales of the whole K range: sb_l[0][kb] (wn 0/1), sb_l[1][kb]
-  float *sb_l = reinterpret_cast<float *>(smem + (G1 ? L::MAIN : L::RING));
+  float *sb_l = reinterpret_cast<float *>(smem + L::RING);
   {
     const float *s0 = p.B_scale + ((size_t)e * (p.N_total / 128) + ti.nblk0) * KB;
     const float *s1 = p.B_scale + ((size_t)e * (p.N_total / 128) + ti.nblk1) * KB;
@@ -312,7 +364,8 @@ __global__ __launch_bounds__(256 * WM) void gemm_tile_kernel(GemmParams p) {
       sb_l[KB + i] = s1[i];
     }
   }
-  const float *sb_w = sb_l + half * KB;
+  // GEMM1: gate scales at sb_w[kb], up scales at sb_w[KB + kb]
+  const float *sb_w = G1 ? sb_l : sb_l + half * KB;
   __syncthreads();
 
   // ---- direct-load sources
@@ -390,6 +443,7 @@ __global__ __launch_bounds__(256 * WM) void gemm_tile_kernel(GemmParams p) {
     const float *sa_ =                                                                  \
         reinterpret_cast<const float *>(TILE_STAGE(st) + L::SCL) + r16 * MTW + wm * MT; \
     const float sbv_ = tile_f1(sb_w + (kb));                                            \
+    const float sbu_ = G1 ? tile_f1(sb_w + KB + (kb)) : sbv_;                           \
     float sav_[MT];                                                                     \
     _Pragma("unroll") for (int q_ = 0; q_ < MT / 4; ++q_) {                             \
       const float4 v_ = tile_f4(sa_ + 4 * q_);                                          \
@@ -413,6 +467,7 @@ __global__ __launch_bounds__(256 * WM) void gemm_tile_kernel(GemmParams p) {
       const v8i af_ = an_;                                                              \
       if (m + 1 < MT) an_ = tile_frag(as_ + (m + 1) * 2048, rd_lo, rd_hi);              \
       const float c_ = sav_[m] * sbv_;                                                  \
+      const float cu_ = G1 ? sav_[m] * sbu_ : c_;                                       \
       const v4f z_ = {0.f, 0.f, 0.f, 0.f};                                              \
       v4f t_[4];                                                                        \
       _Pragma("unroll") for (int n = 0; n < 4; ++n) t_[n] =                             \
@@ -420,7 +475,7 @@ __global__ __launch_bounds__(256 * WM) void gemm_tile_kernel(GemmParams p) {
                                                            0, 0, 0);                    \
       _Pragma("unroll") for (int n = 0; n < 4; ++n)                                     \
           _Pragma("unroll") for (int i = 0; i < 4; ++i)                                 \
-              acc[m][n][i] = __builtin_fmaf(t_[n][i], c_, acc[m][n][i]);               \
+              acc[m][n][i] = __builtin_fmaf(t_[n][i], n < 2 ? c_ : cu_, acc[m][n][i]); \
     }                                                                                   \
   } while (0)
 
@@ -446,10 +501,8 @@ __global__ __launch_bounds__(256 * WM) void gemm_tile_kernel(GemmParams p) {
     st_rd = st_rd + 1 == S ? 0 : st_rd + 1;
     st_ld = st_ld + 1 == S ? 0 : st_ld + 1;
   }
-  // the last steps' (clamped) loads may still be landing in the ring, which
-  // the GEMM1 epilogue reuses
+  // the last steps' (clamped) loads may still be landing in the ring
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-  __syncthreads();
 
 
   // accumulator element (m, n, i) of this lane: tile row 16 MT wm + 16m + r16,
@@ -460,66 +513,10 @@ __global__ __launch_bounds__(256 * WM) void gemm_tile_kernel(GemmParams p) {
     return;
   }
 
-  // SwiGLU: the up waves hand their accumulators to the gate waves of the
-  // same rows through LDS (lane-private slots), the gate waves apply
-  // silu(gate) * up.
-  float *xch = reinterpret_cast<float *>(smem);
-  const int pair = 2 * wm + (wn & 1);  // gate wave <-> up wave pair
-  if (wn >= 2) {
-#pragma unroll
-    for (int m = 0; m < MT; ++m)
-#pragma unroll
-      for (int n = 0; n < 4; ++n)
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-          xch[(((pair * MT + m) * 4 + n) * 4 + i) * kWave + lane] = acc[m][n][i];
-  }
-  __syncthreads();
-  if (wn < 2) {
-#pragma unroll
-    for (int m = 0; m < MT; ++m) {
-      float mx = 0.0f;
-#pragma unroll
-      for (int n = 0; n < 4; ++n)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const float u = xch[(((pair * MT + m) * 4 + n) * 4 + i) * kWave + lane];
-          acc[m][n][i] = swiglu_spec(acc[m][n][i], u);
-          mx = fmaxf(mx, fabsf(acc[m][n][i]));
-        }
-      // the row's 64 columns of this wave sit in lanes r16, r16+16, r16+32, r16+48
-      mx = fmaxf(mx, __shfl_xor(mx, 16));
-      mx = fmaxf(mx, __shfl_xor(mx, 32));
-      if (g4 == 0) amax_l[wn][wrow + 16 * m + r16] = mx;
-    }
-  }
-  __syncthreads();
-  if (wn >= 2) return;
-  const int IB = p.I / 128;
-#pragma unroll
-  for (int m = 0; m < MT; ++m) {
-    const int r = wrow + 16 * m + r16;
-    const float amax = fmaxf(amax_l[0][r], amax_l[1][r]);
-    const float scale = (amax > 0.0f) ? amax / 448.0f : 1.0f;
-    if (r < nrows) {
-      uint8_t *arow = p.act + (size_t)(row0 + r) * p.I + nb * 128 + 64 * wn + 4 * g4;
-#pragma unroll
-      for (int n = 0; n < 4; ++n) {
-        uint32_t q = 0u;
-        if (amax > 0.0f)
-          q = e4m3x2_rne_sat(acc[m][n][0] / scale, acc[m][n][1] / scale) |
-              (e4m3x2_rne_sat(acc[m][n][2] / scale, acc[m][n][3] / scale) << 16);
-        *reinterpret_cast<uint32_t *>(arow + 16 * n) = q;
-      }
-      if (wn == 0 && g4 == 0) {
-        p.act_scale[(size_t)(row0 + r) * IB + nb] = scale;
-        if (p.act_scale_k) p.act_scale_k[(size_t)nb * p.P_max + row0 + r] = scale;
-      }
-    }
-  }
+  tile_store_act<MT, BM>(p, acc, amax_l, row0, nrows, nb, wn, wrow, r16, g4);
 }
 
-// GEMM2 on large tiles as a persistent grid: one workgroup per CU walks the
+// The large-tile GEMMs as a persistent grid: one workgroup per CU walks the
 // work items tile_item(b), tile_item(b + grid), ... (the grid a multiple of
 // 8, so every item runs on the XCD the one-shot launch would give it, in the
 // same rounds).  The LDS ring runs on across items: the last S-1 K steps of
@@ -527,9 +524,8 @@ __global__ __launch_bounds__(256 * WM) void gemm_tile_kernel(GemmParams p) {
 // into the other half of a double buffer, so the next item's setup and first
 // loads hide behind the current item's math, and the current item's Y
 // stores go out while the next item's loads are in flight.  Needs KB >= S.
-template <int MT, int WM, int S>
-__global__ __launch_bounds__(256 * WM) void gemm2_tile_persist_kernel(GemmParams p) {
-  constexpr bool G1 = false;
+template <bool G1, int MT, int WM, int S>
+__global__ __launch_bounds__(256 * WM) void tile_persist_kernel(GemmParams p) {
   using L = TileLayout<MT, WM, S>;
   constexpr int NT = L::THREADS;
   constexpr int BM = L::BM;
@@ -537,6 +533,7 @@ __global__ __launch_bounds__(256 * WM) void gemm2_tile_persist_kernel(GemmParams
   static_assert(MT % 4 == 0, "row scales are read four at a time");
 
   __shared__ int tb[1028];
+  __shared__ float amax_l[4][BM];
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
 
   const int tid = threadIdx.x;
@@ -583,9 +580,9 @@ __global__ __launch_bounds__(256 * WM) void gemm2_tile_persist_kernel(GemmParams
     }
   };
 
-  TileItem ti = tile_decode<false, BM>(p, tb, item, wn);
+  TileItem ti = tile_decode<G1, BM>(p, tb, item, wn);
   TileSrc<JA, JB, kPfLoads> src;
-  tile_sources<false, MT, WM>(p, ti, wave, lane, src);
+  tile_sources<G1, MT, WM>(p, ti, wave, lane, src);
   const size_t sa_kb = (size_t)p.sa_kb;
   const int fr = tile_swz(r16);
   const int rd_lo = r16 * 128 + 16 * ((2 * g4) ^ fr);
@@ -609,11 +606,12 @@ __global__ __launch_bounds__(256 * WM) void gemm2_tile_persist_kernel(GemmParams
 
   int st_rd = 0, st_ld = S - 1;
   int cur = 0;  // scale buffer of the item being computed
-  int row0 = ti.row0, nrows = ti.nrows, wrow0 = ti.wrow0;
+  int row0 = ti.row0, nrows = ti.nrows, wrow0 = ti.wrow0, nb = ti.nb;
   bool more = false;
   const int wrow = 16 * MT * wm;
   while (true) {
-    const float *sb_w = sbufs + cur * SBP + half * KB;
+    // GEMM1: gate scales at sb_w[kb], up scales at sb_w[KB + kb]
+    const float *sb_w = sbufs + cur * SBP + (G1 ? 0 : half * KB);
     for (int it = 0; it < KB; ++it) {
       const bool nxt = it >= KB - (S - 1);  // this step loads the next item
       if (it == KB - (S - 1)) {
@@ -621,8 +619,8 @@ __global__ __launch_bounds__(256 * WM) void gemm2_tile_persist_kernel(GemmParams
         const int ni = tile_item(v, n_items);
         more = ni >= 0;
         if (more) {
-          ti = tile_decode<false, BM>(p, tb, ni, wn);
-          tile_sources<false, MT, WM>(p, ti, wave, lane, src);
+          ti = tile_decode<G1, BM>(p, tb, ni, wn);
+          tile_sources<G1, MT, WM>(p, ti, wave, lane, src);
           load_sb(ti, cur ^ 1);
         }
       }
@@ -636,7 +634,10 @@ __global__ __launch_bounds__(256 * WM) void gemm2_tile_persist_kernel(GemmParams
       st_rd = st_rd + 1 == S ? 0 : st_rd + 1;
       st_ld = st_ld + 1 == S ? 0 : st_ld + 1;
     }
-    if (wrow0 < p.N_total) tile_store_y<MT>(p, acc, row0, nrows, wrow0, wrow, r16, g4);
+    if (G1)
+      tile_store_act<MT, BM>(p, acc, amax_l, row0, nrows, nb, wn, wrow, r16, g4);
+    else if (wrow0 < p.N_total)
+      tile_store_y<MT>(p, acc, row0, nrows, wrow0, wrow, r16, g4);
 #pragma unroll
     for (int m = 0; m < MT; ++m)
 #pragma unroll
@@ -645,6 +646,7 @@ __global__ __launch_bounds__(256 * WM) void gemm2_tile_persist_kernel(GemmParams
     row0 = ti.row0;
     nrows = ti.nrows;
     wrow0 = ti.wrow0;
+    nb = ti.nb;
     cur ^= 1;
   }
   // the last steps' loads may still be landing in the ring
@@ -664,25 +666,25 @@ hipError_t launch_tile(const GemmParams &p, int grid, hipStream_t st) {
   // (to the size at the largest supported K, 512 blocks)
   static hipError_t attr = hipFuncSetAttribute(reinterpret_cast<const void *>(k),
                                                hipFuncAttributeMaxDynamicSharedMemorySize,
-                                               (int)L::bytes(G1, 512));
+                                               (int)L::bytes(512));
   if (attr != hipSuccess) return attr;
-  hipLaunchKernelGGL(k, dim3(grid), dim3(L::THREADS), L::bytes(G1, p.KB), st, p);
+  hipLaunchKernelGGL(k, dim3(grid), dim3(L::THREADS), L::bytes(p.KB), st, p);
   return hipGetLastError();
 }
 
-// The persistent GEMM2: as many workgroups as the device has CUs (a
+// The persistent grid: as many workgroups as the device has CUs (a
 // multiple of 8, at most the one-shot grid); one fits a CU (its LDS ring).
 // (Its dynamic LDS, the ring and the scale double buffer, must leave room for
-// the kernel's static tile_base copy in the CU's 160 KB; larger K ranges use
-// the one-shot kernel.)
-constexpr int kPersistMaxLds = 160 * 1024 - 1028 * (int)sizeof(int);
+// the kernel's static tile_base copy and row amax in the CU's 160 KB; larger
+// K ranges use the one-shot kernel.)
+constexpr int kPersistMaxLds = 160 * 1024 - 1028 * (int)sizeof(int) - 4 * 256 * (int)sizeof(float);
 
-template <int MT, int WM, int S>
+template <bool G1, int MT, int WM, int S>
 hipError_t launch_persist(const GemmParams &p, int grid, hipStream_t st) {
   using L = TileLayout<MT, WM, S>;
-  auto k = gemm2_tile_persist_kernel<MT, WM, S>;
+  auto k = tile_persist_kernel<G1, MT, WM, S>;
   const size_t lds = (size_t)L::RING + sizeof(float) * 2 * (size_t)((2 * p.KB + kWave - 1) / kWave * kWave);
-  if (lds > (size_t)kPersistMaxLds) return launch_tile<false, MT, WM, S>(p, grid, st);
+  if (lds > (size_t)kPersistMaxLds) return launch_tile<G1, MT, WM, S>(p, grid, st);
   static hipError_t attr = hipFuncSetAttribute(reinterpret_cast<const void *>(k),
                                                hipFuncAttributeMaxDynamicSharedMemorySize, kPersistMaxLds);
   if (attr != hipSuccess) return attr;
@@ -699,10 +701,11 @@ hipError_t launch_persist(const GemmParams &p, int grid, hipStream_t st) {
 
 template <bool G1, int MT, int WM, int S>
 hipError_t launch_any(const GemmParams &p, int grid, hipStream_t st) {
-  // (the eight-wave tiles keep the one-shot launch: with two waves per SIMD
-  // the persistent loop's extra state spills registers, measured slower)
+  // (GEMM2 only: GEMM1's 56-step items gained nothing from it, measured at
+  // prefill; the eight-wave tiles keep the one-shot launch: with two waves per
+  // SIMD the persistent loop's extra state spills registers, measured slower)
   if constexpr (!G1 && WM == 1) {
-    if (p.KB >= S) return launch_persist<MT, WM, S>(p, grid, st);
+    if (p.KB >= S) return launch_persist<G1, MT, WM, S>(p, grid, st);
   }
   return launch_tile<G1, MT, WM, S>(p, grid, st);
 }
