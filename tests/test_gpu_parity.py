@@ -157,7 +157,8 @@ def test_route_ties_bitexact(M):
 # ------------------------------------------------------------ whole layer
 FULL_CASES = [("tiny", 0), ("small_ragged", 0), ("small_ragged", 1), ("small_dense", 0), ("small_g6", 0),
               ("small_many", 0), ("small_t64", 0), ("small_t64", 1), ("small_t128", 0), ("small_t128", 2),
-              ("small_t256", 0), ("small_decode_all", 0), ("small_wide_i", 0), ("decode", 0),
+              ("small_t256", 0), ("small_t256_h640", 0), ("small_decode_all", 0), ("small_wide_i", 0),
+              ("decode", 0),
               ("decode", 1), ("mid", 0), ("median", 0)]
 
 

@@ -109,6 +109,11 @@ PARITY_CONFIGS: dict[str, MoEConfig] = {
     "small_wide_i": MoEConfig("small_wide_i", T=16, H=256, I=8192, num_experts=16,
                               num_local_experts=16, local_expert_offset=0, n_group=4,
                               topk_group=4, top_k=8),
+    # ~320 rows per expert with H = 640: 256-row tiles whose GEMM2 items take
+    # the 256-column blocks in pairs, the last pair a single (ragged) block
+    "small_t256_h640": MoEConfig("small_t256_h640", T=640, H=640, I=256, num_experts=8,
+                                 num_local_experts=8, local_expert_offset=0, n_group=2,
+                                 topk_group=2, top_k=4),
     # ~320 rows per expert: 256-row M-tiles with a ragged second tile
     "small_t256": MoEConfig("small_t256", T=640, H=384, I=256, num_experts=8,
                             num_local_experts=8, local_expert_offset=0, n_group=2,
