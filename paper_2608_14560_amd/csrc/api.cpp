@@ -62,6 +62,7 @@ struct Plan {
   bool gu1;      // ... and over gate and up rows (the fewest rows per expert)
   bool tile;     // large-tile kernels (BM >= 64)
   bool fused_combine;  // GEMM2 with the combine in its epilogue (T <= 16)
+  bool perm_in_gemm1;  // the narrow GEMM1 builds the permutation itself (T <= 16)
   int64_t P_max;
   size_t off_ids, off_w, off_offsets, off_perm_token, off_perm_pair, off_pair_row, off_chunk_counts,
       off_tile_base, off_n_items, off_act, off_act_scale, off_act_scale_k, off_hs_k, off_abuf, off_Y,
@@ -96,6 +97,10 @@ Plan make_plan(const moe_shape_t *s) {
   // at most 16 tokens: one 16-row tile per expert, and GEMM2 workgroups that
   // own output columns of every token sum the experts themselves
   p.fused_combine = p.BM == 16 && s->T <= combine_max_tokens() && combine_fits((int)p.P_max, s->I);
+  // at most 16 tokens with gate/up-split GEMM1 items: the GEMM1 workgroups
+  // rebuild the permutation from the routing ids (at most 256 pairs) and the
+  // permutation launch is skipped
+  p.perm_in_gemm1 = p.fused_combine && p.gu1 && TK <= 256 && s->T <= 16;
   p.nchunks = (int)((s->T + kChunkTokens - 1) / kChunkTokens);
   if (p.nchunks < 1) p.nchunks = 1;
   const int64_t touched = TK < s->num_local_experts ? TK : s->num_local_experts;
@@ -202,14 +207,7 @@ hipError_t enqueue_projection(const moe_shape_t *s, const Plan &pl, const Router
   return launch_router_partials(q, st);
 }
 
-moe_status_t enqueue_route(const moe_shape_t *s, const Plan &pl, const RouterIn &in,
-                           const float *bias, const Ptrs &r, void *ws, hipStream_t st,
-                           void *const *ev, int &stage) {
-  auto mark = [&]() {
-    if (ev) (void)hipEventRecord(static_cast<hipEvent_t>(ev[stage]), st);
-    ++stage;
-  };
-  const RouteParams rp = route_params(s, pl, in, bias, r, ws);
+PermuteParams permute_params(const moe_shape_t *s, const Plan &pl, const Ptrs &r, void *ws) {
   PermuteParams pp{};
   pp.topk_ids = r.ids;
   pp.chunk_counts = at<int32_t>(ws, pl.off_chunk_counts);
@@ -227,13 +225,27 @@ moe_status_t enqueue_route(const moe_shape_t *s, const Plan &pl, const RouterIn 
   pp.BM = pl.BM;
   pp.items_per_tile1 = pl.NB1 * pl.S1;
   pp.items_per_tile2 = pl.NB2 * pl.S2;
+  return pp;
+}
+
+// Stages (1) and (2); with skip_permute the permutation is left to the
+// narrow GEMM1 (its stage events are still recorded, around nothing).
+moe_status_t enqueue_route(const moe_shape_t *s, const Plan &pl, const RouterIn &in,
+                           const float *bias, const Ptrs &r, void *ws, hipStream_t st,
+                           void *const *ev, int &stage, bool skip_permute = false) {
+  auto mark = [&]() {
+    if (ev) (void)hipEventRecord(static_cast<hipEvent_t>(ev[stage]), st);
+    ++stage;
+  };
+  const RouteParams rp = route_params(s, pl, in, bias, r, ws);
+  const PermuteParams pp = permute_params(s, pl, r, ws);
   mark();
   MOE_TRY_HIP(enqueue_projection(s, pl, in, ws, st));
   MOE_TRY_HIP(launch_route(rp, st));
   mark();
-  MOE_TRY_HIP(launch_permute_count(pp, st));
+  if (!skip_permute) MOE_TRY_HIP(launch_permute_count(pp, st));
   mark();
-  MOE_TRY_HIP(launch_permute_scatter(pp, st));
+  if (!skip_permute) MOE_TRY_HIP(launch_permute_scatter(pp, st));
   return MOE_OK;
 }
 
@@ -315,7 +327,8 @@ moe_status_t fused_impl(const moe_shape_t *s, const uint8_t *hidden, const float
   const Ptrs r = route_ptrs(pl, ws, ro);
   int stage = 0;
   const RouterIn rin{logits, hidden, hidden_scale, router_weight};
-  if ((rc = enqueue_route(s, pl, rin, bias, r, ws, st, ev, stage)) != MOE_OK) return rc;
+  if ((rc = enqueue_route(s, pl, rin, bias, r, ws, st, ev, stage, pl.perm_in_gemm1)) != MOE_OK)
+    return rc;
   auto mark = [&]() {
     if (ev) (void)hipEventRecord(static_cast<hipEvent_t>(ev[stage]), st);
     ++stage;
@@ -357,8 +370,9 @@ moe_status_t fused_impl(const moe_shape_t *s, const uint8_t *hidden, const float
   g1.S = pl.S1;
   mark();
   const int grid1 = round8((int64_t)pl.max_tiles * pl.NB1 * pl.S1);
+  if (pl.perm_in_gemm1) g1.perm = permute_params(s, pl, r, ws);
   if (pl.narrow1)
-    MOE_TRY_HIP(launch_gemm1_narrow(g1, grid1, pl.gu1, st));
+    MOE_TRY_HIP(launch_gemm1_narrow(g1, grid1, pl.gu1, pl.perm_in_gemm1, st));
   else if (pl.tile)
     MOE_TRY_HIP(launch_gemm_tile(g1, true, pl.BM, grid1, st));
   else

@@ -30,6 +30,7 @@
 // same lane.  A and B tiles are staged through LDS (double buffered, rows
 // padded to 144 bytes).
 #include "moe_device.h"
+#include "scatter_device.h"
 
 namespace moe {
 namespace {
@@ -467,11 +468,98 @@ __global__ __launch_bounds__(kStreamWaves * kWave) void gemm2_stream_kernel(Gemm
 // SwiGLU output goes to a_buf [P, I] fp32 and requant_kernel (the next launch)
 // re-quantises it: no cross-workgroup synchronisation.  Values and codes are
 // bit-identical to the single-item epilogue.
-template <int D, bool GU>
+// Stage (2) inside the narrow GEMM1 for batches of at most 16 tokens (T K <=
+// 256 pairs): every workgroup rebuilds the permutation from the routing ids
+// in LDS -- bits[e] marks the tokens holding local expert e, so a pair's row
+// is offset[e] plus the count of its expert's tokens below it, the same
+// stable (expert, token) order as the permutation kernel -- and workgroup 0
+// writes the permuted-order arrays the later launches read.  Returns the
+// GEMM1 work-item count.  Every thread of the 128-thread workgroup calls it.
+constexpr int kNarrowPermThreads = 2 * kWave;
+
+__device__ int narrow_permute(const GemmParams &p, int *tb, int *off, unsigned *bits,
+                              int (*wsum)[2]) {
+  constexpr int NT = kNarrowPermThreads;
+  const PermuteParams &q = p.perm;
+  const int tid = threadIdx.x;
+  const int TK = q.T * q.K;
+  int le[2], tk[2];
+#pragma unroll
+  for (int u = 0; u < 2; ++u) {
+    const int pr = tid + NT * u;
+    const int x = q.topk_ids[min(pr, TK - 1)] - q.offset;
+    le[u] = (pr < TK && x >= 0 && x < q.El) ? x : -1;
+    tk[u] = pr / q.K;
+  }
+  for (int e = tid; e < q.El; e += NT) bits[e] = 0u;
+  __syncthreads();
+#pragma unroll
+  for (int u = 0; u < 2; ++u)
+    if (le[u] >= 0) atomicOr(&bits[le[u]], 1u << tk[u]);
+  __syncthreads();
+  // offsets and M-tile prefix: each thread a contiguous run of experts
+  const int per = (q.El + NT - 1) / NT;
+  const int e0 = tid * per;
+  int tot_run = 0, tiles_run = 0;
+  for (int e = e0; e < e0 + per && e < q.El; ++e) {
+    const int n = __popc(bits[e]);
+    tot_run += n;
+    tiles_run += (n + q.BM - 1) / q.BM;
+  }
+  int run_start, tile_start, P, n_tiles;
+  scatter_block_scan2<NT>(tot_run, tiles_run, wsum, run_start, tile_start, P, n_tiles);
+  const bool writer = blockIdx.x == 0;
+  int acc = run_start, tacc = tile_start;
+  for (int e = e0; e < e0 + per && e < q.El; ++e) {
+    const int n = __popc(bits[e]);
+    off[e] = acc;
+    tb[e] = tacc;
+    if (writer) {
+      q.expert_offsets[e] = acc;
+      q.tile_base[e] = tacc;
+    }
+    acc += n;
+    tacc += (n + q.BM - 1) / q.BM;
+  }
+  if (tid == 0) {
+    off[q.El] = P;
+    tb[q.El] = n_tiles;
+    if (writer) {
+      q.expert_offsets[q.El] = P;
+      q.tile_base[q.El] = n_tiles;
+      q.n_items[0] = n_tiles * q.items_per_tile1;
+      q.n_items[1] = n_tiles * q.items_per_tile2;
+    }
+  }
+  __syncthreads();
+  if (writer) {
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      const int pr = tid + NT * u;
+      if (pr < TK) {
+        int row = -1;
+        if (le[u] >= 0) {
+          row = off[le[u]] + __popc(bits[le[u]] & ((1u << tk[u]) - 1u));
+          q.perm_token[row] = tk[u];
+          q.perm_pair[row] = pr;
+        }
+        q.pair_row[pr] = row;
+      }
+    }
+  }
+  return n_tiles * q.items_per_tile1;
+}
+
+template <int D, bool GU, bool PERM>
 __global__ __launch_bounds__((GU ? 2 : 1) * kWave) void gemm1_narrow_kernel(GemmParams p) {
   constexpr int NT = (GU ? 2 : 1) * kWave;
   constexpr int kCols = GU ? 16 : 32;  // intermediate columns per item
+  static_assert(!PERM || (GU && NT == kNarrowPermThreads), "in-kernel permutation: two-wave items");
   __shared__ int tb[1028];
+  __shared__ int pm_off[PERM ? 1028 : 1];        // expert offsets (PERM)
+  __shared__ unsigned pm_bits[PERM ? 1024 : 1];  // tokens of each local expert (PERM)
+  __shared__ int pm_tok[PERM ? 16 : 1];          // the item's rows' tokens (PERM)
+  __shared__ int pm_wsum[PERM ? NT / kWave : 1][2];
   extern __shared__ __attribute__((aligned(16))) float scales[];  // sa[16][KB], sb[2][KB]
 
   const int tid = threadIdx.x;
@@ -480,13 +568,15 @@ __global__ __launch_bounds__((GU ? 2 : 1) * kWave) void gemm1_narrow_kernel(Gemm
   const int r16 = lane & 15;
   const int frag_off = (lane >> 4) * 32;
 
-  const int n_items = *p.n_items;
+  const int n_items = PERM ? narrow_permute(p, tb, pm_off, pm_bits, pm_wsum) : *p.n_items;
   const int per_xcd = (n_items + 7) / 8;
   const int item = (blockIdx.x & 7) * per_xcd + (blockIdx.x >> 3);
   if ((int)(blockIdx.x >> 3) >= per_xcd || item >= n_items) return;
 
-  for (int i = tid; i <= p.El; i += NT) tb[i] = p.tile_base[i];
-  __syncthreads();
+  if (!PERM) {
+    for (int i = tid; i <= p.El; i += NT) tb[i] = p.tile_base[i];
+    __syncthreads();
+  }
 
   const int X = p.NB;  // column groups per M-tile (no K split)
   const int qt = item / X;
@@ -501,12 +591,25 @@ __global__ __launch_bounds__((GU ? 2 : 1) * kWave) void gemm1_narrow_kernel(Gemm
   const int mt_idx = local % nt_e;
   const int j = local / nt_e;       // kCols-column group
   const int blk = j * kCols / 128;  // its 128-column block
-  const int seg0 = p.expert_offsets[e];
-  const int seg1 = p.expert_offsets[e + 1];
+  const int seg0 = PERM ? pm_off[e] : p.expert_offsets[e];
+  const int seg1 = PERM ? pm_off[e + 1] : p.expert_offsets[e + 1];
   const int row0 = seg0 + mt_idx * 16;
   const int nrows = min(16, seg1 - row0);
   const int KB = p.KB;
   const size_t K = (size_t)p.K;
+  if (PERM) {
+    // the expert's rows in token order: row r is its r-th marked token (at
+    // most 16 tokens, so one M-tile); ragged tails repeat the last row
+    if (tid < 16) {
+      unsigned m = pm_bits[e];
+      const int r = min(tid, nrows - 1);
+      for (int k = 0; k < r; ++k) m &= m - 1u;
+      pm_tok[tid] = __builtin_ctz(m);
+    }
+    __syncthreads();
+  }
+  // token of row r of the tile (r < 16, clamped by the caller)
+  auto row_token = [&](int r) { return PERM ? pm_tok[r] : p.perm_token[row0 + r]; };
 
   float *sa_l = scales;
   float *sb_l = scales + 16 * KB;
@@ -540,7 +643,7 @@ __global__ __launch_bounds__((GU ? 2 : 1) * kWave) void gemm1_narrow_kernel(Gemm
   } while (0)
   // the lane's activation row (ragged tails repeat the last row) and its
   // first D fragments
-  const int asrc = p.perm_token[row0 + min(r16, nrows - 1)];
+  const int asrc = row_token(min(r16, nrows - 1));
   const uint8_t *a_ptr = p.A + (size_t)asrc * K + frag_off;
   v8i ra[D];
   constexpr int kSaPer = 16;  // scale registers per thread on the fast path
@@ -555,7 +658,7 @@ __global__ __launch_bounds__((GU ? 2 : 1) * kWave) void gemm1_narrow_kernel(Gemm
 #pragma unroll
     for (int q = 0; q < kSaPer; ++q) {
       const int r = min(tid + q * NT, last) / KB;
-      srcv[q] = p.perm_token[row0 + min(r, nrows - 1)];
+      srcv[q] = row_token(min(r, nrows - 1));
     }
 #pragma unroll
     for (int d = 0; d < D; ++d) ra[d] = *reinterpret_cast<const v8i *>(a_ptr + (size_t)min(d, KB - 1) * 128);
@@ -580,7 +683,7 @@ __global__ __launch_bounds__((GU ? 2 : 1) * kWave) void gemm1_narrow_kernel(Gemm
   } else {
     for (int i = tid; i < 16 * KB; i += NT) {
       const int r = i / KB, kb = i % KB;
-      const int src = p.perm_token[row0 + min(r, nrows - 1)];
+      const int src = row_token(min(r, nrows - 1));
       sa_l[i] = p.A_scale[(size_t)src * KB + kb];
     }
     for (int i = tid; i < KB; i += NT) {
@@ -1015,13 +1118,20 @@ hipError_t launch_gemm1(const GemmParams &p, int BM, int grid, hipStream_t st) {
   if (grid <= 0) return hipSuccess;
   return BM == 32 ? launch_gemm_bm<32, true>(p, grid, st) : hipErrorInvalidValue;
 }
-hipError_t launch_gemm1_narrow(const GemmParams &p, int grid, bool gate_up_split, hipStream_t st) {
+hipError_t launch_gemm1_narrow(const GemmParams &p, int grid, bool gate_up_split, bool permute,
+                               hipStream_t st) {
   if (grid <= 0) return hipSuccess;
   const size_t lds = sizeof(float) * 18 * (size_t)p.KB;
-  if (gate_up_split)
-    hipLaunchKernelGGL((gemm1_narrow_kernel<kStreamDepth, true>), dim3(grid), dim3(2 * kWave), lds, st, p);
-  else
-    hipLaunchKernelGGL((gemm1_narrow_kernel<kStreamDepth, false>), dim3(grid), dim3(kWave), lds, st, p);
+  if (permute) {
+    if (!gate_up_split || p.perm.T * p.perm.K > 2 * kNarrowPermThreads || p.perm.T > 16 ||
+        p.perm.El > 1024 || p.perm.BM != 16)
+      return hipErrorInvalidValue;
+    hipLaunchKernelGGL((gemm1_narrow_kernel<kStreamDepth, true, true>), dim3(grid), dim3(2 * kWave), lds, st, p);
+  } else if (gate_up_split) {
+    hipLaunchKernelGGL((gemm1_narrow_kernel<kStreamDepth, true, false>), dim3(grid), dim3(2 * kWave), lds, st, p);
+  } else {
+    hipLaunchKernelGGL((gemm1_narrow_kernel<kStreamDepth, false, false>), dim3(grid), dim3(kWave), lds, st, p);
+  }
   return hipGetLastError();
 }
 int gemm1_narrow_cols(bool gate_up_split) { return gate_up_split ? 16 : 32; }

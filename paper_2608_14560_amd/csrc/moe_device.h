@@ -188,6 +188,9 @@ struct PermuteParams {
 constexpr int kChunkTokens = 256;   // tokens per permute workgroup
 
 struct GemmParams {
+  // (narrow GEMM1 of at most 16 tokens only) the routing's permutation, built
+  // by the GEMM1 workgroups themselves instead of a permutation launch
+  PermuteParams perm;
   // A operand: GEMM1 gathers hidden rows through perm_token; GEMM2 reads the
   // permuted activation rows directly.
   const uint8_t *A;          // [rows, K]
@@ -266,7 +269,10 @@ hipError_t launch_gather_scales(const int32_t *expert_offsets, int El, const int
                                 const float *hidden_scale, float *hs_k, int KB, int P_max,
                                 hipStream_t st);
 hipError_t launch_gemm1(const GemmParams &p, int BM, int grid, hipStream_t st);
-hipError_t launch_gemm1_narrow(const GemmParams &p, int grid, bool gate_up_split, hipStream_t st);
+// permute: the workgroups build the permutation themselves (p.perm; at most
+// 16 tokens, gate/up-split items) instead of reading a permutation launch's
+hipError_t launch_gemm1_narrow(const GemmParams &p, int grid, bool gate_up_split, bool permute,
+                               hipStream_t st);
 int gemm1_narrow_cols(bool gate_up_split);
 hipError_t launch_requant(const GemmParams &p, int P_max, hipStream_t st);
 hipError_t launch_gemm2(const GemmParams &p, int BM, int grid, hipStream_t st);
