@@ -662,12 +662,15 @@ template <bool G1, int MT, int WM, int S>
 hipError_t launch_tile(const GemmParams &p, int grid, hipStream_t st) {
   using L = TileLayout<MT, WM, S>;
   auto k = gemm_tile_kernel<G1, MT, WM, S>;
-  // the dynamic LDS limit is a property of the code object: raise it once
-  // (to the size at the largest supported K, 512 blocks)
+  // the dynamic LDS limit is a property of the code object: raise it once,
+  // to the size at the largest supported K (512 blocks) or what the CU's
+  // 160 KB leave beside the kernel's static arrays, whichever is smaller
+  constexpr int kStatic = 1028 * (int)sizeof(int) + 4 * L::BM * (int)sizeof(float);
+  const int cap = (int)L::bytes(512) < 160 * 1024 - kStatic ? (int)L::bytes(512) : 160 * 1024 - kStatic;
   static hipError_t attr = hipFuncSetAttribute(reinterpret_cast<const void *>(k),
-                                               hipFuncAttributeMaxDynamicSharedMemorySize,
-                                               (int)L::bytes(512));
+                                               hipFuncAttributeMaxDynamicSharedMemorySize, cap);
   if (attr != hipSuccess) return attr;
+  if (L::bytes(p.KB) > (size_t)cap) return hipErrorInvalidValue;
   hipLaunchKernelGGL(k, dim3(grid), dim3(L::THREADS), L::bytes(p.KB), st, p);
   return hipGetLastError();
 }
@@ -718,9 +721,11 @@ hipError_t launch_gemm_tile(const GemmParams &p, bool g1, int BM, int grid, hipS
   if (grid <= 0) return hipSuccess;
   if (p.S != 1) return hipErrorInvalidValue;  // full-K items only
   switch (BM) {
-    // 64 / 128 rows: 4 waves, three-stage ring (loads two K-steps ahead)
+    // 64 / 128 rows: three-stage ring (loads two K-steps ahead); GEMM1's
+    // 128-row tiles as 8 waves of 64 rows (two per SIMD: prefill GEMM1
+    // 333 -> 324 us), GEMM2's as 4 waves of 128 rows (the persistent grid)
     case 64: return g1 ? launch_any<true, 4, 1, 3>(p, grid, st) : launch_any<false, 4, 1, 3>(p, grid, st);
-    case 128: return g1 ? launch_any<true, 8, 1, 3>(p, grid, st) : launch_any<false, 8, 1, 3>(p, grid, st);
+    case 128: return g1 ? launch_any<true, 4, 2, 3>(p, grid, st) : launch_any<false, 8, 1, 3>(p, grid, st);
     // 256 rows: 8 waves (two per SIMD), two-stage ring
     case 256: return g1 ? launch_any<true, 8, 2, 2>(p, grid, st) : launch_any<false, 8, 2, 2>(p, grid, st);
     default: return hipErrorInvalidValue;
