@@ -19,6 +19,9 @@ struct ScatterLds {
   int hist[SINGLE ? kPermMaxEl : 1];
   unsigned long long bits[kPermTokenWaves][kPermMaxEl];
   int wsum[NT / kWave][2];
+  int cbase[kPermMaxEl];  // chunk-local start of each expert's pairs
+  int srow[kChunkTokens * kPermMaxK];   // the chunk's pairs in output order:
+  int spair[kChunkTokens * kPermMaxK];  // row and t K + j
 };
 
 // Inclusive scan over the wave with DPP: a window of four lanes (row_shr 1, 2,
@@ -149,6 +152,17 @@ __device__ void scatter_chunk(const PermuteParams &p, int chunk, const int32_t *
     p.n_items[1] = n_tiles * p.items_per_tile2;
   }
 
+  // chunk-local starts of the experts' pair runs: one more scan over the
+  // experts' counts in this chunk (same contiguous runs per thread)
+  int crun = 0;
+  for (int e = e0; e < e0 + per && e < p.El; ++e) crun += cnt(chunk, e);
+  int cstart, dummy_s, cpairs, dummy_t;
+  scatter_block_scan2<NT>(crun, 0, sh.wsum, cstart, dummy_s, cpairs, dummy_t);
+  for (int e = e0; e < e0 + per && e < p.El; ++e) {
+    sh.cbase[e] = cstart;
+    cstart += cnt(chunk, e);
+  }
+
   // rank the chunk's pairs: bit `lane` of bits[w][e] marks that the lane's
   // token holds local expert e
 #pragma unroll
@@ -163,15 +177,26 @@ __device__ void scatter_chunk(const PermuteParams &p, int chunk, const int32_t *
         int row = -1;
         const int e = le[j];
         if (e >= 0) {
-          row = sh.base[e];
-          for (int i = 0; i < w; ++i) row += __popcll(sh.bits[i][e]);
-          row += __popcll(sh.bits[w][e] & below);
-          p.perm_token[row] = t;
-          p.perm_pair[row] = t * p.K + j;
+          int rank = 0;  // among the chunk's pairs of expert e
+          for (int i = 0; i < w; ++i) rank += __popcll(sh.bits[i][e]);
+          rank += __popcll(sh.bits[w][e] & below);
+          row = sh.base[e] + rank;
+          // staged in output order: the chunk's pairs of an expert are one
+          // contiguous run of rows
+          const int li = sh.cbase[e] + rank;
+          sh.srow[li] = row;
+          sh.spair[li] = t * p.K + j;
         }
         p.pair_row[(size_t)t * p.K + j] = row;
       }
     }
+  }
+  __syncthreads();
+  // coalesced writes: consecutive threads, consecutive rows of a run
+  for (int i = threadIdx.x; i < cpairs; i += NT) {
+    const int row = sh.srow[i], pr = sh.spair[i];
+    p.perm_token[row] = pr / p.K;
+    p.perm_pair[row] = pr;
   }
 }
 
