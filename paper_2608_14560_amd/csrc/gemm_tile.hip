@@ -321,6 +321,65 @@ __device__ __forceinline__ void tile_store_act(const GemmParams &p, const v4f (&
   }
 }
 
+// GEMM2's epilogue through LDS (one-shot kernels, where the ring is free once
+// every wave has drained its loads): the wave's fp16 codes go to its own LDS
+// region as [16 MT rows][64 columns] (128-byte rows, 16-byte chunk c of row r
+// in slot c ^ (r % 8)), its exponents as [16 MT rows][4 chunks], and are read
+// back row-contiguously, so each global store instruction writes whole
+// 128-byte lines (8 rows x 8 lanes x 16 bytes) instead of 32-byte pieces of
+// four lines.  Same codes and exponents as tile_store_y.
+template <int MT>
+__device__ __forceinline__ void tile_store_y_lds(const GemmParams &p, const v4f (&acc)[MT][4], int row0,
+                                                 int nrows, int wrow0, int wrow, int lane,
+                                                 uint8_t *wl) {
+  constexpr int R = 16 * MT;  // the wave's rows
+  const int r16 = lane & 15, g4 = lane >> 4;
+  uint8_t *el = wl + R * 128;  // exponents
+#pragma unroll
+  for (int m = 0; m < MT; ++m) {
+    const int lr = 16 * m + r16;
+    int ex[4];
+#pragma unroll
+    for (int n = 0; n < 4; ++n) {
+      float mx = fmaxf(fmaxf(fabsf(acc[m][n][0]), fabsf(acc[m][n][1])),
+                       fmaxf(fabsf(acc[m][n][2]), fabsf(acc[m][n][3])));
+      mx = fmaxf(mx, __shfl_xor(mx, 16));
+      mx = fmaxf(mx, __shfl_xor(mx, 32));
+      ex[n] = y16_exponent(mx);
+    }
+#pragma unroll
+    for (int n = 0; n < 4; ++n) {
+      uint2 c;
+      c.x = (uint32_t)y16_code(acc[m][n][0], ex[n]) | ((uint32_t)y16_code(acc[m][n][1], ex[n]) << 16);
+      c.y = (uint32_t)y16_code(acc[m][n][2], ex[n]) | ((uint32_t)y16_code(acc[m][n][3], ex[n]) << 16);
+      const int ch = (2 * n + (g4 >> 1)) ^ (lr & 7);  // 16-byte chunk of columns 16n + 4g4
+      *reinterpret_cast<uint2 *>(wl + lr * 128 + ch * 16 + 8 * (g4 & 1)) = c;
+    }
+    int eg = ex[0];
+#pragma unroll
+    for (int n = 1; n < 4; ++n) eg = g4 == n ? ex[n] : eg;
+    el[lr * 4 + g4] = (uint8_t)(int8_t)eg;
+  }
+  // the wave reads back only its own region: its LDS operations are in order
+  // (the empty asm keeps the compiler from moving reads above the writes)
+  asm volatile("" ::: "memory");
+  const int HC = p.H / kYChunk;
+#pragma unroll
+  for (int k = 0; k < R / 8; ++k) {
+    const int lr = 8 * k + (lane >> 3), c = lane & 7;
+    const u32x4 v = *reinterpret_cast<const u32x4 *>(wl + lr * 128 + ((c ^ (lr & 7)) * 16));
+    if (wrow + lr < nrows)
+      *reinterpret_cast<u32x4 *>(p.Y + (size_t)(row0 + wrow + lr) * p.H + wrow0 + 8 * c) = v;
+  }
+#pragma unroll
+  for (int k = 0; k < R / 64; ++k) {
+    const int lr = 64 * k + lane;
+    const uint32_t v = *reinterpret_cast<const uint32_t *>(el + lr * 4);
+    if (wrow + lr < nrows)
+      *reinterpret_cast<uint32_t *>(p.Ye + (size_t)(row0 + wrow + lr) * HC + wrow0 / kYChunk) = v;
+  }
+}
+
 template <bool G1, int MT, int WM, int S>
 __global__ __launch_bounds__(256 * WM) void gemm_tile_kernel(GemmParams p) {
   using L = TileLayout<MT, WM, S>;
@@ -509,7 +568,11 @@ __global__ __launch_bounds__(256 * WM) void gemm_tile_kernel(GemmParams p) {
   // column 16n + 4*g4 + i of the wave's 64 columns
   const int wrow = 16 * MT * wm;
   if (!G1) {
-    if (wrow0 < p.N_total) tile_store_y<MT>(p, acc, row0, nrows, wrow0, wrow, r16, g4);
+    // every wave's loads have drained: the ring is free for the staging
+    asm volatile("s_barrier" ::: "memory");
+    static_assert(L::RING >= 4 * WM * (16 * MT * 132), "Y staging fits the ring");
+    if (wrow0 < p.N_total)
+      tile_store_y_lds<MT>(p, acc, row0, nrows, wrow0, wrow, lane, smem + wave * (16 * MT * 132));
     return;
   }
 
