@@ -494,8 +494,11 @@ __global__ __launch_bounds__(256 * WM) void gemm_tile_kernel(GemmParams p) {
 // K block kbl) and the last of them the prefetches (K block kbp); the
 // scheduling barrier after them lets everything but vector-memory
 // instructions move across (mask 0x78F), so the loads stay among that
-// block's MFMAs while the math keeps its free order.
-#define TILE_COMPUTE(st, kb, stl, kbl, kbp)                                              \
+// block's MFMAs while the math keeps its free order.  Only the first MV row
+// blocks (a compile-time count) are multiplied: the others hold no pairs of
+// the item, and their loads are still issued so that every wave's vmcnt
+// bookkeeping is the same.
+#define TILE_COMPUTE(st, kb, stl, kbl, kbp, MV)                                          \
   do {                                                                                  \
     const uint8_t *as_ = TILE_STAGE(st) + wm * MT * 2048;                               \
     const uint8_t *bs_ = TILE_STAGE(st) + L::A_BYTES + wn * 8192;                       \
@@ -514,7 +517,8 @@ __global__ __launch_bounds__(256 * WM) void gemm_tile_kernel(GemmParams p) {
     v8i bf_[4];                                                                         \
     _Pragma("unroll") for (int n = 0; n < 4; ++n) bf_[n] =                              \
         tile_frag(bs_ + n * 2048, rd_lo, rd_hi);                                        \
-    v8i an_ = tile_frag(as_, rd_lo, rd_hi);                                             \
+    v8i an_ = {};                                                                       \
+    if ((MV) > 0) an_ = tile_frag(as_, rd_lo, rd_hi);                                   \
     _Pragma("unroll") for (int m = 0; m < MT; ++m) {                                    \
       if (m < kSpread) {                                                                \
         _Pragma("unroll") for (int j_ = (m * kGroup) / kSpread;                         \
@@ -523,8 +527,9 @@ __global__ __launch_bounds__(256 * WM) void gemm_tile_kernel(GemmParams p) {
         if (m == kSpread - 1) TILE_PREFETCH(kbp);                                       \
         __builtin_amdgcn_sched_barrier(0x78F);                                          \
       }                                                                                 \
+      if (m >= (MV)) continue;                                                          \
       const v8i af_ = an_;                                                              \
-      if (m + 1 < MT) an_ = tile_frag(as_ + (m + 1) * 2048, rd_lo, rd_hi);              \
+      if (m + 1 < (MV)) an_ = tile_frag(as_ + (m + 1) * 2048, rd_lo, rd_hi);            \
       const float c_ = sav_[m] * sbv_;                                                  \
       const float cu_ = G1 ? sav_[m] * sbu_ : c_;                                       \
       const v4f z_ = {0.f, 0.f, 0.f, 0.f};                                              \
@@ -552,14 +557,28 @@ __global__ __launch_bounds__(256 * WM) void gemm_tile_kernel(GemmParams p) {
   }
   asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(kWait) : "memory");
 
-  int st_rd = 0, st_ld = S - 1;
-  for (int it = 0; it < KB; ++it) {
-    TILE_COMPUTE(st_rd, it, st_ld, min(it + S - 1, KB - 1), min(it + S, KB - 1));
-    __builtin_amdgcn_sched_barrier(0);
-    asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(kWait) : "memory");
-    st_rd = st_rd + 1 == S ? 0 : st_rd + 1;
-    st_ld = st_ld + 1 == S ? 0 : st_ld + 1;
-  }
+// the K loop with the first MV row blocks of the wave multiplied
+#define TILE_KLOOP(MV)                                                                  \
+  do {                                                                                  \
+    int st_rd = 0, st_ld = S - 1;                                                       \
+    for (int it = 0; it < KB; ++it) {                                                   \
+      TILE_COMPUTE(st_rd, it, st_ld, min(it + S - 1, KB - 1), min(it + S, KB - 1), MV); \
+      __builtin_amdgcn_sched_barrier(0);                                                \
+      asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(kWait) : "memory"); \
+      st_rd = st_rd + 1 == S ? 0 : st_rd + 1;                                           \
+      st_ld = st_ld + 1 == S ? 0 : st_ld + 1;                                           \
+    }                                                                                   \
+  } while (0)
+  // A ragged tile (an expert's last M-tile, or a tile taller than the
+  // expert's rows) leaves whole 16-row blocks of a wave without pairs: the
+  // wave then multiplies only its first MT/2 or MT/4 blocks, or none (their
+  // accumulators stay zero and the epilogue stores no row past the tile's).
+  const int mv = __builtin_amdgcn_readfirstlane(min(MT, max(0, (nrows - 16 * MT * wm + 15) >> 4)));
+  if (mv > MT / 2) TILE_KLOOP(MT);
+  else if (mv > MT / 4) TILE_KLOOP(MT / 2);
+  else if (mv > 0) TILE_KLOOP(MT / 4);
+  else TILE_KLOOP(0);
+#undef TILE_KLOOP
   // the last steps' (clamped) loads may still be landing in the ring
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
 
@@ -691,7 +710,7 @@ __global__ __launch_bounds__(256 * WM) void tile_persist_kernel(GemmParams p) {
       // loads repeat the current item's last block: in bounds, never read)
       const int kbl = !nxt ? it + S - 1 : (more ? it + S - 1 - KB : KB - 1);
       const int kbp = !nxt ? min(it + S, KB - 1) : (more ? min(it + S - KB, KB - 1) : KB - 1);
-      TILE_COMPUTE(st_rd, it, st_ld, kbl, kbp);
+      TILE_COMPUTE(st_rd, it, st_ld, kbl, kbp, MT);
       __builtin_amdgcn_sched_barrier(0);
       asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(kWait) : "memory");
       st_rd = st_rd + 1 == S ? 0 : st_rd + 1;
