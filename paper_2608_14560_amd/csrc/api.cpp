@@ -299,7 +299,11 @@ moe_status_t enqueue_gemm2_combine(const moe_shape_t *s, const Plan &pl, const P
                       : launch_gemm2(g2, pl.BM, grid2, st));
 
   // weighted combine in slot order, one bf16 rounding per element
-  FinalizeParams f{g2.Y, g2.Ye, r.pair_row, r.w, out, s->T, s->H, s->top_k};
+  // a chunk of 16 columns per thread where a token has at least 4 resident
+  // slots on average, half a chunk otherwise (more threads for the latency of
+  // the two dependent round trips when most slots are absent)
+  const int cw = (int64_t)s->top_k * s->num_local_experts >= 4 * (int64_t)s->num_experts ? 16 : 8;
+  FinalizeParams f{g2.Y, g2.Ye, r.pair_row, r.w, out, s->T, s->H, s->top_k, cw};
   mark();
   MOE_TRY_HIP(launch_finalize(f, st));
   return MOE_OK;

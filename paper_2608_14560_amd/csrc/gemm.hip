@@ -818,55 +818,66 @@ __global__ __launch_bounds__(256) void requant_kernel(GemmParams p) {
 // order, of w_j * Y[pair_row[t, j]]), Y read back from its fp16 codes and
 // chunk exponents (exact).  All K pair rows and weights are loaded first,
 // then the Y codes and exponents of the resident slots, so a token costs two
-// dependent round trips, not 2K.  A thread owns 8 columns (half a chunk).
-// KM >= K slots (4, 8 or 16).
-template <int KM>
-__global__ __launch_bounds__(256) void finalize_kernel(FinalizeParams p) {
+// dependent round trips, not 2K.  Workgroup (t, y) holds token t, and its
+// thread i the CW consecutive columns starting at CW (y * blockDim + i)
+// (CW = 16: one exponent byte and 32 bytes of codes per slot; CW = 8: half a
+// chunk): the token's slots are uniform over the workgroup (absent slots
+// branch around their loads without splitting a wave) and a wave's loads of
+// one slot are contiguous.  KM >= K slots (4, 8 or 16).
+constexpr int kFinalizeMaxThreads = 512;
+template <int KM, int CW>
+__global__ __launch_bounds__(kFinalizeMaxThreads) void finalize_kernel(FinalizeParams p) {
+  constexpr int NV = CW / 8;  // 16-byte pieces per slot
+  const int HC = p.H / kYChunk;
   const int t = blockIdx.x;
-  const int n0 = (blockIdx.y * 256 + threadIdx.x) * 8;
-  if (n0 >= p.H) return;
+  const int c0 = (blockIdx.y * blockDim.x + threadIdx.x) * CW;
+  if (c0 >= p.H) return;
   int pr[KM];
   float w[KM];
 #pragma unroll
   for (int j = 0; j < KM; ++j) {
     const int jj = min(j, p.K - 1);
-    pr[j] = p.pair_row[(size_t)t * p.K + jj];
+    pr[j] = j < p.K ? p.pair_row[(size_t)t * p.K + jj] : -1;
     w[j] = p.topk_w[(size_t)t * p.K + jj];
   }
-  // the token is the workgroup's, so pr[j] is uniform: absent slots branch
-  // around their loads without splitting the wave
-  const int HC = p.H / kYChunk;
-  uint4 yc[KM];
+  uint4 yc[KM][NV];
   int ye[KM];
 #pragma unroll
   for (int j = 0; j < KM; ++j) {
-    yc[j] = uint4{0u, 0u, 0u, 0u};
+#pragma unroll
+    for (int v = 0; v < NV; ++v) yc[j][v] = uint4{0u, 0u, 0u, 0u};
     ye[j] = 0;
     if (pr[j] >= 0) {
-      yc[j] = *reinterpret_cast<const uint4 *>(p.Y + (size_t)pr[j] * p.H + n0);
-      ye[j] = p.Ye[(size_t)pr[j] * HC + n0 / kYChunk];
+      const uint4 *yr = reinterpret_cast<const uint4 *>(p.Y + (size_t)pr[j] * p.H + c0);
+#pragma unroll
+      for (int v = 0; v < NV; ++v) yc[j][v] = yr[v];
+      ye[j] = p.Ye[(size_t)pr[j] * HC + c0 / kYChunk];
     }
   }
-  float acc[8];
+  float acc[CW];
 #pragma unroll
-  for (int c = 0; c < 8; ++c) acc[c] = 0.0f;
+  for (int c = 0; c < CW; ++c) acc[c] = 0.0f;
 #pragma unroll
   for (int j = 0; j < KM; ++j) {
-    if (j < p.K && pr[j] >= 0) {
-      const uint32_t u[4] = {yc[j].x, yc[j].y, yc[j].z, yc[j].w};
+    if (pr[j] >= 0) {
 #pragma unroll
-      for (int c = 0; c < 8; ++c) {
-        const float y = y16_value((uint16_t)(u[c >> 1] >> (16 * (c & 1))), ye[j]);
+      for (int c = 0; c < CW; ++c) {
+        const uint4 q = yc[j][c >> 3];
+        const uint32_t u = (c & 7) < 2 ? q.x : ((c & 7) < 4 ? q.y : ((c & 7) < 6 ? q.z : q.w));
+        const float y = y16_value((uint16_t)(u >> (16 * (c & 1))), ye[j]);
         acc[c] = __builtin_fmaf(w[j], y, acc[c]);
       }
     }
   }
-  uint4 o;
-  o.x = (uint32_t)f32_to_bf16_rne(acc[0]) | ((uint32_t)f32_to_bf16_rne(acc[1]) << 16);
-  o.y = (uint32_t)f32_to_bf16_rne(acc[2]) | ((uint32_t)f32_to_bf16_rne(acc[3]) << 16);
-  o.z = (uint32_t)f32_to_bf16_rne(acc[4]) | ((uint32_t)f32_to_bf16_rne(acc[5]) << 16);
-  o.w = (uint32_t)f32_to_bf16_rne(acc[6]) | ((uint32_t)f32_to_bf16_rne(acc[7]) << 16);
-  *reinterpret_cast<uint4 *>(p.out + (size_t)t * p.H + n0) = o;
+  uint4 *orow = reinterpret_cast<uint4 *>(p.out + (size_t)t * p.H + c0);
+#pragma unroll
+  for (int v = 0; v < NV; ++v) {
+    const float *a = acc + 8 * v;
+    orow[v] = uint4{(uint32_t)f32_to_bf16_rne(a[0]) | ((uint32_t)f32_to_bf16_rne(a[1]) << 16),
+                    (uint32_t)f32_to_bf16_rne(a[2]) | ((uint32_t)f32_to_bf16_rne(a[3]) << 16),
+                    (uint32_t)f32_to_bf16_rne(a[4]) | ((uint32_t)f32_to_bf16_rne(a[5]) << 16),
+                    (uint32_t)f32_to_bf16_rne(a[6]) | ((uint32_t)f32_to_bf16_rne(a[7]) << 16)};
+  }
 }
 
 // GEMM2 and the weighted combine of stage (4) in one kernel, for batches of at
@@ -1152,16 +1163,28 @@ hipError_t launch_gemm2(const GemmParams &p, int BM, int grid, hipStream_t st) {
   }
 }
 
+template <int CW>
+hipError_t launch_finalize_cw(const FinalizeParams &p, hipStream_t st) {
+  // 16 columns per thread: one workgroup per token where the row fits
+  // (H = 7168: 448 threads).  8 columns: column blocks of 256 threads (when
+  // most slots are absent, more and shorter workgroups per token measured
+  // faster: prefill 28.2 -> 25.8 us against 512-thread blocks)
+  const int cap = CW == 16 ? kFinalizeMaxThreads : 256;
+  const int per_token = p.H / CW;
+  const int nt = per_token < cap ? (per_token + kWave - 1) / kWave * kWave : cap;
+  const dim3 grid(p.T, (per_token + nt - 1) / nt);
+  if (p.K <= 4)
+    hipLaunchKernelGGL((finalize_kernel<4, CW>), grid, dim3(nt), 0, st, p);
+  else if (p.K <= 8)
+    hipLaunchKernelGGL((finalize_kernel<8, CW>), grid, dim3(nt), 0, st, p);
+  else
+    hipLaunchKernelGGL((finalize_kernel<16, CW>), grid, dim3(nt), 0, st, p);
+  return hipGetLastError();
+}
+
 hipError_t launch_finalize(const FinalizeParams &p, hipStream_t st) {
   if (p.T == 0) return hipSuccess;
-  dim3 grid(p.T, (p.H + 2047) / 2048);
-  if (p.K <= 4)
-    hipLaunchKernelGGL(finalize_kernel<4>, grid, dim3(256), 0, st, p);
-  else if (p.K <= 8)
-    hipLaunchKernelGGL(finalize_kernel<8>, grid, dim3(256), 0, st, p);
-  else
-    hipLaunchKernelGGL(finalize_kernel<16>, grid, dim3(256), 0, st, p);
-  return hipGetLastError();
+  return p.cw == 16 ? launch_finalize_cw<16>(p, st) : launch_finalize_cw<8>(p, st);
 }
 
 int combine_max_tokens() { return kCombineTokens; }

@@ -230,6 +230,7 @@ struct FinalizeParams {
   const float *topk_w;       // [T, K]
   uint16_t *out;             // [T, H] bf16
   int T, H, K;
+  int cw;                    // columns per thread: 16 or 8
 };
 
 // The weighted combine fused into GEMM2 (batches of at most 16 tokens).
