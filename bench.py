@@ -607,7 +607,7 @@ def run_config(cfg, steps: int, warmup: int, rotate: int, cold_calls: int, weigh
 # the metric's workloads, in order; the last one is the line's `value`
 METRIC_CONFIGS = ("decode", "mid", "prefill", "skewed")
 # CPU oracle sample per workload: tokens (all threads); single-thread tokens
-CPU_TOKENS = {"tiny": 8, "decode": 16, "mid": 256, "prefill": 1024, "skewed": 384, "median": 64,
+CPU_TOKENS = {"tiny": 8, "decode": 16, "mid": 256, "prefill": 1024, "skewed": 1152, "median": 64,
               "long": 1024}
 CPU_TOKENS_1T = {"tiny": 8, "decode": 16, "mid": 16}
 
