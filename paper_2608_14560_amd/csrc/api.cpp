@@ -63,6 +63,7 @@ struct Plan {
   bool tile;     // large-tile kernels (BM >= 64)
   bool fused_combine;  // GEMM2 with the combine in its epilogue (T <= 16)
   bool perm_in_gemm1;  // the narrow GEMM1 builds the permutation itself (T <= 16)
+  int ks1;             // narrow GEMM1: K ranges per item, each on its own waves
   int64_t P_max;
   size_t off_ids, off_w, off_offsets, off_perm_token, off_perm_pair, off_pair_row, off_chunk_counts,
       off_tile_base, off_n_items, off_act, off_act_scale, off_act_scale_k, off_hs_k, off_abuf, off_Y,
@@ -101,6 +102,10 @@ Plan make_plan(const moe_shape_t *s) {
   // rebuild the permutation from the routing ids (at most 256 pairs) and the
   // permutation launch is skipped
   p.perm_in_gemm1 = p.fused_combine && p.gu1 && TK <= 256 && s->T <= 16;
+  // 32-column items (more than 2 rows per expert): each item's K range in two
+  // halves on separate waves (twice the waves streaming; mid GEMM1 188 -> 172
+  // us); the two-wave gate/up items measured no better with it (decode)
+  p.ks1 = p.gu1 ? 1 : 2;
   p.nchunks = (int)((s->T + kChunkTokens - 1) / kChunkTokens);
   if (p.nchunks < 1) p.nchunks = 1;
   const int64_t touched = TK < s->num_local_experts ? TK : s->num_local_experts;
@@ -376,7 +381,7 @@ moe_status_t fused_impl(const moe_shape_t *s, const uint8_t *hidden, const float
   const int grid1 = round8((int64_t)pl.max_tiles * pl.NB1 * pl.S1);
   if (pl.perm_in_gemm1) g1.perm = permute_params(s, pl, r, ws);
   if (pl.narrow1)
-    MOE_TRY_HIP(launch_gemm1_narrow(g1, grid1, pl.gu1, pl.perm_in_gemm1, st));
+    MOE_TRY_HIP(launch_gemm1_narrow(g1, grid1, pl.gu1, pl.perm_in_gemm1, pl.ks1, st));
   else if (pl.tile)
     MOE_TRY_HIP(launch_gemm_tile(g1, true, pl.BM, grid1, st));
   else

@@ -475,17 +475,19 @@ __global__ __launch_bounds__(kStreamWaves * kWave) void gemm2_stream_kernel(Gemm
 // stable (expert, token) order as the permutation kernel -- and workgroup 0
 // writes the permuted-order arrays the later launches read.  Returns the
 // GEMM1 work-item count.  Every thread of the 128-thread workgroup calls it.
-constexpr int kNarrowPermThreads = 2 * kWave;
+constexpr int kNarrowPermPairs = 256;  // routed pairs the in-kernel permutation takes
 
+template <int NT>
 __device__ int narrow_permute(const GemmParams &p, int *tb, int *off, unsigned *bits,
                               int (*wsum)[2]) {
-  constexpr int NT = kNarrowPermThreads;
+  constexpr int PPT = kNarrowPermPairs / NT;  // pairs per thread
+  static_assert(PPT * NT == kNarrowPermPairs, "pairs split evenly over the threads");
   const PermuteParams &q = p.perm;
   const int tid = threadIdx.x;
   const int TK = q.T * q.K;
-  int le[2], tk[2];
+  int le[PPT], tk[PPT];
 #pragma unroll
-  for (int u = 0; u < 2; ++u) {
+  for (int u = 0; u < PPT; ++u) {
     const int pr = tid + NT * u;
     const int x = q.topk_ids[min(pr, TK - 1)] - q.offset;
     le[u] = (pr < TK && x >= 0 && x < q.El) ? x : -1;
@@ -494,7 +496,7 @@ __device__ int narrow_permute(const GemmParams &p, int *tb, int *off, unsigned *
   for (int e = tid; e < q.El; e += NT) bits[e] = 0u;
   __syncthreads();
 #pragma unroll
-  for (int u = 0; u < 2; ++u)
+  for (int u = 0; u < PPT; ++u)
     if (le[u] >= 0) atomicOr(&bits[le[u]], 1u << tk[u]);
   __syncthreads();
   // offsets and M-tile prefix: each thread a contiguous run of experts
@@ -534,7 +536,7 @@ __device__ int narrow_permute(const GemmParams &p, int *tb, int *off, unsigned *
   __syncthreads();
   if (writer) {
 #pragma unroll
-    for (int u = 0; u < 2; ++u) {
+    for (int u = 0; u < PPT; ++u) {
       const int pr = tid + NT * u;
       if (pr < TK) {
         int row = -1;
@@ -550,11 +552,13 @@ __device__ int narrow_permute(const GemmParams &p, int *tb, int *off, unsigned *
   return n_tiles * q.items_per_tile1;
 }
 
-template <int D, bool GU, bool PERM>
-__global__ __launch_bounds__((GU ? 2 : 1) * kWave) void gemm1_narrow_kernel(GemmParams p) {
-  constexpr int NT = (GU ? 2 : 1) * kWave;
+template <int D, bool GU, bool PERM, int KS>
+__global__ __launch_bounds__((GU ? 2 : 1) * KS * kWave) void gemm1_narrow_kernel(GemmParams p) {
+  constexpr int NR = GU ? 2 : 1;  // waves per K range (gate / up)
+  constexpr int NT = NR * KS * kWave;
   constexpr int kCols = GU ? 16 : 32;  // intermediate columns per item
-  static_assert(!PERM || (GU && NT == kNarrowPermThreads), "in-kernel permutation: two-wave items");
+  static_assert(!PERM || GU, "in-kernel permutation: gate/up-split items");
+  static_assert(KS == 1 || KS == 2 || KS == 4, "K split in 1, 2 or 4 ranges");
   __shared__ int tb[1028];
   __shared__ int pm_off[PERM ? 1028 : 1];        // expert offsets (PERM)
   __shared__ unsigned pm_bits[PERM ? 1024 : 1];  // tokens of each local expert (PERM)
@@ -568,7 +572,7 @@ __global__ __launch_bounds__((GU ? 2 : 1) * kWave) void gemm1_narrow_kernel(Gemm
   const int r16 = lane & 15;
   const int frag_off = (lane >> 4) * 32;
 
-  const int n_items = PERM ? narrow_permute(p, tb, pm_off, pm_bits, pm_wsum) : *p.n_items;
+  const int n_items = PERM ? narrow_permute<NT>(p, tb, pm_off, pm_bits, pm_wsum) : *p.n_items;
   const int per_xcd = (n_items + 7) / 8;
   const int item = (blockIdx.x & 7) * per_xcd + (blockIdx.x >> 3);
   if ((int)(blockIdx.x >> 3) >= per_xcd || item >= n_items) return;
@@ -597,6 +601,13 @@ __global__ __launch_bounds__((GU ? 2 : 1) * kWave) void gemm1_narrow_kernel(Gemm
   const int nrows = min(16, seg1 - row0);
   const int KB = p.KB;
   const size_t K = (size_t)p.K;
+  // the wave's role (GU: 0 gate, 1 up) and its K blocks [kb0, kb1): with
+  // KS > 1 the K ranges run on separate waves, their sums added in fixed
+  // order (range 0, then 1, ...) before the SwiGLU
+  const int role = GU ? (wave % NR) : 0;
+  const int kh = wave / NR;
+  const int KBh = (KB + KS - 1) / KS;
+  const int kb0 = min(kh * KBh, KB), kb1 = min(kb0 + KBh, KB);
   if (PERM) {
     // the expert's rows in token order: row r is its r-th marked token (at
     // most 16 tokens, so one M-tile); ragged tails repeat the last row
@@ -624,7 +635,7 @@ __global__ __launch_bounds__((GU ? 2 : 1) * kWave) void gemm1_narrow_kernel(Gemm
   // under way.
   const int col0 = j * kCols + r16, col1 = col0 + 16;
   const uint8_t *bexp = p.B + (size_t)e * p.N_total * K;
-  const uint8_t *g0 = bexp + ((size_t)col0 + (GU && wave ? p.I : 0)) * K + frag_off;
+  const uint8_t *g0 = bexp + ((size_t)col0 + (GU && role ? p.I : 0)) * K + frag_off;
   const uint8_t *g1 = bexp + (size_t)col1 * K + frag_off;
   const uint8_t *u0 = g0 + (size_t)p.I * K;
   const uint8_t *u1 = g1 + (size_t)p.I * K;
@@ -632,7 +643,7 @@ __global__ __launch_bounds__((GU ? 2 : 1) * kWave) void gemm1_narrow_kernel(Gemm
 #define MOE_WPREFETCH()                                                     \
   do {                                                                      \
     _Pragma("unroll") for (int d = 0; d < D; ++d) {                         \
-      const size_t o = (size_t)min(d, KB - 1) * 128;                        \
+      const size_t o = (size_t)max(min(kb0 + d, kb1 - 1), 0) * 128;         \
       rg0[d] = *reinterpret_cast<const v8i *>(g0 + o);                      \
       if (!GU) {                                                            \
         rg1[d] = *reinterpret_cast<const v8i *>(g1 + o);                    \
@@ -661,7 +672,8 @@ __global__ __launch_bounds__((GU ? 2 : 1) * kWave) void gemm1_narrow_kernel(Gemm
       srcv[q] = row_token(min(r, nrows - 1));
     }
 #pragma unroll
-    for (int d = 0; d < D; ++d) ra[d] = *reinterpret_cast<const v8i *>(a_ptr + (size_t)min(d, KB - 1) * 128);
+    for (int d = 0; d < D; ++d)
+      ra[d] = *reinterpret_cast<const v8i *>(a_ptr + (size_t)max(min(kb0 + d, kb1 - 1), 0) * 128);
     float sav[kSaPer];
 #pragma unroll
     for (int q = 0; q < kSaPer; ++q) {
@@ -691,7 +703,8 @@ __global__ __launch_bounds__((GU ? 2 : 1) * kWave) void gemm1_narrow_kernel(Gemm
       sb_l[KB + i] = su[i];
     }
 #pragma unroll
-    for (int d = 0; d < D; ++d) ra[d] = *reinterpret_cast<const v8i *>(a_ptr + (size_t)min(d, KB - 1) * 128);
+    for (int d = 0; d < D; ++d)
+      ra[d] = *reinterpret_cast<const v8i *>(a_ptr + (size_t)max(min(kb0 + d, kb1 - 1), 0) * 128);
     MOE_WPREFETCH();
   }
 #undef MOE_WPREFETCH
@@ -700,17 +713,18 @@ __global__ __launch_bounds__((GU ? 2 : 1) * kWave) void gemm1_narrow_kernel(Gemm
     // wave 0 streams the 16 gate rows, wave 1 the matching 16 up rows; the up
     // accumulators meet the gate ones in LDS for the SwiGLU
     __shared__ float up_l[4][kWave];
+    __shared__ float half_l[KS > 1 ? KS - 1 : 1][NR][4][kWave];
     const int col = col0;
-    const float *sbw = sb_l + (wave ? KB : 0);
+    const float *sbw = sb_l + (role ? KB : 0);
     __syncthreads();  // scales staged
 
     v4f acc = {0.f, 0.f, 0.f, 0.f};
     const int srow = 4 * (lane >> 4);
-    for (int base = 0; base < KB; base += D) {
+    for (int base = kb0; base < kb1; base += D) {
 #pragma unroll
       for (int d = 0; d < D; ++d) {
         const int kb = base + d;
-        if (kb < KB) {
+        if (kb < kb1) {
           const v4f z = {0.f, 0.f, 0.f, 0.f};
           const v4f t = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(ra[d], rg0[d], z, 0, 0, 0, 0, 0, 0);
           const float sw = sbw[kb];
@@ -720,17 +734,30 @@ __global__ __launch_bounds__((GU ? 2 : 1) * kWave) void gemm1_narrow_kernel(Gemm
             acc[i] = __builtin_fmaf(t[i], sa * sw, acc[i]);
           }
         }
-        const size_t o = (size_t)min(kb + D, KB - 1) * 128;
+        const size_t o = (size_t)min(kb + D, kb1 - 1) * 128;
         ra[d] = *reinterpret_cast<const v8i *>(a_ptr + o);
         rg0[d] = *reinterpret_cast<const v8i *>(g0 + o);
       }
     }
-    if (wave == 1) {
+    if (KS > 1) {
+      if (kh > 0) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) half_l[kh - 1][role][i][lane] = acc[i];
+      }
+      __syncthreads();
+      if (kh == 0) {
+#pragma unroll
+        for (int h = 0; h < KS - 1; ++h)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) acc[i] += half_l[h][role][i][lane];
+      }
+    }
+    if (kh == 0 && role == 1) {
 #pragma unroll
       for (int i = 0; i < 4; ++i) up_l[i][lane] = acc[i];
     }
     __syncthreads();
-    if (wave == 0) {
+    if (kh == 0 && role == 0) {
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int r = srow + i;
@@ -746,11 +773,11 @@ __global__ __launch_bounds__((GU ? 2 : 1) * kWave) void gemm1_narrow_kernel(Gemm
 
   v4f ag0 = {0.f, 0.f, 0.f, 0.f}, ag1 = ag0, au0 = ag0, au1 = ag0;
   const int srow = 4 * (lane >> 4);
-  for (int base = 0; base < KB; base += D) {
+  for (int base = kb0; base < kb1; base += D) {
 #pragma unroll
     for (int d = 0; d < D; ++d) {
       const int kb = base + d;
-      if (kb < KB) {
+      if (kb < kb1) {
         const v4f z = {0.f, 0.f, 0.f, 0.f};
         const v4f tg0 = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(ra[d], rg0[d], z, 0, 0, 0, 0, 0, 0);
         const v4f tg1 = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(ra[d], rg1[d], z, 0, 0, 0, 0, 0, 0);
@@ -766,13 +793,37 @@ __global__ __launch_bounds__((GU ? 2 : 1) * kWave) void gemm1_narrow_kernel(Gemm
           au1[i] = __builtin_fmaf(tu1[i], sa * su, au1[i]);
         }
       }
-      const size_t o = (size_t)min(kb + D, KB - 1) * 128;
+      const size_t o = (size_t)min(kb + D, kb1 - 1) * 128;
       ra[d] = *reinterpret_cast<const v8i *>(a_ptr + o);
       rg0[d] = *reinterpret_cast<const v8i *>(g0 + o);
       rg1[d] = *reinterpret_cast<const v8i *>(g1 + o);
       ru0[d] = *reinterpret_cast<const v8i *>(u0 + o);
       ru1[d] = *reinterpret_cast<const v8i *>(u1 + o);
     }
+  }
+  if (KS > 1) {
+    // the other K ranges' sums join the first's through LDS, in range order
+    __shared__ float half_l[KS > 1 ? KS - 1 : 1][4][4][kWave];
+    if (kh > 0) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        half_l[kh - 1][0][i][lane] = ag0[i];
+        half_l[kh - 1][1][i][lane] = ag1[i];
+        half_l[kh - 1][2][i][lane] = au0[i];
+        half_l[kh - 1][3][i][lane] = au1[i];
+      }
+    }
+    __syncthreads();
+    if (kh > 0) return;
+#pragma unroll
+    for (int h = 0; h < KS - 1; ++h)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        ag0[i] += half_l[h][0][i][lane];
+        ag1[i] += half_l[h][1][i][lane];
+        au0[i] += half_l[h][2][i][lane];
+        au1[i] += half_l[h][3][i][lane];
+      }
   }
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
@@ -1129,21 +1180,38 @@ hipError_t launch_gemm1(const GemmParams &p, int BM, int grid, hipStream_t st) {
   if (grid <= 0) return hipSuccess;
   return BM == 32 ? launch_gemm_bm<32, true>(p, grid, st) : hipErrorInvalidValue;
 }
-hipError_t launch_gemm1_narrow(const GemmParams &p, int grid, bool gate_up_split, bool permute,
-                               hipStream_t st) {
-  if (grid <= 0) return hipSuccess;
+template <int KS>
+hipError_t launch_gemm1_narrow_ks(const GemmParams &p, int grid, bool gate_up_split, bool permute,
+                                  hipStream_t st) {
   const size_t lds = sizeof(float) * 18 * (size_t)p.KB;
-  if (permute) {
-    if (!gate_up_split || p.perm.T * p.perm.K > 2 * kNarrowPermThreads || p.perm.T > 16 ||
+  if constexpr (KS > 2) {
+    // (gate/up-split items take at most two K ranges)
+    if (permute || gate_up_split) return hipErrorInvalidValue;
+  } else if (permute) {
+    if (!gate_up_split || p.perm.T * p.perm.K > kNarrowPermPairs || p.perm.T > 16 ||
         p.perm.El > 1024 || p.perm.BM != 16)
       return hipErrorInvalidValue;
-    hipLaunchKernelGGL((gemm1_narrow_kernel<kStreamDepth, true, true>), dim3(grid), dim3(2 * kWave), lds, st, p);
+    hipLaunchKernelGGL((gemm1_narrow_kernel<kStreamDepth, true, true, KS>), dim3(grid), dim3(2 * KS * kWave),
+                       lds, st, p);
+    return hipGetLastError();
   } else if (gate_up_split) {
-    hipLaunchKernelGGL((gemm1_narrow_kernel<kStreamDepth, true, false>), dim3(grid), dim3(2 * kWave), lds, st, p);
-  } else {
-    hipLaunchKernelGGL((gemm1_narrow_kernel<kStreamDepth, false, false>), dim3(grid), dim3(kWave), lds, st, p);
+    hipLaunchKernelGGL((gemm1_narrow_kernel<kStreamDepth, true, false, KS>), dim3(grid), dim3(2 * KS * kWave),
+                       lds, st, p);
+    return hipGetLastError();
+  }
+  {
+    hipLaunchKernelGGL((gemm1_narrow_kernel<kStreamDepth, false, false, KS>), dim3(grid), dim3(KS * kWave),
+                       lds, st, p);
   }
   return hipGetLastError();
+}
+hipError_t launch_gemm1_narrow(const GemmParams &p, int grid, bool gate_up_split, bool permute,
+                               int k_split, hipStream_t st) {
+  if (grid <= 0) return hipSuccess;
+  if (k_split == 1) return launch_gemm1_narrow_ks<1>(p, grid, gate_up_split, permute, st);
+  if (k_split == 2) return launch_gemm1_narrow_ks<2>(p, grid, gate_up_split, permute, st);
+  if (k_split == 4) return launch_gemm1_narrow_ks<4>(p, grid, gate_up_split, permute, st);
+  return hipErrorInvalidValue;
 }
 int gemm1_narrow_cols(bool gate_up_split) { return gate_up_split ? 16 : 32; }
 hipError_t launch_requant(const GemmParams &p, int P_max, hipStream_t st) {

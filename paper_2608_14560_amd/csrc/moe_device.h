@@ -272,8 +272,10 @@ hipError_t launch_gather_scales(const int32_t *expert_offsets, int El, const int
 hipError_t launch_gemm1(const GemmParams &p, int BM, int grid, hipStream_t st);
 // permute: the workgroups build the permutation themselves (p.perm; at most
 // 16 tokens, gate/up-split items) instead of reading a permutation launch's
+// k_split: 1, or 2 (each item's K range in two halves on separate waves,
+// their sums added in fixed order)
 hipError_t launch_gemm1_narrow(const GemmParams &p, int grid, bool gate_up_split, bool permute,
-                               hipStream_t st);
+                               int k_split, hipStream_t st);
 int gemm1_narrow_cols(bool gate_up_split);
 hipError_t launch_requant(const GemmParams &p, int P_max, hipStream_t st);
 hipError_t launch_gemm2(const GemmParams &p, int BM, int grid, hipStream_t st);
