@@ -51,6 +51,11 @@ struct TileLayout {
   static constexpr int SCL = A_BYTES + 4 * 8192;
   static constexpr int STAGE = SCL + 4 * WM * 256;
   static constexpr int JUNK = 4 * WM * 256;  // landing area of the L2 prefetches
+  // row-scale slots: row r16's MTW block scales at r16 * SS; rows 80 (or 48)
+  // bytes apart put the 16 rows' float4 reads in distinct LDS banks (at 64
+  // or 32 bytes they conflict four or two ways)
+  static constexpr int SS = MT * WM >= 8 ? MT * WM + 4 : MT * WM;
+  static_assert(16 * SS <= 64 * 4 * WM, "row-scale slots fit the workgroup's lanes");
   static constexpr int RING = S * STAGE + JUNK;
   static size_t bytes(int KB) { return (size_t)RING + sizeof(float) * 2 * (size_t)KB; }
 };
@@ -223,12 +228,15 @@ __device__ __forceinline__ void tile_sources(const GemmParams &p, const TileItem
       src.pf[j] = Bexp + (size_t)min(row, p.N_total - 1) * K;
     }
   }
-  // row scales: slot s = (row % 16) * MTW + row / 16; lane L of wave w loads
-  // slot 64 w + L (slots >= BM are loaded but never read).  They come from
-  // the K-block-major copy sa_tile (permuted rows): the 64 lanes' rows lie
-  // within one tile, so a K step's scale load touches a few cache lines.
+  // row scales: row 16 j + r16 at slot r16 * SS + j (j < MTW; the other
+  // slots are padding); lane L of wave w loads slot 64 w + L (padding and
+  // slots past the tile are loaded but never read).  They come from the
+  // K-block-major copy sa_tile (permuted rows): the 64 lanes' rows lie within
+  // one tile, so a K step's scale load touches a few cache lines.
+  constexpr int SS = TileLayout<MT, WM, 2>::SS;
   const int sl = 64 * wave + lane;
-  const int r = sl < BM ? 16 * (sl % MTW) + sl / MTW : t.nrows - 1;
+  const int sr = sl / SS, sj = sl % SS;
+  const int r = (sr < 16 && sj < MTW) ? 16 * sj + sr : t.nrows - 1;
   src.s = p.sa_tile + (size_t)(t.row0 + min(r, t.nrows - 1)) * p.sa_row;
 }
 
@@ -503,7 +511,7 @@ __global__ __launch_bounds__(256 * WM) void gemm_tile_kernel(GemmParams p) {
     const uint8_t *as_ = TILE_STAGE(st) + wm * MT * 2048;                               \
     const uint8_t *bs_ = TILE_STAGE(st) + L::A_BYTES + wn * 8192;                       \
     const float *sa_ =                                                                  \
-        reinterpret_cast<const float *>(TILE_STAGE(st) + L::SCL) + r16 * MTW + wm * MT; \
+        reinterpret_cast<const float *>(TILE_STAGE(st) + L::SCL) + r16 * L::SS + wm * MT; \
     const float sbv_ = tile_f1(sb_w + (kb));                                            \
     const float sbu_ = G1 ? tile_f1(sb_w + KB + (kb)) : sbv_;                           \
     float sav_[MT];                                                                     \
