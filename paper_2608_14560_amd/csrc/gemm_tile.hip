@@ -332,7 +332,9 @@ __device__ __forceinline__ void tile_store_act(const GemmParams &p, const v4f (&
 // GEMM2's epilogue through LDS (one-shot kernels, where the ring is free once
 // every wave has drained its loads): the wave's fp16 codes go to its own LDS
 // region as [16 MT rows][64 columns] (128-byte rows, 16-byte chunk c of row r
-// in slot c ^ (r % 8)), its exponents as [16 MT rows][4 chunks], and are read
+// in slot c ^ (r % 8) ^ (r / 8 % 2), so that rows r and r + 8 of a write
+// fall in different banks), its exponents as [16 MT rows][4 chunks] (one
+// dword per row), and are read
 // back row-contiguously, so each global store instruction writes whole
 // 128-byte lines (8 rows x 8 lanes x 16 bytes) instead of 32-byte pieces of
 // four lines.  Same codes and exponents as tile_store_y.
@@ -360,13 +362,14 @@ __device__ __forceinline__ void tile_store_y_lds(const GemmParams &p, const v4f 
       uint2 c;
       c.x = (uint32_t)y16_code(acc[m][n][0], ex[n]) | ((uint32_t)y16_code(acc[m][n][1], ex[n]) << 16);
       c.y = (uint32_t)y16_code(acc[m][n][2], ex[n]) | ((uint32_t)y16_code(acc[m][n][3], ex[n]) << 16);
-      const int ch = (2 * n + (g4 >> 1)) ^ (lr & 7);  // 16-byte chunk of columns 16n + 4g4
+      const int ch = (2 * n + (g4 >> 1)) ^ (lr & 7) ^ ((lr >> 3) & 1);  // chunk of columns 16n + 4g4
       *reinterpret_cast<uint2 *>(wl + lr * 128 + ch * 16 + 8 * (g4 & 1)) = c;
     }
-    int eg = ex[0];
-#pragma unroll
-    for (int n = 1; n < 4; ++n) eg = g4 == n ? ex[n] : eg;
-    el[lr * 4 + g4] = (uint8_t)(int8_t)eg;
+    // every lane of the row holds its four exponents: one dword per row
+    if (g4 == 0)
+      *reinterpret_cast<uint32_t *>(el + lr * 4) =
+          (uint32_t)(uint8_t)(int8_t)ex[0] | ((uint32_t)(uint8_t)(int8_t)ex[1] << 8) |
+          ((uint32_t)(uint8_t)(int8_t)ex[2] << 16) | ((uint32_t)(uint8_t)(int8_t)ex[3] << 24);
   }
   // the wave reads back only its own region: its LDS operations are in order
   // (the empty asm keeps the compiler from moving reads above the writes)
@@ -375,7 +378,7 @@ __device__ __forceinline__ void tile_store_y_lds(const GemmParams &p, const v4f 
 #pragma unroll
   for (int k = 0; k < R / 8; ++k) {
     const int lr = 8 * k + (lane >> 3), c = lane & 7;
-    const u32x4 v = *reinterpret_cast<const u32x4 *>(wl + lr * 128 + ((c ^ (lr & 7)) * 16));
+    const u32x4 v = *reinterpret_cast<const u32x4 *>(wl + lr * 128 + ((c ^ (lr & 7) ^ ((lr >> 3) & 1)) * 16));
     if (wrow + lr < nrows)
       *reinterpret_cast<u32x4 *>(p.Y + (size_t)(row0 + wrow + lr) * p.H + wrow0 + 8 * c) = v;
   }
