@@ -558,7 +558,7 @@ __global__ __launch_bounds__((GU ? 2 : 1) * KS * kWave) void gemm1_narrow_kernel
   constexpr int NT = NR * KS * kWave;
   constexpr int kCols = GU ? 16 : 32;  // intermediate columns per item
   static_assert(!PERM || GU, "in-kernel permutation: gate/up-split items");
-  static_assert(KS == 1 || KS == 2 || KS == 4, "K split in 1, 2 or 4 ranges");
+  static_assert(KS == 1 || KS == 2, "K split in one or two ranges");
   __shared__ int tb[1028];
   __shared__ int pm_off[PERM ? 1028 : 1];        // expert offsets (PERM)
   __shared__ unsigned pm_bits[PERM ? 1024 : 1];  // tokens of each local expert (PERM)
@@ -1184,10 +1184,7 @@ template <int KS>
 hipError_t launch_gemm1_narrow_ks(const GemmParams &p, int grid, bool gate_up_split, bool permute,
                                   hipStream_t st) {
   const size_t lds = sizeof(float) * 18 * (size_t)p.KB;
-  if constexpr (KS > 2) {
-    // (gate/up-split items take at most two K ranges)
-    if (permute || gate_up_split) return hipErrorInvalidValue;
-  } else if (permute) {
+  if (permute) {
     if (!gate_up_split || p.perm.T * p.perm.K > kNarrowPermPairs || p.perm.T > 16 ||
         p.perm.El > 1024 || p.perm.BM != 16)
       return hipErrorInvalidValue;
@@ -1210,7 +1207,6 @@ hipError_t launch_gemm1_narrow(const GemmParams &p, int grid, bool gate_up_split
   if (grid <= 0) return hipSuccess;
   if (k_split == 1) return launch_gemm1_narrow_ks<1>(p, grid, gate_up_split, permute, st);
   if (k_split == 2) return launch_gemm1_narrow_ks<2>(p, grid, gate_up_split, permute, st);
-  if (k_split == 4) return launch_gemm1_narrow_ks<4>(p, grid, gate_up_split, permute, st);
   return hipErrorInvalidValue;
 }
 int gemm1_narrow_cols(bool gate_up_split) { return gate_up_split ? 16 : 32; }
