@@ -8,13 +8,18 @@
 //         G = sum_kb (A_kb W13_kb^T) * sa[row,kb] * sw[n/128,kb]   (fp32)
 //         then a = silu(gate) * up, per-row 1x128 amax, scale = amax/448,
 //         FP8 re-quantisation -> act [P, I] e4m3 + act_scale.
-//  GEMM2: Y = sum_kb (act_kb W2_kb^T) * sa2 * sw2 -> Y [P, H] fp32
+//  GEMM2: Y = sum_kb (act_kb W2_kb^T) * sa2 * sw2 (fp32), stored as fp16
+//         codes with a power-of-two exponent per row and 16 columns
+//         (Y [P, H] + Ye [P, H/16]; the scaling is exact)
 //  finalize: out[t] = bf16( sum over resident slots j (slot order) of
 //            w_j * Y[pair_row[t,j]] ).
 //
-// Kernels here: the column-split GEMM1 and its re-quantisation launch plus
-// the streaming GEMM2 (16-row tiles), the LDS-staged GEMM1/GEMM2 for 32-row
-// tiles, the finalize, and test hooks.  Larger tiles are in gemm_tile.hip.
+// Kernels here: the column-split GEMM1 (its K range optionally in two
+// halves on separate waves; at most 16 tokens, the permutation rebuilt in
+// each workgroup) and its re-quantisation launch, the streaming GEMM2
+// (16-row tiles), GEMM2 with the combine in its epilogue (at most 16
+// tokens), the LDS-staged GEMM1/GEMM2 for 32-row tiles, the finalize, and
+// test hooks.  Larger tiles are in gemm_tile.hip.
 //
 // Work items of an expert are contiguous; workgroup b is mapped to item
 // (b % 8) * ceil(n/8) + b / 8 so neighbouring items land on the same XCD

@@ -27,8 +27,8 @@
 // row block.  Each 128-K step is one v_mfma_f32_16x16x128_f8f6f4 per
 // sub-tile, started from zero and promoted into the fp32 accumulator with
 // one FMA by (activation scale * weight-block scale), in K order -- the same
-// arithmetic as the small-tile kernels (the matrix cores' block sum does not
-// depend on which operand comes first).
+// arithmetic as the small-tile kernels that keep one K range per item (the
+// matrix cores' block sum does not depend on which operand comes first).
 #include "moe_device.h"
 
 namespace moe {
