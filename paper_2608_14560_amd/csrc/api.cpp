@@ -66,7 +66,7 @@ struct Plan {
   int ks1;             // narrow GEMM1: K ranges per item, each on its own waves
   int64_t P_max;
   size_t off_ids, off_w, off_offsets, off_perm_token, off_perm_pair, off_pair_row, off_chunk_counts,
-      off_tile_base, off_n_items, off_act, off_act_scale, off_act_scale_k, off_hs_k, off_abuf, off_Y,
+      off_tile_base, off_tile_tab, off_n_items, off_act, off_act_scale, off_act_scale_k, off_hs_k, off_abuf, off_Y,
       off_Ye, off_partials, total;
 };
 
@@ -125,6 +125,7 @@ Plan make_plan(const moe_shape_t *s) {
   p.off_pair_row = take(sizeof(int32_t) * p.P_max);
   p.off_chunk_counts = take(sizeof(int32_t) * (size_t)p.nchunks * s->num_local_experts);
   p.off_tile_base = take(sizeof(int32_t) * (s->num_local_experts + 1));
+  p.off_tile_tab = take(4 * sizeof(int32_t) * (size_t)p.max_tiles);
   p.off_n_items = take(sizeof(int32_t) * 2);
   p.off_act = take((size_t)p.P_max * s->I);
   p.off_act_scale = take(sizeof(float) * (size_t)p.P_max * (s->I / 128));
@@ -221,6 +222,7 @@ PermuteParams permute_params(const moe_shape_t *s, const Plan &pl, const Ptrs &r
   pp.perm_pair = at<int32_t>(ws, pl.off_perm_pair);
   pp.pair_row = r.pair_row;
   pp.tile_base = at<int32_t>(ws, pl.off_tile_base);
+  pp.tile_tab = at<int32_t>(ws, pl.off_tile_tab);
   pp.n_items = at<int32_t>(ws, pl.off_n_items);
   pp.T = s->T;
   pp.K = s->top_k;
@@ -269,6 +271,7 @@ moe_status_t enqueue_gemm2_combine(const moe_shape_t *s, const Plan &pl, const P
   GemmParams g2{};
   g2.expert_offsets = r.offsets;
   g2.tile_base = at<int32_t>(ws, pl.off_tile_base);
+  g2.tile_tab = at<int32_t>(ws, pl.off_tile_tab);
   g2.perm_token = r.perm_token;
   g2.Y = at<uint16_t>(ws, pl.off_Y);
   g2.Ye = at<int8_t>(ws, pl.off_Ye);
@@ -346,6 +349,7 @@ moe_status_t fused_impl(const moe_shape_t *s, const uint8_t *hidden, const float
   GemmParams g{};
   g.expert_offsets = r.offsets;
   g.tile_base = at<int32_t>(ws, pl.off_tile_base);
+  g.tile_tab = at<int32_t>(ws, pl.off_tile_tab);
   g.perm_token = r.perm_token;
   g.abuf = at<float>(ws, pl.off_abuf);
   g.act = at<uint8_t>(ws, pl.off_act);

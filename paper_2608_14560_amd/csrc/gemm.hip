@@ -320,7 +320,6 @@ constexpr int kStreamWaves = 8;
 template <int D, bool ALDS>
 __global__ __launch_bounds__(kStreamWaves * kWave) void gemm2_stream_kernel(GemmParams p) {
   constexpr int NW = kStreamWaves;
-  __shared__ int tb[1028];
   extern __shared__ __attribute__((aligned(16))) float scales[];  // sa[16][KB], sb[KB] (+1 row), A tile
 
   const int tid = threadIdx.x;
@@ -334,25 +333,18 @@ __global__ __launch_bounds__(kStreamWaves * kWave) void gemm2_stream_kernel(Gemm
   const int item = (blockIdx.x & 7) * per_xcd + (blockIdx.x >> 3);
   if ((int)(blockIdx.x >> 3) >= per_xcd || item >= n_items) return;
 
-  for (int i = tid; i <= p.El; i += NW * kWave) tb[i] = p.tile_base[i];
-  __syncthreads();
-
+  // the item's M-tile entry: expert, its first M-tile, first row, rows
   const int X = p.NB * p.S;
-  const int qt = item / X;
-  int lo = 0, hi = p.El;
-  while (hi - lo > 1) {
-    const int mid = (lo + hi) >> 1;
-    if (tb[mid] <= qt) lo = mid; else hi = mid;
-  }
-  const int e = lo;
-  const int nt_e = tb[e + 1] - tb[e];
-  const int local = item - tb[e] * X;
+  const int4 te = reinterpret_cast<const int4 *>(p.tile_tab)[__builtin_amdgcn_readfirstlane(item / X)];
+  const int e = te.x;
+  const int nt_e = (te.w + 15) / 16;
+  const int local = item - te.y * X;
   const int mt_idx = local % nt_e;
   const int rest = local / nt_e;
   const int s = rest % p.S;
   const int nb = rest / p.S;
-  const int seg0 = p.expert_offsets[e];
-  const int seg1 = p.expert_offsets[e + 1];
+  const int seg0 = te.z;
+  const int seg1 = te.z + te.w;
   const int row0 = seg0 + mt_idx * 16;
   const int nrows = min(16, seg1 - row0);
   const int kb0 = (s * p.KB) / p.S;
@@ -524,6 +516,9 @@ __device__ int narrow_permute(const GemmParams &p, int *tb, int *off, unsigned *
     if (writer) {
       q.expert_offsets[e] = acc;
       q.tile_base[e] = tacc;
+      const int nt = (n + q.BM - 1) / q.BM;
+      for (int t = 0; t < nt; ++t)
+        reinterpret_cast<int4 *>(q.tile_tab)[tacc + t] = make_int4(e, tacc, acc, n);
     }
     acc += n;
     tacc += (n + q.BM - 1) / q.BM;
@@ -564,7 +559,7 @@ __global__ __launch_bounds__((GU ? 2 : 1) * KS * kWave) void gemm1_narrow_kernel
   constexpr int kCols = GU ? 16 : 32;  // intermediate columns per item
   static_assert(!PERM || GU, "in-kernel permutation: gate/up-split items");
   static_assert(KS == 1 || KS == 2, "K split in one or two ranges");
-  __shared__ int tb[1028];
+  __shared__ int tb[PERM ? 1028 : 1];            // M-tile prefix (PERM)
   __shared__ int pm_off[PERM ? 1028 : 1];        // expert offsets (PERM)
   __shared__ unsigned pm_bits[PERM ? 1024 : 1];  // tokens of each local expert (PERM)
   __shared__ int pm_tok[PERM ? 16 : 1];          // the item's rows' tokens (PERM)
@@ -582,26 +577,34 @@ __global__ __launch_bounds__((GU ? 2 : 1) * KS * kWave) void gemm1_narrow_kernel
   const int item = (blockIdx.x & 7) * per_xcd + (blockIdx.x >> 3);
   if ((int)(blockIdx.x >> 3) >= per_xcd || item >= n_items) return;
 
-  if (!PERM) {
-    for (int i = tid; i <= p.El; i += NT) tb[i] = p.tile_base[i];
-    __syncthreads();
-  }
-
-  const int X = p.NB;  // column groups per M-tile (no K split)
+  // the item's expert, its M-tile count and first M-tile, its rows: from the
+  // workgroup's own permutation (PERM), else from the item's M-tile entry
+  const int X = p.NB;  // column groups per M-tile
   const int qt = item / X;
-  int lo = 0, hi = p.El;
-  while (hi - lo > 1) {
-    const int mid = (lo + hi) >> 1;
-    if (tb[mid] <= qt) lo = mid; else hi = mid;
+  int e, nt_e, tb_e, seg0, seg1;
+  if (PERM) {
+    int lo = 0, hi = p.El;
+    while (hi - lo > 1) {
+      const int mid = (lo + hi) >> 1;
+      if (tb[mid] <= qt) lo = mid; else hi = mid;
+    }
+    e = lo;
+    nt_e = tb[e + 1] - tb[e];
+    tb_e = tb[e];
+    seg0 = pm_off[e];
+    seg1 = pm_off[e + 1];
+  } else {
+    const int4 te = reinterpret_cast<const int4 *>(p.tile_tab)[__builtin_amdgcn_readfirstlane(qt)];
+    e = te.x;
+    nt_e = (te.w + 15) / 16;
+    tb_e = te.y;
+    seg0 = te.z;
+    seg1 = te.z + te.w;
   }
-  const int e = lo;
-  const int nt_e = tb[e + 1] - tb[e];
-  const int local = item - tb[e] * X;
+  const int local = item - tb_e * X;
   const int mt_idx = local % nt_e;
   const int j = local / nt_e;       // kCols-column group
   const int blk = j * kCols / 128;  // its 128-column block
-  const int seg0 = PERM ? pm_off[e] : p.expert_offsets[e];
-  const int seg1 = PERM ? pm_off[e + 1] : p.expert_offsets[e + 1];
   const int row0 = seg0 + mt_idx * 16;
   const int nrows = min(16, seg1 - row0);
   const int KB = p.KB;
@@ -974,7 +977,6 @@ __global__ __launch_bounds__(kCombineWaves * kWave) void gemm2_combine_kernel(Ge
                                                                              CombineParams c) {
   constexpr int NW = kCombineWaves;
   constexpr int NT = NW * kWave;
-  __shared__ int tb[1028];
   __shared__ float acc_l[NW][kCombineTokens][16];
   extern __shared__ __attribute__((aligned(16))) int dyn[];
   const CombineLayout Ly(p.P_max, p.K);
@@ -997,21 +999,19 @@ __global__ __launch_bounds__(kCombineWaves * kWave) void gemm2_combine_kernel(Ge
   const int KB = p.KB;
   const size_t K = (size_t)p.K;
 
-  for (int i = tid; i <= p.El; i += NT) tb[i] = p.tile_base[i];
+  // the tiles' entries (expert, first row, rows), loaded for every possible
+  // tile together with the tile count (at most 16 tokens: one tile per
+  // resident expert, so at most min(P_max, El); entries past the count are
+  // left over from other batches and never used)
   for (int i = tid; i < NW * kCombineTokens * 16; i += NT) (&acc_l[0][0][0])[i] = 0.0f;
-  __syncthreads();
-  const int n_tiles = tb[p.El];
+  const int n_tiles = p.tile_base[p.El];
   const int P = p.expert_offsets[p.El];
-  for (int q = tid; q < n_tiles; q += NT) {
-    int lo = 0, hi = p.El;
-    while (hi - lo > 1) {
-      const int mid = (lo + hi) >> 1;
-      if (tb[mid] <= q) lo = mid; else hi = mid;
-    }
-    const int row0 = p.expert_offsets[lo] + 16 * (q - tb[lo]);
-    t_e[q] = lo;
+  for (int q = tid; q < min(p.P_max, p.El); q += NT) {
+    const int4 te = reinterpret_cast<const int4 *>(p.tile_tab)[q];
+    const int row0 = te.z + 16 * (q - te.y);
+    t_e[q] = te.x;
     t_row0[q] = row0;
-    t_n[q] = min(16, p.expert_offsets[lo + 1] - row0);
+    t_n[q] = min(16, te.z + te.w - row0);
   }
   __syncthreads();
 

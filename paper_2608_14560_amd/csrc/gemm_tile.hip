@@ -117,26 +117,23 @@ struct TileItem {
 };
 
 template <bool G1, int BM>
-__device__ __forceinline__ TileItem tile_decode(const GemmParams &p, const int *tb, int item, int wn) {
+__device__ __forceinline__ TileItem tile_decode(const GemmParams &p, int item, int wn) {
   TileItem t;
   const int NB = p.NB;
-  const int qt = item / NB;
-  int lo = 0, hi = p.El;
-  while (hi - lo > 1) {
-    const int mid = (lo + hi) >> 1;
-    if (tb[mid] <= qt) lo = mid; else hi = mid;
-  }
-  t.e = lo;
-  t.nt_e = tb[lo + 1] - tb[lo];
-  const int local = item - tb[lo] * NB;
+  // the item's M-tile entry: its expert, the expert's first M-tile, first
+  // row and row count (one 16-byte load, uniform over the workgroup)
+  const int4 te = reinterpret_cast<const int4 *>(p.tile_tab)[__builtin_amdgcn_readfirstlane(item / NB)];
+  t.e = te.x;
+  t.nt_e = (te.w + BM - 1) / BM;
+  const int local = item - te.y * NB;
   const int G = (NB + kGroupN - 1) / kGroupN;
   const int grp = min(local / (kGroupN * t.nt_e), G - 1);
   const int wi = local - grp * kGroupN * t.nt_e;
   const int gsz = min(kGroupN, NB - kGroupN * grp);
   t.mt_idx = wi / gsz;
   t.nb = kGroupN * grp + wi % gsz;
-  t.row0 = p.expert_offsets[lo] + t.mt_idx * BM;
-  t.nrows = min(BM, p.expert_offsets[lo + 1] - t.row0);
+  t.row0 = te.z + t.mt_idx * BM;
+  t.nrows = min(BM, te.z + te.w - t.row0);
   const int half = wn >> 1;  // GEMM1: 0 gate, 1 up.  GEMM2: 128-column half
   if (G1) {
     // the wave's 64 weight rows: gate rows wrow0 .. wrow0+31 and the
@@ -400,7 +397,6 @@ __global__ __launch_bounds__(256 * WM) void gemm_tile_kernel(GemmParams p) {
   constexpr int MTW = MT * WM;  // 16-row blocks of the tile
   static_assert(MT % 4 == 0, "row scales are read four at a time");
 
-  __shared__ int tb[1028];
   __shared__ float amax_l[4][BM];
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
 
@@ -415,11 +411,8 @@ __global__ __launch_bounds__(256 * WM) void gemm_tile_kernel(GemmParams p) {
   const int item = tile_item(blockIdx.x, *p.n_items);
   if (item < 0) return;
 
-  for (int i = tid; i <= p.El; i += NT) tb[i] = p.tile_base[i];
-  __syncthreads();
-
   // ---- decode the work item
-  const TileItem ti = tile_decode<G1, BM>(p, tb, item, wn);
+  const TileItem ti = tile_decode<G1, BM>(p, item, wn);
   const int e = ti.e, nb = ti.nb, row0 = ti.row0, nrows = ti.nrows, wrow0 = ti.wrow0;
   const int KB = p.KB;
   const int half = wn >> 1;
@@ -625,7 +618,6 @@ __global__ __launch_bounds__(256 * WM) void tile_persist_kernel(GemmParams p) {
   constexpr int MTW = MT * WM;
   static_assert(MT % 4 == 0, "row scales are read four at a time");
 
-  __shared__ int tb[1028];
   __shared__ float amax_l[4][BM];
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
 
@@ -641,9 +633,6 @@ __global__ __launch_bounds__(256 * WM) void tile_persist_kernel(GemmParams p) {
   int v = blockIdx.x;
   int item = tile_item(v, n_items);
   if (item < 0) return;
-
-  for (int i = tid; i <= p.El; i += NT) tb[i] = p.tile_base[i];
-  __syncthreads();
 
   const int KB = p.KB;
   const int half = wn >> 1;
@@ -673,7 +662,7 @@ __global__ __launch_bounds__(256 * WM) void tile_persist_kernel(GemmParams p) {
     }
   };
 
-  TileItem ti = tile_decode<G1, BM>(p, tb, item, wn);
+  TileItem ti = tile_decode<G1, BM>(p, item, wn);
   TileSrc<JA, JB, kPfLoads> src;
   tile_sources<G1, MT, WM>(p, ti, wave, lane, src);
   const size_t sa_kb = (size_t)p.sa_kb;
@@ -712,7 +701,7 @@ __global__ __launch_bounds__(256 * WM) void tile_persist_kernel(GemmParams p) {
         const int ni = tile_item(v, n_items);
         more = ni >= 0;
         if (more) {
-          ti = tile_decode<G1, BM>(p, tb, ni, wn);
+          ti = tile_decode<G1, BM>(p, ni, wn);
           tile_sources<G1, MT, WM>(p, ti, wave, lane, src);
           load_sb(ti, cur ^ 1);
         }
@@ -758,7 +747,7 @@ hipError_t launch_tile(const GemmParams &p, int grid, hipStream_t st) {
   // the dynamic LDS limit is a property of the code object: raise it once,
   // to the size at the largest supported K (512 blocks) or what the CU's
   // 160 KB leave beside the kernel's static arrays, whichever is smaller
-  constexpr int kStatic = 1028 * (int)sizeof(int) + 4 * L::BM * (int)sizeof(float);
+  constexpr int kStatic = 4 * L::BM * (int)sizeof(float);
   const int cap = (int)L::bytes(512) < 160 * 1024 - kStatic ? (int)L::bytes(512) : 160 * 1024 - kStatic;
   static hipError_t attr = hipFuncSetAttribute(reinterpret_cast<const void *>(k),
                                                hipFuncAttributeMaxDynamicSharedMemorySize, cap);
@@ -771,9 +760,9 @@ hipError_t launch_tile(const GemmParams &p, int grid, hipStream_t st) {
 // The persistent grid: as many workgroups as the device has CUs (a
 // multiple of 8, at most the one-shot grid); one fits a CU (its LDS ring).
 // (Its dynamic LDS, the ring and the scale double buffer, must leave room for
-// the kernel's static tile_base copy and row amax in the CU's 160 KB; larger
-// K ranges use the one-shot kernel.)
-constexpr int kPersistMaxLds = 160 * 1024 - 1028 * (int)sizeof(int) - 4 * 256 * (int)sizeof(float);
+// the kernel's static row amax in the CU's 160 KB; larger K ranges use the
+// one-shot kernel.)
+constexpr int kPersistMaxLds = 160 * 1024 - 4 * 256 * (int)sizeof(float);
 
 template <bool G1, int MT, int WM, int S>
 hipError_t launch_persist(const GemmParams &p, int grid, hipStream_t st) {

@@ -180,6 +180,9 @@ struct PermuteParams {
   int32_t *perm_pair;        // [T*K]  t*K + j of each permuted row
   int32_t *pair_row;         // [T, K]
   int32_t *tile_base;        // [El + 1] first M-tile of each expert
+  // [M-tiles, 4]: per M-tile of the batch its expert e, tile_base[e],
+  // expert_offsets[e] and e's row count (one 16-byte load per work item)
+  int32_t *tile_tab;
   int32_t *n_items;          // [2] work items of GEMM1 and GEMM2
   int T, K, El, offset, nchunks;
   int BM, items_per_tile1, items_per_tile2;
@@ -200,6 +203,7 @@ struct GemmParams {
   const float *B_scale;
   const int32_t *expert_offsets;
   const int32_t *tile_base;
+  const int32_t *tile_tab;   // see PermuteParams
   const int32_t *perm_token;
   const int32_t *n_items;    // device count of work items
   float *abuf;               // GEMM1 column-split SwiGLU output [P_max, I] fp32

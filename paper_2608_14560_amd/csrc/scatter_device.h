@@ -74,7 +74,7 @@ __device__ void scatter_block_scan2(int a, int b, int (*wsum)[2], int &pa, int &
 // the first 256 holds token 256 chunk + t and keeps its K expert ids in
 // registers for the three passes (count, mark, rank).  `ids` is the [T, K]
 // routing output.  Workgroup 0 also writes expert_offsets, the M-tile prefix
-// of every expert and the GEMM work-item counts (one combined scan of the
+// of every expert, the per-M-tile table and the GEMM work-item counts (one combined scan of the
 // per-expert pair counts and tile counts).  Every thread of the workgroup must
 // call it (it contains barriers).
 template <int NT, bool SINGLE>
@@ -140,6 +140,9 @@ __device__ void scatter_chunk(const PermuteParams &p, int chunk, const int32_t *
     if (chunk == 0) {
       p.expert_offsets[e] = acc;
       p.tile_base[e] = tacc;
+      const int nt = (tot + p.BM - 1) / p.BM;
+      for (int t = 0; t < nt; ++t)
+        reinterpret_cast<int4 *>(p.tile_tab)[tacc + t] = make_int4(e, tacc, acc, tot);
     }
     sh.base[e] += acc;
     acc += tot;
