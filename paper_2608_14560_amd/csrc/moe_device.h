@@ -38,8 +38,8 @@ __device__ __forceinline__ uint32_t e4m3x2_rne_sat(float a, float b) {
 // magnitude m 2^x (m in [0.5, 1)) is scaled by 2^-(x - 15) into
 // [2^14, 2^15), every value of the chunk is rounded to fp16 (nearest even)
 // after that exact scaling, and the combine multiplies by 2^e back (exact).
-// The rounding error is at most 2^-12 of the chunk's largest magnitude, half
-// of fp32's bytes.  An all-zero chunk gets exponent 0; a chunk below 2^-113
+// The rounding error is at most 2^-11 of the chunk's largest magnitude (half
+// an fp16 ulp at [2^14, 2^15) is 8), in half of fp32's bytes.  An all-zero chunk gets exponent 0; a chunk below 2^-113
 // keeps exponent -128 (its scaled values still stay below 2^15).
 constexpr int kYChunk = 16;
 
