@@ -31,7 +31,10 @@ SOURCES = {
     "indexer.hip": ["-ffp-contract=off"],
     "permute.hip": [],
     "gemm.hip": [],
-    "gemm_tile.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"],
+    # the large-tile GEMMs: MFMA results in VGPRs (the promotion FMAs read
+    # them) and LLVM's ILP-maximising scheduler (measured: skewed 3311 -> 3290
+    # us, prefill 551 -> 549 us over three alternating runs)
+    "gemm_tile.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form", "-mllvm", "-amdgpu-sched-strategy=max-ilp"],
     "api.cpp": ["-x", "hip"],
     "dsa_api.cpp": ["-x", "hip"],
     "attention.hip": [],
