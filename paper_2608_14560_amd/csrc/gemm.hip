@@ -452,8 +452,8 @@ __global__ __launch_bounds__(kStreamWaves * kWave) void gemm2_stream_kernel(Gemm
 // GEMM1 for small batches, split over columns: a work item is one 16-row
 // M-tile and 32 intermediate columns, so a handful of resident experts still
 // yields several work items per CU (HBM streaming needs all 256 CUs busy;
-// splitting K instead would change the promotion order that decides the FP8
-// codes).  One wave streams the gate and up rows of both 16-column halves of
+// splitting K across workgroups would need a cross-workgroup reduction before
+// the SwiGLU).  One wave streams the gate and up rows of both 16-column halves of
 // the item against one A fragment (the tile's 16 gathered rows): four MFMAs
 // per 128-K step with a D-stage register prefetch ring (unconditional, so
 // loads stay in flight); SwiGLU pairs then sit in the same lane.  Four weight
