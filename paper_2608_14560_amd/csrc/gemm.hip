@@ -463,8 +463,10 @@ __global__ __launch_bounds__(kStreamWaves * kWave) void gemm2_stream_kernel(Gemm
 // and wave 1 the up rows, so twice as many waves stream (the chip's streaming
 // rate needs many waves per CU); the up half meets the gate half in LDS.  The
 // SwiGLU output goes to a_buf [P, I] fp32 and requant_kernel (the next launch)
-// re-quantises it: no cross-workgroup synchronisation.  Values and codes are
-// bit-identical to the single-item epilogue.
+// re-quantises it: no cross-workgroup synchronisation.  The re-quantisation
+// applies the large-tile epilogue's operations (amax, scale, rounding) to the
+// same fp32 values; with the K range in two halves (KS = 2) those sums differ
+// from one pass over K by fp32 rounding order only.
 // Stage (2) inside the narrow GEMM1 for batches of at most 16 tokens (T K <=
 // 256 pairs): every workgroup rebuilds the permutation from the routing ids
 // in LDS -- bits[e] marks the tokens holding local expert e, so a pair's row
