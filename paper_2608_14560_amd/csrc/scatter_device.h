@@ -20,6 +20,8 @@ struct ScatterLds {
   unsigned long long bits[kPermTokenWaves][kPermMaxEl];
   int wsum[NT / kWave][2];
   int cbase[kPermMaxEl];  // chunk-local start of each expert's pairs
+  int tot[kPermMaxEl];    // each expert's pairs over all chunks
+  int mine[kPermMaxEl];   // each expert's pairs in this chunk
   int srow[kChunkTokens * kPermMaxK];   // the chunk's pairs in output order:
   int spair[kChunkTokens * kPermMaxK];  // row and t K + j
 };
@@ -120,13 +122,22 @@ __device__ void scatter_chunk(const PermuteParams &p, int chunk, const int32_t *
   const int e0 = threadIdx.x * per;
   int tot_run = 0, tiles_run = 0;
   for (int e = e0; e < e0 + per && e < p.El; ++e) {
-    int tot = 0, before = 0;
-    for (int c = 0; c < p.nchunks; ++c) {
-      const int n = cnt(c, e);
-      tot += n;
-      if (c < chunk) before += n;
+    int tot = 0, before = 0, mine = 0;
+    // the chunks' counts eight at a time, so that their loads go out together
+    for (int c0 = 0; c0 < p.nchunks; c0 += 8) {
+      int v[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) v[u] = c0 + u < p.nchunks ? cnt(c0 + u, e) : 0;
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        tot += v[u];
+        before += c0 + u < chunk ? v[u] : 0;
+        mine += c0 + u == chunk ? v[u] : 0;
+      }
     }
     sh.base[e] = before;  // chunk-local part; the expert offset is added below
+    sh.tot[e] = tot;
+    sh.mine[e] = mine;
     tot_run += tot;
     tiles_run += (tot + p.BM - 1) / p.BM;
   }
@@ -135,8 +146,7 @@ __device__ void scatter_chunk(const PermuteParams &p, int chunk, const int32_t *
   // walk the run again: expert offsets, M-tile prefix
   int acc = run_start, tacc = tile_start;
   for (int e = e0; e < e0 + per && e < p.El; ++e) {
-    int tot = 0;
-    for (int c = 0; c < p.nchunks; ++c) tot += cnt(c, e);
+    const int tot = sh.tot[e];
     if (chunk == 0) {
       p.expert_offsets[e] = acc;
       p.tile_base[e] = tacc;
@@ -158,12 +168,12 @@ __device__ void scatter_chunk(const PermuteParams &p, int chunk, const int32_t *
   // chunk-local starts of the experts' pair runs: one more scan over the
   // experts' counts in this chunk (same contiguous runs per thread)
   int crun = 0;
-  for (int e = e0; e < e0 + per && e < p.El; ++e) crun += cnt(chunk, e);
+  for (int e = e0; e < e0 + per && e < p.El; ++e) crun += sh.mine[e];
   int cstart, dummy_s, cpairs, dummy_t;
   scatter_block_scan2<NT>(crun, 0, sh.wsum, cstart, dummy_s, cpairs, dummy_t);
   for (int e = e0; e < e0 + per && e < p.El; ++e) {
     sh.cbase[e] = cstart;
-    cstart += cnt(chunk, e);
+    cstart += sh.mine[e];
   }
 
   // rank the chunk's pairs: bit `lane` of bits[w][e] marks that the lane's
