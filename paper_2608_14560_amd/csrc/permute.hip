@@ -27,9 +27,14 @@ __global__ __launch_bounds__(kThreads) void count_kernel(PermuteParams p) {
   __syncthreads();
   const int t = blockIdx.x * kChunkTokens + threadIdx.x;
   if (t < p.T) {
-    for (int j = 0; j < p.K; ++j) {
-      const int le = p.topk_ids[(size_t)t * p.K + j] - p.offset;
-      if (le >= 0 && le < p.El) atomicAdd(&hist[le], 1);
+    // the token's ids loaded together (clamped index), then counted
+    int ids[kPermMaxK];
+#pragma unroll
+    for (int j = 0; j < kPermMaxK; ++j) ids[j] = p.topk_ids[(size_t)t * p.K + min(j, p.K - 1)];
+#pragma unroll
+    for (int j = 0; j < kPermMaxK; ++j) {
+      const int le = ids[j] - p.offset;
+      if (j < p.K && le >= 0 && le < p.El) atomicAdd(&hist[le], 1);
     }
   }
   __syncthreads();
@@ -64,9 +69,19 @@ __global__ __launch_bounds__(kThreads) void gather_scales_kernel(const int32_t *
   const int n = min(kGatherRows, P - r0);
   if (threadIdx.x < kGatherRows) tok[threadIdx.x] = perm_token[r0 + min((int)threadIdx.x, n - 1)];
   __syncthreads();
-  for (int i = threadIdx.x; i < kGatherRows * KB; i += kThreads) {
-    const int row = i / KB, kb = i % KB;
-    tr[kb * (kGatherRows + 1) + row] = hidden_scale[(size_t)tok[row] * KB + kb];
+  // eight loads per thread go out together before their LDS stores
+  for (int i0 = threadIdx.x; i0 < kGatherRows * KB; i0 += 8 * kThreads) {
+    float v[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int i = min(i0 + u * kThreads, kGatherRows * KB - 1);
+      v[u] = hidden_scale[(size_t)tok[i / KB] * KB + i % KB];
+    }
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int i = i0 + u * kThreads;
+      if (i < kGatherRows * KB) tr[(i % KB) * (kGatherRows + 1) + i / KB] = v[u];
+    }
   }
   __syncthreads();
   for (int i = threadIdx.x; i < kGatherRows * KB; i += kThreads) {
