@@ -4,6 +4,7 @@
 // on the device and the grids are sized from host-known upper bounds.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cmath>
 #include <cstdint>
 #include <mutex>
@@ -77,6 +78,12 @@ Plan make_plan(const moe_shape_t *s) {
   // expected rows per resident expert under uniform routing picks the M tile
   const double avg = (double)TK / s->num_experts;
   p.BM = avg <= 16 ? 16 : (avg <= 48 ? 32 : (avg <= 96 ? 64 : (avg <= 192 ? 128 : 256)));
+  // the eight-wave tiles (128 and 256 rows) address their operands with
+  // 32-bit offsets from per-matrix bases: rows x row length of the activation
+  // operands and of one expert's weights must stay below 2^32 bytes
+  const uint64_t big = std::max<uint64_t>({(uint64_t)p.P_max * (uint64_t)s->H, (uint64_t)p.P_max * (uint64_t)s->I,
+                                           2ull * (uint64_t)s->I * (uint64_t)s->H});
+  if (p.BM >= 128 && big >= (1ull << 32)) p.BM = 64;
   p.tile = p.BM >= 64;
   // GEMM1 keeps the whole K range in one item: its epilogue (SwiGLU and the
   // 1x128 re-quantisation) needs complete sums, and a K split would add a

@@ -73,6 +73,19 @@ __device__ __forceinline__ void lds_load16(const void *g, uint8_t *lds) {
 __device__ __forceinline__ void lds_load4(const void *g, uint8_t *lds) {
   __builtin_amdgcn_global_load_lds(g, (lds_void *)lds, 4, 0, 0);
 }
+// The same through a buffer resource: a per-lane 32-bit offset (VGPR) plus a
+// uniform one (SGPR), so a K step's loads need no address arithmetic.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t tile_rsrc(const void *base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), (short)0, (int)bytes, 0x00020000);
+}
+__device__ __forceinline__ void lds_bload16(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff,
+                                            uint8_t *lds) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void *)lds, 16, voff, soff, 0, 0);
+}
+__device__ __forceinline__ void lds_bload4(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff,
+                                           uint8_t *lds) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void *)lds, 4, voff, soff, 0, 0);
+}
 
 // LDS reads of the K loop go through restrict-qualified pointers, so after
 // inlining they carry alias-scope metadata.  Without it the compiler cannot
@@ -235,6 +248,78 @@ __device__ __forceinline__ void tile_sources(const GemmParams &p, const TileItem
   const int sr = sl / SS, sj = sl % SS;
   const int r = (sr < 16 && sj < MTW) ? 16 * sj + sr : t.nrows - 1;
   src.s = p.sa_tile + (size_t)(t.row0 + min(r, t.nrows - 1)) * p.sa_row;
+}
+
+// The loads of the 8-wave tiles alternate between the two waves of each SIMD
+// (waves wn and wn + 4): in a K step one of them issues the whole group of
+// both -- their A blocks, the column wave's eight weight blocks, both waves'
+// row scales and L2 prefetches -- and the other issues none, so that while
+// the loading wave waits at issue for a free request slot its partner keeps
+// the SIMD's matrix core busy.  The sources are 32-bit byte offsets from
+// bases that are uniform over the wave (the activation rows from A, a weight
+// row from its 8-row block's first row, the row scales from sa_tile), so the
+// loads take the scalar-base address form and each K step only moves the
+// bases.
+template <int JA, int PF>
+struct TileSrcPair {
+  uint32_t a[2 * JA];  // A rows: wave wn's blocks, then wave wn + 4's
+  uint32_t b[2];       // lane offset in an 8-row weight block, even / odd block
+  uint32_t s[2];       // row-scale byte offsets of wave wn's slot, of wave wn + 4's
+  const uint8_t *pf[2 * (PF > 0 ? PF : 1)];
+};
+
+template <bool G1, int MT, int WM, int JA, int PF>
+__device__ __forceinline__ void tile_sources_pair(const GemmParams &p, const TileItem &t, int wn, int lane,
+                                                  TileSrcPair<JA, PF> &src) {
+  constexpr int BM = 16 * MT * WM;
+  constexpr int MTW = MT * WM;
+  constexpr int SS = TileLayout<MT, WM, 2>::SS;
+  const uint32_t K = (uint32_t)p.K;
+  const int sw_l = lane >> 3;
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    const int w = wn + 4 * h;
+#pragma unroll
+    for (int j = 0; j < JA; ++j) {
+      const int r = 8 * (w * JA + j) + sw_l;
+      const int rr = min(r, t.nrows - 1);
+      const int row = G1 ? p.perm_token[t.row0 + rr] : t.row0 + rr;
+      // (24-bit products: row < 2^24 and K < 2^24; a 32-bit multiply-add
+      // would otherwise be formed as a 64-bit one and hold a register pair)
+      src.a[h * JA + j] = __umul24((uint32_t)row, K) + 16 * ((lane & 7) ^ tile_swz(r));
+    }
+    const int sl = 64 * w + lane;
+    const int sr = sl / SS, sj = sl % SS;
+    const int r = (sr < 16 && sj < MTW) ? 16 * sj + sr : t.nrows - 1;
+    src.s[h] = 4u * __umul24((uint32_t)(t.row0 + min(r, t.nrows - 1)), (uint32_t)p.sa_row);
+  }
+  // row 8 blk + sw_l of weight block blk: chunk (lane & 7) ^ sw_l ^ (blk & 1)
+#pragma unroll
+  for (int q = 0; q < 2; ++q) src.b[q] = __umul24((uint32_t)sw_l, K) + 16 * ((lane & 7) ^ sw_l ^ q);
+  const uint8_t *Bexp = p.B + (size_t)t.e * p.N_total * p.K;
+  const int ms = t.nt_e >= 4 ? 4 : (t.nt_e >= 2 ? 2 : 1);
+  const int a_share = BM / kGroupN;
+  const int w_share = 256 / ms;
+  const int a_first = (t.nb % kGroupN) * a_share;
+  const int w_first = (t.mt_idx % ms) * w_share;
+#pragma unroll
+  for (int h = 0; h < 2; ++h)
+#pragma unroll
+    for (int j = 0; j < PF; ++j) {
+      const int w = wn + 4 * h;
+      int line = (w * PF + j) * kWave + lane;
+      if (line >= a_share + w_share) line = 0;
+      if (line < a_share) {
+        const int rr = min(a_first + line, t.nrows - 1);
+        src.pf[h * PF + j] = p.A + (size_t)(G1 ? p.perm_token[t.row0 + rr] : t.row0 + rr) * p.K;
+      } else {
+        const int c = w_first + line - a_share;
+        const int w2 = c >> 6, rr = c & 63;
+        const int row = G1 ? (rr < 32 ? t.nb * 128 + 32 * w2 + rr : p.I + t.nb * 128 + 32 * w2 + rr - 32)
+                           : t.nb * kTileCols + 64 * w2 + rr;
+        src.pf[h * PF + j] = Bexp + (size_t)min(row, p.N_total - 1) * p.K;
+      }
+    }
 }
 
 // GEMM2's epilogue: the wave's accumulators (rows wrow + 16 m + r16 of the
@@ -402,7 +487,7 @@ __global__ __launch_bounds__(256 * WM) void gemm_tile_kernel(GemmParams p) {
 
   const int tid = threadIdx.x;
   const int lane = tid & (kWave - 1);
-  const int wave = tid / kWave;
+  const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);  // uniform: scalar LDS addresses
   const int wn = wave & 3;
   const int wm = wave >> 2;
   const int r16 = lane & 15;
@@ -415,6 +500,13 @@ __global__ __launch_bounds__(256 * WM) void gemm_tile_kernel(GemmParams p) {
   const TileItem ti = tile_decode<G1, BM>(p, item, wn);
   const int e = ti.e, nb = ti.nb, row0 = ti.row0, nrows = ti.nrows, wrow0 = ti.wrow0;
   const int KB = p.KB;
+  // (alternating loads) buffer resources of the A rows, the expert's weights
+  // and the row scales; every offset into them fits 32 bits (the plan keeps
+  // rows x row length of the 8-wave tiles' operands below 2^32 bytes)
+  const __amdgpu_buffer_rsrc_t rs_a = tile_rsrc(p.A, 0xffffffffu);
+  const __amdgpu_buffer_rsrc_t rs_b =
+      tile_rsrc(p.B + (size_t)e * p.N_total * p.K, (uint32_t)p.N_total * (uint32_t)p.K);
+  const __amdgpu_buffer_rsrc_t rs_s = tile_rsrc(p.sa_tile, 4u * (uint32_t)p.P_max * (uint32_t)p.KB);
   const int half = wn >> 1;
 
   // weight-block scales of the whole K range: sb_l[0][kb] (wn 0/1), sb_l[1][kb]
@@ -435,8 +527,14 @@ __global__ __launch_bounds__(256 * WM) void gemm_tile_kernel(GemmParams p) {
   constexpr int JA = BM / 8 / (4 * WM);  // A blocks per wave
   constexpr int JB = 8 / WM;             // weight blocks per wave
   constexpr int kPfLoads = (BM / kGroupN + 256 + 4 * WM * kWave - 1) / (4 * WM * kWave);
+  // the 8-wave tiles alternate a K step's loads between the waves of a SIMD
+  constexpr bool kAlt = WM == 2;
   TileSrc<JA, JB, kPfLoads> src;
-  tile_sources<G1, MT, WM>(p, ti, wave, lane, src);
+  TileSrcPair<JA, kPfLoads> srcp;
+  if constexpr (kAlt)
+    tile_sources_pair<G1, MT, WM>(p, ti, wn, lane, srcp);
+  else
+    tile_sources<G1, MT, WM>(p, ti, wave, lane, src);
   const size_t sa_kb = (size_t)p.sa_kb;
   // this lane's two 16-byte pieces of a fragment (rows 16m + r16 of a block)
   const int fr = tile_swz(r16);
@@ -469,6 +567,14 @@ __global__ __launch_bounds__(256 * WM) void gemm_tile_kernel(GemmParams p) {
   constexpr int kSpread = MT / 2;
   static_assert(kWait < 64, "vmcnt holds 6 bits");
   static_assert(S >= 2, "LDS ring depth");
+  // alternating loads: the loading wave's group and prefetches; at a step's
+  // end it waits for its group when the ring has two stages (that stage is
+  // read next) and for nothing of its own with three (its partner loaded
+  // the next stage a step earlier and waits for that group now)
+  constexpr int kGroupP = 2 * JA + 8 + 2;
+  constexpr int kPfP = 2 * kPfLoads;
+  constexpr int kWaitLd = S == 2 ? kPfP : kGroupP + kPfP;
+  static_assert(!kAlt || (S <= 3 && JB * WM == 8 && kWaitLd < 64), "alternating loads");
 
 #define TILE_STAGE(st) (smem + (st) * L::STAGE)
 // load j of the group for stage st, K block kb: the wave's A blocks, then its
@@ -490,6 +596,39 @@ __global__ __launch_bounds__(256 * WM) void gemm_tile_kernel(GemmParams p) {
     _Pragma("unroll") for (int j = 0; j < kPfLoads; ++j)                                \
         lds_load4(src.pf[j] + (size_t)(kb) * 128, smem + S * L::STAGE + wave * 256);    \
   } while (0)
+// load j of a wave pair's group (alternating loads): the A blocks of wave wn
+// and of wave wn + 4, the column wave's eight weight blocks, the two waves'
+// row scales
+#define TILE_DMA_P(st, kb, j)                                                           \
+  do {                                                                                  \
+    uint8_t *d_ = TILE_STAGE(st);                                                       \
+    if ((j) < 2 * JA) {                                                                 \
+      const int jj_ = (j) < 2 * JA ? (j) : 0;                                           \
+      lds_bload16(rs_a, srcp.a[jj_], (uint32_t)(kb) * 128u,                             \
+                  d_ + ((wn + 4 * (jj_ / JA)) * JA + jj_ % JA) * 1024);                 \
+    } else if ((j) < 2 * JA + 8) {                                                      \
+      const int blk_ = (j) - 2 * JA;                                                    \
+      const int r0_ = G1 ? (blk_ < 4 ? wrow0 + 8 * blk_ : p.I + wrow0 + 8 * (blk_ - 4))  \
+                         : min(wrow0 + 8 * blk_, p.N_total - 8);                        \
+      lds_bload16(rs_b, srcp.b[blk_ & 1], (uint32_t)r0_ * (uint32_t)p.K + (uint32_t)(kb) * 128u, \
+                  d_ + L::A_BYTES + wn * 8192 + blk_ * 1024);                           \
+    } else {                                                                            \
+      const int h_ = (j) - 2 * JA - 8 < 1 ? 0 : 1;                                      \
+      lds_bload4(rs_s, srcp.s[h_], (uint32_t)(kb) * (uint32_t)sa_kb * 4u,               \
+                 d_ + L::SCL + (wn + 4 * h_) * 256);                                    \
+    }                                                                                   \
+  } while (0)
+#define TILE_PREFETCH_P(kb)                                                             \
+  do {                                                                                  \
+    _Pragma("unroll") for (int j = 0; j < kPfP; ++j)                                    \
+        lds_load4(srcp.pf[j] + (size_t)(kb) * 128, smem + S * L::STAGE + wave * 256);   \
+  } while (0)
+#define TILE_NODMA(st, kb, j) \
+  do {                        \
+  } while (0)
+#define TILE_NOPF(kb) \
+  do {                \
+  } while (0)
 // One K-step of the wave's 16 MT x 64 block: per 16-row block m, four MFMAs
 // (one per 16-column sub-tile), each started from zero and promoted with one
 // FMA per accumulator; the next block's A fragment is read while this one
@@ -507,7 +646,7 @@ __global__ __launch_bounds__(256 * WM) void gemm_tile_kernel(GemmParams p) {
 // blocks (a compile-time count) are multiplied: the others hold no pairs of
 // the item, and their loads are still issued so that every wave's vmcnt
 // bookkeeping is the same.
-#define TILE_COMPUTE(st, kb, stl, kbl, kbp, MV)                                          \
+#define TILE_COMPUTE(st, kb, stl, kbl, kbp, MV, DMA, NG, PFM)                            \
   do {                                                                                  \
     const uint8_t *as_ = TILE_STAGE(st) + wm * MT * 2048;                               \
     const uint8_t *bs_ = TILE_STAGE(st) + L::A_BYTES + wn * 8192;                       \
@@ -531,10 +670,10 @@ __global__ __launch_bounds__(256 * WM) void gemm_tile_kernel(GemmParams p) {
     if ((MV) > 0) an_ = tile_frag(as_, rd_lo, rd_hi);                                   \
     _Pragma("unroll") for (int m = 0; m < MT; ++m) {                                    \
       if (m < kSpread) {                                                                \
-        _Pragma("unroll") for (int j_ = (m * kGroup) / kSpread;                         \
-                               j_ < ((m + 1) * kGroup) / kSpread; ++j_)                 \
-            TILE_DMA_J(stl, kbl, j_);                                                   \
-        if (m == kSpread - 1) TILE_PREFETCH(kbp);                                       \
+        _Pragma("unroll") for (int j_ = (m * (NG)) / kSpread;                           \
+                               j_ < ((m + 1) * (NG)) / kSpread; ++j_)                   \
+            DMA(stl, kbl, j_);                                                          \
+        if (m == kSpread - 1) PFM(kbp);                                                 \
         __builtin_amdgcn_sched_barrier(0x78F);                                          \
       }                                                                                 \
       if (m >= (MV)) continue;                                                          \
@@ -558,26 +697,63 @@ __global__ __launch_bounds__(256 * WM) void gemm_tile_kernel(GemmParams p) {
   // barrier would wait for every outstanding load.
   // (the prologue issues stages 0 .. S-2 each followed by its prefetch, so
   // it has the same shape as S-1 loop steps)
+  // (alternating loads: stage st is loaded by the waves with wm = st % 2)
+  const int wmu = __builtin_amdgcn_readfirstlane(wm);
+  if constexpr (kAlt) {
 #pragma unroll
-  for (int st = 0; st < S - 1; ++st) {
+    for (int st = 0; st < S - 1; ++st) {
+      if (wmu == (st & 1)) {
 #pragma unroll
-    for (int j = 0; j < kGroup; ++j) TILE_DMA_J(st, min(st, KB - 1), j);
-    TILE_PREFETCH(min(st + 1, KB - 1));
-    __builtin_amdgcn_sched_barrier(0);
+        for (int j = 0; j < kGroupP; ++j) TILE_DMA_P(st, min(st, KB - 1), j);
+        TILE_PREFETCH_P(min(st + 1, KB - 1));
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(kPfP) : "memory");
+  } else {
+#pragma unroll
+    for (int st = 0; st < S - 1; ++st) {
+#pragma unroll
+      for (int j = 0; j < kGroup; ++j) TILE_DMA_J(st, min(st, KB - 1), j);
+      TILE_PREFETCH(min(st + 1, KB - 1));
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(kWait) : "memory");
   }
-  asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(kWait) : "memory");
 
 // the K loop with the first MV row blocks of the wave multiplied
+// one K step it: the math of stage st_rd with loads of macro DMA (group size
+// NG) and prefetch macro PFM, then this wave's wait (vmcnt W) and the barrier
+#define TILE_STEP(MV, DMA, NG, PFM, W)                                                  \
+  do {                                                                                  \
+    TILE_COMPUTE(st_rd, it, st_ld, min(it + S - 1, KB - 1), min(it + S, KB - 1), MV,     \
+                 DMA, NG, PFM);                                                         \
+    __builtin_amdgcn_sched_barrier(0);                                                  \
+    if (kPrio) __builtin_amdgcn_s_setprio(0);                                           \
+    asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(W) : "memory");    \
+    st_rd = st_rd + 1 == S ? 0 : st_rd + 1;                                             \
+    st_ld = st_ld + 1 == S ? 0 : st_ld + 1;                                             \
+    ++it;                                                                               \
+  } while (0)
+// The K loop with the first MV row blocks of the wave multiplied.  With
+// alternating loads a wave loads in every other step (step it: the waves with
+// wm = (it + S - 1) % 2); the loop body is one loading step and one step
+// without loads, entered at the first loading step of this wave, so both
+// roles stay in one straight-line body (a branch between two versions of a
+// step would join their accumulators every step).
 #define TILE_KLOOP(MV)                                                                  \
   do {                                                                                  \
-    int st_rd = 0, st_ld = S - 1;                                                       \
-    for (int it = 0; it < KB; ++it) {                                                   \
-      TILE_COMPUTE(st_rd, it, st_ld, min(it + S - 1, KB - 1), min(it + S, KB - 1), MV); \
-      __builtin_amdgcn_sched_barrier(0);                                                \
-      if (kPrio) __builtin_amdgcn_s_setprio(0);                                         \
-      asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(kWait) : "memory"); \
-      st_rd = st_rd + 1 == S ? 0 : st_rd + 1;                                           \
-      st_ld = st_ld + 1 == S ? 0 : st_ld + 1;                                           \
+    int st_rd = 0, st_ld = S - 1, it = 0;                                               \
+    if constexpr (!kAlt) {                                                              \
+      while (it < KB) TILE_STEP(MV, TILE_DMA_J, kGroup, TILE_PREFETCH, kWait);          \
+    } else {                                                                            \
+      if (wmu != ((S - 1) & 1)) TILE_STEP(MV, TILE_NODMA, 0, TILE_NOPF, kPfP);           \
+      while (it + 1 < KB) {                                                             \
+        TILE_STEP(MV, TILE_DMA_P, kGroupP, TILE_PREFETCH_P, kWaitLd);                    \
+        TILE_STEP(MV, TILE_NODMA, 0, TILE_NOPF, kPfP);                                   \
+      }                                                                                 \
+      /* the last step's loads would only repeat the last K block */                    \
+      if (it < KB) TILE_STEP(MV, TILE_NODMA, 0, TILE_NOPF, kPfP);                        \
     }                                                                                   \
   } while (0)
   // A ragged tile (an expert's last M-tile, or a tile taller than the
@@ -590,6 +766,7 @@ __global__ __launch_bounds__(256 * WM) void gemm_tile_kernel(GemmParams p) {
   else if (mv > 0) TILE_KLOOP(MT / 4);
   else TILE_KLOOP(0);
 #undef TILE_KLOOP
+#undef TILE_STEP
   // the last steps' (clamped) loads may still be landing in the ring
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
 
@@ -718,7 +895,7 @@ __global__ __launch_bounds__(256 * WM) void tile_persist_kernel(GemmParams p) {
       // loads repeat the current item's last block: in bounds, never read)
       const int kbl = !nxt ? it + S - 1 : (more ? it + S - 1 - KB : KB - 1);
       const int kbp = !nxt ? min(it + S, KB - 1) : (more ? min(it + S - KB, KB - 1) : KB - 1);
-      TILE_COMPUTE(st_rd, it, st_ld, kbl, kbp, MT);
+      TILE_COMPUTE(st_rd, it, st_ld, kbl, kbp, MT, TILE_DMA_J, kGroup, TILE_PREFETCH);
       __builtin_amdgcn_sched_barrier(0);
       asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(kWait) : "memory");
       st_rd = st_rd + 1 == S ? 0 : st_rd + 1;
@@ -746,6 +923,10 @@ __global__ __launch_bounds__(256 * WM) void tile_persist_kernel(GemmParams p) {
 #undef TILE_COMPUTE
 #undef TILE_PREFETCH
 #undef TILE_DMA_J
+#undef TILE_DMA_P
+#undef TILE_PREFETCH_P
+#undef TILE_NODMA
+#undef TILE_NOPF
 #undef TILE_STAGE
 
 template <bool G1, int MT, int WM, int S>
