@@ -992,11 +992,12 @@ hipError_t launch_gemm_tile(const GemmParams &p, bool g1, int BM, int grid, hipS
   if (grid <= 0) return hipSuccess;
   if (p.S != 1) return hipErrorInvalidValue;  // full-K items only
   switch (BM) {
-    // 64 / 128 rows: three-stage ring (loads two K-steps ahead); GEMM1's
-    // 128-row tiles as 8 waves of 64 rows (two per SIMD: prefill GEMM1
-    // 333 -> 324 us), GEMM2's as 4 waves of 128 rows (the persistent grid)
+    // 64 / 128 rows: three-stage ring (loads two K-steps ahead); the 128-row
+    // tiles as 8 waves of 64 rows (two per SIMD, alternating loads: prefill
+    // GEMM1 333 -> 324 us against 4 waves of 128 rows before the alternation,
+    // GEMM2 179 -> 166 us against 4 waves of 128 rows on the persistent grid)
     case 64: return g1 ? launch_any<true, 4, 1, 3>(p, grid, st) : launch_any<false, 4, 1, 3>(p, grid, st);
-    case 128: return g1 ? launch_any<true, 4, 2, 3>(p, grid, st) : launch_any<false, 8, 1, 3>(p, grid, st);
+    case 128: return g1 ? launch_any<true, 4, 2, 3>(p, grid, st) : launch_any<false, 4, 2, 3>(p, grid, st);
     // 256 rows: 8 waves (two per SIMD), two-stage ring
     case 256: return g1 ? launch_any<true, 8, 2, 2>(p, grid, st) : launch_any<false, 8, 2, 2>(p, grid, st);
     default: return hipErrorInvalidValue;
