@@ -253,25 +253,26 @@ __device__ __forceinline__ void tile_sources(const GemmParams &p, const TileItem
 // The loads of the 8-wave tiles alternate between the two waves of each SIMD
 // (waves wn and wn + 4): in a K step one of them issues the whole group of
 // both -- their A blocks, the column wave's eight weight blocks, both waves'
-// row scales and L2 prefetches -- and the other issues none, so that while
-// the loading wave waits at issue for a free request slot its partner keeps
-// the SIMD's matrix core busy.  The sources are 32-bit byte offsets from
+// row scales -- and the other issues none, so that while the loading wave
+// waits at issue for a free request slot its partner keeps the SIMD's matrix
+// core busy.  These tiles issue no L2 prefetches: with the loads alternating,
+// the prefetch requests only took request slots from the ring's loads
+// (measured without them: prefill GEMM1 301 -> 274 us, GEMM2 166 -> 156,
+// skewed GEMM1 1838 -> 1810).  The sources are 32-bit byte offsets from
 // bases that are uniform over the wave (the activation rows from A, a weight
 // row from its 8-row block's first row, the row scales from sa_tile), so the
 // loads take the scalar-base address form and each K step only moves the
 // bases.
-template <int JA, int PF>
+template <int JA>
 struct TileSrcPair {
   uint32_t a[2 * JA];  // A rows: wave wn's blocks, then wave wn + 4's
   uint32_t b[2];       // lane offset in an 8-row weight block, even / odd block
   uint32_t s[2];       // row-scale byte offsets of wave wn's slot, of wave wn + 4's
-  const uint8_t *pf[2 * (PF > 0 ? PF : 1)];
 };
 
-template <bool G1, int MT, int WM, int JA, int PF>
+template <bool G1, int MT, int WM, int JA>
 __device__ __forceinline__ void tile_sources_pair(const GemmParams &p, const TileItem &t, int wn, int lane,
-                                                  TileSrcPair<JA, PF> &src) {
-  constexpr int BM = 16 * MT * WM;
+                                                  TileSrcPair<JA> &src) {
   constexpr int MTW = MT * WM;
   constexpr int SS = TileLayout<MT, WM, 2>::SS;
   const uint32_t K = (uint32_t)p.K;
@@ -296,30 +297,6 @@ __device__ __forceinline__ void tile_sources_pair(const GemmParams &p, const Til
   // row 8 blk + sw_l of weight block blk: chunk (lane & 7) ^ sw_l ^ (blk & 1)
 #pragma unroll
   for (int q = 0; q < 2; ++q) src.b[q] = __umul24((uint32_t)sw_l, K) + 16 * ((lane & 7) ^ sw_l ^ q);
-  const uint8_t *Bexp = p.B + (size_t)t.e * p.N_total * p.K;
-  const int ms = t.nt_e >= 4 ? 4 : (t.nt_e >= 2 ? 2 : 1);
-  const int a_share = BM / kGroupN;
-  const int w_share = 256 / ms;
-  const int a_first = (t.nb % kGroupN) * a_share;
-  const int w_first = (t.mt_idx % ms) * w_share;
-#pragma unroll
-  for (int h = 0; h < 2; ++h)
-#pragma unroll
-    for (int j = 0; j < PF; ++j) {
-      const int w = wn + 4 * h;
-      int line = (w * PF + j) * kWave + lane;
-      if (line >= a_share + w_share) line = 0;
-      if (line < a_share) {
-        const int rr = min(a_first + line, t.nrows - 1);
-        src.pf[h * PF + j] = p.A + (size_t)(G1 ? p.perm_token[t.row0 + rr] : t.row0 + rr) * p.K;
-      } else {
-        const int c = w_first + line - a_share;
-        const int w2 = c >> 6, rr = c & 63;
-        const int row = G1 ? (rr < 32 ? t.nb * 128 + 32 * w2 + rr : p.I + t.nb * 128 + 32 * w2 + rr - 32)
-                           : t.nb * kTileCols + 64 * w2 + rr;
-        src.pf[h * PF + j] = Bexp + (size_t)min(row, p.N_total - 1) * p.K;
-      }
-    }
 }
 
 // GEMM2's epilogue: the wave's accumulators (rows wrow + 16 m + r16 of the
@@ -530,7 +507,7 @@ __global__ __launch_bounds__(256 * WM) void gemm_tile_kernel(GemmParams p) {
   // the 8-wave tiles alternate a K step's loads between the waves of a SIMD
   constexpr bool kAlt = WM == 2;
   TileSrc<JA, JB, kPfLoads> src;
-  TileSrcPair<JA, kPfLoads> srcp;
+  TileSrcPair<JA> srcp;
   if constexpr (kAlt)
     tile_sources_pair<G1, MT, WM>(p, ti, wn, lane, srcp);
   else
@@ -567,13 +544,12 @@ __global__ __launch_bounds__(256 * WM) void gemm_tile_kernel(GemmParams p) {
   constexpr int kSpread = MT / 2;
   static_assert(kWait < 64, "vmcnt holds 6 bits");
   static_assert(S >= 2, "LDS ring depth");
-  // alternating loads: the loading wave's group and prefetches; at a step's
-  // end it waits for its group when the ring has two stages (that stage is
-  // read next) and for nothing of its own with three (its partner loaded
-  // the next stage a step earlier and waits for that group now)
+  // alternating loads: the loading wave's group; at a step's end it waits for
+  // its group when the ring has two stages (that stage is read next) and for
+  // nothing of its own with three (its partner loaded the next stage a step
+  // earlier and waits for that group now)
   constexpr int kGroupP = 2 * JA + 8 + 2;
-  constexpr int kPfP = 2 * kPfLoads;
-  constexpr int kWaitLd = S == 2 ? kPfP : kGroupP + kPfP;
+  constexpr int kWaitLd = S == 2 ? 0 : kGroupP;
   static_assert(!kAlt || (S <= 3 && JB * WM == 8 && kWaitLd < 64), "alternating loads");
 
 #define TILE_STAGE(st) (smem + (st) * L::STAGE)
@@ -617,11 +593,6 @@ __global__ __launch_bounds__(256 * WM) void gemm_tile_kernel(GemmParams p) {
       lds_bload4(rs_s, srcp.s[h_], (uint32_t)(kb) * (uint32_t)sa_kb * 4u,               \
                  d_ + L::SCL + (wn + 4 * h_) * 256);                                    \
     }                                                                                   \
-  } while (0)
-#define TILE_PREFETCH_P(kb)                                                             \
-  do {                                                                                  \
-    _Pragma("unroll") for (int j = 0; j < kPfP; ++j)                                    \
-        lds_load4(srcp.pf[j] + (size_t)(kb) * 128, smem + S * L::STAGE + wave * 256);   \
   } while (0)
 #define TILE_NODMA(st, kb, j) \
   do {                        \
@@ -705,11 +676,10 @@ __global__ __launch_bounds__(256 * WM) void gemm_tile_kernel(GemmParams p) {
       if (wmu == (st & 1)) {
 #pragma unroll
         for (int j = 0; j < kGroupP; ++j) TILE_DMA_P(st, min(st, KB - 1), j);
-        TILE_PREFETCH_P(min(st + 1, KB - 1));
       }
       __builtin_amdgcn_sched_barrier(0);
     }
-    asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(kPfP) : "memory");
+    asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
   } else {
 #pragma unroll
     for (int st = 0; st < S - 1; ++st) {
@@ -747,13 +717,13 @@ __global__ __launch_bounds__(256 * WM) void gemm_tile_kernel(GemmParams p) {
     if constexpr (!kAlt) {                                                              \
       while (it < KB) TILE_STEP(MV, TILE_DMA_J, kGroup, TILE_PREFETCH, kWait);          \
     } else {                                                                            \
-      if (wmu != ((S - 1) & 1)) TILE_STEP(MV, TILE_NODMA, 0, TILE_NOPF, kPfP);           \
+      if (wmu != ((S - 1) & 1)) TILE_STEP(MV, TILE_NODMA, 0, TILE_NOPF, 0);              \
       while (it + 1 < KB) {                                                             \
-        TILE_STEP(MV, TILE_DMA_P, kGroupP, TILE_PREFETCH_P, kWaitLd);                    \
-        TILE_STEP(MV, TILE_NODMA, 0, TILE_NOPF, kPfP);                                   \
+        TILE_STEP(MV, TILE_DMA_P, kGroupP, TILE_NOPF, kWaitLd);                          \
+        TILE_STEP(MV, TILE_NODMA, 0, TILE_NOPF, 0);                                      \
       }                                                                                 \
       /* the last step's loads would only repeat the last K block */                    \
-      if (it < KB) TILE_STEP(MV, TILE_NODMA, 0, TILE_NOPF, kPfP);                        \
+      if (it < KB) TILE_STEP(MV, TILE_NODMA, 0, TILE_NOPF, 0);                           \
     }                                                                                   \
   } while (0)
   // A ragged tile (an expert's last M-tile, or a tile taller than the
@@ -924,7 +894,6 @@ __global__ __launch_bounds__(256 * WM) void tile_persist_kernel(GemmParams p) {
 #undef TILE_PREFETCH
 #undef TILE_DMA_J
 #undef TILE_DMA_P
-#undef TILE_PREFETCH_P
 #undef TILE_NODMA
 #undef TILE_NOPF
 #undef TILE_STAGE
