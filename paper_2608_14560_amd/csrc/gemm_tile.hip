@@ -539,7 +539,11 @@ __global__ __launch_bounds__(256 * WM) void gemm_tile_kernel(GemmParams p) {
   // the 256-row GEMM1 tiles raise their waves' issue priority for a step's
   // math and drop it before the step's barrier (measured: skewed GEMM1
   // 1968 -> 1934 us over three alternating runs; the 128-row prefill tiles
-  // lost 6 us with it, GEMM2 unchanged)
+  // lost 6 us with it, GEMM2 unchanged).  With alternating loads the loading
+  // wave of a step runs above its partner for the whole step, so that its
+  // loads and MFMAs issue first and the partner fills the gaps (skewed GEMM1
+  // 1785 -> 1763 us, GEMM2 1065 -> 1057, prefill GEMM1 274 -> 271 over two
+  // alternating runs)
   constexpr bool kPrio = G1 && L::BM == 256;
   constexpr int kSpread = MT / 2;
   static_assert(kWait < 64, "vmcnt holds 6 bits");
@@ -633,7 +637,8 @@ __global__ __launch_bounds__(256 * WM) void gemm_tile_kernel(GemmParams p) {
       sav_[4 * q_ + 2] = v_.z;                                                          \
       sav_[4 * q_ + 3] = v_.w;                                                          \
     }                                                                                   \
-    if (kPrio) __builtin_amdgcn_s_setprio(1);                                           \
+    if (kAlt && (NG) > 0) __builtin_amdgcn_s_setprio(2);                                \
+    else if (kPrio) __builtin_amdgcn_s_setprio(1);                                      \
     v8i bf_[4];                                                                         \
     _Pragma("unroll") for (int n = 0; n < 4; ++n) bf_[n] =                              \
         tile_frag(bs_ + n * 2048, rd_lo, rd_hi);                                        \
@@ -699,7 +704,7 @@ __global__ __launch_bounds__(256 * WM) void gemm_tile_kernel(GemmParams p) {
     TILE_COMPUTE(st_rd, it, st_ld, min(it + S - 1, KB - 1), min(it + S, KB - 1), MV,     \
                  DMA, NG, PFM);                                                         \
     __builtin_amdgcn_sched_barrier(0);                                                  \
-    if (kPrio) __builtin_amdgcn_s_setprio(0);                                           \
+    if (kPrio || kAlt) __builtin_amdgcn_s_setprio(0);                                   \
     asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(W) : "memory");    \
     st_rd = st_rd + 1 == S ? 0 : st_rd + 1;                                             \
     st_ld = st_ld + 1 == S ? 0 : st_ld + 1;                                             \
@@ -796,6 +801,7 @@ __global__ __launch_bounds__(256 * WM) void tile_persist_kernel(GemmParams p) {
   constexpr int kGroup = JA + JB + 1;
   constexpr int kWait = (S - 2) * (kGroup + kPfLoads) + kPfLoads;
   constexpr bool kPrio = false;  // (see gemm_tile_kernel)
+  constexpr bool kAlt = false;
   constexpr int kSpread = MT / 2;
   static_assert(kWait < 64, "vmcnt holds 6 bits");
   static_assert(S >= 2, "LDS ring depth");
