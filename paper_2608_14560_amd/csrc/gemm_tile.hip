@@ -57,7 +57,9 @@ struct TileLayout {
   static constexpr int SS = MT * WM >= 8 ? MT * WM + 4 : MT * WM;
   static_assert(16 * SS <= 64 * 4 * WM, "row-scale slots fit the workgroup's lanes");
   static constexpr int RING = S * STAGE + JUNK;
-  static size_t bytes(int KB) { return (size_t)RING + sizeof(float) * 2 * (size_t)KB; }
+  // the ring, then the two weight-scale rows of an item (2 KB floats, filled
+  // 64 at a time by direct loads)
+  static size_t bytes(int KB) { return (size_t)RING + sizeof(float) * (size_t)((2 * KB + 63) / 64 * 64); }
 };
 
 typedef __attribute__((address_space(3))) void lds_void;
@@ -355,7 +357,7 @@ __device__ __forceinline__ void tile_store_act(const GemmParams &p, const v4f (&
     for (int h = 0; h < 2; ++h)
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        a[m][h][i] = swiglu_spec(acc[m][h][i], acc[m][h + 2][i]);
+        a[m][h][i] = swiglu_fast(acc[m][h][i], acc[m][h + 2][i]);
         mx = fmaxf(mx, fabsf(a[m][h][i]));
       }
     // the row's 32 columns of this wave sit in lanes r16, r16+16, r16+32, r16+48
@@ -486,19 +488,22 @@ __global__ __launch_bounds__(256 * WM) void gemm_tile_kernel(GemmParams p) {
   const __amdgpu_buffer_rsrc_t rs_s = tile_rsrc(p.sa_tile, 4u * (uint32_t)p.P_max * (uint32_t)p.KB);
   const int half = wn >> 1;
 
-  // weight-block scales of the whole K range: sb_l[0][kb] (wn 0/1), sb_l[1][kb]
+  // weight-block scales of the whole K range: sb_l[0][kb] (wn 0/1), sb_l[1][kb].
+  // Wave 0 loads them straight into LDS before its first stage's loads, so
+  // the prologue's wait and barrier cover them (no round trip through
+  // registers and no barrier of their own in front of the A-row lookups:
+  // skewed GEMM1 spends ~14 us per item outside its K loop)
   float *sb_l = reinterpret_cast<float *>(smem + L::RING);
-  {
+  if (wave == 0) {
     const float *s0 = p.B_scale + ((size_t)e * (p.N_total / 128) + ti.nblk0) * KB;
     const float *s1 = p.B_scale + ((size_t)e * (p.N_total / 128) + ti.nblk1) * KB;
-    for (int i = tid; i < KB; i += NT) {
-      sb_l[i] = s0[i];
-      sb_l[KB + i] = s1[i];
+    for (int c = 0; c < 2 * KB; c += kWave) {
+      const int i = c + lane;
+      lds_load4(i < KB ? s0 + i : s1 + min(i - KB, KB - 1), reinterpret_cast<uint8_t *>(sb_l + c));
     }
   }
   // GEMM1: gate scales at sb_w[kb], up scales at sb_w[KB + kb]
   const float *sb_w = G1 ? sb_l : sb_l + half * KB;
-  __syncthreads();
 
   // ---- direct-load sources
   constexpr int JA = BM / 8 / (4 * WM);  // A blocks per wave

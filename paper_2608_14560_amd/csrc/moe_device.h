@@ -92,6 +92,32 @@ __device__ __forceinline__ float swiglu_spec(float g, float u) {
   return silu * u;
 }
 
+// SwiGLU for the large-tile GEMM1 epilogue, where it runs on every element
+// of a tile (64 per lane of a 256-row tile) and its cost is not hidden behind
+// loads: silu(g) * u with sigma(g) = 1 / (1 + 2^t), t = -g log2(e), from the
+// hardware's base-2 exponential and reciprocal (each within about an ulp).
+// t is carried in two parts -- its fp32 rounding and the remainder (a fused
+// multiply-add, plus -g times the constant's own fp32 tail) -- and
+// 2^t = 2^t_hi (1 + t_lo ln 2), so the exponential keeps a few-ulp relative
+// accuracy for any |g|; one Newton step refines the reciprocal.  Relative
+// error of the result a few u (u = 2^-24), inside the 8 u the re-quantised
+// intermediate's admissible set allows; sigma is exactly 1 where 2^t is below
+// half an ulp of 1 (g >= 17), so SwiGLU is g * u there.  The routing keeps
+// the fixed sequence above (its sigmoid decides expert selection).
+__device__ __forceinline__ float swiglu_fast(float g, float u) {
+  const float kLog2e = 0x1.715476p+0f;     // log2(e) rounded to fp32
+  const float kLog2eLo = 0x1.4ae0c0p-26f;  // log2(e) - kLog2e
+  const float kLn2 = 0x1.62e430p-1f;
+  const float z = -g;
+  const float t = z * kLog2e;
+  const float tl = __builtin_fmaf(z, kLog2eLo, __builtin_fmaf(z, kLog2e, -t));
+  const float e = __builtin_amdgcn_exp2f(t) * __builtin_fmaf(tl, kLn2, 1.0f);
+  const float d = 1.0f + e;
+  const float s0 = __builtin_amdgcn_rcpf(d);
+  const float s = __builtin_fmaf(s0, __builtin_fmaf(-d, s0, 1.0f), s0);
+  return (g * s) * u;
+}
+
 // Total order used by every selection of the routing stage: the larger value
 // wins, equal values go to the lower index.
 __device__ __forceinline__ bool beats(float va, int ia, float vb, int ib) {
