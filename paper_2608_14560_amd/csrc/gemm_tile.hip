@@ -374,12 +374,13 @@ __device__ __forceinline__ void tile_store_act(const GemmParams &p, const v4f (&
     const float scale = (amax > 0.0f) ? amax / 448.0f : 1.0f;
     if (r < nrows) {
       uint8_t *arow = p.act + (size_t)(row0 + r) * p.I + nb * 128 + 32 * wn + 4 * g4;
+      const DivBy ds(scale);  // the row's eight quotients share the divisor
 #pragma unroll
       for (int h = 0; h < 2; ++h) {
         uint32_t q = 0u;
         if (amax > 0.0f)
-          q = e4m3x2_rne_sat(a[m][h][0] / scale, a[m][h][1] / scale) |
-              (e4m3x2_rne_sat(a[m][h][2] / scale, a[m][h][3] / scale) << 16);
+          q = e4m3x2_rne_sat(ds(a[m][h][0]), ds(a[m][h][1])) |
+              (e4m3x2_rne_sat(ds(a[m][h][2]), ds(a[m][h][3])) << 16);
         *reinterpret_cast<uint32_t *>(arow + 16 * h) = q;
       }
       if (wn == 0 && g4 == 0) {

@@ -118,6 +118,27 @@ __device__ __forceinline__ float swiglu_fast(float g, float u) {
   return (g * s) * u;
 }
 
+// The correctly rounded quotient v / b of several values by one divisor b:
+// y = 1 / b (one correctly rounded division per divisor), then per value
+// q = v y refined by its exact remainder, q' = q + (v - q b) y (two fused
+// multiply-adds) -- with y the rounded reciprocal and q within an ulp, this
+// correction rounds to the same result as the division (Markstein's
+// theorem for round-to-nearest).  A divisor below 2^-100 has both operands
+// scaled by 2^64 first (exact), so y stays finite.
+struct DivBy {
+  float b, y, pre;
+  __device__ __forceinline__ explicit DivBy(float d) {
+    pre = d < 0x1p-100f ? 0x1p64f : 1.0f;
+    b = d * pre;
+    y = 1.0f / b;
+  }
+  __device__ __forceinline__ float operator()(float v) const {
+    const float vv = v * pre;
+    const float q = vv * y;
+    return __builtin_fmaf(__builtin_fmaf(-q, b, vv), y, q);
+  }
+};
+
 // Total order used by every selection of the routing stage: the larger value
 // wins, equal values go to the lower index.
 __device__ __forceinline__ bool beats(float va, int ia, float vb, int ib) {
