@@ -328,13 +328,13 @@ __device__ __forceinline__ void tile_store_y(const GemmParams &p, const v4f (&ac
         uint2 c;
         c.x = (uint32_t)y16_code(acc[m][n][0], ex[n]) | ((uint32_t)y16_code(acc[m][n][1], ex[n]) << 16);
         c.y = (uint32_t)y16_code(acc[m][n][2], ex[n]) | ((uint32_t)y16_code(acc[m][n][3], ex[n]) << 16);
-        *reinterpret_cast<uint2 *>(yrow + 16 * n) = c;
+        __builtin_nontemporal_store(u32x2{c.x, c.y}, reinterpret_cast<u32x2 *>(yrow + 16 * n));
       }
       // lane r16 + 16 g4 stores the exponent of chunk g4
       int eg = ex[0];
 #pragma unroll
       for (int n = 1; n < 4; ++n) eg = g4 == n ? ex[n] : eg;
-      p.Ye[(size_t)(row0 + r) * HC + wrow0 / kYChunk + g4] = (int8_t)eg;
+      __builtin_nontemporal_store((int8_t)eg, p.Ye + (size_t)(row0 + r) * HC + wrow0 / kYChunk + g4);
     }
   }
 }
@@ -399,7 +399,12 @@ __device__ __forceinline__ void tile_store_act(const GemmParams &p, const v4f (&
 // dword per row), and are read
 // back row-contiguously, so each global store instruction writes whole
 // 128-byte lines (8 rows x 8 lanes x 16 bytes) instead of 32-byte pieces of
-// four lines.  Same codes and exponents as tile_store_y.
+// four lines.  Same codes and exponents as tile_store_y.  Both write Y
+// non-temporally: its 0.94 GB at the skewed load would otherwise fill the
+// XCDs' L2 with lines no GEMM workgroup reads again, evicting the weight
+// panels and activation tiles the concurrent items share (measured: skewed
+// layer 3149 -> 3076 us over two alternating runs, the combine that reads Y
+// back 227 -> 202 us, GEMM1 of the next call 1818 -> 1771)
 template <int MT>
 __device__ __forceinline__ void tile_store_y_lds(const GemmParams &p, const v4f (&acc)[MT][4], int row0,
                                                  int nrows, int wrow0, int wrow, int lane,
@@ -442,14 +447,14 @@ __device__ __forceinline__ void tile_store_y_lds(const GemmParams &p, const v4f 
     const int lr = 8 * k + (lane >> 3), c = lane & 7;
     const u32x4 v = *reinterpret_cast<const u32x4 *>(wl + lr * 128 + ((c ^ (lr & 7) ^ ((lr >> 3) & 1)) * 16));
     if (wrow + lr < nrows)
-      *reinterpret_cast<u32x4 *>(p.Y + (size_t)(row0 + wrow + lr) * p.H + wrow0 + 8 * c) = v;
+      __builtin_nontemporal_store(v, reinterpret_cast<u32x4 *>(p.Y + (size_t)(row0 + wrow + lr) * p.H + wrow0 + 8 * c));
   }
 #pragma unroll
   for (int k = 0; k < R / 64; ++k) {
     const int lr = 64 * k + lane;
     const uint32_t v = *reinterpret_cast<const uint32_t *>(el + lr * 4);
     if (wrow + lr < nrows)
-      *reinterpret_cast<uint32_t *>(p.Ye + (size_t)(row0 + wrow + lr) * HC + wrow0 / kYChunk) = v;
+      __builtin_nontemporal_store(v, reinterpret_cast<uint32_t *>(p.Ye + (size_t)(row0 + wrow + lr) * HC + wrow0 / kYChunk));
   }
 }
 
