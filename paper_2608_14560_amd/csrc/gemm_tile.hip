@@ -427,8 +427,8 @@ __device__ __forceinline__ void tile_store_y_lds(const GemmParams &p, const v4f 
 #pragma unroll
     for (int n = 0; n < 4; ++n) {
       uint2 c;
-      c.x = (uint32_t)y16_code(acc[m][n][0], ex[n]) | ((uint32_t)y16_code(acc[m][n][1], ex[n]) << 16);
-      c.y = (uint32_t)y16_code(acc[m][n][2], ex[n]) | ((uint32_t)y16_code(acc[m][n][3], ex[n]) << 16);
+      c.x = y16_code2(acc[m][n][0], acc[m][n][1], ex[n]);
+      c.y = y16_code2(acc[m][n][2], acc[m][n][3], ex[n]);
       const int ch = (2 * n + (g4 >> 1)) ^ (lr & 7) ^ ((lr >> 3) & 1);  // chunk of columns 16n + 4g4
       *reinterpret_cast<uint2 *>(wl + lr * 128 + ch * 16 + 8 * (g4 & 1)) = c;
     }

@@ -52,6 +52,14 @@ __device__ __forceinline__ uint16_t y16_code(float y, int e) {
   const _Float16 h = (_Float16)__builtin_amdgcn_ldexpf(y, -e);
   return __builtin_bit_cast(uint16_t, h);
 }
+// two codes of one chunk packed as (lo, hi) in one dword: the same values as
+// y16_code, by the packed fp32 -> fp16 conversion (nearest even)
+__device__ __forceinline__ uint32_t y16_code2(float y0, float y1, int e) {
+  typedef float f32x2_ __attribute__((ext_vector_type(2)));
+  typedef _Float16 f16x2_ __attribute__((ext_vector_type(2)));
+  const f32x2_ v = {__builtin_amdgcn_ldexpf(y0, -e), __builtin_amdgcn_ldexpf(y1, -e)};
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, f16x2_));
+}
 __device__ __forceinline__ float y16_value(uint16_t c, int e) {
   return __builtin_amdgcn_ldexpf((float)__builtin_bit_cast(_Float16, c), e);
 }
