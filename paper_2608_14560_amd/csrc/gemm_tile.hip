@@ -19,7 +19,9 @@
 // Every K-step's operands -- the A tile (rows gathered through perm_token
 // for GEMM1), its row scales and the 256 weight rows -- go straight from
 // global memory into an S-stage LDS ring (direct loads issued S-1 K-steps
-// ahead, no registers), with one barrier per K-step.
+// ahead, no registers), with one barrier per K-step.  In the eight-wave
+// tiles the two waves of a SIMD take turns issuing a step's loads (see
+// TileSrcPair), so one of them always has only math to issue.
 //
 // The weight fragment is the MFMA's first operand and the activation fragment
 // its second, so lane l holds output columns 4*(l/16)+i (i = 0..3) of token
