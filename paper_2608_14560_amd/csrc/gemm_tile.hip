@@ -466,7 +466,6 @@ __global__ __launch_bounds__(256 * WM) void gemm_tile_kernel(GemmParams p) {
   constexpr int NT = L::THREADS;
   static_assert(NT == 256 * WM, "launch bound");
   constexpr int BM = L::BM;
-  constexpr int MTW = MT * WM;  // 16-row blocks of the tile
   static_assert(MT % 4 == 0, "row scales are read four at a time");
 
   __shared__ float amax_l[4][BM];
@@ -785,9 +784,7 @@ __global__ __launch_bounds__(256 * WM) void gemm_tile_kernel(GemmParams p) {
 template <bool G1, int MT, int WM, int S>
 __global__ __launch_bounds__(256 * WM) void tile_persist_kernel(GemmParams p) {
   using L = TileLayout<MT, WM, S>;
-  constexpr int NT = L::THREADS;
   constexpr int BM = L::BM;
-  constexpr int MTW = MT * WM;
   static_assert(MT % 4 == 0, "row scales are read four at a time");
 
   __shared__ float amax_l[4][BM];
